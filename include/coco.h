@@ -1,0 +1,199 @@
+/*
+ * coco.h -- C ABI of the layer-replica hot path on one MI355X (gfx950).
+ *
+ * A layer replica (Sec. 3.1 of the paper, replication mechanism) holds a full
+ * copy of the weights of one or more consecutive decoder layers plus its own
+ * partition of the paged key/value cache, and runs the unchanged layer on its
+ * sub-batch: the rows of the in-flight batch it was given. The library does
+ * exactly that step on one GPU:
+ *
+ *   gather rows -> RMSNorm -> QKV projection -> RoPE + KV append ->
+ *   paged GQA attention -> O projection + residual -> RMSNorm ->
+ *   SwiGLU MLP + residual -> scatter rows
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Pointers. Every data pointer is a DEVICE pointer into memory the caller
+ *   owns (weights, caches, hidden buffer, index arrays). The library borrows
+ *   weights and caches for the handle's lifetime and the rest for the call.
+ *   The only memory the library owns is its workspace, allocated once in
+ *   coco_layer_init and sized by the config (the paper's persistent memory
+ *   pool with fixed addresses, Sec. 5.2, CUDA-graph compatibility).
+ * Streams. `stream` is a hipStream_t (NULL = the null stream). Work is
+ *   enqueued on it; calls return without synchronising, never allocate, and
+ *   keep every address fixed, so a call can be captured in a HIP graph --
+ *   except with validation switched on, which copies index arrays to the host.
+ * Element types. dtype COCO_BF16: weights, hidden, caches and k/v inputs are
+ *   bfloat16 (uint16 bit patterns); accumulation and softmax are fp32.
+ *   dtype COCO_F32: all of those are float32.
+ * Errors. A negative return is an error; coco_last_error() gives a message
+ *   (thread-local). Host-checkable faults return COCO_EINVAL before anything
+ *   is enqueued; a failed launch returns COCO_EHIP. Device-side contents of
+ *   index arrays are checked only in validation mode (coco_layer_set_validate).
+ * Threads. A handle is not thread-safe; calls that overlap on one handle
+ *   (including from different streams) race on its workspace.
+ *
+ * Layouts
+ * -------
+ * Weights of one layer, nn.Linear layout ([out][in], row-major):
+ *   w_qkv     [(Hq + 2*Hkv) * hd][d]   query heads, then key heads, then value
+ *                                      heads, hd rows each
+ *   w_o       [d][Hq * hd]
+ *   w_gate_up [2*F][d]                 F gate rows, then F up rows
+ *   w_down    [d][F]
+ *   gamma_attn, gamma_mlp [d]          RMSNorm gains
+ * Paged cache of one layer, with block size B = 16 tokens:
+ *   k_cache [num_blocks][Hkv][B][hd]   token-major inside a block
+ *   v_cache [num_blocks][Hkv][hd][B]   dimension-major inside a block
+ *   Token t of sequence s lives in block block_table[s][t / 16], slot t % 16.
+ *   Keys are stored after rotation (RoPE), values as projected.
+ * Batch arrays (int32, device):
+ *   row_idx[n_rows]        hidden row of each call row; distinct, < hidden_rows
+ *   positions[n_rows]      absolute position of each call row's token
+ *   seq_starts[n_seqs+1]   prefill: call rows of sequence s are
+ *                          seq_starts[s] .. seq_starts[s+1]-1, in position
+ *                          order. NULL = decode: call row i is sequence i
+ *                          (then n_seqs == n_rows).
+ *   block_table[n_seqs][max_blocks_per_seq]   physical block ids, -1 unused
+ *   ctx_lens[n_seqs]       cached tokens of sequence s once this call's tokens
+ *                          are appended (decode: positions[i] + 1)
+ * Every token attends to the cached keys of its own sequence at positions
+ * 0 .. its own position (causal), its own key included.
+ */
+#ifndef COCO_H
+#define COCO_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct coco_layer* coco_layer_t;
+typedef void* coco_stream_t; /* hipStream_t */
+
+enum {
+  COCO_OK = 0,
+  COCO_EINVAL = -1, /* bad argument or unsupported configuration */
+  COCO_ENOMEM = -2, /* workspace allocation failed (init only) */
+  COCO_EHIP = -3,   /* a HIP runtime call or kernel launch failed */
+  COCO_ESTATE = -4  /* handle unusable (e.g. destroyed, or a previous HIP fault) */
+};
+
+enum { COCO_BF16 = 0, COCO_F32 = 1 };
+
+typedef struct {
+  int32_t d_model;            /* d */
+  int32_t n_q_heads;          /* Hq */
+  int32_t n_kv_heads;         /* Hkv; Hq % Hkv == 0 */
+  int32_t head_dim;           /* hd; 128 for COCO_BF16, even and <= 256 for COCO_F32 */
+  int32_t d_ffn;              /* F */
+  int32_t n_layers;           /* layers held by this handle */
+  int32_t dtype;              /* COCO_BF16 or COCO_F32 */
+  int32_t block_size;         /* must be 16 */
+  int32_t max_rows;           /* largest n_rows of any call (decode rows or prefill tokens) */
+  int32_t max_seqs;           /* largest n_seqs of any call */
+  int32_t max_blocks_per_seq; /* row stride of block_table */
+  float rope_theta;           /* RoPE base theta */
+  float rms_eps;              /* RMSNorm epsilon */
+} coco_layer_config;
+
+typedef struct {
+  const void* w_qkv;
+  const void* w_o;
+  const void* w_gate_up;
+  const void* w_down;
+  const void* gamma_attn;
+  const void* gamma_mlp;
+  void* k_cache;
+  void* v_cache;
+  int64_t num_blocks; /* blocks in this layer's k_cache and v_cache */
+} coco_layer_weights;
+
+/* Create a replica handle for n_layers consecutive layers (Sec. 3.1: the
+ * replicated unit is a span of consecutive layers). `layers` points to
+ * cfg->n_layers host structs of device pointers; they are copied. Allocates
+ * the workspace on the current HIP device. Returns COCO_EINVAL for an
+ * unsupported shape (bf16: head_dim != 128, Hq/Hkv > 16, d, F or Hq*hd not
+ * multiples of 128), COCO_ENOMEM if the workspace does not fit. */
+int coco_layer_init(const coco_layer_config* cfg, const coco_layer_weights* layers,
+                    coco_layer_t* out);
+
+/* Release the workspace and the handle. Waits for work on the device first.
+ * NULL is ignored. */
+void coco_layer_destroy(coco_layer_t h);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* coco_last_error(void);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int coco_version(void);
+
+/* Switch device-side argument validation on (1) or off (0). When on, every
+ * forward/append copies its index arrays to the host, synchronising the
+ * stream, and rejects duplicate or out-of-range row_idx, non-increasing
+ * positions within a sequence, positions >= ctx_lens, ctx_lens beyond the
+ * block table, and block ids outside [0, num_blocks) with COCO_EINVAL before
+ * launching. Off by default. */
+int coco_layer_set_validate(coco_layer_t h, int32_t on);
+
+/* Write n_tok tokens of keys and values into layer `layer`'s paged cache
+ * (Sec. 3.1: each replica appends key/value entries to its own partition).
+ * k, v: [n_tok][Hkv][hd] in the handle's dtype, k already rotated.
+ * seq_idx[n_tok]: sequence of each token (row of block_table, < n_seqs).
+ * positions[n_tok]: position of each token. A bit copy: the stored values
+ * equal the inputs bit for bit. Tokens must name distinct (sequence,
+ * position) pairs. */
+int coco_kv_append(coco_layer_t h, int32_t layer, const void* k, const void* v,
+                   const int32_t* seq_idx, const int32_t* positions, int32_t n_tok,
+                   const int32_t* block_table, int32_t n_seqs, coco_stream_t stream);
+
+/* One decoder layer on the call rows of `hidden` ([hidden_rows][d], updated
+ * in place): rows named in row_idx receive the layer output, every other row
+ * is left untouched (Sec. 3.1: the replica processes its sub-batch and the
+ * outputs are gathered back on the batch axis). The call's keys and values
+ * are appended to the layer's cache before attention. n_rows == 0 is a no-op.
+ * Results do not depend on which other rows share the call: any partition of
+ * a decode batch, and any request-aligned partition of a prefill batch, gives
+ * output rows and cache bytes identical bit for bit to the whole batch
+ * (Sec. 5.2: outputs bit-wise consistent with the baseline). */
+int coco_layer_forward(coco_layer_t h, int32_t layer, void* hidden, int64_t hidden_rows,
+                       const int32_t* row_idx, int32_t n_rows, const int32_t* positions,
+                       const int32_t* seq_starts, int32_t n_seqs,
+                       const int32_t* block_table, const int32_t* ctx_lens,
+                       coco_stream_t stream);
+
+/* Layers first_layer .. first_layer+n_layers-1 as one replicated segment
+ * (Sec. 3.1: consecutive layers are replicated as a unit, activations stay in
+ * local memory and transfers happen only at the segment boundaries): one
+ * gather, every layer on the resident rows, one scatter. Between layers the
+ * rows are held in the handle's dtype, so the result equals n_layers
+ * successive coco_layer_forward calls bit for bit. */
+int coco_layer_span_forward(coco_layer_t h, int32_t first_layer, int32_t n_layers,
+                            void* hidden, int64_t hidden_rows, const int32_t* row_idx,
+                            int32_t n_rows, const int32_t* positions,
+                            const int32_t* seq_starts, int32_t n_seqs,
+                            const int32_t* block_table, const int32_t* ctx_lens,
+                            coco_stream_t stream);
+
+/* Copy an intermediate buffer of the last call into `dst` (device memory of
+ * at least dst_bytes bytes), for inspection by tests. which = COCO_WS_*;
+ * row i holds call row i of the last layer run. Copies min(dst_bytes, buffer
+ * size) bytes on `stream`. */
+enum {
+  COCO_WS_X = 0,  /* layer input rows, [max_rows][d], dtype */
+  COCO_WS_H = 1,  /* RMSNorm_1 output, [max_rows][d], dtype */
+  COCO_WS_Q = 2,  /* rotated queries, [max_rows][Hq*hd], dtype */
+  COCO_WS_O = 3,  /* attention output, [max_rows][Hq*hd], dtype */
+  COCO_WS_X1 = 4, /* residual after the O projection, [max_rows][d], fp32 */
+  COCO_WS_H2 = 5, /* RMSNorm_2 output, [max_rows][d], dtype */
+  COCO_WS_U = 6   /* SwiGLU activation, [max_rows][F], dtype */
+};
+int coco_layer_workspace(coco_layer_t h, int32_t which, void* dst, int64_t dst_bytes,
+                         coco_stream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* COCO_H */

@@ -1,0 +1,197 @@
+"""ctypes binding of libcoco.so: argument marshalling only.
+
+Every function has the name of the C entry point it calls (see
+include/coco.h for semantics, layouts and errors). Tensors are torch tensors
+on the GPU; only their device addresses are passed. Negative return codes
+raise CocoError with the library's message. There is no fallback: if the
+library is not built, importing this module raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libcoco.so")
+
+COCO_OK, COCO_EINVAL, COCO_ENOMEM, COCO_EHIP, COCO_ESTATE = 0, -1, -2, -3, -4
+COCO_BF16, COCO_F32 = 0, 1
+COCO_WS_X, COCO_WS_H, COCO_WS_Q, COCO_WS_O, COCO_WS_X1, COCO_WS_H2, COCO_WS_U = range(7)
+
+EXPORTS = ["coco_layer_init", "coco_layer_destroy", "coco_last_error", "coco_version",
+           "coco_layer_set_validate", "coco_kv_append", "coco_layer_forward",
+           "coco_layer_span_forward", "coco_layer_workspace"]
+
+
+class CocoError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"coco error {code}: {msg}")
+        self.code = code
+
+
+class coco_layer_config(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "d_model", "n_q_heads", "n_kv_heads", "head_dim", "d_ffn", "n_layers", "dtype",
+        "block_size", "max_rows", "max_seqs", "max_blocks_per_seq")] + [
+        ("rope_theta", ctypes.c_float), ("rms_eps", ctypes.c_float)]
+
+
+class coco_layer_weights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in (
+        "w_qkv", "w_o", "w_gate_up", "w_down", "gamma_attn", "gamma_mlp", "k_cache",
+        "v_cache")] + [("num_blocks", ctypes.c_int64)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
+    lib = ctypes.CDLL(LIB_PATH)
+    i32, i64, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p
+    sig = {
+        "coco_layer_init": (ctypes.c_int, [ctypes.POINTER(coco_layer_config),
+                                           ctypes.POINTER(coco_layer_weights),
+                                           ctypes.POINTER(vp)]),
+        "coco_layer_destroy": (None, [vp]),
+        "coco_last_error": (ctypes.c_char_p, []),
+        "coco_version": (ctypes.c_int, []),
+        "coco_layer_set_validate": (ctypes.c_int, [vp, i32]),
+        "coco_kv_append": (ctypes.c_int, [vp, i32, vp, vp, vp, vp, i32, vp, i32, vp]),
+        "coco_layer_forward": (ctypes.c_int, [vp, i32, vp, i64, vp, i32, vp, vp, i32, vp, vp,
+                                              vp]),
+        "coco_layer_span_forward": (ctypes.c_int, [vp, i32, i32, vp, i64, vp, i32, vp, vp, i32,
+                                                   vp, vp, vp]),
+        "coco_layer_workspace": (ctypes.c_int, [vp, i32, vp, i64, vp]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    return lib
+
+
+_lib = _load()
+
+
+def _check(rc: int) -> int:
+    if rc < 0:
+        raise CocoError(rc, _lib.coco_last_error().decode())
+    return rc
+
+
+def _ptr(t, dtype=None, what="tensor"):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{what} must be a torch tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{what} must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{what} must be {dtype}, got {t.dtype}")
+    return t.data_ptr() if t.numel() else None
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if isinstance(stream, torch.cuda.Stream) else stream
+
+
+class Handle:
+    """An initialised replica; keeps the borrowed tensors alive."""
+
+    def __init__(self, raw, cfg, keep):
+        self.raw = raw
+        self.cfg = cfg
+        self._keep = keep
+
+    def __del__(self):
+        if getattr(self, "raw", None):
+            _lib.coco_layer_destroy(self.raw)
+            self.raw = None
+
+
+def coco_version() -> int:
+    return _lib.coco_version()
+
+
+def coco_last_error() -> str:
+    return _lib.coco_last_error().decode()
+
+
+def make_config(d_model, n_q_heads, n_kv_heads, head_dim, d_ffn, n_layers, dtype, max_rows,
+                max_seqs, max_blocks_per_seq, rope_theta, rms_eps, block_size=16):
+    return coco_layer_config(d_model, n_q_heads, n_kv_heads, head_dim, d_ffn, n_layers,
+                             COCO_BF16 if dtype in ("bf16", COCO_BF16) else COCO_F32,
+                             block_size, max_rows, max_seqs, max_blocks_per_seq,
+                             float(rope_theta), float(rms_eps))
+
+
+def coco_layer_init(cfg: coco_layer_config, layers) -> Handle:
+    """layers: list of dicts with w_qkv, w_o, w_gate_up, w_down, gamma_attn,
+    gamma_mlp, k_cache, v_cache (device tensors)."""
+    arr = (coco_layer_weights * len(layers))()
+    keep = []
+    for i, w in enumerate(layers):
+        for k in ("w_qkv", "w_o", "w_gate_up", "w_down", "gamma_attn", "gamma_mlp", "k_cache",
+                  "v_cache"):
+            setattr(arr[i], k, _ptr(w[k], what=k))
+            keep.append(w[k])
+        arr[i].num_blocks = int(w["k_cache"].shape[0])
+    raw = ctypes.c_void_p()
+    _check(_lib.coco_layer_init(ctypes.byref(cfg), arr, ctypes.byref(raw)))
+    return Handle(raw, cfg, keep)
+
+
+def coco_layer_destroy(h: Handle) -> None:
+    if h.raw:
+        _lib.coco_layer_destroy(h.raw)
+        h.raw = None
+
+
+def coco_layer_set_validate(h: Handle, on: bool) -> None:
+    _check(_lib.coco_layer_set_validate(h.raw, 1 if on else 0))
+
+
+def coco_kv_append(h: Handle, layer: int, k, v, seq_idx, positions, block_table, stream=None):
+    i32 = torch.int32
+    _check(_lib.coco_kv_append(h.raw, layer, _ptr(k, what="k"), _ptr(v, what="v"),
+                               _ptr(seq_idx, i32, "seq_idx"), _ptr(positions, i32, "positions"),
+                               int(positions.numel()), _ptr(block_table, i32, "block_table"),
+                               int(block_table.shape[0]), _stream(stream)))
+
+
+def coco_layer_forward(h: Handle, layer: int, hidden, row_idx, positions, seq_starts,
+                       block_table, ctx_lens, stream=None):
+    i32 = torch.int32
+    n_seqs = int(ctx_lens.numel())
+    _check(_lib.coco_layer_forward(
+        h.raw, layer, _ptr(hidden, what="hidden"), int(hidden.shape[0]),
+        _ptr(row_idx, i32, "row_idx"), int(row_idx.numel()), _ptr(positions, i32, "positions"),
+        _ptr(seq_starts, i32, "seq_starts"), n_seqs, _ptr(block_table, i32, "block_table"),
+        _ptr(ctx_lens, i32, "ctx_lens"), _stream(stream)))
+
+
+def coco_layer_span_forward(h: Handle, first_layer: int, n_layers: int, hidden, row_idx,
+                            positions, seq_starts, block_table, ctx_lens, stream=None):
+    i32 = torch.int32
+    n_seqs = int(ctx_lens.numel())
+    _check(_lib.coco_layer_span_forward(
+        h.raw, first_layer, n_layers, _ptr(hidden, what="hidden"), int(hidden.shape[0]),
+        _ptr(row_idx, i32, "row_idx"), int(row_idx.numel()), _ptr(positions, i32, "positions"),
+        _ptr(seq_starts, i32, "seq_starts"), n_seqs, _ptr(block_table, i32, "block_table"),
+        _ptr(ctx_lens, i32, "ctx_lens"), _stream(stream)))
+
+
+def coco_layer_workspace(h: Handle, which: int, dst, stream=None) -> None:
+    _check(_lib.coco_layer_workspace(h.raw, which, _ptr(dst, what="dst"),
+                                     dst.numel() * dst.element_size(), _stream(stream)))
+
+
+def raw_call(name: str, *args) -> int:
+    """Call an entry point with raw ctypes arguments and return its code
+    (used by error-path tests that pass deliberately bad arguments)."""
+    return getattr(_lib, name)(*args)

@@ -1,0 +1,380 @@
+// Grouped-query attention over the paged key/value cache.
+//
+// Cache layout per layer (block = 16 tokens):
+//   K [blocks][Hkv][16 tokens][hd]   V [blocks][Hkv][hd][16 tokens]
+//
+// MFMA dataflow (bf16, hd = 128), shared by decode and prefill. A wave owns 16
+// "query columns" and walks the key blocks of one key/value head:
+//   S^T[16 tok][16 col] = K_blk[16][hd] . Q^T[hd][16]   4 x mfma 16x16x32
+//   online softmax per column (column max/sum over the 4 lanes of a column)
+//   O^T[hd][16 col]    += V^T_blk[hd][16] . P^T[16][16] 8 x mfma 16x16x16
+// With S^T the probabilities come out of the first MFMA already in the
+// B-operand layout of the second, and O^T keeps a column's rescale factor in
+// the lane that computed it: no cross-lane shuffles besides the column
+// max/sum. K rows are read as 16-byte vectors, V^T rows as 8-byte vectors;
+// storing V dimension-major inside a block is what makes the second read
+// contiguous.
+//
+// Decode: the columns are the G = Hq/Hkv query heads of one token (padded to
+// 16). A workgroup handles (sequence, kv head, 256-token partition); its four
+// waves take interleaved blocks and merge in LDS in wave order; partitions
+// are merged by a second kernel in partition order. Partitions depend only on
+// the sequence's own length, so results are independent of the batch.
+// Prefill: the columns are 16 query tokens of one head, masked causally by
+// absolute position.
+#include <math.h>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace coco {
+
+namespace {
+
+constexpr int HD = 128;
+constexpr int kAttnThreads = 256;
+constexpr float kLog2e = 1.4426950408889634f;
+
+struct WaveState {
+  float m;        // running column max (log2 domain)
+  float l;        // this lane's share of the running column sum
+  f32x4_t o[8];   // O^T tiles: rows hd = 16n + 4*j4 + r, column c16
+};
+
+__device__ __forceinline__ void wave_state_init(WaveState& ws) {
+  ws.m = -INFINITY;
+  ws.l = 0.f;
+#pragma unroll
+  for (int n = 0; n < 8; ++n) ws.o[n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+}
+
+// One 16-token key block. `valid(r)` says whether token 4*j4+r of the block is
+// visible to this lane's column.
+template <typename Valid>
+__device__ __forceinline__ void attend_block(WaveState& ws, const u32x4_t kf[4],
+                                             const u32x2_t vf[8], const bf16x8_t qf[4],
+                                             float scale_log2, Valid valid) {
+  f32x4_t s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+    s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kf[t]), qf[t], s,
+                                                0, 0, 0);
+  float sc[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) sc[r] = valid(r) ? s[r] * scale_log2 : -INFINITY;
+  float mb = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
+  mb = fmaxf(mb, __shfl_xor(mb, 16, kWave));
+  mb = fmaxf(mb, __shfl_xor(mb, 32, kWave));
+  const float m_new = fmaxf(ws.m, mb);
+  const float alpha = exp2f(ws.m - m_new);
+  float p[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) p[r] = exp2f(sc[r] - m_new);
+  ws.l = ws.l * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
+  ws.m = m_new;
+  const uint32_t p01 = pack_bf16x2(p[0], p[1]), p23 = pack_bf16x2(p[2], p[3]);
+  const s16x4_t pf = __builtin_bit_cast(s16x4_t, u32x2_t{p01, p23});
+#pragma unroll
+  for (int n = 0; n < 8; ++n) {
+    ws.o[n] = ws.o[n] * alpha;
+    ws.o[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4_t, vf[n]), pf,
+                                                        ws.o[n], 0, 0, 0);
+  }
+}
+
+__device__ __forceinline__ void load_kv(const bf16_t* kb, const bf16_t* vb, int c16, int j4,
+                                        u32x4_t kf[4], u32x2_t vf[8]) {
+#pragma unroll
+  for (int t = 0; t < 4; ++t) kf[t] = *(const u32x4_t*)(kb + c16 * HD + t * 32 + j4 * 8);
+#pragma unroll
+  for (int n = 0; n < 8; ++n) vf[n] = *(const u32x2_t*)(vb + (n * 16 + c16) * 16 + j4 * 4);
+}
+
+// Column sum of this lane's share: lanes c16, c16+16, c16+32, c16+48.
+__device__ __forceinline__ float column_sum(float l) {
+  l = l + __shfl_xor(l, 16, kWave);
+  return l + __shfl_xor(l, 32, kWave);
+}
+
+// ---------------------------------------------------------------- decode
+__global__ __launch_bounds__(kAttnThreads) void attn_decode_kernel(
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ k_cache,
+    const bf16_t* __restrict__ v_cache, const int32_t* __restrict__ block_table, int max_blocks,
+    const int32_t* __restrict__ ctx_lens, int Hq, int Hkv, float* __restrict__ part_o,
+    float* __restrict__ part_ml, int max_splits, float scale_log2) {
+  __shared__ float sm_m[4][16], sm_l[4][16];
+  __shared__ float sm_o[4][16][HD + 4];
+
+  const int sp = blockIdx.x, g = blockIdx.y, s = blockIdx.z;
+  const int ctx = ctx_lens[s];
+  const int t0 = sp * kDecodeSplit;
+  if (t0 >= ctx) return;
+  const int t1 = min(ctx, t0 + kDecodeSplit);
+  const int G = Hq / Hkv;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int c16 = lane & 15, j4 = lane >> 4;
+
+  bf16x8_t qf[4];
+  {
+    const int cq = c16 < G ? c16 : G - 1;  // padded columns read a real head, then zero
+    const bf16_t* qp = q + ((int64_t)s * Hq + g * G + cq) * HD + j4 * 8;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      qf[t] = (c16 < G) ? __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(qp + t * 32))
+                        : __builtin_bit_cast(bf16x8_t, u32x4_t{0u, 0u, 0u, 0u});
+  }
+
+  WaveState ws;
+  wave_state_init(ws);
+  const int b_first = t0 / kBlockTokens, b_last = (t1 - 1) / kBlockTokens;
+  const int32_t* bt = block_table + (int64_t)s * max_blocks;
+  const int64_t head_stride = (int64_t)kBlockTokens * HD;
+
+  int b = b_first + wv;
+  if (b <= b_last) {
+    u32x4_t kf[4], kn[4];
+    u32x2_t vf[8], vn[8];
+    int64_t pb = bt[b];
+    load_kv(k_cache + (pb * Hkv + g) * head_stride, v_cache + (pb * Hkv + g) * head_stride, c16,
+            j4, kf, vf);
+    for (; b <= b_last; b += 4) {
+      const int bn = b + 4;
+      if (bn <= b_last) {
+        const int64_t pn = bt[bn];
+        load_kv(k_cache + (pn * Hkv + g) * head_stride, v_cache + (pn * Hkv + g) * head_stride,
+                c16, j4, kn, vn);
+      }
+      const int tok0 = b * kBlockTokens + j4 * 4;
+      attend_block(ws, kf, vf, qf, scale_log2, [&](int r) { return tok0 + r < t1; });
+#pragma unroll
+      for (int t = 0; t < 4; ++t) kf[t] = kn[t];
+#pragma unroll
+      for (int n = 0; n < 8; ++n) vf[n] = vn[n];
+    }
+  }
+
+  const float l_col = column_sum(ws.l);
+  if (j4 == 0) {
+    sm_m[wv][c16] = ws.m;
+    sm_l[wv][c16] = l_col;
+  }
+#pragma unroll
+  for (int n = 0; n < 8; ++n)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sm_o[wv][c16][n * 16 + j4 * 4 + r] = ws.o[n][r];
+  __syncthreads();
+
+  for (int e = threadIdx.x; e < G * HD; e += kAttnThreads) {
+    const int col = e / HD, dim = e - col * HD;
+    const float mx = fmaxf(fmaxf(sm_m[0][col], sm_m[1][col]), fmaxf(sm_m[2][col], sm_m[3][col]));
+    float acc = 0.f, L = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float f = exp2f(sm_m[w][col] - mx);
+      acc += f * sm_o[w][col][dim];
+      L += f * sm_l[w][col];
+    }
+    const int64_t idx = ((int64_t)s * Hq + g * G + col) * max_splits + sp;
+    part_o[idx * HD + dim] = acc;
+    if (dim == 0) {
+      part_ml[idx * 2 + 0] = mx;
+      part_ml[idx * 2 + 1] = L;
+    }
+  }
+}
+
+// Merge the partitions of one (sequence, query head) in partition order.
+__global__ __launch_bounds__(HD) void attn_combine_kernel(const float* __restrict__ part_o,
+                                                          const float* __restrict__ part_ml,
+                                                          const int32_t* __restrict__ ctx_lens,
+                                                          int Hq, int max_splits,
+                                                          bf16_t* __restrict__ o) {
+  const int h = blockIdx.x, s = blockIdx.y, dim = threadIdx.x;
+  const int nsp = (ctx_lens[s] + kDecodeSplit - 1) / kDecodeSplit;
+  const int64_t base = ((int64_t)s * Hq + h) * max_splits;
+  float mx = -INFINITY;
+  for (int sp = 0; sp < nsp; ++sp) mx = fmaxf(mx, part_ml[(base + sp) * 2]);
+  float acc = 0.f, L = 0.f;
+  for (int sp = 0; sp < nsp; ++sp) {
+    const float f = exp2f(part_ml[(base + sp) * 2] - mx);
+    acc += f * part_o[(base + sp) * HD + dim];
+    L += f * part_ml[(base + sp) * 2 + 1];
+  }
+  o[((int64_t)s * Hq + h) * HD + dim] = (bf16_t)f32_to_bf16(nsp > 0 ? acc / L : 0.f);
+}
+
+// ---------------------------------------------------------------- prefill
+// Workgroup = (sequence, 64-row tile of its call rows, query head); wave w
+// takes rows 16w..16w+15 of the tile as its columns.
+__global__ __launch_bounds__(kAttnThreads) void attn_prefill_kernel(
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ k_cache,
+    const bf16_t* __restrict__ v_cache, const int32_t* __restrict__ block_table, int max_blocks,
+    const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ positions,
+    const int32_t* __restrict__ seq_starts, int n_seqs, int Hq, int Hkv, float scale_log2,
+    bf16_t* __restrict__ o) {
+  // Find (sequence, tile) of this workgroup.
+  int tile = blockIdx.x, s = 0;
+  for (; s < n_seqs; ++s) {
+    const int nt = (seq_starts[s + 1] - seq_starts[s] + 63) / 64;
+    if (tile < nt) break;
+    tile -= nt;
+  }
+  if (s >= n_seqs) return;
+  const int h = blockIdx.y;
+  const int g = h / (Hq / Hkv);
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int c16 = lane & 15, j4 = lane >> 4;
+  const int row_end = seq_starts[s + 1];
+  const int row0 = seq_starts[s] + tile * 64 + wv * 16;
+  if (row0 >= row_end) return;
+  const int last_row = min(row_end, row0 + 16) - 1;
+  const int row = row0 + c16;
+  const bool valid_col = row <= last_row;
+  const int pos = positions[valid_col ? row : last_row];
+  const int kmax = min(ctx_lens[s] - 1, positions[last_row]);
+
+  bf16x8_t qf[4];
+  {
+    const bf16_t* qp = q + ((int64_t)(valid_col ? row : last_row) * Hq + h) * HD + j4 * 8;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) qf[t] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(qp + t * 32));
+  }
+
+  WaveState ws;
+  wave_state_init(ws);
+  const int32_t* bt = block_table + (int64_t)s * max_blocks;
+  const int64_t head_stride = (int64_t)kBlockTokens * HD;
+  const int b_last = kmax / kBlockTokens;
+  u32x4_t kf[4], kn[4];
+  u32x2_t vf[8], vn[8];
+  {
+    const int64_t pb = bt[0];
+    load_kv(k_cache + (pb * Hkv + g) * head_stride, v_cache + (pb * Hkv + g) * head_stride, c16,
+            j4, kf, vf);
+  }
+  for (int b = 0; b <= b_last; ++b) {
+    if (b + 1 <= b_last) {
+      const int64_t pn = bt[b + 1];
+      load_kv(k_cache + (pn * Hkv + g) * head_stride, v_cache + (pn * Hkv + g) * head_stride,
+              c16, j4, kn, vn);
+    }
+    const int tok0 = b * kBlockTokens + j4 * 4;
+    attend_block(ws, kf, vf, qf, scale_log2, [&](int r) { return tok0 + r <= pos; });
+#pragma unroll
+    for (int t = 0; t < 4; ++t) kf[t] = kn[t];
+#pragma unroll
+    for (int n = 0; n < 8; ++n) vf[n] = vn[n];
+  }
+  const float inv = 1.0f / column_sum(ws.l);
+  if (valid_col) {
+    bf16_t* op = o + ((int64_t)row * Hq + h) * HD;
+#pragma unroll
+    for (int n = 0; n < 8; ++n) {
+      const uint32_t lo = pack_bf16x2(ws.o[n][0] * inv, ws.o[n][1] * inv);
+      const uint32_t hi = pack_bf16x2(ws.o[n][2] * inv, ws.o[n][3] * inv);
+      *(u32x2_t*)(op + n * 16 + j4 * 4) = u32x2_t{lo, hi};
+    }
+  }
+}
+
+// ---------------------------------------------------------------- fp32 path
+__global__ __launch_bounds__(64) void attn_f32_kernel(
+    const float* __restrict__ q, const float* __restrict__ k_cache,
+    const float* __restrict__ v_cache, const int32_t* __restrict__ block_table, int max_blocks,
+    const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ positions,
+    const int32_t* __restrict__ seq_starts, int n_seqs, int Hq, int Hkv, int hd,
+    float* __restrict__ o) {
+  const int i = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
+  const int s = row_to_seq(seq_starts, n_seqs, i);
+  const int g = h / (Hq / Hkv);
+  const int n = min(ctx_lens[s], positions[i] + 1);
+  const float scale = 1.0f / sqrtf((float)hd);
+  constexpr int kMaxPer = 4;  // hd <= 256
+  float qv[kMaxPer], acc[kMaxPer];
+#pragma unroll
+  for (int u = 0; u < kMaxPer; ++u) {
+    const int e = lane + u * 64;
+    qv[u] = e < hd ? q[((int64_t)i * Hq + h) * hd + e] : 0.f;
+    acc[u] = 0.f;
+  }
+  float m = -INFINITY, l = 0.f;
+  const int32_t* bt = block_table + (int64_t)s * max_blocks;
+  for (int t = 0; t < n; ++t) {
+    const int64_t blk = bt[t / kBlockTokens];
+    const int slot = t % kBlockTokens;
+    const float* kr = k_cache + ((blk * Hkv + g) * kBlockTokens + slot) * hd;
+    float d = 0.f;
+#pragma unroll
+    for (int u = 0; u < kMaxPer; ++u) {
+      const int e = lane + u * 64;
+      if (e < hd) d = fmaf(qv[u], kr[e], d);
+    }
+    const float z = wave_sum(d) * scale;
+    const float m_new = fmaxf(m, z);
+    const float alpha = expf(m - m_new), p = expf(z - m_new);
+    l = l * alpha + p;
+    m = m_new;
+#pragma unroll
+    for (int u = 0; u < kMaxPer; ++u) {
+      const int e = lane + u * 64;
+      if (e < hd)
+        acc[u] = acc[u] * alpha + p * v_cache[((blk * Hkv + g) * hd + e) * kBlockTokens + slot];
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < kMaxPer; ++u) {
+    const int e = lane + u * 64;
+    if (e < hd) o[((int64_t)i * Hq + h) * hd + e] = n > 0 ? acc[u] / l : 0.f;
+  }
+}
+
+}  // namespace
+
+int decode_max_splits(int max_blocks_per_seq) {
+  return (max_blocks_per_seq * kBlockTokens + kDecodeSplit - 1) / kDecodeSplit;
+}
+
+hipError_t launch_attn_decode_bf16(const uint16_t* q, const uint16_t* k_cache,
+                                   const uint16_t* v_cache, const int32_t* block_table,
+                                   int max_blocks, const int32_t* ctx_lens, int n_seqs, int Hq,
+                                   int Hkv, float* part_o, float* part_ml, int max_splits,
+                                   uint16_t* o, hipStream_t st) {
+  if (n_seqs <= 0) return hipSuccess;
+  const float scale_log2 = kLog2e / sqrtf((float)HD);
+  hipLaunchKernelGGL(attn_decode_kernel, dim3(max_splits, Hkv, n_seqs), dim3(kAttnThreads), 0,
+                     st, q, k_cache, v_cache, block_table, max_blocks, ctx_lens, Hq, Hkv, part_o,
+                     part_ml, max_splits, scale_log2);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(attn_combine_kernel, dim3(Hq, n_seqs), dim3(HD), 0, st, part_o, part_ml,
+                     ctx_lens, Hq, max_splits, o);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_prefill_bf16(const uint16_t* q, const uint16_t* k_cache,
+                                    const uint16_t* v_cache, const int32_t* block_table,
+                                    int max_blocks, const int32_t* ctx_lens,
+                                    const int32_t* positions, const int32_t* seq_starts,
+                                    int n_seqs, int n_rows, int Hq, int Hkv, uint16_t* o,
+                                    hipStream_t st) {
+  if (n_rows <= 0) return hipSuccess;
+  const float scale_log2 = kLog2e / sqrtf((float)HD);
+  const int tiles = (n_rows + 63) / 64 + n_seqs;  // upper bound on per-sequence tiles
+  hipLaunchKernelGGL(attn_prefill_kernel, dim3(tiles, Hq), dim3(kAttnThreads), 0, st, q,
+                     k_cache, v_cache, block_table, max_blocks, ctx_lens, positions, seq_starts,
+                     n_seqs, Hq, Hkv, scale_log2, o);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_f32(const float* q, const float* k_cache, const float* v_cache,
+                           const int32_t* block_table, int max_blocks, const int32_t* ctx_lens,
+                           const int32_t* positions, const int32_t* seq_starts, int n_seqs,
+                           int n_rows, int Hq, int Hkv, int hd, float* o, hipStream_t st) {
+  if (n_rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(attn_f32_kernel, dim3(n_rows, Hq), dim3(64), 0, st, q, k_cache, v_cache,
+                     block_table, max_blocks, ctx_lens, positions, seq_starts, n_seqs, Hq, Hkv,
+                     hd, o);
+  return hipGetLastError();
+}
+
+}  // namespace coco

@@ -1,0 +1,495 @@
+// C ABI of the layer-replica hot path: handle, workspace, argument checks and
+// the launch sequence of one decoder layer / one span of layers.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/coco.h"
+#include "common.h"
+#include "kernels.h"
+
+using namespace coco;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define HIPCHK(expr)                                                                  \
+  do {                                                                                \
+    hipError_t e_ = (expr);                                                           \
+    if (e_ != hipSuccess) return fail(COCO_EHIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+}  // namespace
+
+struct coco_layer {
+  coco_layer_config cfg;
+  std::vector<coco_layer_weights> layers;
+  int device = 0;
+  bool validate = false;
+  char* ws = nullptr;
+  size_t ws_bytes = 0;
+  // workspace carve-out
+  void *x = nullptr, *h = nullptr, *q = nullptr, *o = nullptr, *h2 = nullptr, *u = nullptr;
+  float *x1 = nullptr, *part = nullptr, *attn_o = nullptr, *attn_ml = nullptr;
+  double* inv_freq = nullptr;
+  size_t act_rows_bytes[7] = {};
+  int max_splits = 0;
+  int dec_rows = 0;
+};
+
+namespace {
+
+size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+int elem_bytes(int dtype) { return dtype == COCO_BF16 ? 2 : 4; }
+
+int gemm_splits(const coco_layer_config& c, int N, int K) {
+  return c.dtype == COCO_BF16 ? skinny_splits(N, K) : 1;
+}
+
+int check_config(const coco_layer_config* c) {
+  if (!c) return fail(COCO_EINVAL, "config is NULL");
+  if (c->d_model <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->head_dim <= 0 ||
+      c->d_ffn <= 0 || c->n_layers <= 0 || c->max_rows <= 0 || c->max_seqs <= 0 ||
+      c->max_blocks_per_seq <= 0)
+    return fail(COCO_EINVAL, "config sizes must be positive");
+  if (c->block_size != kBlockTokens) return fail(COCO_EINVAL, "block_size must be 16");
+  if (c->n_q_heads % c->n_kv_heads) return fail(COCO_EINVAL, "n_q_heads %% n_kv_heads != 0");
+  if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.f))
+    return fail(COCO_EINVAL, "rms_eps must be >= 0 and rope_theta > 0");
+  if (c->dtype == COCO_BF16) {
+    if (c->head_dim != 128) return fail(COCO_EINVAL, "bf16 path needs head_dim == 128");
+    if (c->n_q_heads / c->n_kv_heads > 16)
+      return fail(COCO_EINVAL, "bf16 path needs n_q_heads / n_kv_heads <= 16");
+    if (c->d_model % 128 || c->d_ffn % 128)
+      return fail(COCO_EINVAL, "bf16 path needs d_model and d_ffn multiples of 128");
+  } else if (c->dtype == COCO_F32) {
+    if (c->head_dim % 2 || c->head_dim > 256)
+      return fail(COCO_EINVAL, "fp32 path needs an even head_dim <= 256");
+  } else {
+    return fail(COCO_EINVAL, "unknown dtype %d", c->dtype);
+  }
+  return COCO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* coco_last_error(void) { return g_err.c_str(); }
+
+int coco_version(void) { return 100; }
+
+int coco_layer_init(const coco_layer_config* cfg, const coco_layer_weights* layers,
+                    coco_layer_t* out) {
+  if (!out) return fail(COCO_EINVAL, "out is NULL");
+  *out = nullptr;
+  int rc = check_config(cfg);
+  if (rc) return rc;
+  if (!layers) return fail(COCO_EINVAL, "layers is NULL");
+  const coco_layer_config& c = *cfg;
+  for (int l = 0; l < c.n_layers; ++l) {
+    const coco_layer_weights& w = layers[l];
+    if (!w.w_qkv || !w.w_o || !w.w_gate_up || !w.w_down || !w.gamma_attn || !w.gamma_mlp ||
+        !w.k_cache || !w.v_cache)
+      return fail(COCO_EINVAL, "layer %d has a NULL weight or cache pointer", l);
+    if (w.num_blocks <= 0) return fail(COCO_EINVAL, "layer %d: num_blocks must be > 0", l);
+  }
+
+  coco_layer* H = new coco_layer();
+  H->cfg = c;
+  H->layers.assign(layers, layers + c.n_layers);
+  (void)hipGetDevice(&H->device);
+
+  const int eb = elem_bytes(c.dtype);
+  const int64_t R = c.max_rows, d = c.d_model, F = c.d_ffn;
+  const int64_t qd = (int64_t)c.n_q_heads * c.head_dim;
+  const int64_t nqkv = (int64_t)(c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
+  int64_t part_elems = 0;
+  const int64_t shapes[4][2] = {{nqkv, d}, {d, qd}, {2 * F, d}, {d, F}};
+  for (auto& s : shapes) {
+    const int64_t e = (int64_t)gemm_splits(c, (int)s[0], (int)s[1]) * R * s[0];
+    if (e > part_elems) part_elems = e;
+  }
+  H->max_splits = decode_max_splits(c.max_blocks_per_seq);
+  H->dec_rows = c.max_rows < c.max_seqs ? c.max_rows : c.max_seqs;
+
+  size_t off = 0;
+  size_t offs[12];
+  const size_t sizes[12] = {
+      align256(R * d * eb),          // x
+      align256(R * d * eb),          // h
+      align256(R * qd * eb),         // q
+      align256(R * qd * eb),         // o
+      align256(R * d * eb),          // h2
+      align256(R * F * eb),          // u
+      align256(R * d * 4),           // x1
+      align256(part_elems * 4),      // part
+      c.dtype == COCO_BF16 ? align256((size_t)H->dec_rows * c.n_q_heads * H->max_splits * 128 * 4) : 0,
+      c.dtype == COCO_BF16 ? align256((size_t)H->dec_rows * c.n_q_heads * H->max_splits * 2 * 4) : 0,
+      align256((size_t)(c.head_dim / 2) * 8),  // inv_freq
+      0};
+  for (int i = 0; i < 12; ++i) {
+    offs[i] = off;
+    off += sizes[i];
+  }
+  H->ws_bytes = off;
+  if (hipMalloc((void**)&H->ws, H->ws_bytes) != hipSuccess) {
+    (void)hipGetLastError();
+    delete H;
+    return fail(COCO_ENOMEM, "workspace of %zu bytes does not fit", off);
+  }
+  H->x = H->ws + offs[0];
+  H->h = H->ws + offs[1];
+  H->q = H->ws + offs[2];
+  H->o = H->ws + offs[3];
+  H->h2 = H->ws + offs[4];
+  H->u = H->ws + offs[5];
+  H->x1 = (float*)(H->ws + offs[6]);
+  H->part = (float*)(H->ws + offs[7]);
+  H->attn_o = (float*)(H->ws + offs[8]);
+  H->attn_ml = (float*)(H->ws + offs[9]);
+  H->inv_freq = (double*)(H->ws + offs[10]);
+  H->act_rows_bytes[COCO_WS_X] = R * d * eb;
+  H->act_rows_bytes[COCO_WS_H] = R * d * eb;
+  H->act_rows_bytes[COCO_WS_Q] = R * qd * eb;
+  H->act_rows_bytes[COCO_WS_O] = R * qd * eb;
+  H->act_rows_bytes[COCO_WS_X1] = R * d * 4;
+  H->act_rows_bytes[COCO_WS_H2] = R * d * eb;
+  H->act_rows_bytes[COCO_WS_U] = R * F * eb;
+
+  // RoPE inverse frequencies theta^(-2j/hd), in fp64.
+  std::vector<double> inv(c.head_dim / 2);
+  for (int j = 0; j < c.head_dim / 2; ++j)
+    inv[j] = pow((double)c.rope_theta, -2.0 * j / (double)c.head_dim);
+  if (hipMemcpy(H->inv_freq, inv.data(), inv.size() * 8, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemset(H->ws, 0, offs[10]) != hipSuccess) {
+    (void)hipGetLastError();
+    (void)hipFree(H->ws);
+    delete H;
+    return fail(COCO_EHIP, "workspace initialisation failed");
+  }
+  *out = H;
+  return COCO_OK;
+}
+
+void coco_layer_destroy(coco_layer_t H) {
+  if (!H) return;
+  int cur = 0;
+  (void)hipGetDevice(&cur);
+  (void)hipSetDevice(H->device);
+  (void)hipDeviceSynchronize();
+  (void)hipFree(H->ws);
+  (void)hipSetDevice(cur);
+  delete H;
+}
+
+int coco_layer_set_validate(coco_layer_t H, int32_t on) {
+  if (!H) return fail(COCO_EINVAL, "handle is NULL");
+  H->validate = on != 0;
+  return COCO_OK;
+}
+
+int coco_layer_workspace(coco_layer_t H, int32_t which, void* dst, int64_t dst_bytes,
+                         coco_stream_t stream) {
+  if (!H || !dst) return fail(COCO_EINVAL, "NULL argument");
+  void* p[7] = {H->x, H->h, H->q, H->o, H->x1, H->h2, H->u};
+  if (which < 0 || which > 6) return fail(COCO_EINVAL, "unknown workspace id %d", which);
+  if (dst_bytes < 0) return fail(COCO_EINVAL, "dst_bytes < 0");
+  const size_t n = (size_t)dst_bytes < H->act_rows_bytes[which] ? (size_t)dst_bytes
+                                                                 : H->act_rows_bytes[which];
+  HIPCHK(hipSetDevice(H->device));
+  HIPCHK(hipMemcpyAsync(dst, p[which], n, hipMemcpyDeviceToDevice, (hipStream_t)stream));
+  return COCO_OK;
+}
+
+}  // extern "C"
+
+// ----------------------------------------------------------------------------
+// Validation of device-side index arrays (debug mode; synchronises).
+// ----------------------------------------------------------------------------
+namespace {
+
+template <typename V>
+int fetch(std::vector<V>& dst, const V* src, size_t n, hipStream_t st) {
+  dst.resize(n);
+  if (n == 0) return COCO_OK;
+  HIPCHK(hipMemcpyAsync(dst.data(), src, n * sizeof(V), hipMemcpyDeviceToHost, st));
+  HIPCHK(hipStreamSynchronize(st));
+  return COCO_OK;
+}
+
+int validate_batch(coco_layer* H, int64_t hidden_rows, const int32_t* row_idx, int n_rows,
+                   const int32_t* positions, const int32_t* seq_starts, int n_seqs,
+                   const int32_t* block_table, const int32_t* ctx_lens, int first_layer,
+                   int n_layers, hipStream_t st) {
+  const coco_layer_config& c = H->cfg;
+  std::vector<int32_t> ri, pos, ss, bt, cl;
+  int rc;
+  if ((rc = fetch(ri, row_idx, n_rows, st)) || (rc = fetch(pos, positions, n_rows, st)) ||
+      (rc = fetch(cl, ctx_lens, n_seqs, st)) ||
+      (rc = fetch(bt, block_table, (size_t)n_seqs * c.max_blocks_per_seq, st)))
+    return rc;
+  if (seq_starts) {
+    if ((rc = fetch(ss, seq_starts, n_seqs + 1, st))) return rc;
+  } else {
+    ss.resize(n_seqs + 1);
+    for (int s = 0; s <= n_seqs; ++s) ss[s] = s;
+  }
+  std::vector<char> seen(hidden_rows, 0);
+  for (int i = 0; i < n_rows; ++i) {
+    if (ri[i] < 0 || ri[i] >= hidden_rows)
+      return fail(COCO_EINVAL, "row_idx[%d] = %d out of range [0, %lld)", i, ri[i],
+                  (long long)hidden_rows);
+    if (seen[ri[i]]) return fail(COCO_EINVAL, "row_idx[%d] = %d is a duplicate", i, ri[i]);
+    seen[ri[i]] = 1;
+  }
+  if (ss[0] != 0 || ss[n_seqs] != n_rows)
+    return fail(COCO_EINVAL, "seq_starts must run from 0 to n_rows");
+  int64_t min_blocks = INT64_MAX;
+  for (int l = first_layer; l < first_layer + n_layers; ++l)
+    if (H->layers[l].num_blocks < min_blocks) min_blocks = H->layers[l].num_blocks;
+  for (int s = 0; s < n_seqs; ++s) {
+    if (ss[s + 1] < ss[s]) return fail(COCO_EINVAL, "seq_starts not monotone at %d", s);
+    if (cl[s] < 1 || cl[s] > c.max_blocks_per_seq * kBlockTokens)
+      return fail(COCO_EINVAL, "ctx_lens[%d] = %d out of range", s, cl[s]);
+    for (int i = ss[s]; i < ss[s + 1]; ++i) {
+      if (pos[i] < 0 || pos[i] >= cl[s])
+        return fail(COCO_EINVAL, "positions[%d] = %d not in [0, ctx_lens[%d] = %d)", i, pos[i],
+                    s, cl[s]);
+      if (i > ss[s] && pos[i] <= pos[i - 1])
+        return fail(COCO_EINVAL, "positions of sequence %d not increasing at row %d", s, i);
+    }
+    const int nb = (cl[s] + kBlockTokens - 1) / kBlockTokens;
+    for (int b = 0; b < nb; ++b) {
+      const int32_t v = bt[(size_t)s * c.max_blocks_per_seq + b];
+      if (v < 0 || v >= min_blocks)
+        return fail(COCO_EINVAL, "block_table[%d][%d] = %d out of range [0, %lld)", s, b, v,
+                    (long long)min_blocks);
+    }
+  }
+  return COCO_OK;
+}
+
+// ----------------------------------------------------------------------------
+// Launch sequence.
+// ----------------------------------------------------------------------------
+template <typename T>
+int gemm(coco_layer* H, const T* A, const T* W, int M, int N, int K, int* S, hipStream_t st);
+
+template <>
+int gemm<bf16_t>(coco_layer* H, const bf16_t* A, const bf16_t* W, int M, int N, int K, int* S,
+                 hipStream_t st) {
+  *S = skinny_splits(N, K);
+  HIPCHK(launch_gemm_skinny_bf16(A, W, H->part, M, N, K, *S, st));
+  return COCO_OK;
+}
+
+template <>
+int gemm<float>(coco_layer* H, const float* A, const float* W, int M, int N, int K, int* S,
+                hipStream_t st) {
+  *S = 1;
+  HIPCHK(launch_gemm_f32(A, W, H->part, M, N, K, st));
+  return COCO_OK;
+}
+
+template <typename T>
+int attention(coco_layer* H, const coco_layer_weights& w, int M, const int32_t* positions,
+              const int32_t* seq_starts, int n_seqs, const int32_t* bt, const int32_t* ctx,
+              hipStream_t st);
+
+template <>
+int attention<bf16_t>(coco_layer* H, const coco_layer_weights& w, int M,
+                      const int32_t* positions, const int32_t* seq_starts, int n_seqs,
+                      const int32_t* bt, const int32_t* ctx, hipStream_t st) {
+  const coco_layer_config& c = H->cfg;
+  if (!seq_starts) {
+    HIPCHK(launch_attn_decode_bf16((const bf16_t*)H->q, (const bf16_t*)w.k_cache,
+                                   (const bf16_t*)w.v_cache, bt, c.max_blocks_per_seq, ctx,
+                                   n_seqs, c.n_q_heads, c.n_kv_heads, H->attn_o, H->attn_ml,
+                                   H->max_splits, (bf16_t*)H->o, st));
+  } else {
+    HIPCHK(launch_attn_prefill_bf16((const bf16_t*)H->q, (const bf16_t*)w.k_cache,
+                                    (const bf16_t*)w.v_cache, bt, c.max_blocks_per_seq, ctx,
+                                    positions, seq_starts, n_seqs, M, c.n_q_heads, c.n_kv_heads,
+                                    (bf16_t*)H->o, st));
+  }
+  return COCO_OK;
+}
+
+template <>
+int attention<float>(coco_layer* H, const coco_layer_weights& w, int M, const int32_t* positions,
+                     const int32_t* seq_starts, int n_seqs, const int32_t* bt,
+                     const int32_t* ctx, hipStream_t st) {
+  const coco_layer_config& c = H->cfg;
+  HIPCHK(launch_attn_f32((const float*)H->q, (const float*)w.k_cache, (const float*)w.v_cache,
+                         bt, c.max_blocks_per_seq, ctx, positions, seq_starts, n_seqs, M,
+                         c.n_q_heads, c.n_kv_heads, c.head_dim, (float*)H->o, st));
+  return COCO_OK;
+}
+
+template <typename T>
+int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx, int M,
+             const int32_t* positions, const int32_t* seq_starts, int n_seqs,
+             const int32_t* bt, const int32_t* ctx, hipStream_t st) {
+  const coco_layer_config& c = H->cfg;
+  const int d = c.d_model, Hq = c.n_q_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.d_ffn;
+  const int nqkv = (Hq + 2 * Hkv) * hd;
+  T* x = (T*)H->x;
+  T* h = (T*)H->h;
+  T* q = (T*)H->q;
+  T* o = (T*)H->o;
+  T* h2 = (T*)H->h2;
+  T* u = (T*)H->u;
+  int S, rc;
+  for (int l = first; l < first + nl; ++l) {
+    const coco_layer_weights& w = H->layers[l];
+    const bool first_l = l == first, last_l = l == first + nl - 1;
+    // Gather (first layer of the segment) + RMSNorm_1.
+    HIPCHK(launch_gather_rmsnorm<T>(first_l ? hidden : x, first_l ? row_idx : nullptr, M, d,
+                                    (const T*)w.gamma_attn, c.rms_eps, first_l ? x : nullptr, h,
+                                    st));
+    // QKV projection, RoPE, local cache append.
+    if ((rc = gemm<T>(H, h, (const T*)w.w_qkv, M, nqkv, d, &S, st))) return rc;
+    HIPCHK(launch_qkv_epilogue<T>(H->part, S, M, Hq, Hkv, hd, positions, seq_starts, n_seqs, bt,
+                                  c.max_blocks_per_seq, H->inv_freq, q, (T*)w.k_cache,
+                                  (T*)w.v_cache, st));
+    // Attention over the paged cache.
+    if ((rc = attention<T>(H, w, M, positions, seq_starts, n_seqs, bt, ctx, st))) return rc;
+    // O projection + residual + RMSNorm_2.
+    if ((rc = gemm<T>(H, o, (const T*)w.w_o, M, d, Hq * hd, &S, st))) return rc;
+    HIPCHK(launch_residual_rmsnorm<T>(H->part, S, M, d, x, (const T*)w.gamma_mlp, c.rms_eps,
+                                      H->x1, h2, st));
+    // SwiGLU MLP.
+    if ((rc = gemm<T>(H, h2, (const T*)w.w_gate_up, M, 2 * F, d, &S, st))) return rc;
+    HIPCHK(launch_swiglu<T>(H->part, S, M, F, u, st));
+    if ((rc = gemm<T>(H, u, (const T*)w.w_down, M, d, F, &S, st))) return rc;
+    // Residual; the last layer of the segment scatters to the full batch.
+    HIPCHK(launch_residual_scatter<T>(H->part, S, M, d, H->x1, last_l ? hidden : x,
+                                      last_l ? row_idx : nullptr, st));
+  }
+  return COCO_OK;
+}
+
+int check_batch(coco_layer* H, int first, int nl, const void* hidden, int64_t hidden_rows,
+                const int32_t* row_idx, int n_rows, const int32_t* positions,
+                const int32_t* seq_starts, int n_seqs, const int32_t* bt, const int32_t* ctx) {
+  const coco_layer_config& c = H->cfg;
+  if (first < 0 || nl < 1 || first + nl > c.n_layers)
+    return fail(COCO_EINVAL, "layers [%d, %d) outside [0, %d)", first, first + nl, c.n_layers);
+  if (n_rows < 0 || n_rows > c.max_rows)
+    return fail(COCO_EINVAL, "n_rows = %d outside [0, max_rows = %d]", n_rows, c.max_rows);
+  if (n_rows == 0) return COCO_OK;
+  if (!hidden || !row_idx || !positions || !bt || !ctx)
+    return fail(COCO_EINVAL, "NULL batch pointer");
+  if (hidden_rows < 1) return fail(COCO_EINVAL, "hidden_rows must be >= 1");
+  if (n_seqs < 1 || n_seqs > c.max_seqs)
+    return fail(COCO_EINVAL, "n_seqs = %d outside [1, max_seqs = %d]", n_seqs, c.max_seqs);
+  if (!seq_starts) {
+    if (n_seqs != n_rows)
+      return fail(COCO_EINVAL, "decode (seq_starts NULL) needs n_seqs == n_rows");
+    if (n_seqs > H->dec_rows)
+      return fail(COCO_EINVAL, "decode batch larger than min(max_rows, max_seqs)");
+  } else if (n_seqs > n_rows) {
+    return fail(COCO_EINVAL, "more sequences than rows");
+  }
+  return COCO_OK;
+}
+
+int forward_impl(coco_layer* H, int first, int nl, void* hidden, int64_t hidden_rows,
+                 const int32_t* row_idx, int n_rows, const int32_t* positions,
+                 const int32_t* seq_starts, int n_seqs, const int32_t* bt, const int32_t* ctx,
+                 coco_stream_t stream) {
+  if (!H) return fail(COCO_EINVAL, "handle is NULL");
+  int rc = check_batch(H, first, nl, hidden, hidden_rows, row_idx, n_rows, positions,
+                       seq_starts, n_seqs, bt, ctx);
+  if (rc || n_rows == 0) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  HIPCHK(hipSetDevice(H->device));
+  if (H->validate &&
+      (rc = validate_batch(H, hidden_rows, row_idx, n_rows, positions, seq_starts, n_seqs, bt,
+                           ctx, first, nl, st)))
+    return rc;
+  if (H->cfg.dtype == COCO_BF16)
+    return run_span<bf16_t>(H, first, nl, (bf16_t*)hidden, row_idx, n_rows, positions,
+                            seq_starts, n_seqs, bt, ctx, st);
+  return run_span<float>(H, first, nl, (float*)hidden, row_idx, n_rows, positions, seq_starts,
+                         n_seqs, bt, ctx, st);
+}
+
+}  // namespace
+
+extern "C" {
+
+int coco_layer_forward(coco_layer_t H, int32_t layer, void* hidden, int64_t hidden_rows,
+                       const int32_t* row_idx, int32_t n_rows, const int32_t* positions,
+                       const int32_t* seq_starts, int32_t n_seqs, const int32_t* block_table,
+                       const int32_t* ctx_lens, coco_stream_t stream) {
+  return forward_impl(H, layer, 1, hidden, hidden_rows, row_idx, n_rows, positions, seq_starts,
+                      n_seqs, block_table, ctx_lens, stream);
+}
+
+int coco_layer_span_forward(coco_layer_t H, int32_t first_layer, int32_t n_layers, void* hidden,
+                            int64_t hidden_rows, const int32_t* row_idx, int32_t n_rows,
+                            const int32_t* positions, const int32_t* seq_starts, int32_t n_seqs,
+                            const int32_t* block_table, const int32_t* ctx_lens,
+                            coco_stream_t stream) {
+  return forward_impl(H, first_layer, n_layers, hidden, hidden_rows, row_idx, n_rows, positions,
+                      seq_starts, n_seqs, block_table, ctx_lens, stream);
+}
+
+int coco_kv_append(coco_layer_t H, int32_t layer, const void* k, const void* v,
+                   const int32_t* seq_idx, const int32_t* positions, int32_t n_tok,
+                   const int32_t* block_table, int32_t n_seqs, coco_stream_t stream) {
+  if (!H) return fail(COCO_EINVAL, "handle is NULL");
+  const coco_layer_config& c = H->cfg;
+  if (layer < 0 || layer >= c.n_layers) return fail(COCO_EINVAL, "layer %d out of range", layer);
+  if (n_tok < 0) return fail(COCO_EINVAL, "n_tok < 0");
+  if (n_tok == 0) return COCO_OK;
+  if (!k || !v || !seq_idx || !positions || !block_table)
+    return fail(COCO_EINVAL, "NULL argument");
+  if (n_seqs < 1) return fail(COCO_EINVAL, "n_seqs must be >= 1");
+  hipStream_t st = (hipStream_t)stream;
+  HIPCHK(hipSetDevice(H->device));
+  if (H->validate) {
+    std::vector<int32_t> si, pos, bt;
+    int rc;
+    if ((rc = fetch(si, seq_idx, n_tok, st)) || (rc = fetch(pos, positions, n_tok, st)) ||
+        (rc = fetch(bt, block_table, (size_t)n_seqs * c.max_blocks_per_seq, st)))
+      return rc;
+    for (int t = 0; t < n_tok; ++t) {
+      if (si[t] < 0 || si[t] >= n_seqs) return fail(COCO_EINVAL, "seq_idx[%d] out of range", t);
+      if (pos[t] < 0 || pos[t] >= c.max_blocks_per_seq * kBlockTokens)
+        return fail(COCO_EINVAL, "positions[%d] out of range", t);
+      const int32_t b = bt[(size_t)si[t] * c.max_blocks_per_seq + pos[t] / kBlockTokens];
+      if (b < 0 || b >= H->layers[layer].num_blocks)
+        return fail(COCO_EINVAL, "token %d maps to block %d outside the pool", t, b);
+    }
+  }
+  const coco_layer_weights& w = H->layers[layer];
+  if (c.dtype == COCO_BF16)
+    HIPCHK(launch_kv_append<bf16_t>((const bf16_t*)k, (const bf16_t*)v, seq_idx, positions, n_tok,
+                                    c.n_kv_heads, c.head_dim, block_table, c.max_blocks_per_seq,
+                                    (bf16_t*)w.k_cache, (bf16_t*)w.v_cache, st));
+  else
+    HIPCHK(launch_kv_append<float>((const float*)k, (const float*)v, seq_idx, positions, n_tok,
+                                   c.n_kv_heads, c.head_dim, block_table, c.max_blocks_per_seq,
+                                   (float*)w.k_cache, (float*)w.v_cache, st));
+  return COCO_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,84 @@
+// Host-side launchers of the gfx950 kernels (internal to libcoco).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace coco {
+
+// ---------------------------------------------------------------- row kernels
+// x_out[i] = src[row_idx ? row_idx[i] : i];  h_out[i] = RMSNorm(x) * gamma.
+// x_out may be null (span layers after the first read x in place).
+template <typename T>
+hipError_t launch_gather_rmsnorm(const T* src, const int32_t* row_idx, int M, int d,
+                                 const T* gamma, float eps, T* x_out, T* h_out,
+                                 hipStream_t st);
+
+// Sum of S split-K partials of the QKV projection, RoPE on query and key
+// heads, queries to q_out [M][Hq*hd], keys/values into the paged cache.
+template <typename T>
+hipError_t launch_qkv_epilogue(const float* part, int S, int M, int Hq, int Hkv, int hd,
+                               const int32_t* positions, const int32_t* seq_starts,
+                               int n_seqs, const int32_t* block_table, int max_blocks,
+                               const double* inv_freq, T* q_out, T* k_cache, T* v_cache,
+                               hipStream_t st);
+
+// x1 = x + sum_s part[s]  (fp32);  h2 = RMSNorm(x1) * gamma.
+template <typename T>
+hipError_t launch_residual_rmsnorm(const float* part, int S, int M, int d, const T* x,
+                                   const T* gamma, float eps, float* x1, T* h2,
+                                   hipStream_t st);
+
+// u = silu(sum_s gate) * sum_s up, part rows [2F] = gate then up.
+template <typename T>
+hipError_t launch_swiglu(const float* part, int S, int M, int F, T* u, hipStream_t st);
+
+// y = x1 + sum_s part[s];  out[row_idx ? row_idx[i] : i] = y.
+template <typename T>
+hipError_t launch_residual_scatter(const float* part, int S, int M, int d, const float* x1,
+                                   T* out, const int32_t* row_idx, hipStream_t st);
+
+// Bit copy of [n][Hkv][hd] keys/values into the paged cache.
+template <typename T>
+hipError_t launch_kv_append(const T* k, const T* v, const int32_t* seq_idx,
+                            const int32_t* positions, int n, int Hkv, int hd,
+                            const int32_t* block_table, int max_blocks, T* k_cache,
+                            T* v_cache, hipStream_t st);
+
+// ---------------------------------------------------------------- GEMMs
+// part[s][m][n] = sum_{k in slice s} A[m][k] * W[n][k]   (bf16 in, fp32 out)
+// The split count S and the K-order of every output element depend only on
+// (N, K), never on M: rows are independent and batch-invariant.
+int skinny_splits(int N, int K);
+hipError_t launch_gemm_skinny_bf16(const uint16_t* A, const uint16_t* W, float* part, int M,
+                                   int N, int K, int S, hipStream_t st);
+
+// part[0][m][n] = sum_k A[m][k] * W[n][k], fp32 (tiny fp32 configurations).
+hipError_t launch_gemm_f32(const float* A, const float* W, float* part, int M, int N, int K,
+                           hipStream_t st);
+
+// ---------------------------------------------------------------- attention
+constexpr int kDecodeSplit = 256;  // tokens per split-KV partition
+int decode_max_splits(int max_blocks_per_seq);
+
+hipError_t launch_attn_decode_bf16(const uint16_t* q, const uint16_t* k_cache,
+                                   const uint16_t* v_cache, const int32_t* block_table,
+                                   int max_blocks, const int32_t* ctx_lens, int n_seqs,
+                                   int Hq, int Hkv, float* part_o, float* part_ml,
+                                   int max_splits, uint16_t* o, hipStream_t st);
+
+hipError_t launch_attn_prefill_bf16(const uint16_t* q, const uint16_t* k_cache,
+                                    const uint16_t* v_cache, const int32_t* block_table,
+                                    int max_blocks, const int32_t* ctx_lens,
+                                    const int32_t* positions, const int32_t* seq_starts,
+                                    int n_seqs, int n_rows, int Hq, int Hkv, uint16_t* o,
+                                    hipStream_t st);
+
+// fp32 path: one wave per (row, query head), decode and prefill alike.
+hipError_t launch_attn_f32(const float* q, const float* k_cache, const float* v_cache,
+                           const int32_t* block_table, int max_blocks,
+                           const int32_t* ctx_lens, const int32_t* positions,
+                           const int32_t* seq_starts, int n_seqs, int n_rows, int Hq,
+                           int Hkv, int hd, float* o, hipStream_t st);
+
+}  // namespace coco

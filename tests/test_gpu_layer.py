@@ -1,0 +1,300 @@
+"""GPU parity of the HIP layer against the fp64 oracle, and the bit-exact
+properties of the path (all through the C ABI).
+
+Sizes here finish in seconds on the oracle yet span several GEMM tiles,
+several split-KV partitions (256 tokens) and ragged tails. Full-size configs
+are in test_gpu_fullsize.py.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_04181_amd as coco
+import workloads as W
+from harness import (TOL, Replica, gpu_cache_tokens, log, normwise_err, oracle_decode_rows,
+                     oracle_prefill_seqs, ragged_decode_batch, ragged_prefill_batch,
+                     small_bf16_shape, to64)
+from workloads import device as WD
+
+pytestmark = pytest.mark.gpu
+
+# Context lengths hitting block (16) and partition (256) edges; 0 prior = the
+# token attends only to itself.
+DECODE_PRIORS = [0, 1, 14, 15, 16, 17, 100, 254, 255, 256, 511, 600, 1000, 3, 2047]
+# The branch y - x is computed from bf16 operands; its normwise error is
+# bounded by the same 2e-2.
+DELTA_TOL = 2e-2
+
+
+def _small_decode(seed=0, shape=None, priors=DECODE_PRIORS, hidden_rows=24):
+    shape = shape or small_bf16_shape()
+    rng = np.random.default_rng(seed)
+    rows = rng.permutation(hidden_rows)[:len(priors)]
+    b = ragged_decode_batch(seed, priors, max_ctx=2049, hidden_rows=hidden_rows, row_idx=rows)
+    return shape, b
+
+
+def _check_rows(name, got, ref, x):
+    e = normwise_err(got, ref)
+    ed = normwise_err(got - x, ref - x)
+    log(f"{name}: output err {e:.2e}, branch err {ed:.2e}")
+    assert e < TOL, f"{name}: output error {e} exceeds {TOL}"
+    assert ed < DELTA_TOL, f"{name}: branch error {ed} exceeds {DELTA_TOL}"
+
+
+def test_c1_tiny_f32_layer_matches_oracle():
+    wl = W.c1_tiny()
+    b, shape = wl.batch, wl.shape
+    rep = Replica.for_batch(shape, "c1", 1, b, max_rows=8, max_seqs=8)
+    hidden = WD.hidden_tensor(shape, "c1", b.hidden_rows)
+    h0 = to64(hidden)
+    rep.forward(0, hidden, WD.batch_tensors(b))
+    torch.cuda.synchronize()
+    ref, rec, cache = oracle_decode_rows(shape, "c1", 0, b, range(b.n_rows), h0, record=True)
+    got = to64(hidden)
+    _check_rows("c1", got[b.row_idx], ref, h0[b.row_idx])
+    # fp32 path: far inside the bound.
+    assert normwise_err(got[b.row_idx] - h0[b.row_idx], ref - h0[b.row_idx]) < 1e-4
+    others = sorted(set(range(b.hidden_rows)) - set(b.row_idx.tolist()))
+    assert np.array_equal(got[others], h0[others])
+    for s in range(b.n_seqs):
+        p = int(b.positions[s])
+        K, V = gpu_cache_tokens(rep.layers[0], b, s, p, p + 1)
+        assert normwise_err(K[0], cache.K[s][p]) < 1e-4
+        assert normwise_err(V[0], cache.V[s][p]) < 1e-4
+
+
+def test_small_bf16_decode_matches_oracle_with_intermediates():
+    shape, b = _small_decode(1)
+    rep = Replica.for_batch(shape, "s1", 1, b)
+    hidden = WD.hidden_tensor(shape, "s1", b.hidden_rows)
+    h0 = to64(hidden)
+    rep.forward(0, hidden, WD.batch_tensors(b))
+    torch.cuda.synchronize()
+    ref, rec, cache = oracle_decode_rows(shape, "s1", 0, b, range(b.n_rows), h0, record=True)
+    got = to64(hidden)
+    M, d, qd, F = b.n_rows, shape.d_model, shape.n_q_heads * 128, shape.d_ffn
+    bf = torch.bfloat16
+    inter = {
+        "h": (coco.COCO_WS_H, d, bf), "q": (coco.COCO_WS_Q, qd, bf), "o": (coco.COCO_WS_O, qd, bf),
+        "x1": (coco.COCO_WS_X1, d, torch.float32), "h2": (coco.COCO_WS_H2, d, bf),
+        "a": (coco.COCO_WS_U, F, bf)}
+    errs = {}
+    for name, (which, cols, dt) in inter.items():
+        errs[name] = normwise_err(to64(rep.workspace(which, M, cols, dt)), rec[name])
+    log("intermediate errors: " + ", ".join(f"{k} {v:.2e}" for k, v in errs.items()))
+    for k, v in errs.items():
+        assert v < TOL, f"intermediate {k}: {v}"
+    _check_rows("small decode", got[b.row_idx], ref, h0[b.row_idx])
+    others = sorted(set(range(b.hidden_rows)) - set(b.row_idx.tolist()))
+    assert np.array_equal(got[others], h0[others])
+    for s in range(b.n_seqs):
+        p = int(b.positions[s])
+        K, V = gpu_cache_tokens(rep.layers[0], b, s, p, p + 1)
+        assert normwise_err(K[0], cache.K[s][p]) < TOL
+        assert normwise_err(V[0], cache.V[s][p]) < TOL
+
+
+def test_small_bf16_prefill_matches_oracle():
+    shape = small_bf16_shape()
+    b = ragged_prefill_batch(2, priors=[0, 3, 16, 300, 40], lens=[1, 15, 64, 100, 77],
+                             max_ctx=512, hidden_rows=300)
+    rep = Replica.for_batch(shape, "s2", 1, b)
+    hidden = WD.hidden_tensor(shape, "s2", b.hidden_rows)
+    h0 = to64(hidden)
+    rep.forward(0, hidden, WD.batch_tensors(b))
+    torch.cuda.synchronize()
+    ref, rec, cache, sub = oracle_prefill_seqs(shape, "s2", 0, b, range(b.n_seqs), h0,
+                                               record=True)
+    got = to64(hidden)
+    e_o = normwise_err(to64(rep.workspace(coco.COCO_WS_O, b.n_rows, shape.n_q_heads * 128,
+                                          torch.bfloat16)), rec["o"])
+    log(f"prefill attention output err {e_o:.2e}")
+    assert e_o < TOL
+    _check_rows("small prefill", got[b.row_idx], ref, h0[b.row_idx])
+    for s in range(b.n_seqs):
+        t0, t1 = int(b.prior_lens[s]), int(b.ctx_lens[s])
+        K, V = gpu_cache_tokens(rep.layers[0], b, s, t0, t1)
+        assert normwise_err(K, cache.K[s][t0:t1]) < TOL
+        assert normwise_err(V, cache.V[s][t0:t1]) < TOL
+
+
+def _kv_snapshot(rep, b):
+    out = []
+    for s in range(b.n_seqs):
+        p0, p1 = int(b.prior_lens[s]), int(b.ctx_lens[s])
+        K, V = gpu_cache_tokens(rep.layers[0], b, s, p0, p1)
+        out.append((K, V))
+    return out
+
+
+def test_decode_split_batch_is_bit_identical():
+    """Any partition of a decode batch into replica shares gives the same
+    output rows and cache bytes as the whole batch (uneven shares too)."""
+    shape, b = _small_decode(3)
+    bt = WD.batch_tensors(b)
+    rep = Replica.for_batch(shape, "s3", 1, b)
+    hidden = WD.hidden_tensor(shape, "s3", b.hidden_rows)
+    whole = hidden.clone()
+    rep.forward(0, whole, bt)
+    torch.cuda.synchronize()
+    kv_whole = _kv_snapshot(rep, b)
+    for parts in (W.even_partition(b.n_rows, 2), W.even_partition(b.n_rows, 5),
+                  [np.array([i]) for i in range(b.n_rows)]):
+        split = hidden.clone()
+        for p in parts:
+            sub = b.select(p)
+            rep.forward(0, split, WD.batch_tensors(sub))
+        torch.cuda.synchronize()
+        assert torch.equal(split.view(torch.int16), whole.view(torch.int16))
+        kv = _kv_snapshot(rep, b)
+        for (k1, v1), (k2, v2) in zip(kv, kv_whole):
+            assert np.array_equal(k1, k2) and np.array_equal(v1, v2)
+
+
+def test_prefill_request_aligned_split_is_bit_identical():
+    shape = small_bf16_shape()
+    b = ragged_prefill_batch(4, priors=[0, 5, 30, 200], lens=[70, 1, 33, 64], max_ctx=512,
+                             hidden_rows=200)
+    rep = Replica.for_batch(shape, "s4", 1, b)
+    hidden = WD.hidden_tensor(shape, "s4", b.hidden_rows)
+    whole = hidden.clone()
+    rep.forward(0, whole, WD.batch_tensors(b))
+    split = hidden.clone()
+    for seqs in ([2, 0], [3], [1]):
+        rep.forward(0, split, WD.batch_tensors(b.select_seqs(seqs)))
+    torch.cuda.synchronize()
+    assert torch.equal(split.view(torch.int16), whole.view(torch.int16))
+
+
+def test_zero_output_projections_give_identity_bit_exactly():
+    """With W_o = W_d = 0 the layer returns its input rows: pins gather ->
+    residual -> scatter bit for bit."""
+    shape, b = _small_decode(5)
+    rep = Replica.for_batch(shape, "s5", 1, b)
+    rep.layers[0]["w_o"].zero_()
+    rep.layers[0]["w_down"].zero_()
+    hidden = WD.hidden_tensor(shape, "s5", b.hidden_rows)
+    h0 = hidden.clone()
+    rep.forward(0, hidden, WD.batch_tensors(b))
+    torch.cuda.synchronize()
+    assert torch.equal(hidden.view(torch.int16), h0.view(torch.int16))
+
+
+def test_block_permutation_gives_bit_identical_output():
+    shape, b = _small_decode(6)
+    rep = Replica.for_batch(shape, "s6", 1, b)
+    hidden = WD.hidden_tensor(shape, "s6", b.hidden_rows)
+    out1 = hidden.clone()
+    pools = {k: rep.layers[0][k].clone() for k in ("k_cache", "v_cache")}
+    rep.forward(0, out1, WD.batch_tensors(b))
+    torch.cuda.synchronize()
+    # Move every physical block to a new place and rewrite the table.
+    perm = np.random.default_rng(0).permutation(b.num_blocks)
+    for k in ("k_cache", "v_cache"):
+        moved = torch.empty_like(pools[k])
+        moved[torch.from_numpy(perm).cuda()] = pools[k]
+        rep.layers[0][k].copy_(moved)
+    b2 = W.Batch(b.hidden_rows, b.row_idx, b.positions, None, b.prior_lens, b.ctx_lens,
+                 np.where(b.block_table >= 0, perm[np.maximum(b.block_table, 0)], -1)
+                 .astype(np.int32), b.num_blocks)
+    out2 = hidden.clone()
+    rep.forward(0, out2, WD.batch_tensors(b2))
+    torch.cuda.synchronize()
+    assert torch.equal(out1.view(torch.int16), out2.view(torch.int16))
+
+
+def test_span_equals_successive_layers_bit_exactly():
+    shape, b = _small_decode(7, priors=[5, 300, 17, 0, 900])
+    L = 3
+    rep = Replica.for_batch(shape, "s7", L, b)
+    pools0 = [{k: t[k].clone() for k in ("k_cache", "v_cache")} for t in rep.layers]
+    hidden = WD.hidden_tensor(shape, "s7", b.hidden_rows)
+    bt = WD.batch_tensors(b)
+    a = hidden.clone()
+    rep.span(0, L, a, bt)
+    torch.cuda.synchronize()
+    for t, p in zip(rep.layers, pools0):
+        for k in p:
+            t[k].copy_(p[k])
+    c = hidden.clone()
+    for l in range(L):
+        rep.forward(l, c, bt)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), c.view(torch.int16))
+
+
+def test_empty_call_is_a_no_op():
+    shape, b = _small_decode(8)
+    rep = Replica.for_batch(shape, "s8", 1, b)
+    hidden = WD.hidden_tensor(shape, "s8", b.hidden_rows)
+    h0 = hidden.clone()
+    bt = WD.batch_tensors(b.select([]))
+    rep.forward(0, hidden, bt)
+    torch.cuda.synchronize()
+    assert torch.equal(hidden.view(torch.int16), h0.view(torch.int16))
+
+
+def test_kv_append_is_a_bit_copy():
+    shape = small_bf16_shape()
+    b = ragged_decode_batch(9, [10, 40, 0], max_ctx=256)
+    rep = Replica.for_batch(shape, "s9", 1, b)
+    n = 20
+    g = torch.Generator(device="cuda").manual_seed(0)
+    k = torch.randn(n, shape.n_kv_heads, 128, device="cuda", generator=g).to(torch.bfloat16)
+    v = torch.randn(n, shape.n_kv_heads, 128, device="cuda", generator=g).to(torch.bfloat16)
+    seq = np.array([0] * 8 + [1] * 7 + [2] * 5, np.int32)
+    pos = np.concatenate([np.arange(3, 11), np.arange(30, 37), np.arange(0, 5)]).astype(np.int32)
+    coco.coco_kv_append(rep.h, 0, k, v, torch.from_numpy(seq).cuda(), torch.from_numpy(pos).cuda(),
+                        WD.batch_tensors(b)["block_table"])
+    torch.cuda.synchronize()
+    kh, vh = to64(k), to64(v)
+    for t in range(n):
+        K, V = gpu_cache_tokens(rep.layers[0], b, int(seq[t]), int(pos[t]), int(pos[t]) + 1)
+        assert np.array_equal(K[0], kh[t]) and np.array_equal(V[0], vh[t])
+
+
+def test_abi_rejects_bad_arguments_and_stays_usable():
+    shape, b = _small_decode(10)
+    rep = Replica.for_batch(shape, "s10", 1, b)
+    hidden = WD.hidden_tensor(shape, "s10", b.hidden_rows)
+    bt = WD.batch_tensors(b)
+    with pytest.raises(coco.CocoError) as e:
+        coco.coco_layer_forward(rep.h, 1, hidden, bt["row_idx"], bt["positions"], None,
+                                bt["block_table"], bt["ctx_lens"])
+    assert e.value.code == -1
+    big = WD.batch_tensors(W.decode_batch(np.random.default_rng(0), np.ones(b.n_rows + 1, int),
+                                          2049, hidden_rows=b.hidden_rows + 1))
+    with pytest.raises(coco.CocoError):
+        coco.coco_layer_forward(rep.h, 0, hidden, big["row_idx"], big["positions"], None,
+                                big["block_table"], big["ctx_lens"])
+    # Validation mode: duplicate rows, out-of-range positions, bad blocks.
+    coco.coco_layer_set_validate(rep.h, True)
+    dup = dict(bt)
+    ri = b.row_idx.copy()
+    ri[1] = ri[0]
+    dup["row_idx"] = torch.from_numpy(ri).cuda()
+    with pytest.raises(coco.CocoError, match="duplicate"):
+        rep.forward(0, hidden, dup)
+    badpos = dict(bt)
+    badpos["positions"] = bt["positions"] + 1
+    with pytest.raises(coco.CocoError, match="positions"):
+        rep.forward(0, hidden, badpos)
+    badbt = dict(bt)
+    t = b.block_table.copy()
+    t[0, 0] = b.num_blocks + 5
+    badbt["block_table"] = torch.from_numpy(t).cuda()
+    with pytest.raises(coco.CocoError, match="block_table"):
+        rep.forward(0, hidden, badbt)
+    # The handle still works after rejected calls.
+    h0 = hidden.clone()
+    rep.forward(0, hidden, bt)
+    torch.cuda.synchronize()
+    assert not torch.equal(hidden, h0)
+
+
+def test_init_rejects_unsupported_shapes():
+    bad = coco.make_config(512, 8, 2, 64, 768, 1, "bf16", 8, 8, 4, 1e4, 1e-5)
+    t = WD.layer_tensors(small_bf16_shape(), "x", 0, 4)
+    with pytest.raises(coco.CocoError, match="head_dim"):
+        coco.coco_layer_init(bad, [t])
