@@ -1,0 +1,328 @@
+#!/usr/bin/env python3
+"""Throughput of the layer-replica hot path on one MI355X.
+
+One step = one pass of the whole path (gather, RMSNorm, QKV, RoPE + cache
+append, paged attention, O projection + residual, RMSNorm, SwiGLU MLP +
+residual, scatter) over one batch, through the C ABI. Default workload: the
+Llama-3-8B-shaped layer, bf16 decode of a 64-request batch with lognormal
+contexts (metric: decode layer-steps/s). Other workloads via --workload.
+
+Prints one JSON line on stdout; per-kernel timings go to stderr. Inputs are
+synthetic (seeded) and resident in HBM before the timed region.
+"""
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode layer-steps/s & prefill tokens/s per layer; % HBM / MFMA peak"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__)
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", default="c2",
+                   choices=["c2", "c3", "c3full", "c4p", "c4d", "c5"])
+    p.add_argument("--cpu-seconds", type=float, default=12.0,
+                   help="target duration of the oracle CPU baseline (0 = skip)")
+    return p.parse_args()
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_sha(files):
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, "paper_2607_04181_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel_kind, workload_name, src_sha):
+    """HBM bytes per launch from a committed rocprofv3 counter summary, or
+    None when there is none or the kernel sources changed since."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel_kind}_{workload_name}.md")
+    if not os.path.exists(path):
+        return None
+    txt = open(path).read()
+    m_sha = re.search(r"kernel_source_sha:\s*(\w+)", txt)
+    m_b = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", txt)
+    if not m_sha or not m_b or m_sha.group(1) != src_sha:
+        return None
+    return float(m_b.group(1))
+
+
+def build_workload(name):
+    import numpy as np
+    import workloads as W
+    if name == "c2":
+        wl = W.c2_llama8b_decode()
+        return wl, wl.batch, 1
+    if name == "c3":
+        wl = W.c3_llama8b_skewed()
+        return wl, wl.batch, 1
+    if name == "c3full":
+        wl = W.c3_llama8b_skewed()
+        wl.name = "llama8b_skewed_all256"
+        return wl, wl.full_batch, 1
+    if name == "c4p":
+        wl = W.c4_qwen32b()
+        return wl, wl.batch, 1
+    if name == "c4d":
+        wl = W.c4_qwen32b()
+        wl.name = "qwen32b_decode_b128"
+        return wl, wl.decode_after, 1
+    if name == "c5":
+        wl = W.c5_llama70b_span()
+        return wl, wl.batch, wl.n_layers
+    raise ValueError(name)
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "single-GPU build: the replica runs on one MI355X; "
+                          "multi-GPU sharding of the row subsets is described in DESIGN.md "
+                          "and not run", "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2607_04181_amd as coco
+    import workloads as W
+    from workloads import device as WD
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    wl, batch, n_layers = build_workload(args.workload)
+    shape = wl.shape
+    t0 = time.time()
+    layers = [WD.layer_tensors(shape, wl.tag, l, batch.num_blocks) for l in range(n_layers)]
+    cfg = coco.make_config(shape.d_model, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
+                           shape.d_ffn, n_layers, shape.dtype, batch.n_rows, batch.n_seqs,
+                           batch.block_table.shape[1], shape.rope_theta, shape.rms_eps)
+    handle = coco.coco_layer_init(cfg, layers)
+    hidden = WD.hidden_tensor(shape, wl.tag, batch.hidden_rows)
+    bt = WD.batch_tensors(batch)
+    torch.cuda.synchronize()
+    log(f"setup {time.time() - t0:.1f}s: {wl.name}, {n_layers} layer(s), rows {batch.n_rows}, "
+        f"blocks {batch.num_blocks}")
+
+    # Oracle inputs for the CPU baseline, taken before the GPU touches them.
+    cpu_inputs = None
+    if args.cpu_seconds > 0:
+        cpu_inputs = prepare_cpu_inputs(wl, batch, layers[0], hidden)
+
+    stream = torch.cuda.current_stream()
+
+    def step():
+        if n_layers == 1:
+            coco.coco_layer_forward(handle, 0, hidden, bt["row_idx"], bt["positions"],
+                                    bt["seq_starts"], bt["block_table"], bt["ctx_lens"], stream)
+        else:
+            coco.coco_layer_span_forward(handle, 0, n_layers, hidden, bt["row_idx"],
+                                         bt["positions"], bt["seq_starts"], bt["block_table"],
+                                         bt["ctx_lens"], stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+
+    # Per-kernel durations: every launch bracketed by HIP events on the stream.
+    coco.coco_layer_set_timing(handle, True)
+    per_kernel = {}
+    for _ in range(args.steps):
+        step()
+        for k, (t, n) in coco.coco_layer_read_timing(handle).items():
+            t0_, n0_ = per_kernel.get(k, (0.0, 0))
+            per_kernel[k] = (t0_ + t, n0_ + n)
+    coco.coco_layer_set_timing(handle, False)
+
+    M = batch.n_rows
+    d, F = shape.d_model, shape.d_ffn
+    Hq, Hkv, hd = shape.n_q_heads, shape.n_kv_heads, shape.head_dim
+    nqkv = (Hq + 2 * Hkv) * hd
+    eb = shape.elem_bytes
+    kvb = shape.kv_bytes_per_token()
+    gemms = {"gemm_qkv": (nqkv, d), "gemm_o": (d, Hq * hd), "gemm_gate_up": (2 * F, d),
+             "gemm_down": (d, F)}
+    sum_ctx = int(np.sum(batch.ctx_lens))
+    is_decode = batch.is_decode
+    # Algorithmic work of one launch of each kernel kind.
+    alg_bytes = {k: N * K * eb + M * K * eb + M * N * eb for k, (N, K) in gemms.items()}
+    alg_flops = {k: 2.0 * M * N * K for k, (N, K) in gemms.items()}
+    if is_decode:
+        alg_bytes["attention"] = sum_ctx * kvb + 2 * M * Hq * hd * eb
+        alg_flops["attention"] = 4.0 * Hq * hd * sum_ctx
+    else:
+        pairs = float(np.sum(batch.positions.astype(np.int64) + 1))
+        alg_flops["attention"] = 4.0 * Hq * hd * pairs
+        alg_bytes["attention"] = sum_ctx * kvb + 2 * M * Hq * hd * eb
+    weight_bytes = shape.param_count() * eb * n_layers
+    step_bytes = weight_bytes + n_layers * (sum_ctx * kvb + M * kvb) + 2 * M * d * eb
+    step_flops = n_layers * (2.0 * M * (shape.param_count() - 2 * d) +
+                             alg_flops["attention"])
+
+    rows = []
+    for k, (tot, n) in per_kernel.items():
+        if n:
+            rows.append((k, tot / n, n, tot))
+    rows.sort(key=lambda r: -r[3])
+    tot_all = sum(r[3] for r in rows)
+    log(f"{'kernel':18s} {'avg us':>9s} {'share':>6s} {'GB/s':>8s} {'TFLOP/s':>8s}")
+    for k, avg, n, tot in rows:
+        gbs = alg_bytes.get(k, 0) / (avg * 1e-3) / 1e9 if k in alg_bytes else float("nan")
+        tfs = alg_flops.get(k, 0) / (avg * 1e-3) / 1e12 if k in alg_flops else float("nan")
+        log(f"{k:18s} {avg * 1e3:9.1f} {tot / tot_all:6.1%} {gbs:8.0f} {tfs:8.1f}")
+
+    cand = [r for r in rows if r[0] in alg_bytes]
+    dom, dom_avg, dom_n, _ = cand[0]
+    bound = "hbm" if is_decode else "mfma"
+    src_sha = kernel_source_sha(["gemm_skinny.hip", "attention.hip", "rows.hip", "common.h"])
+    if bound == "hbm":
+        achieved = alg_bytes[dom] / (dom_avg * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
+    else:
+        achieved = alg_flops[dom] / (dom_avg * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4)}
+    roof["traffic"] = load_traffic(dom, wl.name, src_sha)
+    roof["kernel"] = dom
+    roof["avg_launch_us"] = round(dom_avg * 1e3, 2)
+    roof["algorithmic_per_launch"] = alg_bytes[dom] if bound == "hbm" else alg_flops[dom]
+
+    if is_decode:
+        value = n_layers * 1000.0 / ms
+        unit = "layer-steps/s"
+    else:
+        value = M * 1000.0 / ms
+        unit = "tokens/s per layer"
+    whole = {"step_hbm_bytes": step_bytes, "step_flops": step_flops,
+             "step_GBps": round(step_bytes / (ms * 1e-3) / 1e9, 1),
+             "step_TFLOPs": round(step_flops / (ms * 1e-3) / 1e12, 2)}
+    whole["step_frac_hbm"] = round(whole["step_GBps"] / HBM_PEAK_GBS, 4)
+    whole["step_frac_mfma"] = round(whole["step_TFLOPs"] / MFMA_BF16_PEAK_TFLOPS, 4)
+
+    cpu = None
+    if cpu_inputs is not None:
+        cpu = cpu_baseline(wl, batch, cpu_inputs, args.cpu_seconds, n_layers, is_decode)
+
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": unit, "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": shape.dtype, "data": "synthetic (seeded counter-based generator)",
+        "config": {"workload": wl.name, "d_model": d, "n_q_heads": Hq, "n_kv_heads": Hkv,
+                   "head_dim": hd, "d_ffn": F, "layers": n_layers, "rows": M,
+                   "hidden_rows": batch.hidden_rows, "sum_ctx": sum_ctx,
+                   "mode": "decode" if is_decode else "prefill", "kv_block": 16,
+                   "parallelism": "single GPU (one replica's share)"},
+        "roofline": roof, "whole_step": whole, "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def prepare_cpu_inputs(wl, batch, layer0, hidden):
+    """Host copies of the generator's tensors for the oracle (same bits as
+    the CPU generator would give), taken before any kernel runs."""
+    import numpy as np
+    import torch
+    from oracle.paged import depage_blocks
+
+    def f64(t):
+        return t.detach().to("cpu", torch.float32).numpy().astype(np.float64)
+
+    shape = wl.shape
+    sample_seqs = list(range(batch.n_seqs)) if batch.is_decode else [0]
+    w = {k: f64(layer0[k]) for k in shape.weight_shapes()}
+    K, V = [], []
+    for s in sample_seqs:
+        prior, ctx = int(batch.prior_lens[s]), int(batch.ctx_lens[s])
+        nb = -(-prior // 16)
+        Kc = np.zeros((ctx, shape.n_kv_heads, shape.head_dim))
+        Vc = np.zeros_like(Kc)
+        if nb:
+            idx = torch.from_numpy(batch.block_table[s, :nb].astype(np.int64)).cuda()
+            kb, vb = f64(layer0["k_cache"].index_select(0, idx)), f64(
+                layer0["v_cache"].index_select(0, idx))
+            Kc[:prior], Vc[:prior] = depage_blocks(kb, vb, prior)
+        K.append(Kc)
+        V.append(Vc)
+    return {"w": w, "K": K, "V": V, "hidden": f64(hidden), "seqs": sample_seqs}
+
+
+def cpu_baseline(wl, batch, inp, seconds, n_layers, is_decode):
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info, threadpool_limits
+    except ImportError:  # pragma: no cover
+        threadpool_limits = None
+    share = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+    cores = min(share, len(os.sched_getaffinity(0)))
+    ctx = threadpool_limits(cores) if threadpool_limits else None
+    if ctx:
+        ctx.__enter__()
+    try:
+        used = cores
+        if threadpool_limits:
+            info = threadpool_info()
+            if info:
+                used = max(i.get("num_threads", 1) for i in info)
+        shape = wl.shape
+        if is_decode:
+            sub = batch
+            n_units, unit = 1, "layer-steps/s"
+            sample = f"whole {wl.name} decode step ({batch.n_rows} rows), one layer"
+            seq_starts = None
+        else:
+            sub = batch.select_seqs(inp["seqs"])
+            unit = "tokens/s per layer"
+            sample = (f"request 0 of {wl.name} ({sub.n_rows} of {batch.n_rows} prefill tokens), "
+                      "one layer")
+            seq_starts = sub.seq_starts
+        reps, t_start = 0, time.perf_counter()
+        while True:
+            cache = oracle.KVCache(inp["K"], inp["V"])
+            oracle.layer_forward(inp["w"], shape, inp["hidden"], sub.row_idx, sub.positions,
+                                 seq_starts, sub.ctx_lens, cache)
+            reps += 1
+            el = time.perf_counter() - t_start
+            if el >= seconds:
+                break
+        if is_decode:
+            value = reps / el
+        else:
+            value = reps * sub.n_rows / el
+        return {"value": round(value, 4), "unit": unit, "cores": used, "kind": "oracle",
+                "sample": f"{sample}, {reps} repetition(s) in {el:.1f}s, fp64 numpy"}
+    finally:
+        if ctx:
+            ctx.__exit__(None, None, None)
+
+
+if __name__ == "__main__":
+    main()

@@ -192,6 +192,34 @@ enum {
 int coco_layer_workspace(coco_layer_t h, int32_t which, void* dst, int64_t dst_bytes,
                          coco_stream_t stream);
 
+/* Per-kernel timing for benchmarks (calls of any handle are unaffected while
+ * it is off). When on, every kernel launched by coco_layer_forward /
+ * coco_layer_span_forward on this handle is bracketed by a pair of HIP events
+ * recorded on the call's stream, from a pool of events created here (so
+ * switching it on allocates; timed calls themselves do not). */
+enum {
+  COCO_K_GATHER_NORM = 0,    /* gather + RMSNorm_1 (or RMSNorm_1 inside a span) */
+  COCO_K_GEMM_QKV = 1,       /* QKV projection */
+  COCO_K_QKV_EPILOGUE = 2,   /* split-K sum + RoPE + cache append */
+  COCO_K_ATTENTION = 3,      /* paged attention (decode partitions or prefill) */
+  COCO_K_ATTN_COMBINE = 4,   /* decode partition merge */
+  COCO_K_GEMM_O = 5,         /* O projection */
+  COCO_K_RESIDUAL_NORM = 6,  /* residual + RMSNorm_2 */
+  COCO_K_GEMM_GATE_UP = 7,   /* gate/up projection */
+  COCO_K_SWIGLU = 8,         /* SwiGLU */
+  COCO_K_GEMM_DOWN = 9,      /* down projection */
+  COCO_K_RESIDUAL_SCATTER = 10, /* residual + scatter */
+  COCO_K_COUNT = 11
+};
+int coco_layer_set_timing(coco_layer_t h, int32_t on);
+
+/* Sum of the event-measured durations (milliseconds) and the number of
+ * launches of each kernel kind since timing was switched on or last read;
+ * ms and launches hold n_kinds entries (<= COCO_K_COUNT). Synchronises with
+ * the recorded events, then resets the sums. Returns COCO_ESTATE if more
+ * launches were made than the pool holds (4096 per read). */
+int coco_layer_read_timing(coco_layer_t h, double* ms, int64_t* launches, int32_t n_kinds);
+
 #ifdef __cplusplus
 }
 #endif

@@ -9,5 +9,6 @@ from ._lib import (  # noqa: F401
     COCO_BF16, COCO_F32, COCO_WS_H, COCO_WS_H2, COCO_WS_O, COCO_WS_Q, COCO_WS_U, COCO_WS_X,
     COCO_WS_X1, CocoError, Handle, LIB_PATH, coco_kv_append, coco_last_error, coco_layer_destroy,
     coco_layer_forward, coco_layer_init, coco_layer_set_validate, coco_layer_span_forward,
-    coco_layer_workspace, coco_version, make_config,
+    coco_layer_workspace, coco_version, make_config, coco_layer_set_timing,
+    coco_layer_read_timing, KERNEL_KINDS,
 )

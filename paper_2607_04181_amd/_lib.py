@@ -22,7 +22,10 @@ COCO_WS_X, COCO_WS_H, COCO_WS_Q, COCO_WS_O, COCO_WS_X1, COCO_WS_H2, COCO_WS_U = 
 
 EXPORTS = ["coco_layer_init", "coco_layer_destroy", "coco_last_error", "coco_version",
            "coco_layer_set_validate", "coco_kv_append", "coco_layer_forward",
-           "coco_layer_span_forward", "coco_layer_workspace"]
+           "coco_layer_span_forward", "coco_layer_workspace", "coco_layer_set_timing",
+           "coco_layer_read_timing"]
+KERNEL_KINDS = ["gather_norm", "gemm_qkv", "qkv_epilogue", "attention", "attn_combine", "gemm_o",
+                "residual_norm", "gemm_gate_up", "swiglu", "gemm_down", "residual_scatter"]
 
 
 class CocoError(RuntimeError):
@@ -63,6 +66,9 @@ def _load():
         "coco_layer_span_forward": (ctypes.c_int, [vp, i32, i32, vp, i64, vp, i32, vp, vp, i32,
                                                    vp, vp, vp]),
         "coco_layer_workspace": (ctypes.c_int, [vp, i32, vp, i64, vp]),
+        "coco_layer_set_timing": (ctypes.c_int, [vp, i32]),
+        "coco_layer_read_timing": (ctypes.c_int, [vp, ctypes.POINTER(ctypes.c_double),
+                                                  ctypes.POINTER(i64), i32]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -189,6 +195,19 @@ def coco_layer_span_forward(h: Handle, first_layer: int, n_layers: int, hidden, 
 def coco_layer_workspace(h: Handle, which: int, dst, stream=None) -> None:
     _check(_lib.coco_layer_workspace(h.raw, which, _ptr(dst, what="dst"),
                                      dst.numel() * dst.element_size(), _stream(stream)))
+
+
+def coco_layer_set_timing(h: Handle, on: bool) -> None:
+    _check(_lib.coco_layer_set_timing(h.raw, 1 if on else 0))
+
+
+def coco_layer_read_timing(h: Handle) -> dict:
+    """{kind: (total_ms, launches)} since timing was switched on / last read."""
+    n = len(KERNEL_KINDS)
+    ms = (ctypes.c_double * n)()
+    cnt = (ctypes.c_int64 * n)()
+    _check(_lib.coco_layer_read_timing(h.raw, ms, cnt, n))
+    return {k: (ms[i], cnt[i]) for i, k in enumerate(KERNEL_KINDS)}
 
 
 def raw_call(name: str, *args) -> int:

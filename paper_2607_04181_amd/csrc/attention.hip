@@ -17,8 +17,9 @@
 //
 // Decode: the columns are the G = Hq/Hkv query heads of one token (padded to
 // 16). A workgroup handles (sequence, kv head, 256-token partition); its four
-// waves take interleaved blocks and merge in LDS in wave order; partitions
-// are merged by a second kernel in partition order. Partitions depend only on
+// waves take interleaved blocks (issuing all their loads first) and merge in
+// LDS in wave order; partitions are merged by a second kernel in partition
+// order. Partitions depend only on
 // the sequence's own length, so results are independent of the batch.
 // Prefill: the columns are 16 query tokens of one head, masked causally by
 // absolute position.
@@ -130,26 +131,27 @@ __global__ __launch_bounds__(kAttnThreads) void attn_decode_kernel(
   const int32_t* bt = block_table + (int64_t)s * max_blocks;
   const int64_t head_stride = (int64_t)kBlockTokens * HD;
 
-  int b = b_first + wv;
-  if (b <= b_last) {
-    u32x4_t kf[4], kn[4];
-    u32x2_t vf[8], vn[8];
-    int64_t pb = bt[b];
-    load_kv(k_cache + (pb * Hkv + g) * head_stride, v_cache + (pb * Hkv + g) * head_stride, c16,
-            j4, kf, vf);
-    for (; b <= b_last; b += 4) {
-      const int bn = b + 4;
-      if (bn <= b_last) {
-        const int64_t pn = bt[bn];
-        load_kv(k_cache + (pn * Hkv + g) * head_stride, v_cache + (pn * Hkv + g) * head_stride,
-                c16, j4, kn, vn);
-      }
+  // A partition is 16 blocks: wave wv takes blocks b_first + wv + 4u, u < 4.
+  // All of a wave's key/value loads are issued before any is consumed, so a
+  // wave keeps 32 KB in flight.
+  constexpr int kPerWave = kDecodeSplit / kBlockTokens / 4;
+  u32x4_t kf[kPerWave][4];
+  u32x2_t vf[kPerWave][8];
+#pragma unroll
+  for (int u = 0; u < kPerWave; ++u) {
+    const int b = b_first + wv + 4 * u;
+    if (b <= b_last) {
+      const int64_t pb = bt[b];
+      load_kv(k_cache + (pb * Hkv + g) * head_stride, v_cache + (pb * Hkv + g) * head_stride,
+              c16, j4, kf[u], vf[u]);
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < kPerWave; ++u) {
+    const int b = b_first + wv + 4 * u;
+    if (b <= b_last) {
       const int tok0 = b * kBlockTokens + j4 * 4;
-      attend_block(ws, kf, vf, qf, scale_log2, [&](int r) { return tok0 + r < t1; });
-#pragma unroll
-      for (int t = 0; t < 4; ++t) kf[t] = kn[t];
-#pragma unroll
-      for (int n = 0; n < 8; ++n) vf[n] = vn[n];
+      attend_block(ws, kf[u], vf[u], qf, scale_log2, [&](int r) { return tok0 + r < t1; });
     }
   }
 
@@ -184,22 +186,44 @@ __global__ __launch_bounds__(kAttnThreads) void attn_decode_kernel(
 }
 
 // Merge the partitions of one (sequence, query head) in partition order.
+// Partition weights exp2(m_sp - max) are computed once into LDS (dynamic,
+// 2 * max_splits floats); each thread then owns one head dimension.
 __global__ __launch_bounds__(HD) void attn_combine_kernel(const float* __restrict__ part_o,
                                                           const float* __restrict__ part_ml,
                                                           const int32_t* __restrict__ ctx_lens,
                                                           int Hq, int max_splits,
                                                           bf16_t* __restrict__ o) {
+  extern __shared__ float sm[];  // [0, max_splits): weights; [max_splits, 2*max_splits): l
+  __shared__ float red[HD / kWave];
   const int h = blockIdx.x, s = blockIdx.y, dim = threadIdx.x;
   const int nsp = (ctx_lens[s] + kDecodeSplit - 1) / kDecodeSplit;
   const int64_t base = ((int64_t)s * Hq + h) * max_splits;
   float mx = -INFINITY;
-  for (int sp = 0; sp < nsp; ++sp) mx = fmaxf(mx, part_ml[(base + sp) * 2]);
-  float acc = 0.f, L = 0.f;
-  for (int sp = 0; sp < nsp; ++sp) {
-    const float f = exp2f(part_ml[(base + sp) * 2] - mx);
-    acc += f * part_o[(base + sp) * HD + dim];
-    L += f * part_ml[(base + sp) * 2 + 1];
+  for (int sp = dim; sp < nsp; sp += HD) {
+    const float m = part_ml[(base + sp) * 2];
+    sm[sp] = m;
+    sm[max_splits + sp] = part_ml[(base + sp) * 2 + 1];
+    mx = fmaxf(mx, m);
   }
+  mx = wave_max(mx);
+  if ((dim & (kWave - 1)) == 0) red[dim / kWave] = mx;
+  __syncthreads();
+  mx = fmaxf(red[0], red[1]);
+  for (int sp = dim; sp < nsp; sp += HD) sm[sp] = exp2f(sm[sp] - mx);
+  __syncthreads();
+  float acc = 0.f, L = 0.f;
+  const float* po = part_o + base * HD + dim;
+  int sp = 0;
+  for (; sp + 4 <= nsp; sp += 4) {
+    const float a0 = po[(sp + 0) * HD], a1 = po[(sp + 1) * HD];
+    const float a2 = po[(sp + 2) * HD], a3 = po[(sp + 3) * HD];
+    acc += sm[sp] * a0;
+    acc += sm[sp + 1] * a1;
+    acc += sm[sp + 2] * a2;
+    acc += sm[sp + 3] * a3;
+  }
+  for (; sp < nsp; ++sp) acc += sm[sp] * po[sp * HD];
+  for (sp = 0; sp < nsp; ++sp) L += sm[sp] * sm[max_splits + sp];
   o[((int64_t)s * Hq + h) * HD + dim] = (bf16_t)f32_to_bf16(nsp > 0 ? acc / L : 0.f);
 }
 
@@ -338,16 +362,22 @@ hipError_t launch_attn_decode_bf16(const uint16_t* q, const uint16_t* k_cache,
                                    const uint16_t* v_cache, const int32_t* block_table,
                                    int max_blocks, const int32_t* ctx_lens, int n_seqs, int Hq,
                                    int Hkv, float* part_o, float* part_ml, int max_splits,
-                                   uint16_t* o, hipStream_t st) {
+                                   hipStream_t st) {
   if (n_seqs <= 0) return hipSuccess;
   const float scale_log2 = kLog2e / sqrtf((float)HD);
   hipLaunchKernelGGL(attn_decode_kernel, dim3(max_splits, Hkv, n_seqs), dim3(kAttnThreads), 0,
                      st, q, k_cache, v_cache, block_table, max_blocks, ctx_lens, Hq, Hkv, part_o,
                      part_ml, max_splits, scale_log2);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(attn_combine_kernel, dim3(Hq, n_seqs), dim3(HD), 0, st, part_o, part_ml,
-                     ctx_lens, Hq, max_splits, o);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_combine_bf16(const float* part_o, const float* part_ml,
+                                    const int32_t* ctx_lens, int n_seqs, int Hq, int max_splits,
+                                    uint16_t* o, hipStream_t st) {
+  if (n_seqs <= 0) return hipSuccess;
+  hipLaunchKernelGGL(attn_combine_kernel, dim3(Hq, n_seqs), dim3(HD),
+                     2 * max_splits * sizeof(float), st, part_o, part_ml, ctx_lens, Hq,
+                     max_splits, o);
   return hipGetLastError();
 }
 

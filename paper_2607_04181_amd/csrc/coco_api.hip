@@ -49,7 +49,41 @@ struct coco_layer {
   size_t act_rows_bytes[7] = {};
   int max_splits = 0;
   int dec_rows = 0;
+  // Per-kernel timing (benchmark mode).
+  bool timing = false;
+  std::vector<hipEvent_t> ev;  // pairs: start, stop
+  std::vector<int> ev_kind;    // kind of each recorded pair
+  bool ev_overflow = false;
+  hipStream_t ev_stream = nullptr;
 };
+
+namespace {
+
+constexpr int kTimingPairs = 4096;
+
+// Brackets one kernel launch with events when timing is on.
+struct KernelTimer {
+  coco_layer* H;
+  int kind;
+  int pair = -1;
+  KernelTimer(coco_layer* h, int k, hipStream_t st) : H(h), kind(k) {
+    if (!H->timing) return;
+    const int n = (int)H->ev_kind.size();
+    if (n >= kTimingPairs) {
+      H->ev_overflow = true;
+      return;
+    }
+    pair = n;
+    H->ev_kind.push_back(kind);
+    H->ev_stream = st;
+    (void)hipEventRecord(H->ev[2 * pair], st);
+  }
+  ~KernelTimer() {
+    if (pair >= 0) (void)hipEventRecord(H->ev[2 * pair + 1], H->ev_stream);
+  }
+};
+
+}  // namespace
 
 namespace {
 
@@ -58,7 +92,7 @@ size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 int elem_bytes(int dtype) { return dtype == COCO_BF16 ? 2 : 4; }
 
 int gemm_splits(const coco_layer_config& c, int N, int K) {
-  return c.dtype == COCO_BF16 ? skinny_splits(N, K) : 1;
+  return c.dtype == COCO_BF16 ? skinny_plan(N, K).S : 1;
 }
 
 int check_config(const coco_layer_config* c) {
@@ -77,9 +111,12 @@ int check_config(const coco_layer_config* c) {
       return fail(COCO_EINVAL, "bf16 path needs n_q_heads / n_kv_heads <= 16");
     if (c->d_model % 128 || c->d_ffn % 128)
       return fail(COCO_EINVAL, "bf16 path needs d_model and d_ffn multiples of 128");
+    if (c->d_model > 16384) return fail(COCO_EINVAL, "bf16 path needs d_model <= 16384");
   } else if (c->dtype == COCO_F32) {
     if (c->head_dim % 2 || c->head_dim > 256)
       return fail(COCO_EINVAL, "fp32 path needs an even head_dim <= 256");
+    if (c->d_model % 4 || c->d_ffn % 4 || c->d_model > 16384)
+      return fail(COCO_EINVAL, "fp32 path needs d_model, d_ffn multiples of 4, d_model <= 16384");
   } else {
     return fail(COCO_EINVAL, "unknown dtype %d", c->dtype);
   }
@@ -193,6 +230,7 @@ void coco_layer_destroy(coco_layer_t H) {
   (void)hipGetDevice(&cur);
   (void)hipSetDevice(H->device);
   (void)hipDeviceSynchronize();
+  for (auto& e : H->ev) (void)hipEventDestroy(e);
   (void)hipFree(H->ws);
   (void)hipSetDevice(cur);
   delete H;
@@ -201,6 +239,44 @@ void coco_layer_destroy(coco_layer_t H) {
 int coco_layer_set_validate(coco_layer_t H, int32_t on) {
   if (!H) return fail(COCO_EINVAL, "handle is NULL");
   H->validate = on != 0;
+  return COCO_OK;
+}
+
+int coco_layer_set_timing(coco_layer_t H, int32_t on) {
+  if (!H) return fail(COCO_EINVAL, "handle is NULL");
+  HIPCHK(hipSetDevice(H->device));
+  if (on && H->ev.empty()) {
+    H->ev.resize(2 * kTimingPairs);
+    for (auto& e : H->ev) HIPCHK(hipEventCreate(&e));
+  }
+  H->timing = on != 0;
+  H->ev_kind.clear();
+  H->ev_overflow = false;
+  return COCO_OK;
+}
+
+int coco_layer_read_timing(coco_layer_t H, double* ms, int64_t* launches, int32_t n_kinds) {
+  if (!H || !ms || !launches) return fail(COCO_EINVAL, "NULL argument");
+  if (n_kinds < 0 || n_kinds > COCO_K_COUNT) return fail(COCO_EINVAL, "bad n_kinds");
+  for (int k = 0; k < n_kinds; ++k) {
+    ms[k] = 0.0;
+    launches[k] = 0;
+  }
+  const bool overflow = H->ev_overflow;
+  HIPCHK(hipSetDevice(H->device));
+  for (size_t p = 0; p < H->ev_kind.size(); ++p) {
+    HIPCHK(hipEventSynchronize(H->ev[2 * p + 1]));
+    float t = 0.f;
+    HIPCHK(hipEventElapsedTime(&t, H->ev[2 * p], H->ev[2 * p + 1]));
+    const int k = H->ev_kind[p];
+    if (k < n_kinds) {
+      ms[k] += t;
+      launches[k] += 1;
+    }
+  }
+  H->ev_kind.clear();
+  H->ev_overflow = false;
+  if (overflow) return fail(COCO_ESTATE, "more than %d timed launches between reads", kTimingPairs);
   return COCO_OK;
 }
 
@@ -294,8 +370,10 @@ int gemm(coco_layer* H, const T* A, const T* W, int M, int N, int K, int* S, hip
 template <>
 int gemm<bf16_t>(coco_layer* H, const bf16_t* A, const bf16_t* W, int M, int N, int K, int* S,
                  hipStream_t st) {
-  *S = skinny_splits(N, K);
-  HIPCHK(launch_gemm_skinny_bf16(A, W, H->part, M, N, K, *S, st));
+  const SkinnyPlan plan = skinny_plan(N, K);
+  if (plan.waves == 0) return fail(COCO_EINVAL, "no GEMM plan for N=%d K=%d", N, K);
+  *S = plan.S;
+  HIPCHK(launch_gemm_skinny_bf16(A, W, H->part, M, N, K, plan, st));
   return COCO_OK;
 }
 
@@ -318,11 +396,18 @@ int attention<bf16_t>(coco_layer* H, const coco_layer_weights& w, int M,
                       const int32_t* bt, const int32_t* ctx, hipStream_t st) {
   const coco_layer_config& c = H->cfg;
   if (!seq_starts) {
-    HIPCHK(launch_attn_decode_bf16((const bf16_t*)H->q, (const bf16_t*)w.k_cache,
-                                   (const bf16_t*)w.v_cache, bt, c.max_blocks_per_seq, ctx,
-                                   n_seqs, c.n_q_heads, c.n_kv_heads, H->attn_o, H->attn_ml,
-                                   H->max_splits, (bf16_t*)H->o, st));
+    {
+      KernelTimer t(H, COCO_K_ATTENTION, st);
+      HIPCHK(launch_attn_decode_bf16((const bf16_t*)H->q, (const bf16_t*)w.k_cache,
+                                     (const bf16_t*)w.v_cache, bt, c.max_blocks_per_seq, ctx,
+                                     n_seqs, c.n_q_heads, c.n_kv_heads, H->attn_o, H->attn_ml,
+                                     H->max_splits, st));
+    }
+    KernelTimer t(H, COCO_K_ATTN_COMBINE, st);
+    HIPCHK(launch_attn_combine_bf16(H->attn_o, H->attn_ml, ctx, n_seqs, c.n_q_heads,
+                                    H->max_splits, (bf16_t*)H->o, st));
   } else {
+    KernelTimer t(H, COCO_K_ATTENTION, st);
     HIPCHK(launch_attn_prefill_bf16((const bf16_t*)H->q, (const bf16_t*)w.k_cache,
                                     (const bf16_t*)w.v_cache, bt, c.max_blocks_per_seq, ctx,
                                     positions, seq_starts, n_seqs, M, c.n_q_heads, c.n_kv_heads,
@@ -336,6 +421,7 @@ int attention<float>(coco_layer* H, const coco_layer_weights& w, int M, const in
                      const int32_t* seq_starts, int n_seqs, const int32_t* bt,
                      const int32_t* ctx, hipStream_t st) {
   const coco_layer_config& c = H->cfg;
+  KernelTimer t(H, COCO_K_ATTENTION, st);
   HIPCHK(launch_attn_f32((const float*)H->q, (const float*)w.k_cache, (const float*)w.v_cache,
                          bt, c.max_blocks_per_seq, ctx, positions, seq_starts, n_seqs, M,
                          c.n_q_heads, c.n_kv_heads, c.head_dim, (float*)H->o, st));
@@ -356,32 +442,43 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
   T* h2 = (T*)H->h2;
   T* u = (T*)H->u;
   int S, rc;
+#define TIMED(kind, stmt)                     \
+  do {                                        \
+    KernelTimer timer_(H, kind, st);          \
+    stmt;                                     \
+  } while (0)
   for (int l = first; l < first + nl; ++l) {
     const coco_layer_weights& w = H->layers[l];
     const bool first_l = l == first, last_l = l == first + nl - 1;
     // Gather (first layer of the segment) + RMSNorm_1.
-    HIPCHK(launch_gather_rmsnorm<T>(first_l ? hidden : x, first_l ? row_idx : nullptr, M, d,
-                                    (const T*)w.gamma_attn, c.rms_eps, first_l ? x : nullptr, h,
-                                    st));
+    TIMED(COCO_K_GATHER_NORM,
+          HIPCHK(launch_gather_rmsnorm<T>(first_l ? hidden : x, first_l ? row_idx : nullptr, M,
+                                          d, (const T*)w.gamma_attn, c.rms_eps,
+                                          first_l ? x : nullptr, h, st)));
     // QKV projection, RoPE, local cache append.
-    if ((rc = gemm<T>(H, h, (const T*)w.w_qkv, M, nqkv, d, &S, st))) return rc;
-    HIPCHK(launch_qkv_epilogue<T>(H->part, S, M, Hq, Hkv, hd, positions, seq_starts, n_seqs, bt,
-                                  c.max_blocks_per_seq, H->inv_freq, q, (T*)w.k_cache,
-                                  (T*)w.v_cache, st));
+    TIMED(COCO_K_GEMM_QKV, if ((rc = gemm<T>(H, h, (const T*)w.w_qkv, M, nqkv, d, &S, st))) return rc);
+    TIMED(COCO_K_QKV_EPILOGUE,
+          HIPCHK(launch_qkv_epilogue<T>(H->part, S, M, Hq, Hkv, hd, positions, seq_starts,
+                                        n_seqs, bt, c.max_blocks_per_seq, H->inv_freq, q,
+                                        (T*)w.k_cache, (T*)w.v_cache, st)));
     // Attention over the paged cache.
     if ((rc = attention<T>(H, w, M, positions, seq_starts, n_seqs, bt, ctx, st))) return rc;
     // O projection + residual + RMSNorm_2.
-    if ((rc = gemm<T>(H, o, (const T*)w.w_o, M, d, Hq * hd, &S, st))) return rc;
-    HIPCHK(launch_residual_rmsnorm<T>(H->part, S, M, d, x, (const T*)w.gamma_mlp, c.rms_eps,
-                                      H->x1, h2, st));
+    TIMED(COCO_K_GEMM_O, if ((rc = gemm<T>(H, o, (const T*)w.w_o, M, d, Hq * hd, &S, st))) return rc);
+    TIMED(COCO_K_RESIDUAL_NORM,
+          HIPCHK(launch_residual_rmsnorm<T>(H->part, S, M, d, x, (const T*)w.gamma_mlp,
+                                            c.rms_eps, H->x1, h2, st)));
     // SwiGLU MLP.
-    if ((rc = gemm<T>(H, h2, (const T*)w.w_gate_up, M, 2 * F, d, &S, st))) return rc;
-    HIPCHK(launch_swiglu<T>(H->part, S, M, F, u, st));
-    if ((rc = gemm<T>(H, u, (const T*)w.w_down, M, d, F, &S, st))) return rc;
+    TIMED(COCO_K_GEMM_GATE_UP,
+          if ((rc = gemm<T>(H, h2, (const T*)w.w_gate_up, M, 2 * F, d, &S, st))) return rc);
+    TIMED(COCO_K_SWIGLU, HIPCHK(launch_swiglu<T>(H->part, S, M, F, u, st)));
+    TIMED(COCO_K_GEMM_DOWN, if ((rc = gemm<T>(H, u, (const T*)w.w_down, M, d, F, &S, st))) return rc);
     // Residual; the last layer of the segment scatters to the full batch.
-    HIPCHK(launch_residual_scatter<T>(H->part, S, M, d, H->x1, last_l ? hidden : x,
-                                      last_l ? row_idx : nullptr, st));
+    TIMED(COCO_K_RESIDUAL_SCATTER,
+          HIPCHK(launch_residual_scatter<T>(H->part, S, M, d, H->x1, last_l ? hidden : x,
+                                            last_l ? row_idx : nullptr, st)));
   }
+#undef TIMED
   return COCO_OK;
 }
 

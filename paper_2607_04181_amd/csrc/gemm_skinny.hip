@@ -5,18 +5,22 @@
 // A: [M][K] activations, W: [N][K] weights (nn.Linear layout), both bf16.
 // Decode is bound by reading W once from HBM, so the kernel is built around
 // that stream:
-//   * a workgroup owns 64 output columns and one K-slice; each of its four
-//     waves streams the 16 weight rows of its columns straight into VGPRs
-//     (16-byte loads, 64 contiguous bytes per row per instruction), keeping
-//     PF stages of 128 k in flight;
-//   * the activation tile [rows][128 k] of the stage is shared by the four
-//     waves through LDS (double-buffered, rows padded by 16 bytes);
+//   * a workgroup of WAVES waves owns 16*WAVES output columns and one K-slice;
+//     each wave streams the 16 weight rows of its columns straight into VGPRs
+//     (16-byte loads, 64 contiguous bytes per row per instruction), keeping PF
+//     stages of 128 k in flight;
+//   * the activation tile [rows][128 k] of a stage is shared by the waves
+//     through LDS (double-buffered, rows padded by 16 bytes so the 16 rows a
+//     wave reads per instruction fall in distinct banks);
 //   * each 16x16 output tile is accumulated with v_mfma_f32_16x16x32_bf16 in
 //     ascending k.
-// The K-slicing S (split-K) is a function of (N, K) only and every output
-// element is summed in the same k order for any M, so a row's result does
-// not depend on the other rows in the call (batch invariance). Partials of
-// the S slices are added in slice order by the consumer epilogue.
+// The plan (WAVES, split count S) is chosen from (N, K) alone so that the
+// grid is a whole number of rounds over the 256 CUs; every output element is
+// summed in the same k order for any M, so a row's result does not depend on
+// the other rows in the call (batch invariance). Partials of the S slices
+// are added in slice order by the consumer epilogue.
+#include <math.h>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -24,96 +28,99 @@ namespace coco {
 
 namespace {
 
-constexpr int kBN = 64;        // output columns per workgroup
 constexpr int kBK = 128;       // k per pipeline stage
 constexpr int kPad = 8;        // bf16 elements of LDS row padding
 constexpr int kLdsRow = kBK + kPad;
-constexpr int kThreads = 256;  // 4 waves
-constexpr int kPF = 3;         // weight stages in flight per wave
+constexpr int kCUs = 256;
 
-template <int MT>
-__global__ __launch_bounds__(kThreads) void gemm_skinny_kernel(
+template <int WAVES, int MT, int PF>
+__global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
     const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, float* __restrict__ part, int M,
     int N, int K, int k_slice) {
+  constexpr int NT = WAVES * 64;
+  constexpr int kChunks = MT * 16 * (kBK / 8);  // 16-byte A chunks per stage
+  constexpr int kPerT = (kChunks + NT - 1) / NT;
   __shared__ __attribute__((aligned(16))) bf16_t lds[2][MT * 16][kLdsRow];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wv = tid >> 6;
   const int c16 = lane & 15, j4 = lane >> 4;
-  const int n_col = blockIdx.x * kBN + wv * 16 + c16;  // this lane's weight row
+  const int n_col = blockIdx.x * (16 * WAVES) + wv * 16 + c16;  // this lane's weight row
   const int k_begin = blockIdx.y * k_slice;
   const int stages = k_slice / kBK;
   float* out = part + (int64_t)blockIdx.y * M * N;
 
   const bf16_t* wrow = W + (int64_t)n_col * K + k_begin + j4 * 8;
 
+  // The steady-state loop is branch-free so that the compiler can wait for
+  // exactly the loads each step consumes: prefetches past the slice are
+  // clamped to its last stage (an L2 hit, never used), and stages past the
+  // slice in the final group get a zero activation tile (adding exact zeros
+  // leaves every sum unchanged).
+  const int groups = (stages + PF - 1) / PF;
   for (int m0 = 0; m0 < M; m0 += MT * 16) {
     f32x4_t acc[MT];
 #pragma unroll
     for (int t = 0; t < MT; ++t) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    // Weight ring: kPF stages x 4 k-steps of 8 bf16 per lane.
-    u32x4_t wreg[kPF][4];
+    // Weight ring: PF stages x 4 k-steps of 8 bf16 per lane.
+    u32x4_t wreg[PF][4];
+    auto load_w = [&](int st, int u) {
+      const bf16_t* src = wrow + min(st, stages - 1) * kBK;
 #pragma unroll
-    for (int u = 0; u < kPF; ++u)
-      if (u < stages) {
+      for (int t = 0; t < 4; ++t) wreg[u][t] = *(const u32x4_t*)(src + t * 32);
+    };
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
-          wreg[u][t] = *(const u32x4_t*)(wrow + u * kBK + t * 32);
-      }
+    for (int u = 0; u < PF; ++u) load_w(u, u);
 
-    // Activation staging: MT 16-byte chunks per thread and stage.
-    u32x4_t areg[MT];
-    auto load_a = [&](int st) {
+    // Activation ring: stage x lives in register slot x % 2 from the start of
+    // stage x-2 until it is copied to LDS buffer x % 2 at the end of stage
+    // x-1, so its L2 latency is hidden behind two stages of weight streaming.
+    u32x4_t areg[2][kPerT];
+    auto load_a = [&](int st, int slot) {
+      const int sc = min(st, stages - 1);
 #pragma unroll
-      for (int v = 0; v < MT; ++v) {
-        const int q = tid + v * kThreads;
-        const int row = q >> 4, ch = q & 15;
-        const int m = m0 + row;
-        if (m < M)
-          areg[v] = *(const u32x4_t*)(A + (int64_t)m * K + k_begin + st * kBK + ch * 8);
-        else
-          areg[v] = u32x4_t{0u, 0u, 0u, 0u};
+      for (int v = 0; v < kPerT; ++v) {
+        const int q = min(tid + v * NT, kChunks - 1);
+        const int m = min(m0 + (q >> 4), M - 1);
+        areg[slot][v] = *(const u32x4_t*)(A + (int64_t)m * K + k_begin + sc * kBK + (q & 15) * 8);
       }
     };
-    auto store_a = [&](int buf) {
+    auto store_a = [&](int st, int slot, int buf) {
 #pragma unroll
-      for (int v = 0; v < MT; ++v) {
-        const int q = tid + v * kThreads;
-        const int row = q >> 4, ch = q & 15;
-        *(u32x4_t*)(&lds[buf][row][ch * 8]) = areg[v];
+      for (int v = 0; v < kPerT; ++v) {
+        const int q = tid + v * NT;
+        const bool live = st < stages && m0 + (q >> 4) < M;
+        const u32x4_t val = live ? areg[slot][v] : u32x4_t{0u, 0u, 0u, 0u};
+        if (q < kChunks) *(u32x4_t*)(&lds[buf][q >> 4][(q & 15) * 8]) = val;
       }
     };
 
-    load_a(0);
-    store_a(0);
+    load_a(0, 0);
+    load_a(1, 1);
+    store_a(0, 0, 0);
     __syncthreads();
 
-    for (int st0 = 0; st0 < stages; st0 += kPF) {
+    static_assert(PF % 2 == 0, "ring slots are indexed by stage parity");
+    for (int g = 0; g < groups; ++g) {
 #pragma unroll
-      for (int u = 0; u < kPF; ++u) {
-        const int st = st0 + u;
-        if (st < stages) {
-          const int buf = st & 1;
-          if (st + 1 < stages) load_a(st + 1);
+      for (int u = 0; u < PF; ++u) {
+        const int st = g * PF + u;
+        const int buf = u & 1;  // == st & 1 since PF is even
+        load_a(st + 2, u & 1);
 #pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            const bf16x8_t b = __builtin_bit_cast(bf16x8_t, wreg[u][t]);
+        for (int t = 0; t < 4; ++t) {
+          const bf16x8_t b = __builtin_bit_cast(bf16x8_t, wreg[u][t]);
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-              const bf16x8_t a =
-                  __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(&lds[buf][mt * 16 + c16][t * 32 + j4 * 8]));
-              acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[mt], 0, 0, 0);
-            }
+          for (int mt = 0; mt < MT; ++mt) {
+            const bf16x8_t a = __builtin_bit_cast(
+                bf16x8_t, *(const u32x4_t*)(&lds[buf][mt * 16 + c16][t * 32 + j4 * 8]));
+            acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[mt], 0, 0, 0);
           }
-          if (st + kPF < stages) {
-#pragma unroll
-            for (int t = 0; t < 4; ++t)
-              wreg[u][t] = *(const u32x4_t*)(wrow + (st + kPF) * kBK + t * 32);
-          }
-          if (st + 1 < stages) store_a(buf ^ 1);
-          __syncthreads();
         }
+        load_w(st + PF, u);
+        store_a(st + 1, (u + 1) & 1, buf ^ 1);
+        __syncthreads();
       }
     }
 
@@ -129,28 +136,69 @@ __global__ __launch_bounds__(kThreads) void gemm_skinny_kernel(
   }
 }
 
+template <int WAVES, int MT>
+hipError_t launch_plan(const uint16_t* A, const uint16_t* W, float* part, int M, int N, int K,
+                       int S, hipStream_t st) {
+  // 128-row tiles hold twice the accumulators: a 2-stage weight ring keeps
+  // them out of scratch (two workgroups per CU still keep ~64 KB in flight).
+  constexpr int PF = MT == 4 ? 4 : 2;
+  hipLaunchKernelGGL((gemm_skinny_kernel<WAVES, MT, PF>), dim3(N / (16 * WAVES), S),
+                     dim3(WAVES * 64), 0, st, A, W, part, M, N, K, K / S);
+  return hipGetLastError();
+}
+
+template <int WAVES>
+hipError_t launch_waves(const uint16_t* A, const uint16_t* W, float* part, int M, int N, int K,
+                        int S, hipStream_t st) {
+  return M <= 64 ? launch_plan<WAVES, 4>(A, W, part, M, N, K, S, st)
+                 : launch_plan<WAVES, 8>(A, W, part, M, N, K, S, st);
+}
+
 }  // namespace
 
-int skinny_splits(int N, int K) {
-  const int cols = N / kBN;
-  int S = 1;
-  while (cols * S < 384 && S < 16) S *= 2;
-  while (S > 1 && K % (S * kBK) != 0) S >>= 1;
-  return S;
+// Grid plan from (N, K) only. Scores every (waves, S) that tiles the shape by
+// how evenly the workgroups cover the CUs, how many waves per CU stream
+// weights, and the extra traffic of split-K partials and activation re-reads
+// (costed at a nominal 64 rows).
+SkinnyPlan skinny_plan(int N, int K) {
+  SkinnyPlan best{0, 0};
+  double best_score = -1.0;
+  for (int waves = 4; waves <= 8; ++waves) {
+    const int bn = 16 * waves;
+    if (N % bn) continue;
+    for (int S = 1; S <= 16; S *= 2) {
+      if (K % (S * kBK)) continue;
+      if (S > 1 && K / S < 4 * kBK) continue;
+      const int wgs = (N / bn) * S;
+      const double rounds = ceil((double)wgs / kCUs);
+      const double balance = wgs / (rounds * kCUs);
+      const double waves_per_cu = (double)waves * wgs / kCUs;
+      const double flight = waves_per_cu >= 4.0 ? 1.0 : waves_per_cu / 4.0;
+      const double partial = S > 1 ? 0.5 * 4.0 * S * 64.0 / K : 0.0;
+      const double reread = 0.05 * 64.0 / bn;
+      const double score = balance * flight / (1.0 + partial + reread);
+      if (score > best_score + 1e-12) {
+        best_score = score;
+        best = SkinnyPlan{waves, S};
+      }
+    }
+  }
+  return best;
 }
 
 hipError_t launch_gemm_skinny_bf16(const uint16_t* A, const uint16_t* W, float* part, int M,
-                                   int N, int K, int S, hipStream_t st) {
+                                   int N, int K, SkinnyPlan plan, hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  if (N % kBN != 0 || K % (S * kBK) != 0) return hipErrorInvalidValue;
-  const dim3 grid(N / kBN, S);
-  if (M <= 64)
-    hipLaunchKernelGGL(gemm_skinny_kernel<4>, grid, dim3(kThreads), 0, st, A, W, part, M, N, K,
-                       K / S);
-  else
-    hipLaunchKernelGGL(gemm_skinny_kernel<8>, grid, dim3(kThreads), 0, st, A, W, part, M, N, K,
-                       K / S);
-  return hipGetLastError();
+  if (plan.waves < 4 || plan.waves > 8 || N % (16 * plan.waves) != 0 ||
+      K % (plan.S * kBK) != 0)
+    return hipErrorInvalidValue;
+  switch (plan.waves) {
+    case 4: return launch_waves<4>(A, W, part, M, N, K, plan.S, st);
+    case 5: return launch_waves<5>(A, W, part, M, N, K, plan.S, st);
+    case 6: return launch_waves<6>(A, W, part, M, N, K, plan.S, st);
+    case 7: return launch_waves<7>(A, W, part, M, N, K, plan.S, st);
+    default: return launch_waves<8>(A, W, part, M, N, K, plan.S, st);
+  }
 }
 
 // ----------------------------------------------------------------------------

@@ -47,11 +47,15 @@ hipError_t launch_kv_append(const T* k, const T* v, const int32_t* seq_idx,
 
 // ---------------------------------------------------------------- GEMMs
 // part[s][m][n] = sum_{k in slice s} A[m][k] * W[n][k]   (bf16 in, fp32 out)
-// The split count S and the K-order of every output element depend only on
+// The plan (split count S, workgroup width) and the K-order of every output element depend only on
 // (N, K), never on M: rows are independent and batch-invariant.
-int skinny_splits(int N, int K);
+struct SkinnyPlan {
+  int waves;  // 16-column wave groups per workgroup (4..8)
+  int S;      // K-slices (split-K)
+};
+SkinnyPlan skinny_plan(int N, int K);
 hipError_t launch_gemm_skinny_bf16(const uint16_t* A, const uint16_t* W, float* part, int M,
-                                   int N, int K, int S, hipStream_t st);
+                                   int N, int K, SkinnyPlan plan, hipStream_t st);
 
 // part[0][m][n] = sum_k A[m][k] * W[n][k], fp32 (tiny fp32 configurations).
 hipError_t launch_gemm_f32(const float* A, const float* W, float* part, int M, int N, int K,
@@ -65,7 +69,10 @@ hipError_t launch_attn_decode_bf16(const uint16_t* q, const uint16_t* k_cache,
                                    const uint16_t* v_cache, const int32_t* block_table,
                                    int max_blocks, const int32_t* ctx_lens, int n_seqs,
                                    int Hq, int Hkv, float* part_o, float* part_ml,
-                                   int max_splits, uint16_t* o, hipStream_t st);
+                                   int max_splits, hipStream_t st);
+hipError_t launch_attn_combine_bf16(const float* part_o, const float* part_ml,
+                                    const int32_t* ctx_lens, int n_seqs, int Hq, int max_splits,
+                                    uint16_t* o, hipStream_t st);
 
 hipError_t launch_attn_prefill_bf16(const uint16_t* q, const uint16_t* k_cache,
                                     const uint16_t* v_cache, const int32_t* block_table,

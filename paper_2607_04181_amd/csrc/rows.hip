@@ -2,15 +2,60 @@
 // reduce split-K partials of the projections (RoPE + cache append, residual +
 // RMSNorm, SwiGLU, residual + scatter) and the paged key/value append.
 //
-// Every kernel handles one call row per workgroup (or one element per thread)
-// with a reduction order fixed by the block size alone, so a row's result
-// never depends on which other rows share the call.
+// These kernels move little data (a few MB per step) and are bound by memory
+// latency, so they are written for memory-level parallelism: the split count
+// S is a template parameter (all S partial loads of a column are issued back
+// to back), fp32 partials are read as 16-byte vectors, and grids cover
+// (row, column chunk) rather than one workgroup per row where no row-wide
+// reduction is needed. Every reduction order is fixed by the block shape and
+// S alone, so a row's result never depends on the other rows of the call.
 #include "common.h"
 #include "kernels.h"
 
 namespace coco {
 
+namespace {
+
 constexpr int kRowThreads = 256;
+constexpr int kNormThreads = 1024;
+
+// Sum of S fp32 partials of 4 consecutive columns, in split order.
+template <int S>
+__device__ __forceinline__ f32x4_t sum_parts4(const float* __restrict__ p, int64_t stride) {
+  f32x4_t v[S];
+#pragma unroll
+  for (int s = 0; s < S; ++s) v[s] = *(const f32x4_t*)(p + s * stride);
+  f32x4_t a = v[0];
+#pragma unroll
+  for (int s = 1; s < S; ++s) a += v[s];
+  return a;
+}
+
+template <int S>
+__device__ __forceinline__ float sum_parts1(const float* __restrict__ p, int64_t stride) {
+  float v[S];
+#pragma unroll
+  for (int s = 0; s < S; ++s) v[s] = p[s * stride];
+  float a = v[0];
+#pragma unroll
+  for (int s = 1; s < S; ++s) a += v[s];
+  return a;
+}
+
+__device__ __forceinline__ void unpack_bf16x8(u32x4_t u, float* f) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = __uint_as_float(u[i] << 16);
+    f[2 * i + 1] = __uint_as_float(u[i] & 0xFFFF0000u);
+  }
+}
+
+__device__ __forceinline__ u32x4_t pack_bf16x8(const float* f) {
+  return u32x4_t{pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3]), pack_bf16x2(f[4], f[5]),
+                 pack_bf16x2(f[6], f[7])};
+}
+
+}  // namespace
 
 // ----------------------------------------------------------------------------
 // Segment-boundary gather of the sub-batch rows, fused with the first RMSNorm.
@@ -36,73 +81,113 @@ __global__ __launch_bounds__(kRowThreads) void gather_rmsnorm_kernel(
                    Elem<T>::load(x + c) * inv * Elem<T>::load(gamma + c));
 }
 
+// bf16 rows, d % 8 == 0: 16-byte vectors, row held in registers.
+template <>
+__global__ __launch_bounds__(kRowThreads) void gather_rmsnorm_kernel<bf16_t>(
+    const bf16_t* __restrict__ src, const int32_t* __restrict__ row_idx, int d,
+    const bf16_t* __restrict__ gamma, float eps, bf16_t* __restrict__ x_out,
+    bf16_t* __restrict__ h_out) {
+  __shared__ float red[kRowThreads / kWave];
+  constexpr int kMaxVec = 8;  // d <= 16384
+  const int i = blockIdx.x;
+  const int64_t r = row_idx ? (int64_t)row_idx[i] : (int64_t)i;
+  const int nv = d / 8;
+  const u32x4_t* x = (const u32x4_t*)(src + r * d);
+  u32x4_t xv[kMaxVec];
+  float ss = 0.f;
+#pragma unroll
+  for (int u = 0; u < kMaxVec; ++u) {
+    const int v = threadIdx.x + u * kRowThreads;
+    if (v < nv) {
+      xv[u] = x[v];
+      float f[8];
+      unpack_bf16x8(xv[u], f);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss += f[e] * f[e];
+      if (x_out) ((u32x4_t*)(x_out + (int64_t)i * d))[v] = xv[u];
+    }
+  }
+  ss = block_sum<kRowThreads>(ss, red);
+  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+  const u32x4_t* g = (const u32x4_t*)gamma;
+#pragma unroll
+  for (int u = 0; u < kMaxVec; ++u) {
+    const int v = threadIdx.x + u * kRowThreads;
+    if (v < nv) {
+      float f[8], gf[8];
+      unpack_bf16x8(xv[u], f);
+      unpack_bf16x8(g[v], gf);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) f[e] = f[e] * inv * gf[e];
+      ((u32x4_t*)(h_out + (int64_t)i * d))[v] = pack_bf16x8(f);
+    }
+  }
+}
+
 template <typename T>
 hipError_t launch_gather_rmsnorm(const T* src, const int32_t* row_idx, int M, int d,
                                  const T* gamma, float eps, T* x_out, T* h_out,
                                  hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  hipLaunchKernelGGL(gather_rmsnorm_kernel<T>, dim3(M), dim3(kRowThreads), 0, st, src,
-                     row_idx, d, gamma, eps, x_out, h_out);
+  hipLaunchKernelGGL(gather_rmsnorm_kernel<T>, dim3(M), dim3(kRowThreads), 0, st, src, row_idx,
+                     d, gamma, eps, x_out, h_out);
   return hipGetLastError();
 }
 
 // ----------------------------------------------------------------------------
-// QKV epilogue: reduce the split-K partials, rotate query and key heads to the
-// row's absolute position (rotate-half RoPE, angles in fp64), store queries,
-// append the rotated key and the value to the sequence's cache slot.
+// QKV epilogue: one wave per (row, head). Reduce the split-K partials, rotate
+// query and key heads to the row's absolute position (rotate-half RoPE,
+// angles in fp64), store queries, append the rotated key and the value to
+// the sequence's cache slot.
 // ----------------------------------------------------------------------------
-template <typename T>
-__global__ __launch_bounds__(kRowThreads) void qkv_epilogue_kernel(
-    const float* __restrict__ part, int S, int M, int Hq, int Hkv, int hd,
+template <typename T, int S>
+__global__ __launch_bounds__(kWave) void qkv_epilogue_kernel(
+    const float* __restrict__ part, int M, int Hq, int Hkv, int hd,
     const int32_t* __restrict__ positions, const int32_t* __restrict__ seq_starts, int n_seqs,
     const int32_t* __restrict__ block_table, int max_blocks, const double* __restrict__ inv_freq,
     T* __restrict__ q_out, T* __restrict__ k_cache, T* __restrict__ v_cache) {
-  __shared__ float cs[2][128];
-  const int i = blockIdx.x;
+  const int h = blockIdx.x, i = blockIdx.y, lane = threadIdx.x;
   const int half = hd >> 1;
   const int N = (Hq + 2 * Hkv) * hd;
-  const int pos = positions[i];
-  for (int j = threadIdx.x; j < half; j += kRowThreads) {
-    double sn, cn;
-    sincos((double)pos * inv_freq[j], &sn, &cn);
-    cs[0][j] = (float)cn;
-    cs[1][j] = (float)sn;
-  }
-  __syncthreads();
-  const int seq = row_to_seq(seq_starts, n_seqs, i);
-  const int64_t blk = block_table[(int64_t)seq * max_blocks + pos / kBlockTokens];
-  const int slot = pos % kBlockTokens;
-  const float* p = part + (int64_t)i * N;
   const int64_t pstride = (int64_t)M * N;
-  auto val = [&](int n) {
-    float a = 0.f;
-    for (int s = 0; s < S; ++s) a += p[s * pstride + n];
-    return a;
-  };
-  // Query and key heads: one thread per rotation pair (head, j).
-  const int pairs = (Hq + Hkv) * half;
-  for (int e = threadIdx.x; e < pairs; e += kRowThreads) {
-    const int h = e / half, j = e - h * half;
-    const float lo = val(h * hd + j), hi = val(h * hd + j + half);
-    const float c = cs[0][j], sn = cs[1][j];
-    const float rlo = lo * c - hi * sn, rhi = hi * c + lo * sn;
-    if (h < Hq) {
-      T* q = q_out + (int64_t)i * Hq * hd + h * hd;
-      Elem<T>::store(q + j, rlo);
-      Elem<T>::store(q + j + half, rhi);
-    } else {
-      T* k = k_cache + ((blk * Hkv + (h - Hq)) * kBlockTokens + slot) * hd;
-      Elem<T>::store(k + j, rlo);
-      Elem<T>::store(k + j + half, rhi);
-    }
+  const float* p = part + (int64_t)i * N + (int64_t)h * hd;
+  const int pos = positions[i];
+  int64_t blk = 0;
+  int slot = 0;
+  if (h >= Hq) {
+    const int seq = row_to_seq(seq_starts, n_seqs, i);
+    blk = block_table[(int64_t)seq * max_blocks + pos / kBlockTokens];
+    slot = pos % kBlockTokens;
   }
-  // Value heads: [blk][kvh][dim][slot].
-  for (int e = threadIdx.x; e < Hkv * hd; e += kRowThreads) {
-    const int h = e / hd, dim = e - h * hd;
-    Elem<T>::store(v_cache + ((blk * Hkv + h) * hd + dim) * kBlockTokens + slot,
-                   val((Hq + Hkv) * hd + e));
+  if (h < Hq + Hkv) {
+    for (int j = lane; j < half; j += kWave) {
+      const float lo = sum_parts1<S>(p + j, pstride), hi = sum_parts1<S>(p + j + half, pstride);
+      double sn, cn;
+      sincos((double)pos * inv_freq[j], &sn, &cn);
+      const float c = (float)cn, s = (float)sn;
+      const float rlo = lo * c - hi * s, rhi = hi * c + lo * s;
+      T* dst = h < Hq ? q_out + ((int64_t)i * Hq + h) * hd
+                      : k_cache + ((blk * Hkv + (h - Hq)) * kBlockTokens + slot) * hd;
+      Elem<T>::store(dst + j, rlo);
+      Elem<T>::store(dst + j + half, rhi);
+    }
+  } else {
+    const int kh = h - Hq - Hkv;
+    T* dst = v_cache + (blk * Hkv + kh) * hd * kBlockTokens + slot;
+    for (int e = lane; e < hd; e += kWave)
+      Elem<T>::store(dst + e * kBlockTokens, sum_parts1<S>(p + e, pstride));
   }
 }
+
+#define COCO_SWITCH_S(S, ...)                        \
+  switch (S) {                                       \
+    case 1: { constexpr int S_ = 1; __VA_ARGS__; } break;  \
+    case 2: { constexpr int S_ = 2; __VA_ARGS__; } break;  \
+    case 4: { constexpr int S_ = 4; __VA_ARGS__; } break;  \
+    case 8: { constexpr int S_ = 8; __VA_ARGS__; } break;  \
+    case 16: { constexpr int S_ = 16; __VA_ARGS__; } break; \
+    default: return hipErrorInvalidValue;            \
+  }
 
 template <typename T>
 hipError_t launch_qkv_epilogue(const float* part, int S, int M, int Hq, int Hkv, int hd,
@@ -111,36 +196,55 @@ hipError_t launch_qkv_epilogue(const float* part, int S, int M, int Hq, int Hkv,
                                const double* inv_freq, T* q_out, T* k_cache, T* v_cache,
                                hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  hipLaunchKernelGGL(qkv_epilogue_kernel<T>, dim3(M), dim3(kRowThreads), 0, st, part, S, M,
-                     Hq, Hkv, hd, positions, seq_starts, n_seqs, block_table, max_blocks,
-                     inv_freq, q_out, k_cache, v_cache);
+  const dim3 grid(Hq + 2 * Hkv, M);
+  COCO_SWITCH_S(S, hipLaunchKernelGGL((qkv_epilogue_kernel<T, S_>), grid, dim3(kWave), 0, st,
+                                      part, M, Hq, Hkv, hd, positions, seq_starts, n_seqs,
+                                      block_table, max_blocks, inv_freq, q_out, k_cache,
+                                      v_cache));
   return hipGetLastError();
 }
 
 // ----------------------------------------------------------------------------
 // O-projection epilogue: residual add (kept in fp32) fused with RMSNorm_2.
+// One 1024-thread workgroup per row; every thread owns 4-column vectors.
 // ----------------------------------------------------------------------------
-template <typename T>
-__global__ __launch_bounds__(kRowThreads) void residual_rmsnorm_kernel(
-    const float* __restrict__ part, int S, int M, int d, const T* __restrict__ x,
+template <typename T, int S>
+__global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_kernel(
+    const float* __restrict__ part, int M, int d, const T* __restrict__ x,
     const T* __restrict__ gamma, float eps, float* __restrict__ x1, T* __restrict__ h2) {
-  __shared__ float red[kRowThreads / kWave];
+  __shared__ float red[kNormThreads / kWave];
+  constexpr int kMaxVec = 4;  // d <= 16384
   const int i = blockIdx.x;
   const int64_t pstride = (int64_t)M * d;
+  const int nv = d / 4;
+  f32x4_t a[kMaxVec];
   float ss = 0.f;
-  for (int c = threadIdx.x; c < d; c += kRowThreads) {
-    float a = Elem<T>::load(x + (int64_t)i * d + c);
-    float acc = 0.f;
-    for (int s = 0; s < S; ++s) acc += part[s * pstride + (int64_t)i * d + c];
-    a += acc;
-    x1[(int64_t)i * d + c] = a;
-    ss += a * a;
+#pragma unroll
+  for (int u = 0; u < kMaxVec; ++u) {
+    const int v = threadIdx.x + u * kNormThreads;
+    if (v < nv) {
+      const int c = 4 * v;
+      a[u] = sum_parts4<S>(part + (int64_t)i * d + c, pstride);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        a[u][e] += Elem<T>::load(x + (int64_t)i * d + c + e);
+        ss += a[u][e] * a[u][e];
+      }
+      *(f32x4_t*)(x1 + (int64_t)i * d + c) = a[u];
+    }
   }
-  ss = block_sum<kRowThreads>(ss, red);
+  ss = block_sum<kNormThreads>(ss, red);
   const float inv = 1.0f / sqrtf(ss / (float)d + eps);
-  for (int c = threadIdx.x; c < d; c += kRowThreads)
-    Elem<T>::store(h2 + (int64_t)i * d + c,
-                   x1[(int64_t)i * d + c] * inv * Elem<T>::load(gamma + c));
+#pragma unroll
+  for (int u = 0; u < kMaxVec; ++u) {
+    const int v = threadIdx.x + u * kNormThreads;
+    if (v < nv) {
+      const int c = 4 * v;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        Elem<T>::store(h2 + (int64_t)i * d + c + e, a[u][e] * inv * Elem<T>::load(gamma + c + e));
+    }
+  }
 }
 
 template <typename T>
@@ -148,36 +252,39 @@ hipError_t launch_residual_rmsnorm(const float* part, int S, int M, int d, const
                                    const T* gamma, float eps, float* x1, T* h2,
                                    hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  hipLaunchKernelGGL(residual_rmsnorm_kernel<T>, dim3(M), dim3(kRowThreads), 0, st, part, S,
-                     M, d, x, gamma, eps, x1, h2);
+  if (d % 4 != 0 || d > 4 * 4 * kNormThreads) return hipErrorInvalidValue;
+  COCO_SWITCH_S(S, hipLaunchKernelGGL((residual_rmsnorm_kernel<T, S_>), dim3(M),
+                                      dim3(kNormThreads), 0, st, part, M, d, x, gamma, eps, x1,
+                                      h2));
   return hipGetLastError();
 }
 
 // ----------------------------------------------------------------------------
-// SwiGLU: u = silu(gate) * up from the reduced gate/up partials.
+// SwiGLU: u = silu(gate) * up from the reduced gate/up partials; 4 columns
+// per thread.
 // ----------------------------------------------------------------------------
-template <typename T>
+template <typename T, int S>
 __global__ __launch_bounds__(kRowThreads) void swiglu_kernel(const float* __restrict__ part,
-                                                             int S, int M, int F,
-                                                             T* __restrict__ u) {
+                                                             int M, int F, T* __restrict__ u) {
   const int i = blockIdx.y;
-  const int j = blockIdx.x * kRowThreads + threadIdx.x;
-  if (j >= F) return;
+  const int c = 4 * (blockIdx.x * kRowThreads + threadIdx.x);
+  if (c >= F) return;
   const int64_t pstride = (int64_t)M * 2 * F;
-  const float* p = part + (int64_t)i * 2 * F;
-  float g = 0.f, up = 0.f;
-  for (int s = 0; s < S; ++s) {
-    g += p[s * pstride + j];
-    up += p[s * pstride + F + j];
-  }
-  Elem<T>::store(u + (int64_t)i * F + j, g / (1.0f + expf(-g)) * up);
+  const float* p = part + (int64_t)i * 2 * F + c;
+  const f32x4_t g = sum_parts4<S>(p, pstride);
+  const f32x4_t up = sum_parts4<S>(p + F, pstride);
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    Elem<T>::store(u + (int64_t)i * F + c + e, g[e] / (1.0f + expf(-g[e])) * up[e]);
 }
 
 template <typename T>
 hipError_t launch_swiglu(const float* part, int S, int M, int F, T* u, hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  hipLaunchKernelGGL(swiglu_kernel<T>, dim3((F + kRowThreads - 1) / kRowThreads, M),
-                     dim3(kRowThreads), 0, st, part, S, M, F, u);
+  if (F % 4 != 0) return hipErrorInvalidValue;
+  const dim3 grid((F / 4 + kRowThreads - 1) / kRowThreads, M);
+  COCO_SWITCH_S(S, hipLaunchKernelGGL((swiglu_kernel<T, S_>), grid, dim3(kRowThreads), 0, st,
+                                      part, M, F, u));
   return hipGetLastError();
 }
 
@@ -185,26 +292,28 @@ hipError_t launch_swiglu(const float* part, int S, int M, int F, T* u, hipStream
 // Down-projection epilogue: y = x1 + sum of partials, rounded to the hidden
 // dtype, scattered to the row's place in the full-batch buffer.
 // ----------------------------------------------------------------------------
-template <typename T>
+template <typename T, int S>
 __global__ __launch_bounds__(kRowThreads) void residual_scatter_kernel(
-    const float* __restrict__ part, int S, int M, int d, const float* __restrict__ x1,
+    const float* __restrict__ part, int M, int d, const float* __restrict__ x1,
     T* __restrict__ out, const int32_t* __restrict__ row_idx) {
-  const int i = blockIdx.x;
+  const int i = blockIdx.y;
+  const int c = 4 * (blockIdx.x * kRowThreads + threadIdx.x);
+  if (c >= d) return;
   const int64_t r = row_idx ? (int64_t)row_idx[i] : (int64_t)i;
-  const int64_t pstride = (int64_t)M * d;
-  for (int c = threadIdx.x; c < d; c += kRowThreads) {
-    float acc = 0.f;
-    for (int s = 0; s < S; ++s) acc += part[s * pstride + (int64_t)i * d + c];
-    Elem<T>::store(out + r * d + c, x1[(int64_t)i * d + c] + acc);
-  }
+  const f32x4_t a = sum_parts4<S>(part + (int64_t)i * d + c, (int64_t)M * d);
+  const f32x4_t x = *(const f32x4_t*)(x1 + (int64_t)i * d + c);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) Elem<T>::store(out + r * d + c + e, x[e] + a[e]);
 }
 
 template <typename T>
 hipError_t launch_residual_scatter(const float* part, int S, int M, int d, const float* x1,
                                    T* out, const int32_t* row_idx, hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  hipLaunchKernelGGL(residual_scatter_kernel<T>, dim3(M), dim3(kRowThreads), 0, st, part, S,
-                     M, d, x1, out, row_idx);
+  if (d % 4 != 0) return hipErrorInvalidValue;
+  const dim3 grid((d / 4 + kRowThreads - 1) / kRowThreads, M);
+  COCO_SWITCH_S(S, hipLaunchKernelGGL((residual_scatter_kernel<T, S_>), grid, dim3(kRowThreads),
+                                      0, st, part, M, d, x1, out, row_idx));
   return hipGetLastError();
 }
 
