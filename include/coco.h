@@ -43,10 +43,14 @@
  *   w_down    [d][F]
  *   gamma_attn, gamma_mlp [d]          RMSNorm gains
  * Paged cache of one layer, with block size B = 16 tokens:
- *   k_cache [num_blocks][Hkv][B][hd]   token-major inside a block
- *   v_cache [num_blocks][Hkv][hd][B]   dimension-major inside a block
- *   Token t of sequence s lives in block block_table[s][t / 16], slot t % 16.
- *   Keys are stored after rotation (RoPE), values as projected.
+ *   k_cache, v_cache [num_blocks][Hkv][B * hd]: one tile of B tokens x hd
+ *   dimensions per (block, kv head), in MFMA operand order. Inside a tile,
+ *   token slot t (0..15) and dimension h live at
+ *     K: ((h/32)*64 + ((h%32)/8)*16 + t)*8 + h%8
+ *     V: (((h/32)*64 + (t/4)*16 + h%16)*2 + (h/16)%2)*4 + t%4
+ *   (hd must be a multiple of 32). Token t of sequence s lives in block
+ *   block_table[s][t / 16], slot t % 16. Keys are stored after rotation
+ *   (RoPE), values as projected.
  * Batch arrays (int32, device):
  *   row_idx[n_rows]        hidden row of each call row; distinct, < hidden_rows
  *   positions[n_rows]      absolute position of each call row's token
@@ -86,7 +90,7 @@ typedef struct {
   int32_t d_model;            /* d */
   int32_t n_q_heads;          /* Hq */
   int32_t n_kv_heads;         /* Hkv; Hq % Hkv == 0 */
-  int32_t head_dim;           /* hd; 128 for COCO_BF16, even and <= 256 for COCO_F32 */
+  int32_t head_dim;           /* hd; 128 for COCO_BF16, multiple of 32 <= 256 for COCO_F32 */
   int32_t d_ffn;              /* F */
   int32_t n_layers;           /* layers held by this handle */
   int32_t dtype;              /* COCO_BF16 or COCO_F32 */

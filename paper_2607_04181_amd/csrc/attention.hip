@@ -1,7 +1,7 @@
 // Grouped-query attention over the paged key/value cache.
 //
-// Cache layout per layer (block = 16 tokens):
-//   K [blocks][Hkv][16 tokens][hd]   V [blocks][Hkv][hd][16 tokens]
+// Cache layout per layer (block = 16 tokens): [blocks][Hkv][tile], each tile
+// of 16 tokens x hd in MFMA operand order (k_tile_offset / v_tile_offset).
 //
 // MFMA dataflow (bf16, hd = 128), shared by decode and prefill. A wave owns 16
 // "query columns" and walks the key blocks of one key/value head:
@@ -11,9 +11,8 @@
 // With S^T the probabilities come out of the first MFMA already in the
 // B-operand layout of the second, and O^T keeps a column's rescale factor in
 // the lane that computed it: no cross-lane shuffles besides the column
-// max/sum. K rows are read as 16-byte vectors, V^T rows as 8-byte vectors;
-// storing V dimension-major inside a block is what makes the second read
-// contiguous.
+// max/sum. Because tiles are stored in operand order, every K and V read is a
+// contiguous 1 KB wave load.
 //
 // Decode: the columns are the G = Hq/Hkv query heads of one token (padded to
 // 16). A workgroup handles (sequence, kv head, 256-token partition); its four
@@ -83,12 +82,18 @@ __device__ __forceinline__ void attend_block(WaveState& ws, const u32x4_t kf[4],
   }
 }
 
+// One (block, kv head) tile: four contiguous 1 KB loads each for K and V.
 __device__ __forceinline__ void load_kv(const bf16_t* kb, const bf16_t* vb, int c16, int j4,
                                         u32x4_t kf[4], u32x2_t vf[8]) {
+  const int lane = j4 * 16 + c16;
 #pragma unroll
-  for (int t = 0; t < 4; ++t) kf[t] = *(const u32x4_t*)(kb + c16 * HD + t * 32 + j4 * 8);
+  for (int t = 0; t < 4; ++t) kf[t] = *(const u32x4_t*)(kb + (t * 64 + lane) * 8);
 #pragma unroll
-  for (int n = 0; n < 8; ++n) vf[n] = *(const u32x2_t*)(vb + (n * 16 + c16) * 16 + j4 * 4);
+  for (int p = 0; p < 4; ++p) {
+    const u32x4_t v = *(const u32x4_t*)(vb + (p * 64 + lane) * 8);
+    vf[2 * p] = u32x2_t{v.x, v.y};
+    vf[2 * p + 1] = u32x2_t{v.z, v.w};
+  }
 }
 
 // Column sum of this lane's share: lanes c16, c16+16, c16+32, c16+48.
@@ -98,90 +103,141 @@ __device__ __forceinline__ float column_sum(float l) {
 }
 
 // ---------------------------------------------------------------- decode
-__global__ __launch_bounds__(kAttnThreads) void attn_decode_kernel(
+// Persistent workgroups walk the work list (partition, kv head) in order;
+// partition offsets per sequence (split_off, an exclusive prefix sum of
+// ceil(ctx / 256)) were written by the QKV epilogue. Eight waves take two
+// blocks each of the 256-token partition; each wave scores both blocks
+// first, takes one column max and then accumulates exp * V against it, and
+// the eight wave results are merged in LDS in wave order.
+constexpr int kDecWaves = 8;
+constexpr int kDecBPW = kDecodeSplit / kBlockTokens / kDecWaves;
+
+__global__ __launch_bounds__(kDecWaves * 64) void attn_decode_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k_cache,
     const bf16_t* __restrict__ v_cache, const int32_t* __restrict__ block_table, int max_blocks,
-    const int32_t* __restrict__ ctx_lens, int Hq, int Hkv, float* __restrict__ part_o,
-    float* __restrict__ part_ml, int max_splits, float scale_log2) {
-  __shared__ float sm_m[4][16], sm_l[4][16];
-  __shared__ float sm_o[4][16][HD + 4];
+    const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ split_off, int n_seqs,
+    int Hq, int Hkv, float* __restrict__ part_o, float* __restrict__ part_ml, int max_splits,
+    float scale_log2) {
+  __shared__ float sm_m[kDecWaves][16], sm_l[kDecWaves][16];
+  __shared__ float sm_o[kDecWaves][16][HD + 4];
 
-  const int sp = blockIdx.x, g = blockIdx.y, s = blockIdx.z;
-  const int ctx = ctx_lens[s];
-  const int t0 = sp * kDecodeSplit;
-  if (t0 >= ctx) return;
-  const int t1 = min(ctx, t0 + kDecodeSplit);
+  const int total = split_off[n_seqs] * Hkv;
   const int G = Hq / Hkv;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int c16 = lane & 15, j4 = lane >> 4;
+  const int64_t tile = (int64_t)kBlockTokens * HD;
 
-  bf16x8_t qf[4];
-  {
-    const int cq = c16 < G ? c16 : G - 1;  // padded columns read a real head, then zero
-    const bf16_t* qp = q + ((int64_t)s * Hq + g * G + cq) * HD + j4 * 8;
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-      qf[t] = (c16 < G) ? __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(qp + t * 32))
-                        : __builtin_bit_cast(bf16x8_t, u32x4_t{0u, 0u, 0u, 0u});
-  }
-
-  WaveState ws;
-  wave_state_init(ws);
-  const int b_first = t0 / kBlockTokens, b_last = (t1 - 1) / kBlockTokens;
-  const int32_t* bt = block_table + (int64_t)s * max_blocks;
-  const int64_t head_stride = (int64_t)kBlockTokens * HD;
-
-  // A partition is 16 blocks: wave wv takes blocks b_first + wv + 4u, u < 4.
-  // All of a wave's key/value loads are issued before any is consumed, so a
-  // wave keeps 32 KB in flight.
-  constexpr int kPerWave = kDecodeSplit / kBlockTokens / 4;
-  u32x4_t kf[kPerWave][4];
-  u32x2_t vf[kPerWave][8];
-#pragma unroll
-  for (int u = 0; u < kPerWave; ++u) {
-    const int b = b_first + wv + 4 * u;
-    if (b <= b_last) {
-      const int64_t pb = bt[b];
-      load_kv(k_cache + (pb * Hkv + g) * head_stride, v_cache + (pb * Hkv + g) * head_stride,
-              c16, j4, kf[u], vf[u]);
+  for (int w = blockIdx.x; w < total; w += gridDim.x) {
+    const int item = w / Hkv, g = w - item * Hkv;
+    int lo = 0, hi = n_seqs - 1;  // the s with split_off[s] <= item < split_off[s + 1]
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (split_off[mid] <= item) lo = mid; else hi = mid - 1;
     }
-  }
+    const int s = lo, sp = item - split_off[s];
+    const int ctx = ctx_lens[s];
+    const int t0 = sp * kDecodeSplit;
+    const int t1 = min(ctx, t0 + kDecodeSplit);
+
+    bf16x8_t qf[4];
+    {
+      const int cq = c16 < G ? c16 : G - 1;  // padded columns read a real head, then zero
+      const bf16_t* qp = q + ((int64_t)s * Hq + g * G + cq) * HD + j4 * 8;
 #pragma unroll
-  for (int u = 0; u < kPerWave; ++u) {
-    const int b = b_first + wv + 4 * u;
-    if (b <= b_last) {
+      for (int t = 0; t < 4; ++t)
+        qf[t] = (c16 < G) ? __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(qp + t * 32))
+                          : __builtin_bit_cast(bf16x8_t, u32x4_t{0u, 0u, 0u, 0u});
+    }
+    const int b_first = t0 / kBlockTokens, b_last = (t1 - 1) / kBlockTokens;
+    const int32_t* bt = block_table + (int64_t)s * max_blocks;
+
+    u32x4_t kf[kDecBPW][4];
+    u32x2_t vf[kDecBPW][8];
+#pragma unroll
+    for (int u = 0; u < kDecBPW; ++u) {
+      const int b = b_first + wv + kDecWaves * u;
+      if (b <= b_last) {
+        const int64_t pb = bt[b];
+        load_kv(k_cache + (pb * Hkv + g) * tile, v_cache + (pb * Hkv + g) * tile, c16, j4, kf[u],
+                vf[u]);
+      }
+    }
+    // Pass 1: scores of all of the wave's blocks, one column max.
+    float sc[kDecBPW][4];
+    float m = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < kDecBPW; ++u) {
+      const int b = b_first + wv + kDecWaves * u;
+      f32x4_t a = {0.f, 0.f, 0.f, 0.f};
+      if (b <= b_last) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kf[u][t]),
+                                                      qf[t], a, 0, 0, 0);
+      }
       const int tok0 = b * kBlockTokens + j4 * 4;
-      attend_block(ws, kf[u], vf[u], qf, scale_log2, [&](int r) { return tok0 + r < t1; });
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        sc[u][r] = (b <= b_last && tok0 + r < t1) ? a[r] * scale_log2 : -INFINITY;
+        m = fmaxf(m, sc[u][r]);
+      }
     }
-  }
+    m = fmaxf(m, __shfl_xor(m, 16, kWave));
+    m = fmaxf(m, __shfl_xor(m, 32, kWave));
+    // Pass 2: probabilities against the fixed max, O^T += V^T P^T. A wave
+    // with no block keeps m = -inf and contributes nothing.
+    const float mref = m == -INFINITY ? 0.f : m;
+    float l = 0.f;
+    f32x4_t o[8];
+#pragma unroll
+    for (int n = 0; n < 8; ++n) o[n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int u = 0; u < kDecBPW; ++u) {
+      const int b = b_first + wv + kDecWaves * u;
+      if (b <= b_last) {
+        float p[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) p[r] = exp2f(sc[u][r] - mref);
+        l += (p[0] + p[1]) + (p[2] + p[3]);
+        const s16x4_t pf = __builtin_bit_cast(
+            s16x4_t, u32x2_t{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3])});
+#pragma unroll
+        for (int n = 0; n < 8; ++n)
+          o[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4_t, vf[u][n]),
+                                                           pf, o[n], 0, 0, 0);
+      }
+    }
+    const float l_col = column_sum(l);
+    if (j4 == 0) {
+      sm_m[wv][c16] = m;
+      sm_l[wv][c16] = l_col;
+    }
+#pragma unroll
+    for (int n = 0; n < 8; ++n)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sm_o[wv][c16][n * 16 + j4 * 4 + r] = o[n][r];
+    __syncthreads();
 
-  const float l_col = column_sum(ws.l);
-  if (j4 == 0) {
-    sm_m[wv][c16] = ws.m;
-    sm_l[wv][c16] = l_col;
-  }
+    for (int e = threadIdx.x; e < G * HD; e += kDecWaves * 64) {
+      const int col = e / HD, dim = e - col * HD;
+      float mx = sm_m[0][col];
 #pragma unroll
-  for (int n = 0; n < 8; ++n)
+      for (int v = 1; v < kDecWaves; ++v) mx = fmaxf(mx, sm_m[v][col]);
+      float acc = 0.f, L = 0.f;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) sm_o[wv][c16][n * 16 + j4 * 4 + r] = ws.o[n][r];
-  __syncthreads();
-
-  for (int e = threadIdx.x; e < G * HD; e += kAttnThreads) {
-    const int col = e / HD, dim = e - col * HD;
-    const float mx = fmaxf(fmaxf(sm_m[0][col], sm_m[1][col]), fmaxf(sm_m[2][col], sm_m[3][col]));
-    float acc = 0.f, L = 0.f;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const float f = exp2f(sm_m[w][col] - mx);
-      acc += f * sm_o[w][col][dim];
-      L += f * sm_l[w][col];
+      for (int v = 0; v < kDecWaves; ++v) {
+        const float f = exp2f(sm_m[v][col] - mx);
+        acc += f * sm_o[v][col][dim];
+        L += f * sm_l[v][col];
+      }
+      const int64_t idx = ((int64_t)s * Hq + g * G + col) * max_splits + sp;
+      part_o[idx * HD + dim] = acc;
+      if (dim == 0) {
+        part_ml[idx * 2 + 0] = mx;
+        part_ml[idx * 2 + 1] = L;
+      }
     }
-    const int64_t idx = ((int64_t)s * Hq + g * G + col) * max_splits + sp;
-    part_o[idx * HD + dim] = acc;
-    if (dim == 0) {
-      part_ml[idx * 2 + 0] = mx;
-      part_ml[idx * 2 + 1] = L;
-    }
+    __syncthreads();  // LDS is reused by the next work item
   }
 }
 
@@ -326,12 +382,13 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(
   for (int t = 0; t < n; ++t) {
     const int64_t blk = bt[t / kBlockTokens];
     const int slot = t % kBlockTokens;
-    const float* kr = k_cache + ((blk * Hkv + g) * kBlockTokens + slot) * hd;
+    const float* kt = k_cache + (blk * Hkv + g) * kBlockTokens * hd;
+    const float* vt = v_cache + (blk * Hkv + g) * kBlockTokens * hd;
     float d = 0.f;
 #pragma unroll
     for (int u = 0; u < kMaxPer; ++u) {
       const int e = lane + u * 64;
-      if (e < hd) d = fmaf(qv[u], kr[e], d);
+      if (e < hd) d = fmaf(qv[u], kt[k_tile_offset(slot, e)], d);
     }
     const float z = wave_sum(d) * scale;
     const float m_new = fmaxf(m, z);
@@ -342,7 +399,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(
     for (int u = 0; u < kMaxPer; ++u) {
       const int e = lane + u * 64;
       if (e < hd)
-        acc[u] = acc[u] * alpha + p * v_cache[((blk * Hkv + g) * hd + e) * kBlockTokens + slot];
+        acc[u] = acc[u] * alpha + p * vt[v_tile_offset(slot, e)];
     }
   }
 #pragma unroll
@@ -360,14 +417,18 @@ int decode_max_splits(int max_blocks_per_seq) {
 
 hipError_t launch_attn_decode_bf16(const uint16_t* q, const uint16_t* k_cache,
                                    const uint16_t* v_cache, const int32_t* block_table,
-                                   int max_blocks, const int32_t* ctx_lens, int n_seqs, int Hq,
-                                   int Hkv, float* part_o, float* part_ml, int max_splits,
+                                   int max_blocks, const int32_t* ctx_lens,
+                                   const int32_t* split_off, int n_seqs, int Hq, int Hkv,
+                                   float* part_o, float* part_ml, int max_splits,
                                    hipStream_t st) {
   if (n_seqs <= 0) return hipSuccess;
   const float scale_log2 = kLog2e / sqrtf((float)HD);
-  hipLaunchKernelGGL(attn_decode_kernel, dim3(max_splits, Hkv, n_seqs), dim3(kAttnThreads), 0,
-                     st, q, k_cache, v_cache, block_table, max_blocks, ctx_lens, Hq, Hkv, part_o,
-                     part_ml, max_splits, scale_log2);
+  // Two resident workgroups per CU (LDS bound); the grid never exceeds the work.
+  const int64_t work_bound = (int64_t)n_seqs * max_splits * Hkv;
+  const int grid = (int)(work_bound < 512 ? work_bound : 512);
+  hipLaunchKernelGGL(attn_decode_kernel, dim3(grid), dim3(kDecWaves * 64), 0, st, q, k_cache,
+                     v_cache, block_table, max_blocks, ctx_lens, split_off, n_seqs, Hq, Hkv,
+                     part_o, part_ml, max_splits, scale_log2);
   return hipGetLastError();
 }
 

@@ -46,6 +46,7 @@ struct coco_layer {
   void *x = nullptr, *h = nullptr, *q = nullptr, *o = nullptr, *h2 = nullptr, *u = nullptr;
   float *x1 = nullptr, *part = nullptr, *attn_o = nullptr, *attn_ml = nullptr;
   double* inv_freq = nullptr;
+  int32_t* split_off = nullptr;  // decode attention work list offsets
   size_t act_rows_bytes[7] = {};
   int max_splits = 0;
   int dec_rows = 0;
@@ -113,8 +114,8 @@ int check_config(const coco_layer_config* c) {
       return fail(COCO_EINVAL, "bf16 path needs d_model and d_ffn multiples of 128");
     if (c->d_model > 16384) return fail(COCO_EINVAL, "bf16 path needs d_model <= 16384");
   } else if (c->dtype == COCO_F32) {
-    if (c->head_dim % 2 || c->head_dim > 256)
-      return fail(COCO_EINVAL, "fp32 path needs an even head_dim <= 256");
+    if (c->head_dim % 32 || c->head_dim > 256)
+      return fail(COCO_EINVAL, "fp32 path needs head_dim a multiple of 32, <= 256");
     if (c->d_model % 4 || c->d_ffn % 4 || c->d_model > 16384)
       return fail(COCO_EINVAL, "fp32 path needs d_model, d_ffn multiples of 4, d_model <= 16384");
   } else {
@@ -179,7 +180,7 @@ int coco_layer_init(const coco_layer_config* cfg, const coco_layer_weights* laye
       c.dtype == COCO_BF16 ? align256((size_t)H->dec_rows * c.n_q_heads * H->max_splits * 128 * 4) : 0,
       c.dtype == COCO_BF16 ? align256((size_t)H->dec_rows * c.n_q_heads * H->max_splits * 2 * 4) : 0,
       align256((size_t)(c.head_dim / 2) * 8),  // inv_freq
-      0};
+      align256((size_t)(H->dec_rows + 1) * 4)};  // split_off
   for (int i = 0; i < 12; ++i) {
     offs[i] = off;
     off += sizes[i];
@@ -201,6 +202,7 @@ int coco_layer_init(const coco_layer_config* cfg, const coco_layer_weights* laye
   H->attn_o = (float*)(H->ws + offs[8]);
   H->attn_ml = (float*)(H->ws + offs[9]);
   H->inv_freq = (double*)(H->ws + offs[10]);
+  H->split_off = (int32_t*)(H->ws + offs[11]);
   H->act_rows_bytes[COCO_WS_X] = R * d * eb;
   H->act_rows_bytes[COCO_WS_H] = R * d * eb;
   H->act_rows_bytes[COCO_WS_Q] = R * qd * eb;
@@ -400,8 +402,8 @@ int attention<bf16_t>(coco_layer* H, const coco_layer_weights& w, int M,
       KernelTimer t(H, COCO_K_ATTENTION, st);
       HIPCHK(launch_attn_decode_bf16((const bf16_t*)H->q, (const bf16_t*)w.k_cache,
                                      (const bf16_t*)w.v_cache, bt, c.max_blocks_per_seq, ctx,
-                                     n_seqs, c.n_q_heads, c.n_kv_heads, H->attn_o, H->attn_ml,
-                                     H->max_splits, st));
+                                     H->split_off, n_seqs, c.n_q_heads, c.n_kv_heads, H->attn_o,
+                                     H->attn_ml, H->max_splits, st));
     }
     KernelTimer t(H, COCO_K_ATTN_COMBINE, st);
     HIPCHK(launch_attn_combine_bf16(H->attn_o, H->attn_ml, ctx, n_seqs, c.n_q_heads,
@@ -460,7 +462,11 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
     TIMED(COCO_K_QKV_EPILOGUE,
           HIPCHK(launch_qkv_epilogue<T>(H->part, S, M, Hq, Hkv, hd, positions, seq_starts,
                                         n_seqs, bt, c.max_blocks_per_seq, H->inv_freq, q,
-                                        (T*)w.k_cache, (T*)w.v_cache, st)));
+                                        (T*)w.k_cache, (T*)w.v_cache, ctx,
+                                        (seq_starts == nullptr && c.dtype == COCO_BF16)
+                                            ? H->split_off
+                                            : nullptr,
+                                        st)));
     // Attention over the paged cache.
     if ((rc = attention<T>(H, w, M, positions, seq_starts, n_seqs, bt, ctx, st))) return rc;
     // O projection + residual + RMSNorm_2.

@@ -71,6 +71,22 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return t;
 }
 
+// Paged cache tiles. A (block, kv head) tile holds 16 tokens x hd dims
+// (hd a multiple of 32) in MFMA operand order:
+//  K: element (token t, dim h) at ((h/32)*64 + ((h%32)/8)*16 + t)*8 + h%8, so
+//     1 KB piece s (dims 32s..32s+31) is the A operand of one 16x16x32 MFMA
+//     step with lane i holding token i%16, dims 32s + 8(i/16) .. +8;
+//  V: element (t, h) at (((h/32)*64 + (t/4)*16 + h%16)*2 + (h/16)%2)*4 + t%4,
+//     so lane i of 1 KB piece p holds, for the two 16-dim tiles 2p and 2p+1,
+//     dims 16n + i%16 at tokens 4(i/16) .. +4 (A operands of 16x16x16 MFMAs
+//     computing V^T P^T).
+__device__ __forceinline__ int k_tile_offset(int t, int h) {
+  return (((h >> 5) * 64 + ((h >> 3) & 3) * 16 + t) << 3) + (h & 7);
+}
+__device__ __forceinline__ int v_tile_offset(int t, int h) {
+  return ((((h >> 5) * 64 + (t >> 2) * 16 + (h & 15)) * 2 + ((h >> 4) & 1)) << 2) + (t & 3);
+}
+
 // Sequence of a call row: identity for decode, else the s with
 // seq_starts[s] <= row < seq_starts[s+1].
 __device__ __forceinline__ int row_to_seq(const int32_t* seq_starts, int n_seqs, int row) {

@@ -16,12 +16,14 @@ hipError_t launch_gather_rmsnorm(const T* src, const int32_t* row_idx, int M, in
 
 // Sum of S split-K partials of the QKV projection, RoPE on query and key
 // heads, queries to q_out [M][Hq*hd], keys/values into the paged cache.
+// With split_off non-null (decode), one workgroup also writes the decode
+// attention's partition offsets from ctx_lens.
 template <typename T>
 hipError_t launch_qkv_epilogue(const float* part, int S, int M, int Hq, int Hkv, int hd,
                                const int32_t* positions, const int32_t* seq_starts,
                                int n_seqs, const int32_t* block_table, int max_blocks,
                                const double* inv_freq, T* q_out, T* k_cache, T* v_cache,
-                               hipStream_t st);
+                               const int32_t* ctx_lens, int32_t* split_off, hipStream_t st);
 
 // x1 = x + sum_s part[s]  (fp32);  h2 = RMSNorm(x1) * gamma.
 template <typename T>
@@ -65,11 +67,14 @@ hipError_t launch_gemm_f32(const float* A, const float* W, float* part, int M, i
 constexpr int kDecodeSplit = 256;  // tokens per split-KV partition
 int decode_max_splits(int max_blocks_per_seq);
 
+// split_off[n_seqs + 1]: exclusive prefix sum of each sequence's partition
+// count (written by the QKV epilogue of the same call).
 hipError_t launch_attn_decode_bf16(const uint16_t* q, const uint16_t* k_cache,
                                    const uint16_t* v_cache, const int32_t* block_table,
-                                   int max_blocks, const int32_t* ctx_lens, int n_seqs,
-                                   int Hq, int Hkv, float* part_o, float* part_ml,
-                                   int max_splits, hipStream_t st);
+                                   int max_blocks, const int32_t* ctx_lens,
+                                   const int32_t* split_off, int n_seqs, int Hq, int Hkv,
+                                   float* part_o, float* part_ml, int max_splits,
+                                   hipStream_t st);
 hipError_t launch_attn_combine_bf16(const float* part_o, const float* part_ml,
                                     const int32_t* ctx_lens, int n_seqs, int Hq, int max_splits,
                                     uint16_t* o, hipStream_t st);

@@ -145,8 +145,25 @@ __global__ __launch_bounds__(kWave) void qkv_epilogue_kernel(
     const float* __restrict__ part, int M, int Hq, int Hkv, int hd,
     const int32_t* __restrict__ positions, const int32_t* __restrict__ seq_starts, int n_seqs,
     const int32_t* __restrict__ block_table, int max_blocks, const double* __restrict__ inv_freq,
-    T* __restrict__ q_out, T* __restrict__ k_cache, T* __restrict__ v_cache) {
+    T* __restrict__ q_out, T* __restrict__ k_cache, T* __restrict__ v_cache,
+    const int32_t* __restrict__ ctx_lens, int32_t* __restrict__ split_off) {
   const int h = blockIdx.x, i = blockIdx.y, lane = threadIdx.x;
+  if (split_off != nullptr && h == 0 && i == 0) {
+    // Decode attention work list: exclusive prefix sum of ceil(ctx / 256).
+    int run = 0;
+    if (lane == 0) split_off[0] = 0;
+    for (int base = 0; base < n_seqs; base += kWave) {
+      const int s = base + lane;
+      int v = s < n_seqs ? (ctx_lens[s] + kDecodeSplit - 1) / kDecodeSplit : 0;
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1) {
+        const int t = __shfl_up(v, o, kWave);
+        if (lane >= o) v += t;
+      }
+      if (s < n_seqs) split_off[s + 1] = run + v;
+      run += __shfl(v, kWave - 1, kWave);
+    }
+  }
   const int half = hd >> 1;
   const int N = (Hq + 2 * Hkv) * hd;
   const int64_t pstride = (int64_t)M * N;
@@ -166,16 +183,21 @@ __global__ __launch_bounds__(kWave) void qkv_epilogue_kernel(
       sincos((double)pos * inv_freq[j], &sn, &cn);
       const float c = (float)cn, s = (float)sn;
       const float rlo = lo * c - hi * s, rhi = hi * c + lo * s;
-      T* dst = h < Hq ? q_out + ((int64_t)i * Hq + h) * hd
-                      : k_cache + ((blk * Hkv + (h - Hq)) * kBlockTokens + slot) * hd;
-      Elem<T>::store(dst + j, rlo);
-      Elem<T>::store(dst + j + half, rhi);
+      if (h < Hq) {
+        T* dst = q_out + ((int64_t)i * Hq + h) * hd;
+        Elem<T>::store(dst + j, rlo);
+        Elem<T>::store(dst + j + half, rhi);
+      } else {
+        T* tile = k_cache + (blk * Hkv + (h - Hq)) * kBlockTokens * hd;
+        Elem<T>::store(tile + k_tile_offset(slot, j), rlo);
+        Elem<T>::store(tile + k_tile_offset(slot, j + half), rhi);
+      }
     }
   } else {
     const int kh = h - Hq - Hkv;
-    T* dst = v_cache + (blk * Hkv + kh) * hd * kBlockTokens + slot;
+    T* tile = v_cache + (blk * Hkv + kh) * kBlockTokens * hd;
     for (int e = lane; e < hd; e += kWave)
-      Elem<T>::store(dst + e * kBlockTokens, sum_parts1<S>(p + e, pstride));
+      Elem<T>::store(tile + v_tile_offset(slot, e), sum_parts1<S>(p + e, pstride));
   }
 }
 
@@ -194,13 +216,13 @@ hipError_t launch_qkv_epilogue(const float* part, int S, int M, int Hq, int Hkv,
                                const int32_t* positions, const int32_t* seq_starts,
                                int n_seqs, const int32_t* block_table, int max_blocks,
                                const double* inv_freq, T* q_out, T* k_cache, T* v_cache,
-                               hipStream_t st) {
+                               const int32_t* ctx_lens, int32_t* split_off, hipStream_t st) {
   if (M <= 0) return hipSuccess;
   const dim3 grid(Hq + 2 * Hkv, M);
   COCO_SWITCH_S(S, hipLaunchKernelGGL((qkv_epilogue_kernel<T, S_>), grid, dim3(kWave), 0, st,
                                       part, M, Hq, Hkv, hd, positions, seq_starts, n_seqs,
                                       block_table, max_blocks, inv_freq, q_out, k_cache,
-                                      v_cache));
+                                      v_cache, ctx_lens, split_off));
   return hipGetLastError();
 }
 
@@ -318,7 +340,7 @@ hipError_t launch_residual_scatter(const float* part, int S, int M, int d, const
 }
 
 // ----------------------------------------------------------------------------
-// Paged key/value append (bit copy).
+// Paged key/value append (bit copy into the tile layout).
 // ----------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(kRowThreads) void kv_append_kernel(
@@ -333,8 +355,9 @@ __global__ __launch_bounds__(kRowThreads) void kv_append_kernel(
   const int64_t src = (int64_t)t * Hkv * hd;
   for (int e = threadIdx.x; e < Hkv * hd; e += kRowThreads) {
     const int h = e / hd, dim = e - h * hd;
-    k_cache[((blk * Hkv + h) * kBlockTokens + slot) * hd + dim] = k[src + e];
-    v_cache[((blk * Hkv + h) * hd + dim) * kBlockTokens + slot] = v[src + e];
+    const int64_t tile = (blk * Hkv + h) * kBlockTokens * hd;
+    k_cache[tile + k_tile_offset(slot, dim)] = k[src + e];
+    v_cache[tile + v_tile_offset(slot, dim)] = v[src + e];
   }
 }
 
@@ -355,7 +378,7 @@ hipError_t launch_kv_append(const T* k, const T* v, const int32_t* seq_idx,
   template hipError_t launch_qkv_epilogue<T>(const float*, int, int, int, int, int,          \
                                              const int32_t*, const int32_t*, int,            \
                                              const int32_t*, int, const double*, T*, T*, T*, \
-                                             hipStream_t);                                   \
+                                             const int32_t*, int32_t*, hipStream_t);         \
   template hipError_t launch_residual_rmsnorm<T>(const float*, int, int, int, const T*,      \
                                                  const T*, float, float*, T*, hipStream_t);  \
   template hipError_t launch_swiglu<T>(const float*, int, int, int, T*, hipStream_t);        \

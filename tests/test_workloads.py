@@ -55,7 +55,7 @@ def test_kv_pool_block_subset_matches_full_pool():
     full = W.kv_pool(W.TINY, "c1", 0, 21, "v")
     sub = W.kv_pool(W.TINY, "c1", 0, 21, "v", blocks=np.array([5, 0, 20]))
     assert torch.equal(sub, full[[5, 0, 20]])
-    assert full.shape == (21, 2, 64, 16)
+    assert full.shape == (21, 2, 16 * 64)
 
 
 @pytest.mark.parametrize("cid", sorted(W.ALL))
@@ -98,3 +98,28 @@ def test_even_partition_matches_paper_examples():
         assert [len(p) for p in parts] == c["sizes"]
         assert max(len(p) for p in parts) == math.ceil(c["bs"] / c["v"])
         assert np.array_equal(np.concatenate(parts), np.arange(c["bs"]))
+
+
+def test_depager_matches_the_documented_tile_formula():
+    """The oracle-side de-pager against explicit loops over the layout."""
+    from oracle.paged import depage_blocks
+    rng = np.random.default_rng(0)
+    for hd in (64, 128):
+        nb, Hkv = 3, 2
+        K = rng.normal(size=(nb * 16, Hkv, hd))
+        V = rng.normal(size=(nb * 16, Hkv, hd))
+        kb = np.zeros((nb, Hkv, 16 * hd))
+        vb = np.zeros((nb, Hkv, 16 * hd))
+        for tok in range(nb * 16):
+            b, t = divmod(tok, 16)
+            for g in range(Hkv):
+                for h in range(hd):
+                    kb[b, g, ((h // 32) * 64 + ((h % 32) // 8) * 16 + t) * 8 + h % 8] = K[tok, g, h]
+                    vb[b, g, (((h // 32) * 64 + (t // 4) * 16 + h % 16) * 2 + (h // 16) % 2) * 4
+                       + t % 4] = V[tok, g, h]
+        K2, V2 = depage_blocks(kb, vb, nb * 16 - 5)
+        assert np.array_equal(K2, K[:nb * 16 - 5]) and np.array_equal(V2, V[:nb * 16 - 5])
+        # Each tile formula is a permutation of the tile.
+        from oracle.paged import tile_index
+        ki, vi = tile_index(hd)
+        assert sorted(ki.ravel()) == list(range(16 * hd)) == sorted(vi.ravel())

@@ -209,9 +209,10 @@ def hidden_states(shape: LayerShape, tag: str, rows: int, device="cpu") -> torch
 
 
 def kv_pool_shapes(shape: LayerShape, num_blocks: int):
-    """Paged cache layout: K [blocks, Hkv, block, hd]; V [blocks, Hkv, hd, block]."""
+    """Paged cache pools: K and V are [blocks, Hkv, block * hd] (one tile per
+    block and key/value head; the order inside a tile is the library's)."""
     bs, h, hd = shape.block_size, shape.n_kv_heads, shape.head_dim
-    return (num_blocks, h, bs, hd), (num_blocks, h, hd, bs)
+    return (num_blocks, h, bs * hd), (num_blocks, h, bs * hd)
 
 
 def kv_pool(shape: LayerShape, tag: str, layer: int, num_blocks: int, which: str,
