@@ -1,0 +1,206 @@
+"""Full-size configurations, in the launch configuration bench.py times.
+
+The GPU runs the whole batch; the oracle recomputes sampled output rows one
+by one (decode rows are independent; prefill samples whole requests), and
+properties that hold at any size (split-batch bit identity) are checked on
+the whole batch. Weights of the largest layers reach the oracle as host
+copies of the tensors the counter-based generator produced on the GPU;
+test_generator_is_identical_on_cpu_and_gpu shows these are the bits the CPU
+generator gives.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from harness import (TOL, Replica, gpu_cache_tokens, log, normwise_err, oracle_cache,
+                     oracle_decode_rows, oracle_prefill_seqs, oracle_weights, to64)
+from workloads import device as WD
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+
+def sample_rows(b: W.Batch, k: int, seed: int = 0):
+    """Call rows with the shortest and the longest context plus k-2 seeded
+    others."""
+    ctx = b.ctx_lens
+    rows = {int(np.argmin(ctx)), int(np.argmax(ctx))}
+    rng = np.random.default_rng(seed)
+    for r in rng.permutation(b.n_rows):
+        if len(rows) >= k:
+            break
+        rows.add(int(r))
+    return sorted(rows)
+
+
+def check(name, got, ref, x):
+    e = normwise_err(got, ref)
+    ed = normwise_err(got - x, ref - x)
+    log(f"{name}: output err {e:.2e}, branch err {ed:.2e}")
+    assert e < TOL and ed < TOL, (name, e, ed)
+
+
+def test_generator_is_identical_on_cpu_and_gpu():
+    shape = W.LLAMA8B
+    dev = W.layer_weights(shape, "c2", 0, device="cuda")
+    for name in ("w_qkv", "w_down", "gamma_attn"):
+        n = 4096
+        cpu = W.normal(W.stream_key("c2", name, 0), n, 0.1 if name.startswith("gamma") else 0.02,
+                       1.0 if name.startswith("gamma") else 0.0, start=0)
+        assert torch.equal(cpu.view(torch.int16), dev[name].reshape(-1)[:n].cpu().view(torch.int16))
+    rows = W.weight_rows(shape, "c2", 0, "w_gate_up", 1000, 1003)
+    assert torch.equal(rows.view(torch.int16), dev["w_gate_up"][1000:1003].cpu().view(torch.int16))
+    blocks = np.array([7, 0, 999])
+    kc = W.kv_pool(shape, "c2", 0, 1000, "k", blocks=blocks)
+    kg = W.kv_pool(shape, "c2", 0, 1000, "k", device="cuda")[torch.from_numpy(blocks).cuda()]
+    assert torch.equal(kc.view(torch.int16), kg.cpu().view(torch.int16))
+
+
+def test_c2_llama8b_decode_batch64_sampled_rows():
+    wl = W.c2_llama8b_decode()
+    b, shape = wl.batch, wl.shape
+    rep = Replica.for_batch(shape, wl.tag, 1, b)
+    hidden = WD.hidden_tensor(shape, wl.tag, b.hidden_rows)
+    h0 = to64(hidden)
+    rep.forward(0, hidden, WD.batch_tensors(b))
+    torch.cuda.synchronize()
+    rows = sample_rows(b, 6)
+    ref, _, cache = oracle_decode_rows(shape, wl.tag, 0, b, rows, h0, source="cpu")
+    got = to64(hidden)[b.row_idx[rows]]
+    check("c2 sampled rows", got, ref, h0[b.row_idx[rows]])
+    for j, r in enumerate(rows):
+        p = int(b.positions[r])
+        K, V = gpu_cache_tokens(rep.layers[0], b, r, p, p + 1)
+        assert normwise_err(K[0], cache.K[j][p]) < TOL and normwise_err(V[0], cache.V[j][p]) < TOL
+
+
+def _kv_new_tokens(layer_t, b: W.Batch, seqs):
+    out = []
+    for s in seqs:
+        K, V = gpu_cache_tokens(layer_t, b, s, int(b.prior_lens[s]), int(b.ctx_lens[s]))
+        out.append((K, V))
+    return out
+
+
+def test_c3_skewed_split_is_bit_identical_and_matches_oracle():
+    """The hot replica's Zipf share (96 of 256 rows), the whole 256-row
+    batch, and the share cut into uneven sub-batches of the heterogeneous
+    model (v = 5: 20, 19, 19, 19, 19) give identical rows and cache bytes."""
+    wl = W.c3_llama8b_skewed()
+    full, sub, shape = wl.full_batch, wl.batch, wl.shape
+    rep = Replica.for_batch(shape, wl.tag, 1, full, max_rows=full.n_rows, max_seqs=full.n_seqs)
+    hidden = WD.hidden_tensor(shape, wl.tag, full.hidden_rows)
+    h0 = to64(hidden)
+    # Blocks holding the new tokens of the 96 requests, to restore between runs.
+    new_blocks = np.unique([sub.block_table[s, int(sub.prior_lens[s]) // 16]
+                            for s in range(sub.n_seqs)])
+    idx = torch.from_numpy(new_blocks.astype(np.int64)).cuda()
+    saved = {k: rep.layers[0][k][idx].clone() for k in ("k_cache", "v_cache")}
+
+    def restore():
+        for k in saved:
+            rep.layers[0][k][idx] = saved[k]
+
+    whole = hidden.clone()
+    rep.forward(0, whole, WD.batch_tensors(full))
+    torch.cuda.synchronize()
+    kv_whole = _kv_new_tokens(rep.layers[0], sub, range(sub.n_seqs))
+    rows = sub.row_idx.astype(np.int64)
+
+    restore()
+    share = hidden.clone()
+    rep.forward(0, share, WD.batch_tensors(sub))
+    torch.cuda.synchronize()
+    assert torch.equal(share[rows].view(torch.int16), whole[rows].view(torch.int16))
+    others = np.setdiff1d(np.arange(full.hidden_rows), rows)
+    assert torch.equal(share[others].view(torch.int16), hidden[others].view(torch.int16))
+    for (k1, v1), (k2, v2) in zip(_kv_new_tokens(rep.layers[0], sub, range(sub.n_seqs)), kv_whole):
+        assert np.array_equal(k1, k2) and np.array_equal(v1, v2)
+
+    restore()
+    parts = hidden.clone()
+    for p in W.even_partition(sub.n_rows, 5):
+        rep.forward(0, parts, WD.batch_tensors(sub.select(p)))
+    torch.cuda.synchronize()
+    assert torch.equal(parts[rows].view(torch.int16), whole[rows].view(torch.int16))
+    for (k1, v1), (k2, v2) in zip(_kv_new_tokens(rep.layers[0], sub, range(sub.n_seqs)), kv_whole):
+        assert np.array_equal(k1, k2) and np.array_equal(v1, v2)
+
+    sample = sample_rows(sub, 4, seed=3)
+    ref, _, _ = oracle_decode_rows(shape, wl.tag, 0, sub, sample, h0, source="device",
+                                   dev_layer=rep.layers[0])
+    check("c3 sampled rows", to64(share)[rows[sample]], ref, h0[rows[sample]])
+
+
+def test_c4_qwen32b_prefill_then_decode():
+    wl = W.c4_qwen32b()
+    pre, dec, shape = wl.batch, wl.decode_after, wl.shape
+    rep = Replica.for_batch(shape, wl.tag, 1, pre, max_rows=pre.n_rows, max_seqs=dec.n_seqs)
+    w64 = oracle_weights(shape, wl.tag, 0, "device", rep.layers[0])
+    hidden = WD.hidden_tensor(shape, wl.tag, pre.hidden_rows)
+    h0 = to64(hidden)
+    # Request-aligned split first (fresh cache state is not needed: the
+    # prefill rewrites the same slots with the same values).
+    split = hidden.clone()
+    for seqs in ([2, 0], [3, 1]):
+        rep.forward(0, split, WD.batch_tensors(pre.select_seqs(seqs)))
+    whole = hidden.clone()
+    rep.forward(0, whole, WD.batch_tensors(pre))
+    torch.cuda.synchronize()
+    assert torch.equal(split.view(torch.int16), whole.view(torch.int16))
+    # Oracle on request 1 (512 new tokens after 512 cached).
+    ref, _, cache, sub = oracle_prefill_seqs(shape, wl.tag, 0, pre, [1], h0, source="device",
+                                             dev_layer=rep.layers[0], w64=w64)
+    rows = sub.row_idx.astype(np.int64)
+    check("c4 prefill request 1", to64(whole)[rows], ref, h0[rows])
+    # Request 0 (no cached context): its keys/values feed the decode check.
+    ref0, _, cache0, sub0 = oracle_prefill_seqs(shape, wl.tag, 0, pre, [0], h0, source="device",
+                                                dev_layer=rep.layers[0], w64=w64)
+    rows0 = sub0.row_idx.astype(np.int64)
+    check("c4 prefill request 0", to64(whole)[rows0], ref0, h0[rows0])
+
+    # Batch-128 decode on the same cache: request 0 (keys from the prefill)
+    # and sampled decode-only requests.
+    dh = WD.hidden_tensor(shape, wl.tag + "dec", dec.hidden_rows)
+    d0 = to64(dh)
+    rep.forward(0, dh, WD.batch_tensors(dec))
+    torch.cuda.synchronize()
+    got = to64(dh)
+    sample = [0] + sample_rows(dec.select(range(4, 128)), 3, seed=4)
+    sample = [0] + [s + 4 for s in sample[1:]]
+    for r in sample:
+        sb = dec.select([r])
+        if r == 0:
+            K = np.zeros((int(sb.ctx_lens[0]), shape.n_kv_heads, shape.head_dim))
+            V = np.zeros_like(K)
+            K[:512], V[:512] = cache0.K[0][:512], cache0.V[0][:512]
+            c = oracle.KVCache([K], [V])
+        else:
+            c = oracle_cache(shape, wl.tag, 0, sb, [0], dec.num_blocks, "cpu")
+        out, _ = oracle.layer_forward(w64, shape, d0, sb.row_idx, sb.positions, None,
+                                      sb.ctx_lens, c)
+        check(f"c4 decode row {r}", got[sb.row_idx], out[sb.row_idx], d0[sb.row_idx])
+
+
+def test_c5_llama70b_span8_sampled_rows():
+    wl = W.c5_llama70b_span()
+    b, shape = wl.batch, wl.shape
+    rep = Replica.for_batch(shape, wl.tag, wl.n_layers, b)
+    hidden = WD.hidden_tensor(shape, wl.tag, b.hidden_rows)
+    h0 = to64(hidden)
+    rep.span(0, wl.n_layers, hidden, WD.batch_tensors(b))
+    torch.cuda.synchronize()
+    rows = sample_rows(b, 3, seed=5)
+    sub = b.select(rows)
+    x = h0.copy()
+    for l in range(wl.n_layers):
+        w64 = oracle_weights(shape, wl.tag, l, "device", rep.layers[l])
+        c = oracle_cache(shape, wl.tag, l, sub, range(sub.n_seqs), b.num_blocks, "device",
+                         rep.layers[l])
+        x, _ = oracle.layer_forward(w64, shape, x, sub.row_idx, sub.positions, None,
+                                    sub.ctx_lens, c)
+        del w64
+        log(f"c5 oracle layer {l} done")
+    got = to64(hidden)[sub.row_idx]
+    check("c5 span sampled rows", got, x[sub.row_idx], h0[sub.row_idx])
