@@ -82,15 +82,17 @@ __device__ __forceinline__ void attend_block(WaveState& ws, const u32x4_t kf[4],
   }
 }
 
-// One (block, kv head) tile: four contiguous 1 KB loads each for K and V.
+// One (block, kv head) tile: four contiguous 1 KB loads each for K and V,
+// non-temporal (each tile is read once per step).
 __device__ __forceinline__ void load_kv(const bf16_t* kb, const bf16_t* vb, int c16, int j4,
                                         u32x4_t kf[4], u32x2_t vf[8]) {
   const int lane = j4 * 16 + c16;
 #pragma unroll
-  for (int t = 0; t < 4; ++t) kf[t] = *(const u32x4_t*)(kb + (t * 64 + lane) * 8);
+  for (int t = 0; t < 4; ++t)
+    kf[t] = __builtin_nontemporal_load((const u32x4_t*)(kb + (t * 64 + lane) * 8));
 #pragma unroll
   for (int p = 0; p < 4; ++p) {
-    const u32x4_t v = *(const u32x4_t*)(vb + (p * 64 + lane) * 8);
+    const u32x4_t v = __builtin_nontemporal_load((const u32x4_t*)(vb + (p * 64 + lane) * 8));
     vf[2 * p] = u32x2_t{v.x, v.y};
     vf[2 * p + 1] = u32x2_t{v.z, v.w};
   }

@@ -7,8 +7,9 @@
 // that stream:
 //   * a workgroup of WAVES waves owns 16*WAVES output columns and one K-slice;
 //     each wave streams the 16 weight rows of its columns straight into VGPRs
-//     (16-byte loads, 64 contiguous bytes per row per instruction), keeping PF
-//     stages of 128 k in flight;
+//     (16-byte loads, 64 contiguous bytes per row per instruction; plain
+//     loads measured faster here than non-temporal ones), keeping PF stages
+//     of 128 k in flight;
 //   * the activation tile [rows][128 k] of a stage is shared by the waves
 //     through LDS (double-buffered, rows padded by 16 bytes so the 16 rows a
 //     wave reads per instruction fall in distinct banks);
