@@ -23,7 +23,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-Wall",
          "-Wno-unused-function", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          f"-I{os.path.join(ROOT, 'include')}"]
-SOURCES = ["rows.hip", "gemm_skinny.hip", "attention.hip", "coco_api.hip"]
+SOURCES = ["rows.hip", "gemm_skinny.hip", "gemm_tile.hip", "attention.hip", "coco_api.hip"]
 
 
 def build(verbose: bool = False, jobs: int = 8) -> str:

@@ -92,8 +92,11 @@ size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 int elem_bytes(int dtype) { return dtype == COCO_BF16 ? 2 : 4; }
 
+// Largest split count either GEMM path uses for (N, K).
 int gemm_splits(const coco_layer_config& c, int N, int K) {
-  return c.dtype == COCO_BF16 ? skinny_plan(N, K).S : 1;
+  if (c.dtype != COCO_BF16) return 1;
+  const int a = skinny_plan(N, K).S, b = tile_splits(N, K);
+  return a > b ? a : b;
 }
 
 int check_config(const coco_layer_config* c) {
@@ -366,12 +369,20 @@ int validate_batch(coco_layer* H, int64_t hidden_rows, const int32_t* row_idx, i
 // ----------------------------------------------------------------------------
 // Launch sequence.
 // ----------------------------------------------------------------------------
+// Decode uses the weight-streaming plan (split-K from (N, K) only); prefill
+// uses the large-tile kernel with one split.
 template <typename T>
-int gemm(coco_layer* H, const T* A, const T* W, int M, int N, int K, int* S, hipStream_t st);
+int gemm(coco_layer* H, const T* A, const T* W, int M, int N, int K, bool prefill, int* S,
+         hipStream_t st);
 
 template <>
-int gemm<bf16_t>(coco_layer* H, const bf16_t* A, const bf16_t* W, int M, int N, int K, int* S,
-                 hipStream_t st) {
+int gemm<bf16_t>(coco_layer* H, const bf16_t* A, const bf16_t* W, int M, int N, int K,
+                 bool prefill, int* S, hipStream_t st) {
+  if (prefill) {
+    *S = tile_splits(N, K);
+    HIPCHK(launch_gemm_tile_bf16(A, W, H->part, M, N, K, *S, st));
+    return COCO_OK;
+  }
   const SkinnyPlan plan = skinny_plan(N, K);
   if (plan.waves == 0) return fail(COCO_EINVAL, "no GEMM plan for N=%d K=%d", N, K);
   *S = plan.S;
@@ -380,8 +391,9 @@ int gemm<bf16_t>(coco_layer* H, const bf16_t* A, const bf16_t* W, int M, int N, 
 }
 
 template <>
-int gemm<float>(coco_layer* H, const float* A, const float* W, int M, int N, int K, int* S,
-                hipStream_t st) {
+int gemm<float>(coco_layer* H, const float* A, const float* W, int M, int N, int K,
+                bool prefill, int* S, hipStream_t st) {
+  (void)prefill;
   *S = 1;
   HIPCHK(launch_gemm_f32(A, W, H->part, M, N, K, st));
   return COCO_OK;
@@ -444,6 +456,7 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
   T* h2 = (T*)H->h2;
   T* u = (T*)H->u;
   int S, rc;
+  const bool pre = seq_starts != nullptr;
 #define TIMED(kind, stmt)                     \
   do {                                        \
     KernelTimer timer_(H, kind, st);          \
@@ -458,7 +471,7 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
                                           d, (const T*)w.gamma_attn, c.rms_eps,
                                           first_l ? x : nullptr, h, st)));
     // QKV projection, RoPE, local cache append.
-    TIMED(COCO_K_GEMM_QKV, if ((rc = gemm<T>(H, h, (const T*)w.w_qkv, M, nqkv, d, &S, st))) return rc);
+    TIMED(COCO_K_GEMM_QKV, if ((rc = gemm<T>(H, h, (const T*)w.w_qkv, M, nqkv, d, pre, &S, st))) return rc);
     TIMED(COCO_K_QKV_EPILOGUE,
           HIPCHK(launch_qkv_epilogue<T>(H->part, S, M, Hq, Hkv, hd, positions, seq_starts,
                                         n_seqs, bt, c.max_blocks_per_seq, H->inv_freq, q,
@@ -470,15 +483,15 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
     // Attention over the paged cache.
     if ((rc = attention<T>(H, w, M, positions, seq_starts, n_seqs, bt, ctx, st))) return rc;
     // O projection + residual + RMSNorm_2.
-    TIMED(COCO_K_GEMM_O, if ((rc = gemm<T>(H, o, (const T*)w.w_o, M, d, Hq * hd, &S, st))) return rc);
+    TIMED(COCO_K_GEMM_O, if ((rc = gemm<T>(H, o, (const T*)w.w_o, M, d, Hq * hd, pre, &S, st))) return rc);
     TIMED(COCO_K_RESIDUAL_NORM,
           HIPCHK(launch_residual_rmsnorm<T>(H->part, S, M, d, x, (const T*)w.gamma_mlp,
                                             c.rms_eps, H->x1, h2, st)));
     // SwiGLU MLP.
     TIMED(COCO_K_GEMM_GATE_UP,
-          if ((rc = gemm<T>(H, h2, (const T*)w.w_gate_up, M, 2 * F, d, &S, st))) return rc);
+          if ((rc = gemm<T>(H, h2, (const T*)w.w_gate_up, M, 2 * F, d, pre, &S, st))) return rc);
     TIMED(COCO_K_SWIGLU, HIPCHK(launch_swiglu<T>(H->part, S, M, F, u, st)));
-    TIMED(COCO_K_GEMM_DOWN, if ((rc = gemm<T>(H, u, (const T*)w.w_down, M, d, F, &S, st))) return rc);
+    TIMED(COCO_K_GEMM_DOWN, if ((rc = gemm<T>(H, u, (const T*)w.w_down, M, d, F, pre, &S, st))) return rc);
     // Residual; the last layer of the segment scatters to the full batch.
     TIMED(COCO_K_RESIDUAL_SCATTER,
           HIPCHK(launch_residual_scatter<T>(H->part, S, M, d, H->x1, last_l ? hidden : x,

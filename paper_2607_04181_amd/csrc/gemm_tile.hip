@@ -1,0 +1,191 @@
+// Large-tile GEMM for prefill-sized row counts (bf16 MFMA, fp32 out).
+//
+//   C[m][n] = sum_k A[m][k] * W[n][k]      A: [M][K], W: [N][K], both bf16
+//
+// Prefill is bound by MFMA throughput, so the kernel is built for reuse:
+//   * a 256-thread workgroup computes a 256 x 256 tile; each of its four
+//     waves owns a 128 x 128 sub-tile as 4 x 4 v_mfma_f32_32x32x16_bf16
+//     accumulators (256 fp32 per lane, held in AGPRs);
+//   * 64-deep K stages of A and W tiles are staged through LDS (2 x 64 KB,
+//     double-buffered) with 16-byte chunks XOR-swizzled by row, so the 32
+//     rows a wave reads per MFMA operand fall in distinct banks; the next
+//     stage's global loads are in flight while the current stage is
+//     multiplied;
+//   * workgroups are remapped so that the tiles sharing a W column slab run
+//     on the same XCD (blockIdx % 8) back to back and hit its L2;
+//   * narrow outputs with a long K are split into K-slices (tile_splits, a
+//     function of (N, K) only) so the grid covers the CUs.
+// Every output element is summed over k in ascending 16-steps within its
+// slice, independent of M and of the tile it falls in, so request-aligned
+// prefill splits give identical bits.
+#include "common.h"
+#include "kernels.h"
+
+namespace coco {
+
+namespace {
+
+constexpr int kTM = 256, kTN = 256, kTK = 64;
+constexpr int kTThreads = 256;
+constexpr int kXCDs = 8;
+
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+// LDS element offset of 16-byte chunk c (0..7) of row r in a [256][64] tile.
+__device__ __forceinline__ int swz(int r, int c) { return r * kTK + ((c ^ (r & 7)) << 3); }
+
+__global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __restrict__ A,
+                                                              const bf16_t* __restrict__ W,
+                                                              float* __restrict__ C, int M, int N,
+                                                              int K, int k_slice) {
+  __shared__ __attribute__((aligned(16))) bf16_t lds[2][2][kTM * kTK];  // [buf][A|W]
+
+  const int tiles_m = (M + kTM - 1) / kTM;
+  const int nb = gridDim.x;
+  const int b = blockIdx.x;
+  // XCD-aware order: the workgroups of one XCD take a contiguous range of
+  // logical tiles, M-fastest, so consecutive ones share the W slab.
+  const int full = (nb / kXCDs) * kXCDs;
+  const int lid = b < full ? (b % kXCDs) * (nb / kXCDs) + b / kXCDs : b;
+  const int m0 = (lid % tiles_m) * kTM;
+  const int n0 = (lid / tiles_m) * kTN;
+  const int kb = blockIdx.y * k_slice;           // this workgroup's K-slice
+  C += (int64_t)blockIdx.y * M * N;             // ... and its partial
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wv = tid >> 6;
+  const int wm = wv & 1, wn = wv >> 1;
+  const int l32 = lane & 31, hi = lane >> 5;
+
+  // Global -> register staging: 8 chunks of A and 8 of W per thread.
+  u32x4_t ra[8], rw[8];
+  const int stages = k_slice / kTK;
+  auto load = [&](int st) {
+    const int k0 = kb + min(st, stages - 1) * kTK;
+#pragma unroll
+    for (int v = 0; v < 8; ++v) {
+      const int q = tid + v * kTThreads;
+      const int r = q >> 3, c = q & 7;
+      const int m = min(m0 + r, M - 1), n = min(n0 + r, N - 1);
+      ra[v] = *(const u32x4_t*)(A + (int64_t)m * K + k0 + c * 8);
+      rw[v] = *(const u32x4_t*)(W + (int64_t)n * K + k0 + c * 8);
+    }
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int v = 0; v < 8; ++v) {
+      const int q = tid + v * kTThreads;
+      const int r = q >> 3, c = q & 7;
+      *(u32x4_t*)(&lds[buf][0][swz(r, c)]) = ra[v];
+      *(u32x4_t*)(&lds[buf][1][swz(r, c)]) = rw[v];
+    }
+  };
+
+  f32x16_t acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  auto read_frags = [&](const bf16_t* la, const bf16_t* lw, int kk, bf16x8_t* a, bf16x8_t* w) {
+    const int c = kk * 2 + hi;  // 16-byte chunk holding k = 16kk + 8hi .. +8
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      a[i] = __builtin_bit_cast(
+          bf16x8_t, *(const u32x4_t*)(&la[swz(wm * 128 + i * 32 + l32, c)]));
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      w[j] = __builtin_bit_cast(
+          bf16x8_t, *(const u32x4_t*)(&lw[swz(wn * 128 + j * 32 + l32, c)]));
+  };
+
+  load(0);
+  store(0);
+  __syncthreads();
+  load(1);
+
+  // Per stage: fragments of k-step kk+1 are read while the 16 MFMAs of kk
+  // run; the next stage's tiles go to the other LDS buffer mid-stage and the
+  // stage after that is fetched right behind them; one barrier per stage.
+  for (int st = 0; st < stages; ++st) {
+    const int buf = st & 1;
+    const bf16_t* la = lds[buf][0];
+    const bf16_t* lw = lds[buf][1];
+    bf16x8_t a[2][4], w[2][4];
+    read_frags(la, lw, 0, a[0], w[0]);
+#pragma unroll
+    for (int kk = 0; kk < kTK / 16; ++kk) {
+      const int cur = kk & 1;
+      if (kk + 1 < kTK / 16) read_frags(la, lw, kk + 1, a[cur ^ 1], w[cur ^ 1]);
+      if (kk == 1) store(buf ^ 1);  // stage st+1 (a clamped copy past the end)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] =
+              __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[cur][i], w[cur][j], acc[i][j], 0, 0, 0);
+      if (kk == 1) load(st + 2);
+      // Interleave: one fragment read between MFMAs, then the stage's LDS
+      // writes and global loads alternated.
+      if (kk + 1 < kTK / 16) {
+        for (int g = 0; g < 8; ++g) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+      }
+      if (kk == 1) {
+        for (int g = 0; g < 16; ++g) {
+          __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // DS write
+          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read
+        }
+      }
+    }
+    __syncthreads();
+  }
+
+  // 32x32 accumulator layout: register 4*jj + r of lane l holds row
+  // 8*jj + 4*(l/32) + r, column l%32.
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n = n0 + wn * 128 + j * 32 + l32;
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = m0 + wm * 128 + i * 32 + 8 * jj + 4 * hi + r;
+          if (m < M && n < N) C[(int64_t)m * N + n] = acc[i][j][4 * jj + r];
+        }
+    }
+}
+
+}  // namespace
+
+// K-slices from (N, K) alone: narrow outputs (few 256-column tiles) with a
+// long K are split into ~8k-deep slices so the grid covers the CUs; the
+// partials are summed in slice order by the consumer.
+int tile_splits(int N, int K) {
+  const int tiles_n = (N + kTN - 1) / kTN;
+  if (tiles_n >= 48) return 1;
+  int S = (K + 4096) / 8192;
+  if (S < 1) S = 1;
+  if (S > 4) S = 4;
+  while (S > 1 && (K / kTK) % S != 0) --S;
+  return S;  // 1..4: the split counts the epilogues are built for
+}
+
+hipError_t launch_gemm_tile_bf16(const uint16_t* A, const uint16_t* W, float* C, int M, int N,
+                                 int K, int S, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  if (S < 1 || K % (kTK * S) != 0) return hipErrorInvalidValue;
+  const int tiles = ((M + kTM - 1) / kTM) * ((N + kTN - 1) / kTN);
+  hipLaunchKernelGGL(gemm_tile_kernel, dim3(tiles, S), dim3(kTThreads), 0, st, A, W, C, M, N, K,
+                     K / S);
+  return hipGetLastError();
+}
+
+}  // namespace coco

@@ -59,6 +59,13 @@ SkinnyPlan skinny_plan(int N, int K);
 hipError_t launch_gemm_skinny_bf16(const uint16_t* A, const uint16_t* W, float* part, int M,
                                    int N, int K, SkinnyPlan plan, hipStream_t st);
 
+// part[s][m][n] = sum_{k in slice s} A[m][k] * W[n][k] with 256 x 256 MFMA
+// tiles (prefill; K a multiple of 64 * S). S = tile_splits(N, K); the k
+// order is fixed and M-independent.
+int tile_splits(int N, int K);
+hipError_t launch_gemm_tile_bf16(const uint16_t* A, const uint16_t* W, float* C, int M, int N,
+                                 int K, int S, hipStream_t st);
+
 // part[0][m][n] = sum_k A[m][k] * W[n][k], fp32 (tiny fp32 configurations).
 hipError_t launch_gemm_f32(const float* A, const float* W, float* part, int M, int N, int K,
                            hipStream_t st);

@@ -205,6 +205,7 @@ __global__ __launch_bounds__(kWave) void qkv_epilogue_kernel(
   switch (S) {                                       \
     case 1: { constexpr int S_ = 1; __VA_ARGS__; } break;  \
     case 2: { constexpr int S_ = 2; __VA_ARGS__; } break;  \
+    case 3: { constexpr int S_ = 3; __VA_ARGS__; } break;  \
     case 4: { constexpr int S_ = 4; __VA_ARGS__; } break;  \
     case 8: { constexpr int S_ = 8; __VA_ARGS__; } break;  \
     case 16: { constexpr int S_ = 16; __VA_ARGS__; } break; \
