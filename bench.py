@@ -35,6 +35,9 @@ def parse():
                    choices=["c2", "c3", "c3full", "c4p", "c4d", "c5"])
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="target duration of the oracle CPU baseline (0 = skip)")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="only time a plain 1 GiB device copy (the reference kernel that "
+                        "scales the FETCH_SIZE / WRITE_SIZE counters to bytes)")
     return p.parse_args()
 
 
@@ -42,12 +45,41 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def kernel_source_sha(files):
+def kernel_source_sha():
+    """Digest of every kernel source: a counter summary is only valid for the
+    sources it was taken with."""
+    csrc = os.path.join(ROOT, "paper_2607_04181_amd", "csrc")
     h = hashlib.sha256()
-    for f in files:
-        with open(os.path.join(ROOT, "paper_2607_04181_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".h")):
+            with open(os.path.join(csrc, f), "rb") as fh:
+                h.update(f.encode() + b"\0" + fh.read())
     return h.hexdigest()[:16]
+
+
+def copy_calibration():
+    """A 1 GiB device-to-device copy (torch's copy kernel): 1 GiB read and
+    1 GiB written per launch, the known size the HBM counters are scaled by;
+    also the practical copy bandwidth of the part."""
+    import torch
+    n = 1 << 28  # float32 elements: 1 GiB
+    x = torch.empty(n, device="cuda")
+    x.normal_()
+    y = torch.empty_like(x)
+    for _ in range(3):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 20
+    e0.record()
+    for _ in range(reps):
+        y.copy_(x)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n,
+                      "us_per_copy": round(ms * 1e3, 1),
+                      "GBps_read_plus_write": round(8 * n / (ms * 1e-3) / 1e9, 1)}), flush=True)
 
 
 def load_traffic(kernel_kind, workload_name, src_sha):
@@ -98,6 +130,10 @@ def main():
                           "multi-GPU sharding of the row subsets is described in DESIGN.md "
                           "and not run", "n_gpus": args.gpus}))
         sys.exit(2)
+
+    if args.copy_calibration:
+        copy_calibration()
+        return
 
     import numpy as np
     import torch
@@ -200,7 +236,7 @@ def main():
     cand = [r for r in rows if r[0] in alg_bytes]
     dom, dom_avg, dom_n, _ = cand[0]
     bound = "hbm" if is_decode else "mfma"
-    src_sha = kernel_source_sha(["gemm_skinny.hip", "attention.hip", "rows.hip", "common.h"])
+    src_sha = kernel_source_sha()
     if bound == "hbm":
         achieved = alg_bytes[dom] / (dom_avg * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,

@@ -110,11 +110,37 @@ __device__ __forceinline__ float column_sum(float l) {
 // ceil(ctx / 256)) were written by the QKV epilogue. Eight waves take two
 // blocks each of the 256-token partition; each wave scores both blocks
 // first, takes one column max and then accumulates exp * V against it, and
-// the eight wave results are merged in LDS in wave order.
+// the eight wave results are merged in LDS in wave order. As soon as a
+// wave's key/value registers are consumed it issues the loads of its next
+// work item, so the LDS merge and the partial stores overlap the next
+// item's HBM reads.
 constexpr int kDecWaves = 8;
 constexpr int kDecBPW = kDecodeSplit / kBlockTokens / kDecWaves;
 
-__global__ __launch_bounds__(kDecWaves * 64) void attn_decode_kernel(
+struct DecItem {
+  int s, g, sp, t1, b_first, b_last;
+};
+
+__device__ __forceinline__ DecItem decode_item(int w, int Hkv, const int32_t* split_off,
+                                               const int32_t* ctx_lens, int n_seqs) {
+  DecItem it;
+  const int item = w / Hkv;
+  it.g = w - item * Hkv;
+  int lo = 0, hi = n_seqs - 1;  // the s with split_off[s] <= item < split_off[s + 1]
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (split_off[mid] <= item) lo = mid; else hi = mid - 1;
+  }
+  it.s = lo;
+  it.sp = item - split_off[lo];
+  const int t0 = it.sp * kDecodeSplit;
+  it.t1 = min(ctx_lens[lo], t0 + kDecodeSplit);
+  it.b_first = t0 / kBlockTokens;
+  it.b_last = (it.t1 - 1) / kBlockTokens;
+  return it;
+}
+
+__global__ __launch_bounds__(kDecWaves * 64, 4) void attn_decode_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k_cache,
     const bf16_t* __restrict__ v_cache, const int32_t* __restrict__ block_table, int max_blocks,
     const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ split_off, int n_seqs,
@@ -125,53 +151,54 @@ __global__ __launch_bounds__(kDecWaves * 64) void attn_decode_kernel(
 
   const int total = split_off[n_seqs] * Hkv;
   const int G = Hq / Hkv;
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  // Wave index as a uniform value: block-table reads then go through the
+  // scalar cache and do not wait behind the key/value loads in flight.
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int c16 = lane & 15, j4 = lane >> 4;
   const int64_t tile = (int64_t)kBlockTokens * HD;
+  const int cq = c16 < G ? c16 : G - 1;  // padded columns read a real head
 
-  for (int w = blockIdx.x; w < total; w += gridDim.x) {
-    const int item = w / Hkv, g = w - item * Hkv;
-    int lo = 0, hi = n_seqs - 1;  // the s with split_off[s] <= item < split_off[s + 1]
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (split_off[mid] <= item) lo = mid; else hi = mid - 1;
-    }
-    const int s = lo, sp = item - split_off[s];
-    const int ctx = ctx_lens[s];
-    const int t0 = sp * kDecodeSplit;
-    const int t1 = min(ctx, t0 + kDecodeSplit);
-
-    bf16x8_t qf[4];
-    {
-      const int cq = c16 < G ? c16 : G - 1;  // padded columns read a real head, then zero
-      const bf16_t* qp = q + ((int64_t)s * Hq + g * G + cq) * HD + j4 * 8;
+  u32x4_t kf[kDecBPW][4];
+  u32x2_t vf[kDecBPW][8];
+  u32x4_t qr[4];
+  // Query first: the first MFMA needs it, and loads complete in issue order.
+  auto issue = [&](const DecItem& it) {
+    const bf16_t* qp = q + ((int64_t)it.s * Hq + it.g * G + cq) * HD + j4 * 8;
 #pragma unroll
-      for (int t = 0; t < 4; ++t)
-        qf[t] = (c16 < G) ? __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(qp + t * 32))
-                          : __builtin_bit_cast(bf16x8_t, u32x4_t{0u, 0u, 0u, 0u});
-    }
-    const int b_first = t0 / kBlockTokens, b_last = (t1 - 1) / kBlockTokens;
-    const int32_t* bt = block_table + (int64_t)s * max_blocks;
-
-    u32x4_t kf[kDecBPW][4];
-    u32x2_t vf[kDecBPW][8];
+    for (int t = 0; t < 4; ++t) qr[t] = *(const u32x4_t*)(qp + t * 32);
+    // Unconditional (blocks past the partition re-read its last block, an
+    // L2 hit that is then ignored), so that the waits before each MFMA can
+    // count exactly the loads still in flight behind the ones it needs.
+    const int32_t* bt = block_table + (int64_t)it.s * max_blocks;
 #pragma unroll
     for (int u = 0; u < kDecBPW; ++u) {
-      const int b = b_first + wv + kDecWaves * u;
-      if (b <= b_last) {
-        const int64_t pb = bt[b];
-        load_kv(k_cache + (pb * Hkv + g) * tile, v_cache + (pb * Hkv + g) * tile, c16, j4, kf[u],
-                vf[u]);
-      }
+      const int b = min(it.b_first + wv + kDecWaves * u, it.b_last);
+      const int64_t pb = bt[b];
+      load_kv(k_cache + (pb * Hkv + it.g) * tile, v_cache + (pb * Hkv + it.g) * tile, c16, j4,
+              kf[u], vf[u]);
     }
+  };
+
+  int w = blockIdx.x;
+  DecItem cur{};
+  if (w < total) {
+    cur = decode_item(w, Hkv, split_off, ctx_lens, n_seqs);
+    issue(cur);
+  }
+  for (; w < total; w += gridDim.x) {
+    // Columns c16 >= G repeat head G-1; their results are never stored.
+    bf16x8_t qf[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) qf[t] = __builtin_bit_cast(bf16x8_t, qr[t]);
     // Pass 1: scores of all of the wave's blocks, one column max.
     float sc[kDecBPW][4];
     float m = -INFINITY;
 #pragma unroll
     for (int u = 0; u < kDecBPW; ++u) {
-      const int b = b_first + wv + kDecWaves * u;
+      const int b = cur.b_first + wv + kDecWaves * u;
       f32x4_t a = {0.f, 0.f, 0.f, 0.f};
-      if (b <= b_last) {
+      if (b <= cur.b_last) {
 #pragma unroll
         for (int t = 0; t < 4; ++t)
           a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kf[u][t]),
@@ -180,7 +207,7 @@ __global__ __launch_bounds__(kDecWaves * 64) void attn_decode_kernel(
       const int tok0 = b * kBlockTokens + j4 * 4;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        sc[u][r] = (b <= b_last && tok0 + r < t1) ? a[r] * scale_log2 : -INFINITY;
+        sc[u][r] = (b <= cur.b_last && tok0 + r < cur.t1) ? a[r] * scale_log2 : -INFINITY;
         m = fmaxf(m, sc[u][r]);
       }
     }
@@ -195,8 +222,8 @@ __global__ __launch_bounds__(kDecWaves * 64) void attn_decode_kernel(
     for (int n = 0; n < 8; ++n) o[n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int u = 0; u < kDecBPW; ++u) {
-      const int b = b_first + wv + kDecWaves * u;
-      if (b <= b_last) {
+      const int b = cur.b_first + wv + kDecWaves * u;
+      if (b <= cur.b_last) {
         float p[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) p[r] = exp2f(sc[u][r] - mref);
@@ -218,6 +245,11 @@ __global__ __launch_bounds__(kDecWaves * 64) void attn_decode_kernel(
     for (int n = 0; n < 8; ++n)
 #pragma unroll
       for (int r = 0; r < 4; ++r) sm_o[wv][c16][n * 16 + j4 * 4 + r] = o[n][r];
+    // The registers are free: start the next item's reads now (past the
+    // last item, a repeat of the last one that is never used).
+    const DecItem it = cur;
+    cur = decode_item(min(w + (int)gridDim.x, total - 1), Hkv, split_off, ctx_lens, n_seqs);
+    issue(cur);
     __syncthreads();
 
     for (int e = threadIdx.x; e < G * HD; e += kDecWaves * 64) {
@@ -232,7 +264,7 @@ __global__ __launch_bounds__(kDecWaves * 64) void attn_decode_kernel(
         acc += f * sm_o[v][col][dim];
         L += f * sm_l[v][col];
       }
-      const int64_t idx = ((int64_t)s * Hq + g * G + col) * max_splits + sp;
+      const int64_t idx = ((int64_t)it.s * Hq + it.g * G + col) * max_splits + it.sp;
       part_o[idx * HD + dim] = acc;
       if (dim == 0) {
         part_ml[idx * 2 + 0] = mx;
@@ -425,9 +457,14 @@ hipError_t launch_attn_decode_bf16(const uint16_t* q, const uint16_t* k_cache,
                                    hipStream_t st) {
   if (n_seqs <= 0) return hipSuccess;
   const float scale_log2 = kLog2e / sqrtf((float)HD);
-  // Two resident workgroups per CU (LDS bound); the grid never exceeds the work.
+  // Two resident workgroups per CU (at most 128 registers per lane and 68 KB
+  // of LDS each): a persistent grid of two per CU, never more than the work.
+  int dev = 0, cus = 256;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return hipErrorInvalidDevice;
   const int64_t work_bound = (int64_t)n_seqs * max_splits * Hkv;
-  const int grid = (int)(work_bound < 512 ? work_bound : 512);
+  const int grid = (int)(work_bound < 2 * cus ? work_bound : 2 * cus);
   hipLaunchKernelGGL(attn_decode_kernel, dim3(grid), dim3(kDecWaves * 64), 0, st, q, k_cache,
                      v_cache, block_table, max_blocks, ctx_lens, split_off, n_seqs, Hq, Hkv,
                      part_o, part_ml, max_splits, scale_log2);

@@ -8,8 +8,8 @@
 //   * a workgroup of WAVES waves owns 16*WAVES output columns and one K-slice;
 //     each wave streams the 16 weight rows of its columns straight into VGPRs
 //     (16-byte loads, 64 contiguous bytes per row per instruction; plain
-//     loads measured faster here than non-temporal ones), keeping PF stages
-//     of 128 k in flight;
+//     loads measured faster here than non-temporal ones), keeping two
+//     stages of 128 k in flight;
 //   * the activation tile [rows][128 k] of a stage is shared by the waves
 //     through LDS (double-buffered, rows padded by 16 bytes so the 16 rows a
 //     wave reads per instruction fall in distinct banks);
@@ -140,9 +140,10 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
 template <int WAVES, int MT>
 hipError_t launch_plan(const uint16_t* A, const uint16_t* W, float* part, int M, int N, int K,
                        int S, hipStream_t st) {
-  // 128-row tiles hold twice the accumulators: a 2-stage weight ring keeps
-  // them out of scratch (two workgroups per CU still keep ~64 KB in flight).
-  constexpr int PF = MT == 4 ? 4 : 2;
+  // Two stages of weights in flight per wave (~56 KB per CU at 7 waves) is
+  // enough to cover HBM latency; deeper rings measured slower (more requests
+  // queued behind each other) and cost registers.
+  constexpr int PF = 2;
   hipLaunchKernelGGL((gemm_skinny_kernel<WAVES, MT, PF>), dim3(N / (16 * WAVES), S),
                      dim3(WAVES * 64), 0, st, A, W, part, M, N, K, K / S);
   return hipGetLastError();
