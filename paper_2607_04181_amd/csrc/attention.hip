@@ -4,10 +4,12 @@
 // of 16 tokens x hd in MFMA operand order (k_tile_offset / v_tile_offset).
 //
 // MFMA dataflow (bf16, hd = 128), shared by decode and prefill. A wave owns 16
-// "query columns" and walks the key blocks of one key/value head:
+// "query columns" per column tile and walks the key blocks of one key/value
+// head:
 //   S^T[16 tok][16 col] = K_blk[16][hd] . Q^T[hd][16]   4 x mfma 16x16x32
 //   online softmax per column (column max/sum over the 4 lanes of a column)
-//   O^T[hd][16 col]    += V^T_blk[hd][16] . P^T[16][16] 8 x mfma 16x16x16
+//   O^T[hd][16 col]    += V^T_blk[hd][16] . P^T[16][16] 8 x mfma 16x16x16,
+//                         or 8 x mfma 16x16x32 per pair of blocks
 // With S^T the probabilities come out of the first MFMA already in the
 // B-operand layout of the second, and O^T keeps a column's rescale factor in
 // the lane that computed it: no cross-lane shuffles besides the column
@@ -15,13 +17,14 @@
 // contiguous 1 KB wave load.
 //
 // Decode: the columns are the G = Hq/Hkv query heads of one token (padded to
-// 16). A workgroup handles (sequence, kv head, 256-token partition); its four
-// waves take interleaved blocks (issuing all their loads first) and merge in
-// LDS in wave order; partitions are merged by a second kernel in partition
-// order. Partitions depend only on
-// the sequence's own length, so results are independent of the batch.
+// 16). A workgroup handles (sequence, kv head, 256-token partition); its
+// eight waves take interleaved blocks and merge in LDS in wave order;
+// partitions are merged by a second kernel in partition order. Partitions
+// depend only on the sequence's own length, so results are independent of
+// the batch.
 // Prefill: the columns are 16 query tokens of one head, masked causally by
-// absolute position.
+// absolute position; key/value tiles are shared by the workgroup's waves
+// through LDS.
 #include <math.h>
 
 #include "common.h"
@@ -32,55 +35,7 @@ namespace coco {
 namespace {
 
 constexpr int HD = 128;
-constexpr int kAttnThreads = 256;
 constexpr float kLog2e = 1.4426950408889634f;
-
-struct WaveState {
-  float m;        // running column max (log2 domain)
-  float l;        // this lane's share of the running column sum
-  f32x4_t o[8];   // O^T tiles: rows hd = 16n + 4*j4 + r, column c16
-};
-
-__device__ __forceinline__ void wave_state_init(WaveState& ws) {
-  ws.m = -INFINITY;
-  ws.l = 0.f;
-#pragma unroll
-  for (int n = 0; n < 8; ++n) ws.o[n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-}
-
-// One 16-token key block. `valid(r)` says whether token 4*j4+r of the block is
-// visible to this lane's column.
-template <typename Valid>
-__device__ __forceinline__ void attend_block(WaveState& ws, const u32x4_t kf[4],
-                                             const u32x2_t vf[8], const bf16x8_t qf[4],
-                                             float scale_log2, Valid valid) {
-  f32x4_t s = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int t = 0; t < 4; ++t)
-    s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kf[t]), qf[t], s,
-                                                0, 0, 0);
-  float sc[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) sc[r] = valid(r) ? s[r] * scale_log2 : -INFINITY;
-  float mb = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
-  mb = fmaxf(mb, __shfl_xor(mb, 16, kWave));
-  mb = fmaxf(mb, __shfl_xor(mb, 32, kWave));
-  const float m_new = fmaxf(ws.m, mb);
-  const float alpha = exp2f(ws.m - m_new);
-  float p[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) p[r] = exp2f(sc[r] - m_new);
-  ws.l = ws.l * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
-  ws.m = m_new;
-  const uint32_t p01 = pack_bf16x2(p[0], p[1]), p23 = pack_bf16x2(p[2], p[3]);
-  const s16x4_t pf = __builtin_bit_cast(s16x4_t, u32x2_t{p01, p23});
-#pragma unroll
-  for (int n = 0; n < 8; ++n) {
-    ws.o[n] = ws.o[n] * alpha;
-    ws.o[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4_t, vf[n]), pf,
-                                                        ws.o[n], 0, 0, 0);
-  }
-}
 
 // One (block, kv head) tile: four contiguous 1 KB loads each for K and V,
 // non-temporal (each tile is read once per step).
@@ -96,12 +51,6 @@ __device__ __forceinline__ void load_kv(const bf16_t* kb, const bf16_t* vb, int 
     vf[2 * p] = u32x2_t{v.x, v.y};
     vf[2 * p + 1] = u32x2_t{v.z, v.w};
   }
-}
-
-// Column sum of this lane's share: lanes c16, c16+16, c16+32, c16+48.
-__device__ __forceinline__ float column_sum(float l) {
-  l = l + __shfl_xor(l, 16, kWave);
-  return l + __shfl_xor(l, 32, kWave);
 }
 
 // ---------------------------------------------------------------- decode
@@ -211,8 +160,7 @@ __global__ __launch_bounds__(kDecWaves * 64, 4) void attn_decode_kernel(
         m = fmaxf(m, sc[u][r]);
       }
     }
-    m = fmaxf(m, __shfl_xor(m, 16, kWave));
-    m = fmaxf(m, __shfl_xor(m, 32, kWave));
+    m = col_max4(m);
     // Pass 2: probabilities against the fixed max, O^T += V^T P^T. A wave
     // with no block keeps m = -inf and contributes nothing.
     const float mref = m == -INFINITY ? 0.f : m;
@@ -236,7 +184,7 @@ __global__ __launch_bounds__(kDecWaves * 64, 4) void attn_decode_kernel(
                                                            pf, o[n], 0, 0, 0);
       }
     }
-    const float l_col = column_sum(l);
+    const float l_col = col_sum4(l);
     if (j4 == 0) {
       sm_m[wv][c16] = m;
       sm_l[wv][c16] = l_col;
@@ -318,75 +266,234 @@ __global__ __launch_bounds__(HD) void attn_combine_kernel(const float* __restric
 }
 
 // ---------------------------------------------------------------- prefill
-// Workgroup = (sequence, 64-row tile of its call rows, query head); wave w
-// takes rows 16w..16w+15 of the tile as its columns.
-__global__ __launch_bounds__(kAttnThreads) void attn_prefill_kernel(
+// Workgroup = (sequence, 128-row query tile, query head). Workgroups are
+// remapped so that the query heads of one tile run back to back on one XCD
+// (blockIdx % 8) and share its L2 for the key/value tiles of their group.
+// Wave w takes rows 32w..32w+31 of the tile as two 16-column tiles. The
+// key/value tiles are staged through LDS four blocks (64 keys) at a time by
+// direct global->LDS loads (each wave fetches one block's K and V tiles as
+// eight contiguous 1 KB pieces), double-buffered with one barrier per stage.
+// Per stage a wave scores the 64 keys (S^T = K Q^T), updates its online
+// softmax once, and accumulates O^T += V^T P^T in 32-key MFMA steps: the
+// V^T fragments of two blocks side by side against P^T packed to match (any
+// fixed assignment of keys to MFMA k-slots gives the same sum).
+constexpr int kPfWaves = 4;
+constexpr int kPfRows = kPfWaves * 32;  // query rows per workgroup
+constexpr int kPfBlk = 4;               // key blocks per stage (one per wave)
+constexpr int kTileElems = kBlockTokens * HD;
+constexpr int kXCDs = 8;
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+__global__ __launch_bounds__(kPfWaves * 64, 2) void attn_prefill_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k_cache,
     const bf16_t* __restrict__ v_cache, const int32_t* __restrict__ block_table, int max_blocks,
     const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ positions,
     const int32_t* __restrict__ seq_starts, int n_seqs, int Hq, int Hkv, float scale_log2,
     bf16_t* __restrict__ o) {
-  // Find (sequence, tile) of this workgroup.
-  int tile = blockIdx.x, s = 0;
+  __shared__ __attribute__((aligned(16))) bf16_t kv[2][2][kPfBlk][kTileElems];  // [buf][K|V][blk]
+
+  // Work unit = (tile, kv head) with its G query heads. Units go round-robin
+  // over the XCDs (blockIdx % 8 is the XCD) and a unit's G workgroups run
+  // back to back on its XCD, sharing the group's key/value tiles in that L2.
+  // Tiles are taken last-first: later tiles of a sequence see more keys, so
+  // the long workgroups start early.
+  const int G = Hq / Hkv;
+  const int n_tiles = gridDim.x / Hq;
+  int unit, hg;
+  if ((n_tiles * Hkv) % kXCDs == 0) {
+    const int x = blockIdx.x % kXCDs, k = blockIdx.x / kXCDs;
+    unit = x + kXCDs * (k / G);
+    hg = k % G;
+  } else {
+    unit = blockIdx.x / G;
+    hg = blockIdx.x % G;
+  }
+  int tile = n_tiles - 1 - unit / Hkv;
+  const int g = unit % Hkv;
+  const int h = g * G + hg;
+  int s = 0;
   for (; s < n_seqs; ++s) {
-    const int nt = (seq_starts[s + 1] - seq_starts[s] + 63) / 64;
+    const int nt = (seq_starts[s + 1] - seq_starts[s] + kPfRows - 1) / kPfRows;
     if (tile < nt) break;
     tile -= nt;
   }
-  if (s >= n_seqs) return;
-  const int h = blockIdx.y;
-  const int g = h / (Hq / Hkv);
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  if (s >= n_seqs) return;  // past the last tile: the whole workgroup leaves
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int c16 = lane & 15, j4 = lane >> 4;
-  const int row_end = seq_starts[s + 1];
-  const int row0 = seq_starts[s] + tile * 64 + wv * 16;
-  if (row0 >= row_end) return;
-  const int last_row = min(row_end, row0 + 16) - 1;
-  const int row = row0 + c16;
-  const bool valid_col = row <= last_row;
-  const int pos = positions[valid_col ? row : last_row];
-  const int kmax = min(ctx_lens[s] - 1, positions[last_row]);
-
-  bf16x8_t qf[4];
-  {
-    const bf16_t* qp = q + ((int64_t)(valid_col ? row : last_row) * Hq + h) * HD + j4 * 8;
-#pragma unroll
-    for (int t = 0; t < 4; ++t) qf[t] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(qp + t * 32));
-  }
-
-  WaveState ws;
-  wave_state_init(ws);
+  const int row_begin = seq_starts[s] + tile * kPfRows;
+  const int row_end = min(seq_starts[s + 1], row_begin + kPfRows);
+  // Rows are in position order: the tile's last row sees the most keys.
+  const int kmax = min(ctx_lens[s] - 1, positions[row_end - 1]);
+  const int n_blk = kmax / kBlockTokens + 1;
+  const int stages = (n_blk + kPfBlk - 1) / kPfBlk;
   const int32_t* bt = block_table + (int64_t)s * max_blocks;
-  const int64_t head_stride = (int64_t)kBlockTokens * HD;
-  const int b_last = kmax / kBlockTokens;
-  u32x4_t kf[4], kn[4];
-  u32x2_t vf[8], vn[8];
-  {
-    const int64_t pb = bt[0];
-    load_kv(k_cache + (pb * Hkv + g) * head_stride, v_cache + (pb * Hkv + g) * head_stride, c16,
-            j4, kf, vf);
+
+  // This wave's two column tiles; padded columns repeat the tile's last row
+  // and are never stored.
+  const int w_row0 = row_begin + wv * 32;
+  const int w_kmax = w_row0 < row_end ? positions[min(row_end, w_row0 + 32) - 1] : -1;
+  // Stages whose keys all precede the wave's first row need no causal mask.
+  const int w_kmin = w_row0 < row_end ? positions[w_row0] : -1;
+  int pos[2];
+  bf16x8_t qf[2][4];
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    const int row = min(w_row0 + 16 * c + c16, row_end - 1);
+    pos[c] = positions[row];
+    const bf16_t* qp = q + ((int64_t)row * Hq + h) * HD + j4 * 8;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      qf[c][t] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(qp + t * 32));
   }
-  for (int b = 0; b <= b_last; ++b) {
-    if (b + 1 <= b_last) {
-      const int64_t pn = bt[b + 1];
-      load_kv(k_cache + (pn * Hkv + g) * head_stride, v_cache + (pn * Hkv + g) * head_stride,
-              c16, j4, kn, vn);
+
+  // Wave wv stages block st*4 + wv (clamped to the last block: a repeat that
+  // the causal mask hides) into LDS.
+  auto issue = [&](int st, int buf) {
+    const int blk = min(st * kPfBlk + wv, n_blk - 1);
+    const int64_t tile_off = ((int64_t)bt[blk] * Hkv + g) * kTileElems + lane * 8;
+#pragma unroll
+    for (int pc = 0; pc < 4; ++pc) {
+      __builtin_amdgcn_global_load_lds(k_cache + tile_off + pc * 512,
+                                       (lds_void_t*)&kv[buf][0][wv][pc * 512], 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(v_cache + tile_off + pc * 512,
+                                       (lds_void_t*)&kv[buf][1][wv][pc * 512], 16, 0, 0);
     }
-    const int tok0 = b * kBlockTokens + j4 * 4;
-    attend_block(ws, kf, vf, qf, scale_log2, [&](int r) { return tok0 + r <= pos; });
+  };
+
+  float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.f, 0.f};
+  f32x4_t acc[2][8];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) kf[t] = kn[t];
+  for (int c = 0; c < 2; ++c)
 #pragma unroll
-    for (int n = 0; n < 8; ++n) vf[n] = vn[n];
+    for (int n = 0; n < 8; ++n) acc[c][n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  issue(0, 0);
+  __syncthreads();
+  for (int st = 0; st < stages; ++st) {
+    const int buf = st & 1;
+    if (st + 1 < stages) issue(st + 1, buf ^ 1);
+    if (st * kPfBlk * kBlockTokens <= w_kmax) {
+      const bf16_t* kl = &kv[buf][0][0][lane * 8];
+      const bf16_t* vl = &kv[buf][1][0][lane * 8];
+      // Scores of the stage's 4 blocks for both column tiles; the next
+      // block's K fragments are read while the current block's MFMAs run.
+      f32x4_t sc[2][kPfBlk];
+      u32x4_t kfr[2][4];
+#pragma unroll
+      for (int pc = 0; pc < 4; ++pc) kfr[0][pc] = *(const u32x4_t*)(kl + pc * 512);
+#pragma unroll
+      for (int i = 0; i < kPfBlk; ++i) {
+        if (i + 1 < kPfBlk) {
+#pragma unroll
+          for (int pc = 0; pc < 4; ++pc)
+            kfr[(i + 1) & 1][pc] = *(const u32x4_t*)(kl + (i + 1) * kTileElems + pc * 512);
+        }
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          f32x4_t a = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int pc = 0; pc < 4; ++pc)
+            a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8_t, kfr[i & 1][pc]), qf[c][pc], a, 0, 0, 0);
+          sc[c][i] = a;
+        }
+      }
+      const bool unmasked = (st + 1) * kPfBlk * kBlockTokens - 1 <= w_kmin;
+      // V fragments of the first block pair are read during the softmax.
+      u32x4_t vfr[2][4];
+#pragma unroll
+      for (int pc = 0; pc < 4; ++pc) {
+        vfr[0][pc] = *(const u32x4_t*)(vl + pc * 512);
+        vfr[1][pc] = *(const u32x4_t*)(vl + kTileElems + pc * 512);
+      }
+      // Online softmax, once per 64 keys (log2 domain: p = 2^(s*scale - m)),
+      // P^T packed as two 32-key operands.
+      u32x4_t pk[2][2];
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        float mx = -INFINITY;
+        if (unmasked) {
+#pragma unroll
+          for (int i = 0; i < kPfBlk; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sc[c][i][r]);
+        } else {
+#pragma unroll
+          for (int i = 0; i < kPfBlk; ++i) {
+            const int tok0 = (st * kPfBlk + i) * kBlockTokens + j4 * 4;
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (tok0 + r <= pos[c]) mx = fmaxf(mx, sc[c][i][r]);
+          }
+        }
+        mx = col_max4(mx) * scale_log2;
+        const float m_new = fmaxf(m[c], mx);  // finite: stage 0 always holds key 0
+        const float alpha = __builtin_amdgcn_exp2f(m[c] - m_new);
+        float ps = 0.f;
+        uint32_t pw[kPfBlk][2];
+#pragma unroll
+        for (int i = 0; i < kPfBlk; ++i) {
+          const int tok0 = (st * kPfBlk + i) * kBlockTokens + j4 * 4;
+          float pr[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float e = __builtin_amdgcn_exp2f(fmaf(sc[c][i][r], scale_log2, -m_new));
+            pr[r] = unmasked || tok0 + r <= pos[c] ? e : 0.f;
+          }
+          ps += (pr[0] + pr[1]) + (pr[2] + pr[3]);
+          pw[i][0] = pack_bf16x2(pr[0], pr[1]);
+          pw[i][1] = pack_bf16x2(pr[2], pr[3]);
+        }
+        l[c] = l[c] * alpha + ps;
+        m[c] = m_new;
+#pragma unroll
+        for (int n = 0; n < 8; ++n) acc[c][n] = acc[c][n] * alpha;
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp)
+          pk[c][pp] = u32x4_t{pw[2 * pp][0], pw[2 * pp][1], pw[2 * pp + 1][0], pw[2 * pp + 1][1]};
+      }
+      // O^T += V^T P^T over the two block pairs.
+#pragma unroll
+      for (int pp = 0; pp < 2; ++pp) {
+        if (pp == 1) {
+#pragma unroll
+          for (int pc = 0; pc < 4; ++pc) {
+            vfr[0][pc] = *(const u32x4_t*)(vl + 2 * kTileElems + pc * 512);
+            vfr[1][pc] = *(const u32x4_t*)(vl + 3 * kTileElems + pc * 512);
+          }
+        }
+#pragma unroll
+        for (int pc = 0; pc < 4; ++pc) {
+          const u32x4_t v0 = vfr[0][pc], v1 = vfr[1][pc];
+          const bf16x8_t va = __builtin_bit_cast(bf16x8_t, u32x4_t{v0.x, v0.y, v1.x, v1.y});
+          const bf16x8_t vb = __builtin_bit_cast(bf16x8_t, u32x4_t{v0.z, v0.w, v1.z, v1.w});
+#pragma unroll
+          for (int c = 0; c < 2; ++c) {
+            const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, pk[c][pp]);
+            acc[c][2 * pc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb, acc[c][2 * pc], 0, 0, 0);
+            acc[c][2 * pc + 1] =
+                __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb, pb, acc[c][2 * pc + 1], 0, 0, 0);
+          }
+        }
+      }
+    }
+    __syncthreads();  // stage st+1 landed; buffer st is free for stage st+2
   }
-  const float inv = 1.0f / column_sum(ws.l);
-  if (valid_col) {
-    bf16_t* op = o + ((int64_t)row * Hq + h) * HD;
+
 #pragma unroll
-    for (int n = 0; n < 8; ++n) {
-      const uint32_t lo = pack_bf16x2(ws.o[n][0] * inv, ws.o[n][1] * inv);
-      const uint32_t hi = pack_bf16x2(ws.o[n][2] * inv, ws.o[n][3] * inv);
-      *(u32x2_t*)(op + n * 16 + j4 * 4) = u32x2_t{lo, hi};
+  for (int c = 0; c < 2; ++c) {
+    const int row = w_row0 + 16 * c + c16;
+    const float inv = 1.0f / col_sum4(l[c]);
+    if (row < row_end) {
+      bf16_t* op = o + ((int64_t)row * Hq + h) * HD;
+#pragma unroll
+      for (int n = 0; n < 8; ++n) {
+        const uint32_t lo = pack_bf16x2(acc[c][n][0] * inv, acc[c][n][1] * inv);
+        const uint32_t hi = pack_bf16x2(acc[c][n][2] * inv, acc[c][n][3] * inv);
+        *(u32x2_t*)(op + n * 16 + j4 * 4) = u32x2_t{lo, hi};
+      }
     }
   }
 }
@@ -489,8 +596,11 @@ hipError_t launch_attn_prefill_bf16(const uint16_t* q, const uint16_t* k_cache,
                                     hipStream_t st) {
   if (n_rows <= 0) return hipSuccess;
   const float scale_log2 = kLog2e / sqrtf((float)HD);
-  const int tiles = (n_rows + 63) / 64 + n_seqs;  // upper bound on per-sequence tiles
-  hipLaunchKernelGGL(attn_prefill_kernel, dim3(tiles, Hq), dim3(kAttnThreads), 0, st, q,
+  // Upper bound on the per-sequence 128-row tiles; workgroups past the last
+  // tile return at once.
+  const int64_t tiles = (n_rows + kPfRows - 1) / kPfRows + n_seqs;
+  if (tiles * Hq > 0x7fffffff) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(attn_prefill_kernel, dim3((unsigned)(tiles * Hq)), dim3(kPfWaves * 64), 0, st, q,
                      k_cache, v_cache, block_table, max_blocks, ctx_lens, positions, seq_starts,
                      n_seqs, Hq, Hkv, scale_log2, o);
   return hipGetLastError();
