@@ -3,6 +3,7 @@
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <type_traits>
 
 #include <string>
 #include <vector>
@@ -400,6 +401,11 @@ int gemm<float>(coco_layer* H, const float* A, const float* W, int M, int N, int
 }
 
 template <typename T>
+bool fused_swiglu(bool prefill, int F, int K) {
+  return std::is_same<T, bf16_t>::value && prefill && tile_splits(2 * F, K) == 1;
+}
+
+template <typename T>
 int attention(coco_layer* H, const coco_layer_weights& w, int M, const int32_t* positions,
               const int32_t* seq_starts, int n_seqs, const int32_t* bt, const int32_t* ctx,
               hipStream_t st);
@@ -487,10 +493,17 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
     TIMED(COCO_K_RESIDUAL_NORM,
           HIPCHK(launch_residual_rmsnorm<T>(H->part, S, M, d, x, (const T*)w.gamma_mlp,
                                             c.rms_eps, H->x1, h2, st)));
-    // SwiGLU MLP.
-    TIMED(COCO_K_GEMM_GATE_UP,
-          if ((rc = gemm<T>(H, h2, (const T*)w.w_gate_up, M, 2 * F, d, pre, &S, st))) return rc);
-    TIMED(COCO_K_SWIGLU, HIPCHK(launch_swiglu<T>(H->part, S, M, F, u, st)));
+    // SwiGLU MLP (prefill: SwiGLU in the gate/up GEMM's epilogue when the
+    // GEMM is not split along K).
+    if (fused_swiglu<T>(pre, F, d)) {
+      TIMED(COCO_K_GEMM_GATE_UP,
+            HIPCHK(launch_gemm_tile_swiglu_bf16((const bf16_t*)h2, (const bf16_t*)w.w_gate_up,
+                                                (bf16_t*)u, M, F, d, st)));
+    } else {
+      TIMED(COCO_K_GEMM_GATE_UP,
+            if ((rc = gemm<T>(H, h2, (const T*)w.w_gate_up, M, 2 * F, d, pre, &S, st))) return rc);
+      TIMED(COCO_K_SWIGLU, HIPCHK(launch_swiglu<T>(H->part, S, M, F, u, st)));
+    }
     TIMED(COCO_K_GEMM_DOWN, if ((rc = gemm<T>(H, u, (const T*)w.w_down, M, d, F, pre, &S, st))) return rc);
     // Residual; the last layer of the segment scatters to the full batch.
     TIMED(COCO_K_RESIDUAL_SCATTER,

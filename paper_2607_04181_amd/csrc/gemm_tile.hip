@@ -14,7 +14,9 @@
 //   * workgroups are remapped so that the tiles sharing a W column slab run
 //     on the same XCD (blockIdx % 8) back to back and hit its L2;
 //   * narrow outputs with a long K are split into K-slices (tile_splits, a
-//     function of (N, K) only) so the grid covers the CUs.
+//     function of (N, K) only) so the grid covers the CUs;
+//   * for the gate/up projection a variant pairs gate and up columns inside
+//     each wave and writes silu(gate) * up directly in bf16.
 // Every output element is summed over k in ascending 16-steps within its
 // slice, independent of M and of the tile it falls in, so request-aligned
 // prefill splits give identical bits.
@@ -34,10 +36,16 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 // LDS element offset of 16-byte chunk c (0..7) of row r in a [256][64] tile.
 __device__ __forceinline__ int swz(int r, int c) { return r * kTK + ((c ^ (r & 7)) << 3); }
 
+// FUSE: W is the [2F][K] gate/up matrix; tile column block j holds gate
+// rows and the matching up rows so that each lane owns both factors of its
+// outputs, and the epilogue writes h = silu(gate) * up in bf16 to the [M][F]
+// buffer `H` (N = 2F, one K-slice). Otherwise C is the fp32 partial.
+template <bool FUSE>
 __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __restrict__ A,
                                                               const bf16_t* __restrict__ W,
-                                                              float* __restrict__ C, int M, int N,
-                                                              int K, int k_slice) {
+                                                              float* __restrict__ C,
+                                                              bf16_t* __restrict__ H, int M,
+                                                              int N, int K, int k_slice) {
   __shared__ __attribute__((aligned(16))) bf16_t lds[2][2][kTM * kTK];  // [buf][A|W]
 
   const int tiles_m = (M + kTM - 1) / kTM;
@@ -57,6 +65,15 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
   const int wm = wv & 1, wn = wv >> 1;
   const int l32 = lane & 31, hi = lane >> 5;
 
+  // Fused tile of 128 outputs o0 .. o0+127: tile rows 128w + 32j + i hold
+  // gate row o0 + 64w + 32j + i for j < 2 and up row F + o0 + 64w + 32(j-2) + i.
+  const int F = N / 2, o0 = n0 / 2;
+  auto w_row = [&](int r) {
+    if (!FUSE) return min(n0 + r, N - 1);
+    const int w = r >> 7, j = (r >> 5) & 3, i = r & 31;
+    return (j < 2 ? 0 : F) + o0 + 64 * w + 32 * (j & 1) + i;
+  };
+
   // Global -> register staging: 8 chunks of A and 8 of W per thread.
   u32x4_t ra[8], rw[8];
   const int stages = k_slice / kTK;
@@ -66,7 +83,7 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
     for (int v = 0; v < 8; ++v) {
       const int q = tid + v * kTThreads;
       const int r = q >> 3, c = q & 7;
-      const int m = min(m0 + r, M - 1), n = min(n0 + r, N - 1);
+      const int m = min(m0 + r, M - 1), n = w_row(r);
       ra[v] = *(const u32x4_t*)(A + (int64_t)m * K + k0 + c * 8);
       rw[v] = *(const u32x4_t*)(W + (int64_t)n * K + k0 + c * 8);
     }
@@ -148,6 +165,25 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
 
   // 32x32 accumulator layout: register 4*jj + r of lane l holds row
   // 8*jj + 4*(l/32) + r, column l%32.
+  if (FUSE) {
+    // acc[i][j] (gate) pairs with acc[i][j + 2] (up) element for element;
+    // the same formula as the unfused SwiGLU epilogue.
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int o = o0 + 64 * wn + 32 * j + l32;
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int m = m0 + wm * 128 + i * 32 + 8 * jj + 4 * hi + r;
+            const float g = acc[i][j][4 * jj + r], u = acc[i][j + 2][4 * jj + r];
+            if (m < M) H[(int64_t)m * F + o] = (bf16_t)f32_to_bf16(g / (1.0f + expf(-g)) * u);
+          }
+      }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -183,8 +219,19 @@ hipError_t launch_gemm_tile_bf16(const uint16_t* A, const uint16_t* W, float* C,
   if (M <= 0) return hipSuccess;
   if (S < 1 || K % (kTK * S) != 0) return hipErrorInvalidValue;
   const int tiles = ((M + kTM - 1) / kTM) * ((N + kTN - 1) / kTN);
-  hipLaunchKernelGGL(gemm_tile_kernel, dim3(tiles, S), dim3(kTThreads), 0, st, A, W, C, M, N, K,
-                     K / S);
+  hipLaunchKernelGGL(gemm_tile_kernel<false>, dim3(tiles, S), dim3(kTThreads), 0, st, A, W, C,
+                     nullptr, M, N, K, K / S);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_tile_swiglu_bf16(const uint16_t* A, const uint16_t* W_gate_up,
+                                        uint16_t* H, int M, int F, int K, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  if (F % (kTN / 2) != 0 || K % kTK != 0 || tile_splits(2 * F, K) != 1)
+    return hipErrorInvalidValue;
+  const int tiles = ((M + kTM - 1) / kTM) * (2 * F / kTN);
+  hipLaunchKernelGGL(gemm_tile_kernel<true>, dim3(tiles, 1), dim3(kTThreads), 0, st, A,
+                     W_gate_up, nullptr, H, M, 2 * F, K, K);
   return hipGetLastError();
 }
 

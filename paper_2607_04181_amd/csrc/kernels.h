@@ -65,6 +65,10 @@ hipError_t launch_gemm_skinny_bf16(const uint16_t* A, const uint16_t* W, float* 
 int tile_splits(int N, int K);
 hipError_t launch_gemm_tile_bf16(const uint16_t* A, const uint16_t* W, float* C, int M, int N,
                                  int K, int S, hipStream_t st);
+// Gate/up GEMM with the SwiGLU epilogue: H[M][F] = bf16(silu(A W_g^T) * (A W_u^T))
+// where W_gate_up = [W_g; W_u] is [2F][K]; only for tile_splits(2F, K) == 1.
+hipError_t launch_gemm_tile_swiglu_bf16(const uint16_t* A, const uint16_t* W_gate_up,
+                                        uint16_t* H, int M, int F, int K, hipStream_t st);
 
 // part[0][m][n] = sum_k A[m][k] * W[n][k], fp32 (tiny fp32 configurations).
 hipError_t launch_gemm_f32(const float* A, const float* W, float* part, int M, int N, int K,
