@@ -35,6 +35,8 @@ def parse():
                    choices=["c2", "c3", "c3full", "c4p", "c4d", "c5"])
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="target duration of the oracle CPU baseline (0 = skip)")
+    p.add_argument("--no-graph", action="store_true",
+                   help="skip the HIP-graph replay measurement of the same step")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only time a plain 1 GiB device copy (the reference kernel that "
                         "scales the FETCH_SIZE / WRITE_SIZE counters to bytes)")
@@ -165,14 +167,15 @@ def main():
 
     stream = torch.cuda.current_stream()
 
-    def step():
+    def step(st=None):
+        st = stream if st is None else st
         if n_layers == 1:
             coco.coco_layer_forward(handle, 0, hidden, bt["row_idx"], bt["positions"],
-                                    bt["seq_starts"], bt["block_table"], bt["ctx_lens"], stream)
+                                    bt["seq_starts"], bt["block_table"], bt["ctx_lens"], st)
         else:
             coco.coco_layer_span_forward(handle, 0, n_layers, hidden, bt["row_idx"],
                                          bt["positions"], bt["seq_starts"], bt["block_table"],
-                                         bt["ctx_lens"], stream)
+                                         bt["ctx_lens"], st)
 
     for _ in range(args.warmup):
         step()
@@ -185,6 +188,32 @@ def main():
     e1.record(stream)
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / args.steps
+
+    # The same step captured once as a HIP graph and replayed (the forward
+    # only enqueues kernels on fixed buffers, so it is capturable as is).
+    graph = None
+    if not args.no_graph:
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            step(side)
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step(torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        gms = e0.elapsed_time(e1) / args.steps
+        graph = {"ms_per_step": round(gms, 4)}
+        del g
 
     # Per-kernel durations: every launch bracketed by HIP events on the stream.
     coco.coco_layer_set_timing(handle, True)
@@ -256,6 +285,8 @@ def main():
     else:
         value = M * 1000.0 / ms
         unit = "tokens/s per layer"
+    if graph is not None:
+        graph["value"] = round((n_layers * 1000.0 if is_decode else M * 1000.0) / graph["ms_per_step"], 2)
     whole = {"step_hbm_bytes": step_bytes, "step_flops": step_flops,
              "step_GBps": round(step_bytes / (ms * 1e-3) / 1e9, 1),
              "step_TFLOPs": round(step_flops / (ms * 1e-3) / 1e12, 2)}
@@ -276,7 +307,7 @@ def main():
                    "hidden_rows": batch.hidden_rows, "sum_ctx": sum_ctx,
                    "mode": "decode" if is_decode else "prefill", "kv_block": 16,
                    "parallelism": "single GPU (one replica's share)"},
-        "roofline": roof, "whole_step": whole, "cpu_baseline": cpu,
+        "roofline": roof, "whole_step": whole, "graph_replay": graph, "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
 

@@ -561,17 +561,14 @@ hipError_t launch_attn_decode_bf16(const uint16_t* q, const uint16_t* k_cache,
                                    int max_blocks, const int32_t* ctx_lens,
                                    const int32_t* split_off, int n_seqs, int Hq, int Hkv,
                                    float* part_o, float* part_ml, int max_splits,
-                                   hipStream_t st) {
+                                   int num_cus, hipStream_t st) {
   if (n_seqs <= 0) return hipSuccess;
+  if (num_cus <= 0) return hipErrorInvalidValue;
   const float scale_log2 = kLog2e / sqrtf((float)HD);
   // Two resident workgroups per CU (at most 128 registers per lane and 68 KB
   // of LDS each): a persistent grid of two per CU, never more than the work.
-  int dev = 0, cus = 256;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-    return hipErrorInvalidDevice;
   const int64_t work_bound = (int64_t)n_seqs * max_splits * Hkv;
-  const int grid = (int)(work_bound < 2 * cus ? work_bound : 2 * cus);
+  const int grid = (int)(work_bound < 2 * num_cus ? work_bound : 2 * num_cus);
   hipLaunchKernelGGL(attn_decode_kernel, dim3(grid), dim3(kDecWaves * 64), 0, st, q, k_cache,
                      v_cache, block_table, max_blocks, ctx_lens, split_off, n_seqs, Hq, Hkv,
                      part_o, part_ml, max_splits, scale_log2);

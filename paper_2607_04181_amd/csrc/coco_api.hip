@@ -40,6 +40,7 @@ struct coco_layer {
   coco_layer_config cfg;
   std::vector<coco_layer_weights> layers;
   int device = 0;
+  int num_cus = 0;  // compute units of `device` (persistent grid sizes)
   bool validate = false;
   char* ws = nullptr;
   size_t ws_bytes = 0;
@@ -152,10 +153,16 @@ int coco_layer_init(const coco_layer_config* cfg, const coco_layer_weights* laye
     if (w.num_blocks <= 0) return fail(COCO_EINVAL, "layer %d: num_blocks must be > 0", l);
   }
 
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0)
+    return fail(COCO_EHIP, "cannot query the current device");
   coco_layer* H = new coco_layer();
   H->cfg = c;
   H->layers.assign(layers, layers + c.n_layers);
-  (void)hipGetDevice(&H->device);
+  H->device = dev;
+  H->num_cus = cus;
 
   const int eb = elem_bytes(c.dtype);
   const int64_t R = c.max_rows, d = c.d_model, F = c.d_ffn;
@@ -421,7 +428,7 @@ int attention<bf16_t>(coco_layer* H, const coco_layer_weights& w, int M,
       HIPCHK(launch_attn_decode_bf16((const bf16_t*)H->q, (const bf16_t*)w.k_cache,
                                      (const bf16_t*)w.v_cache, bt, c.max_blocks_per_seq, ctx,
                                      H->split_off, n_seqs, c.n_q_heads, c.n_kv_heads, H->attn_o,
-                                     H->attn_ml, H->max_splits, st));
+                                     H->attn_ml, H->max_splits, H->num_cus, st));
     }
     KernelTimer t(H, COCO_K_ATTN_COMBINE, st);
     HIPCHK(launch_attn_combine_bf16(H->attn_o, H->attn_ml, ctx, n_seqs, c.n_q_heads,

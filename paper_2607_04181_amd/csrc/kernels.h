@@ -85,7 +85,7 @@ hipError_t launch_attn_decode_bf16(const uint16_t* q, const uint16_t* k_cache,
                                    int max_blocks, const int32_t* ctx_lens,
                                    const int32_t* split_off, int n_seqs, int Hq, int Hkv,
                                    float* part_o, float* part_ml, int max_splits,
-                                   hipStream_t st);
+                                   int num_cus, hipStream_t st);
 hipError_t launch_attn_combine_bf16(const float* part_o, const float* part_ml,
                                     const int32_t* ctx_lens, int n_seqs, int Hq, int max_splits,
                                     uint16_t* o, hipStream_t st);
