@@ -24,6 +24,7 @@ sys.path.insert(0, ROOT)
 METRIC = "decode layer-steps/s & prefill tokens/s per layer; % HBM / MFMA peak"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s
+XGMI_LINK_BPS = 153e9           # one MI355X xGMI link, bytes/s (boundary transfers)
 
 
 def parse():
@@ -293,6 +294,24 @@ def main():
     whole["step_frac_hbm"] = round(whole["step_GBps"] / HBM_PEAK_GBS, 4)
     whole["step_frac_mfma"] = round(whole["step_TFLOPs"] / MFMA_BF16_PEAK_TFLOPS, 4)
 
+    # The paper's speedup model (Sec. 4.2) fed with this measured per-layer
+    # time: boundary rows over one xGMI link, bf16 hidden states.
+    full_layers = {4096: 32, 5120: 64, 8192: 80}.get(d)
+    scaling = None
+    if full_layers:
+        t_layer = ms * 1e-3 / n_layers
+        if is_decode:
+            bs_rows, toks = M, 1
+        else:
+            bs_rows, toks = batch.n_seqs, max(1, M // max(1, batch.n_seqs))
+        sm = coco.make_scale_model(full_layers, bs_rows, toks, d, 2.0, t_layer, XGMI_LINK_BPS)
+        L = full_layers
+        scaling = {"model_layers": L, "t_comp_ms": round(t_layer * 1e3, 4),
+                   "link_GBps": XGMI_LINK_BPS / 1e9,
+                   "comm_ms_P2": round(coco.coco_comm_time(sm, 2) * 1e3, 5),
+                   "S": {f"N={N},P={P}": round(coco.coco_speedup(sm, N, P), 4)
+                         for N in (L // 4, L // 2, L) for P in (2, 4)}}
+
     cpu = None
     if cpu_inputs is not None:
         cpu = cpu_baseline(wl, batch, cpu_inputs, args.cpu_seconds, n_layers, is_decode)
@@ -307,7 +326,8 @@ def main():
                    "hidden_rows": batch.hidden_rows, "sum_ctx": sum_ctx,
                    "mode": "decode" if is_decode else "prefill", "kv_block": 16,
                    "parallelism": "single GPU (one replica's share)"},
-        "roofline": roof, "whole_step": whole, "graph_replay": graph, "cpu_baseline": cpu,
+        "roofline": roof, "whole_step": whole, "graph_replay": graph,
+        "scaling_model": scaling, "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
 

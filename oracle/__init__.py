@@ -16,6 +16,9 @@ assumes) applied per selected row, in float64, with the row gather before and
 the scatter after (the segment-boundary scatter/gather of Sec. 3.1). A span of
 consecutive layers (Sec. 3.1) applies it layer after layer.
 
+``oracle/scaling.py`` holds the paper's speedup and cost model (Sec. 4.2) and
+the candidate ranking of its scaling step (Sec. 4.4) in plain float64 Python.
+
 Parity status of each function is in its docstring; every function is pinned
 by the CPU tests (brute force on tiny shapes, closed forms, invariants, and
 library routines of torch in float64).

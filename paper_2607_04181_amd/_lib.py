@@ -23,7 +23,10 @@ COCO_WS_X, COCO_WS_H, COCO_WS_Q, COCO_WS_O, COCO_WS_X1, COCO_WS_H2, COCO_WS_U = 
 EXPORTS = ["coco_layer_init", "coco_layer_destroy", "coco_last_error", "coco_version",
            "coco_layer_set_validate", "coco_kv_append", "coco_layer_forward",
            "coco_layer_span_forward", "coco_layer_workspace", "coco_layer_set_timing",
-           "coco_layer_read_timing"]
+           "coco_layer_read_timing",
+           # include/coco_scaling.h: host arithmetic of the speedup/cost model
+           "coco_split_batch", "coco_comm_time", "coco_speedup", "coco_cost_mem",
+           "coco_cost_comp", "coco_speedup_vec", "coco_scale_candidates"]
 KERNEL_KINDS = ["gather_norm", "gemm_qkv", "qkv_epilogue", "attention", "attn_combine", "gemm_o",
                 "residual_norm", "gemm_gate_up", "swiglu", "gemm_down", "residual_scatter"]
 
@@ -45,6 +48,18 @@ class coco_layer_weights(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in (
         "w_qkv", "w_o", "w_gate_up", "w_down", "gamma_attn", "gamma_mlp", "k_cache",
         "v_cache")] + [("num_blocks", ctypes.c_int64)]
+
+
+class coco_scale_model(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("batch", ctypes.c_int64),
+                ("tokens_per_row", ctypes.c_int64), ("d_hidden", ctypes.c_int64),
+                ("elem_bytes", ctypes.c_double), ("t_comp", ctypes.c_double),
+                ("bandwidth", ctypes.c_double)]
+
+
+class coco_scale_candidate(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("parallel", ctypes.c_int32),
+                ("speedup", ctypes.c_double), ("distance", ctypes.c_int32)]
 
 
 def _load():
@@ -69,6 +84,20 @@ def _load():
         "coco_layer_set_timing": (ctypes.c_int, [vp, i32]),
         "coco_layer_read_timing": (ctypes.c_int, [vp, ctypes.POINTER(ctypes.c_double),
                                                   ctypes.POINTER(i64), i32]),
+        "coco_split_batch": (ctypes.c_int, [i64, i32, ctypes.POINTER(i64)]),
+        "coco_comm_time": (ctypes.c_double, [ctypes.POINTER(coco_scale_model), i32]),
+        "coco_speedup": (ctypes.c_double, [ctypes.POINTER(coco_scale_model), i32, i32]),
+        "coco_cost_mem": (ctypes.c_double, [ctypes.POINTER(coco_scale_model), i32, i32]),
+        "coco_cost_comp": (ctypes.c_double, [ctypes.POINTER(coco_scale_model), i32, i32]),
+        "coco_speedup_vec": (ctypes.c_double, [ctypes.POINTER(coco_scale_model),
+                                               ctypes.POINTER(i32),
+                                               ctypes.POINTER(ctypes.c_double),
+                                               ctypes.POINTER(ctypes.c_double), i32]),
+        "coco_scale_candidates": (ctypes.c_int, [ctypes.POINTER(coco_scale_model), i32, i32, i32,
+                                                 i32, ctypes.c_double, i32,
+                                                 ctypes.POINTER(coco_scale_candidate), i32,
+                                                 ctypes.POINTER(i32), ctypes.POINTER(i32),
+                                                 ctypes.POINTER(ctypes.c_double)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -214,3 +243,59 @@ def raw_call(name: str, *args) -> int:
     """Call an entry point with raw ctypes arguments and return its code
     (used by error-path tests that pass deliberately bad arguments)."""
     return getattr(_lib, name)(*args)
+
+
+# ----------------------------------------------------------------------------
+# Speedup / cost model (include/coco_scaling.h): host arithmetic, no GPU.
+# ----------------------------------------------------------------------------
+def make_scale_model(n_layers: int, batch: int, tokens_per_row: int, d_hidden: int,
+                     elem_bytes: float, t_comp: float, bandwidth: float) -> coco_scale_model:
+    return coco_scale_model(n_layers, batch, tokens_per_row, d_hidden, elem_bytes, t_comp,
+                            bandwidth)
+
+
+def coco_split_batch(bs: int, v: int) -> list:
+    out = (ctypes.c_int64 * max(v, 1))()
+    _check(_lib.coco_split_batch(bs, v, out))
+    return [int(x) for x in out[:v]]
+
+
+def coco_comm_time(m: coco_scale_model, P: int) -> float:
+    return _lib.coco_comm_time(ctypes.byref(m), P)
+
+
+def coco_speedup(m: coco_scale_model, N: int, P: int) -> float:
+    return _lib.coco_speedup(ctypes.byref(m), N, P)
+
+
+def coco_cost_mem(m: coco_scale_model, N: int, P: int) -> float:
+    return _lib.coco_cost_mem(ctypes.byref(m), N, P)
+
+
+def coco_cost_comp(m: coco_scale_model, N: int, P: int) -> float:
+    return _lib.coco_cost_comp(ctypes.byref(m), N, P)
+
+
+def coco_speedup_vec(m: coco_scale_model, v, t_dev, bandwidths) -> float:
+    n_dev = len(t_dev)
+    if len(bandwidths) != n_dev:
+        raise ValueError("one bandwidth per device")
+    vv = (ctypes.c_int32 * len(v))(*[int(x) for x in v])
+    tt = (ctypes.c_double * n_dev)(*[float(x) for x in t_dev])
+    bb = (ctypes.c_double * n_dev)(*[float(x) for x in bandwidths])
+    return _lib.coco_speedup_vec(ctypes.byref(m), vv, tt, bb, n_dev)
+
+
+def coco_scale_candidates(m: coco_scale_model, first: int, p_max: int, n_cur: int, p_cur: int,
+                          latency_over_slo: float, cold_devices: int):
+    """Returns (alpha_req, [(N, P, S, distance), ...] ranked, chosen (N, P) or None)."""
+    cap = 1 + (m.n_layers - first) * max(p_max - 1, 0)
+    out = (coco_scale_candidate * cap)()
+    n_out, chosen, alpha = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_double()
+    _check(_lib.coco_scale_candidates(ctypes.byref(m), first, p_max, n_cur, p_cur,
+                                      latency_over_slo, cold_devices, out, cap,
+                                      ctypes.byref(n_out), ctypes.byref(chosen),
+                                      ctypes.byref(alpha)))
+    ranked = [(c.n_layers, c.parallel, c.speedup, c.distance) for c in out[:n_out.value]]
+    pick = None if chosen.value < 0 else ranked[chosen.value][:2]
+    return alpha.value, ranked, pick

@@ -23,7 +23,8 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-Wall",
          "-Wno-unused-function", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          f"-I{os.path.join(ROOT, 'include')}"]
-SOURCES = ["rows.hip", "gemm_skinny.hip", "gemm_tile.hip", "attention.hip", "coco_api.hip"]
+SOURCES = ["rows.hip", "gemm_skinny.hip", "gemm_tile.hip", "attention.hip", "coco_api.hip",
+           "scaling.cpp"]
 
 
 def build(verbose: bool = False, jobs: int = 8) -> str:
@@ -33,7 +34,7 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
     procs = []
     objs = []
     for src in SOURCES:
-        obj = os.path.join(BUILD, src.replace(".hip", ".o"))
+        obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
         objs.append(obj)
         cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:

@@ -1,4 +1,4 @@
-"""The C ABI library loads and exports every function include/coco.h declares
+"""The C ABI library loads and exports every function include/*.h declares
 (CPU only: no compute calls)."""
 import os
 import re
@@ -7,12 +7,13 @@ import subprocess
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "coco.h")
+HEADERS = [os.path.join(ROOT, "include", f) for f in sorted(os.listdir(os.path.join(ROOT, "include")))
+           if f.endswith(".h")]
 LIB = os.path.join(ROOT, "paper_2607_04181_amd", "libcoco.so")
 
 
 def declared_functions():
-    src = open(HEADER).read()
+    src = "\n".join(open(h).read() for h in HEADERS)
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
     return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w\s\*]+?\b(coco_\w+)\s*\(", src, flags=re.M)))
 
