@@ -407,9 +407,12 @@ int gemm<float>(coco_layer* H, const float* A, const float* W, int M, int N, int
   return COCO_OK;
 }
 
+// SwiGLU runs in the gate/up GEMM's epilogue whenever that GEMM is not split
+// along K (bf16; decode and prefill kernels each have a fused variant).
 template <typename T>
 bool fused_swiglu(bool prefill, int F, int K) {
-  return std::is_same<T, bf16_t>::value && prefill && tile_splits(2 * F, K) == 1;
+  if (!std::is_same<T, bf16_t>::value) return false;
+  return prefill ? tile_splits(2 * F, K) == 1 : skinny_plan(2 * F, K).S == 1;
 }
 
 template <typename T>
@@ -503,9 +506,16 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
     // SwiGLU MLP (prefill: SwiGLU in the gate/up GEMM's epilogue when the
     // GEMM is not split along K).
     if (fused_swiglu<T>(pre, F, d)) {
-      TIMED(COCO_K_GEMM_GATE_UP,
-            HIPCHK(launch_gemm_tile_swiglu_bf16((const bf16_t*)h2, (const bf16_t*)w.w_gate_up,
-                                                (bf16_t*)u, M, F, d, st)));
+      if (pre) {
+        TIMED(COCO_K_GEMM_GATE_UP,
+              HIPCHK(launch_gemm_tile_swiglu_bf16((const bf16_t*)h2, (const bf16_t*)w.w_gate_up,
+                                                  (bf16_t*)u, M, F, d, st)));
+      } else {
+        TIMED(COCO_K_GEMM_GATE_UP,
+              HIPCHK(launch_gemm_skinny_swiglu_bf16((const bf16_t*)h2,
+                                                    (const bf16_t*)w.w_gate_up, (bf16_t*)u, M, F,
+                                                    d, skinny_plan(2 * F, d), st)));
+      }
     } else {
       TIMED(COCO_K_GEMM_GATE_UP,
             if ((rc = gemm<T>(H, h2, (const T*)w.w_gate_up, M, 2 * F, d, pre, &S, st))) return rc);

@@ -11,12 +11,13 @@
 //     loads measured faster here than non-temporal ones), keeping two
 //     stages of 128 k in flight;
 //   * the activation tile [rows][128 k] of a stage is shared by the waves
-//     through LDS (double-buffered, rows padded by 16 bytes so the 16 rows a
-//     wave reads per instruction fall in distinct banks);
+//     through LDS (double-buffered); its 16-byte chunks are XOR-swizzled
+//     with the row (chunk ^ row % 16), so both the row-wise stores and the
+//     16-rows-per-instruction fragment reads hit distinct banks;
 //   * each 16x16 output tile is accumulated with v_mfma_f32_16x16x32_bf16 in
 //     ascending k.
-// The plan (WAVES, split count S) is chosen from (N, K) alone so that the
-// grid is a whole number of rounds over the 256 CUs; every output element is
+// The plan (WAVES, split count S) is chosen from (N, K) alone (skinny_plan);
+// every output element is
 // summed in the same k order for any M, so a row's result does not depend on
 // the other rows in the call (batch invariance). Partials of the S slices
 // are added in slice order by the consumer epilogue.
@@ -30,26 +31,33 @@ namespace coco {
 namespace {
 
 constexpr int kBK = 128;       // k per pipeline stage
-constexpr int kPad = 8;        // bf16 elements of LDS row padding
-constexpr int kLdsRow = kBK + kPad;
 constexpr int kCUs = 256;
 
-template <int WAVES, int MT, int PF>
+// LDS element offset of 16-byte chunk c (0..15) of activation row r.
+__device__ __forceinline__ int a_swz(int r, int c) { return r * kBK + ((c ^ (r & 15)) << 3); }
+
+// FUSE: W is the [2F][K] gate/up matrix (N = 2F, one K-slice). Lanes
+// c16 < 8 of a wave stream gate rows o0..o0+7 and lanes c16 >= 8 the
+// matching up rows, so the epilogue pairs lanes c16 and c16+8 and writes
+// h = silu(gate) * up in bf16 to H[M][F] instead of fp32 partials.
+template <int WAVES, int MT, int PF, bool FUSE>
 __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
-    const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, float* __restrict__ part, int M,
-    int N, int K, int k_slice) {
+    const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, float* __restrict__ part,
+    bf16_t* __restrict__ H, int M, int N, int K, int k_slice) {
   constexpr int NT = WAVES * 64;
   constexpr int kChunks = MT * 16 * (kBK / 8);  // 16-byte A chunks per stage
   constexpr int kPerT = (kChunks + NT - 1) / NT;
-  __shared__ __attribute__((aligned(16))) bf16_t lds[2][MT * 16][kLdsRow];
+  __shared__ __attribute__((aligned(16))) bf16_t lds[2][MT * 16 * kBK];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wv = tid >> 6;
   const int c16 = lane & 15, j4 = lane >> 4;
-  const int n_col = blockIdx.x * (16 * WAVES) + wv * 16 + c16;  // this lane's weight row
+  const int o0 = (blockIdx.x * WAVES + wv) * 8;  // fused: this wave's 8 outputs
+  const int n_col = FUSE ? (c16 < 8 ? o0 + c16 : N / 2 + o0 + c16 - 8)
+                         : blockIdx.x * (16 * WAVES) + wv * 16 + c16;  // this lane's weight row
   const int k_begin = blockIdx.y * k_slice;
   const int stages = k_slice / kBK;
-  float* out = part + (int64_t)blockIdx.y * M * N;
+  float* out = FUSE ? nullptr : part + (int64_t)blockIdx.y * M * N;
 
   const bf16_t* wrow = W + (int64_t)n_col * K + k_begin + j4 * 8;
 
@@ -93,7 +101,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
         const int q = tid + v * NT;
         const bool live = st < stages && m0 + (q >> 4) < M;
         const u32x4_t val = live ? areg[slot][v] : u32x4_t{0u, 0u, 0u, 0u};
-        if (q < kChunks) *(u32x4_t*)(&lds[buf][q >> 4][(q & 15) * 8]) = val;
+        if (q < kChunks) *(u32x4_t*)(&lds[buf][a_swz(q >> 4, q & 15)]) = val;
       }
     };
 
@@ -115,7 +123,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) {
             const bf16x8_t a = __builtin_bit_cast(
-                bf16x8_t, *(const u32x4_t*)(&lds[buf][mt * 16 + c16][t * 32 + j4 * 8]));
+                bf16x8_t, *(const u32x4_t*)(&lds[buf][a_swz(mt * 16 + c16, t * 4 + j4)]));
             acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[mt], 0, 0, 0);
           }
         }
@@ -131,61 +139,84 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int m = m0 + mt * 16 + j4 * 4 + r;
-        if (m < M) out[(int64_t)m * N + n_col] = acc[mt][r];
+        if (FUSE) {
+          // The up value of this lane's output sits 8 lanes up.
+          const float u = __shfl_down(acc[mt][r], 8, 16);
+          const float g = acc[mt][r];
+          if (c16 < 8 && m < M)
+            H[(int64_t)m * (N / 2) + o0 + c16] = (bf16_t)f32_to_bf16(g / (1.0f + expf(-g)) * u);
+        } else if (m < M) {
+          out[(int64_t)m * N + n_col] = acc[mt][r];
+        }
       }
     }
   }
 }
 
-template <int WAVES, int MT>
-hipError_t launch_plan(const uint16_t* A, const uint16_t* W, float* part, int M, int N, int K,
-                       int S, hipStream_t st) {
+template <int WAVES, int MT, bool FUSE>
+hipError_t launch_plan(const uint16_t* A, const uint16_t* W, float* part, uint16_t* H, int M,
+                       int N, int K, int S, hipStream_t st) {
   // Two stages of weights in flight per wave (~56 KB per CU at 7 waves) is
   // enough to cover HBM latency; deeper rings measured slower (more requests
   // queued behind each other) and cost registers.
   constexpr int PF = 2;
-  hipLaunchKernelGGL((gemm_skinny_kernel<WAVES, MT, PF>), dim3(N / (16 * WAVES), S),
-                     dim3(WAVES * 64), 0, st, A, W, part, M, N, K, K / S);
+  hipLaunchKernelGGL((gemm_skinny_kernel<WAVES, MT, PF, FUSE>), dim3(N / (16 * WAVES), S),
+                     dim3(WAVES * 64), 0, st, A, W, part, H, M, N, K, K / S);
   return hipGetLastError();
 }
 
-template <int WAVES>
-hipError_t launch_waves(const uint16_t* A, const uint16_t* W, float* part, int M, int N, int K,
-                        int S, hipStream_t st) {
-  return M <= 64 ? launch_plan<WAVES, 4>(A, W, part, M, N, K, S, st)
-                 : launch_plan<WAVES, 8>(A, W, part, M, N, K, S, st);
+template <int WAVES, bool FUSE>
+hipError_t launch_waves(const uint16_t* A, const uint16_t* W, float* part, uint16_t* H, int M,
+                        int N, int K, int S, hipStream_t st) {
+  return M <= 64 ? launch_plan<WAVES, 4, FUSE>(A, W, part, H, M, N, K, S, st)
+                 : launch_plan<WAVES, 8, FUSE>(A, W, part, H, M, N, K, S, st);
+}
+
+template <bool FUSE>
+hipError_t launch_any(const uint16_t* A, const uint16_t* W, float* part, uint16_t* H, int M,
+                      int N, int K, SkinnyPlan plan, hipStream_t st) {
+  switch (plan.waves) {
+    case 4: return launch_waves<4, FUSE>(A, W, part, H, M, N, K, plan.S, st);
+    case 5: return launch_waves<5, FUSE>(A, W, part, H, M, N, K, plan.S, st);
+    case 6: return launch_waves<6, FUSE>(A, W, part, H, M, N, K, plan.S, st);
+    case 7: return launch_waves<7, FUSE>(A, W, part, H, M, N, K, plan.S, st);
+    default: return launch_waves<8, FUSE>(A, W, part, H, M, N, K, plan.S, st);
+  }
 }
 
 }  // namespace
 
-// Grid plan from (N, K) only. Scores every (waves, S) that tiles the shape by
-// how evenly the workgroups cover the CUs, how many waves per CU stream
-// weights, and the extra traffic of split-K partials and activation re-reads
-// (costed at a nominal 64 rows).
+// Grid plan from (N, K) only (so a row's sums never depend on the batch).
+// Measured on the decode shapes: the best plans fill the 256 CUs with exactly
+// one round of workgroups; among those, K-slices of at least 1024 (eight
+// stages) and then more waves per workgroup win. Without such a plan,
+// the unsplit weight stream with the most waves wins (the kernel is bound by
+// HBM, so a partly filled last round costs little, while split-K partials
+// and short slices cost more).
 SkinnyPlan skinny_plan(int N, int K) {
+  auto valid = [&](int waves, int S) {
+    if (N % (16 * waves)) return false;
+    if (K % (S * kBK)) return false;
+    if (S > 1 && K / S < 4 * kBK) return false;
+    return true;
+  };
   SkinnyPlan best{0, 0};
-  double best_score = -1.0;
-  for (int waves = 4; waves <= 8; ++waves) {
-    const int bn = 16 * waves;
-    if (N % bn) continue;
+  int best_rank = -1;
+  for (int waves = 4; waves <= 8; ++waves)
     for (int S = 1; S <= 16; S *= 2) {
-      if (K % (S * kBK)) continue;
-      if (S > 1 && K / S < 4 * kBK) continue;
-      const int wgs = (N / bn) * S;
-      const double rounds = ceil((double)wgs / kCUs);
-      const double balance = wgs / (rounds * kCUs);
-      const double waves_per_cu = (double)waves * wgs / kCUs;
-      const double flight = waves_per_cu >= 4.0 ? 1.0 : waves_per_cu / 4.0;
-      const double partial = S > 1 ? 0.5 * 4.0 * S * 64.0 / K : 0.0;
-      const double reread = 0.05 * 64.0 / bn;
-      const double score = balance * flight / (1.0 + partial + reread);
-      if (score > best_score + 1e-12) {
-        best_score = score;
+      if (!valid(waves, S)) continue;
+      const int wgs = (N / (16 * waves)) * S;
+      if (wgs != kCUs) continue;
+      const int rank = (K / S >= 8 * kBK ? 100 : 0) + waves * 2 + (S == 1 ? 1 : 0);
+      if (rank > best_rank) {
+        best_rank = rank;
         best = SkinnyPlan{waves, S};
       }
     }
-  }
-  return best;
+  if (best.waves) return best;
+  for (int waves = 8; waves >= 4; --waves)
+    if (valid(waves, 1)) return SkinnyPlan{waves, 1};
+  return best;  // {0, 0}: no plan (N not a multiple of 64 or K of 128)
 }
 
 hipError_t launch_gemm_skinny_bf16(const uint16_t* A, const uint16_t* W, float* part, int M,
@@ -194,13 +225,17 @@ hipError_t launch_gemm_skinny_bf16(const uint16_t* A, const uint16_t* W, float* 
   if (plan.waves < 4 || plan.waves > 8 || N % (16 * plan.waves) != 0 ||
       K % (plan.S * kBK) != 0)
     return hipErrorInvalidValue;
-  switch (plan.waves) {
-    case 4: return launch_waves<4>(A, W, part, M, N, K, plan.S, st);
-    case 5: return launch_waves<5>(A, W, part, M, N, K, plan.S, st);
-    case 6: return launch_waves<6>(A, W, part, M, N, K, plan.S, st);
-    case 7: return launch_waves<7>(A, W, part, M, N, K, plan.S, st);
-    default: return launch_waves<8>(A, W, part, M, N, K, plan.S, st);
-  }
+  return launch_any<false>(A, W, part, nullptr, M, N, K, plan, st);
+}
+
+hipError_t launch_gemm_skinny_swiglu_bf16(const uint16_t* A, const uint16_t* W_gate_up,
+                                          uint16_t* H, int M, int F, int K, SkinnyPlan plan,
+                                          hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  if (plan.S != 1 || plan.waves < 4 || plan.waves > 8 || (2 * F) % (16 * plan.waves) != 0 ||
+      K % kBK != 0)
+    return hipErrorInvalidValue;
+  return launch_any<true>(A, W_gate_up, nullptr, H, M, 2 * F, K, plan, st);
 }
 
 // ----------------------------------------------------------------------------

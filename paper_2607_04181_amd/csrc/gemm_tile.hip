@@ -7,7 +7,7 @@
 //     waves owns a 128 x 128 sub-tile as 4 x 4 v_mfma_f32_32x32x16_bf16
 //     accumulators (256 fp32 per lane, held in AGPRs);
 //   * 64-deep K stages of A and W tiles are staged through LDS (2 x 64 KB,
-//     double-buffered) with 16-byte chunks XOR-swizzled by row, so the 32
+//     double-buffered) with 16-byte chunks XOR-swizzled by row pair, so the
 //     rows a wave reads per MFMA operand fall in distinct banks; the next
 //     stage's global loads are in flight while the current stage is
 //     multiplied;
@@ -34,7 +34,11 @@ constexpr int kXCDs = 8;
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 // LDS element offset of 16-byte chunk c (0..7) of row r in a [256][64] tile.
-__device__ __forceinline__ int swz(int r, int c) { return r * kTK + ((c ^ (r & 7)) << 3); }
+// A 16-lane group of a 16-byte-per-lane LDS access covers 256 bytes (all 64
+// banks) = two 128-byte rows; XOR-ing the chunk with (r / 2) % 8 gives the
+// 16 consecutive rows a fragment read touches, and the two rows a store
+// group writes, 16 distinct 4-bank slots.
+__device__ __forceinline__ int swz(int r, int c) { return r * kTK + ((c ^ ((r >> 1) & 7)) << 3); }
 
 // FUSE: W is the [2F][K] gate/up matrix; tile column block j holds gate
 // rows and the matching up rows so that each lane owns both factors of its

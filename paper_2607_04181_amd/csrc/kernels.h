@@ -58,6 +58,11 @@ struct SkinnyPlan {
 SkinnyPlan skinny_plan(int N, int K);
 hipError_t launch_gemm_skinny_bf16(const uint16_t* A, const uint16_t* W, float* part, int M,
                                    int N, int K, SkinnyPlan plan, hipStream_t st);
+// Decode gate/up GEMM with the SwiGLU epilogue: H[M][F] = bf16(silu(A W_g^T) *
+// (A W_u^T)), W_gate_up = [W_g; W_u] [2F][K]; plan = skinny_plan(2F, K) with S == 1.
+hipError_t launch_gemm_skinny_swiglu_bf16(const uint16_t* A, const uint16_t* W_gate_up,
+                                          uint16_t* H, int M, int F, int K, SkinnyPlan plan,
+                                          hipStream_t st);
 
 // part[s][m][n] = sum_{k in slice s} A[m][k] * W[n][k] with 256 x 256 MFMA
 // tiles (prefill; K a multiple of 64 * S). S = tile_splits(N, K); the k
