@@ -269,23 +269,25 @@ __global__ __launch_bounds__(HD) void attn_combine_kernel(const float* __restric
 // Workgroup = (sequence, 128-row query tile, query head). Workgroups are
 // remapped so that the query heads of one tile run back to back on one XCD
 // (blockIdx % 8) and share its L2 for the key/value tiles of their group.
-// Wave w takes rows 32w..32w+31 of the tile as two 16-column tiles. The
+// Eight waves each take 16 rows of the tile as one 16-column tile. The
 // key/value tiles are staged through LDS four blocks (64 keys) at a time by
-// direct global->LDS loads (each wave fetches one block's K and V tiles as
-// eight contiguous 1 KB pieces), double-buffered with one barrier per stage.
+// direct global->LDS loads (each wave fetches one block's K or V tile as
+// four contiguous 1 KB pieces), double-buffered with one barrier per stage.
 // Per stage a wave scores the 64 keys (S^T = K Q^T), updates its online
 // softmax once, and accumulates O^T += V^T P^T in 32-key MFMA steps: the
 // V^T fragments of two blocks side by side against P^T packed to match (any
 // fixed assignment of keys to MFMA k-slots gives the same sum).
-constexpr int kPfWaves = 4;
-constexpr int kPfRows = kPfWaves * 32;  // query rows per workgroup
-constexpr int kPfBlk = 4;               // key blocks per stage (one per wave)
+constexpr int kPfRows = 128;  // query rows per workgroup
+constexpr int kPfLaunchWaves = 8;  // waves per workgroup, one 16-row column tile each (measured faster than 4 x 2)
+constexpr int kPfBlk = 4;     // key blocks per stage
 constexpr int kTileElems = kBlockTokens * HD;
 constexpr int kXCDs = 8;
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-__global__ __launch_bounds__(kPfWaves * 64, 2) void attn_prefill_kernel(
+// WAVES waves of COLS 16-column tiles each cover the workgroup's 128 rows.
+template <int WAVES, int COLS>
+__global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_prefill_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k_cache,
     const bf16_t* __restrict__ v_cache, const int32_t* __restrict__ block_table, int max_blocks,
     const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ positions,
@@ -330,16 +332,16 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void attn_prefill_kernel(
   const int stages = (n_blk + kPfBlk - 1) / kPfBlk;
   const int32_t* bt = block_table + (int64_t)s * max_blocks;
 
-  // This wave's two column tiles; padded columns repeat the tile's last row
-  // and are never stored.
-  const int w_row0 = row_begin + wv * 32;
-  const int w_kmax = w_row0 < row_end ? positions[min(row_end, w_row0 + 32) - 1] : -1;
+  // This wave's column tiles; padded columns repeat the tile's last row and
+  // are never stored.
+  const int w_row0 = row_begin + wv * 16 * COLS;
+  const int w_kmax = w_row0 < row_end ? positions[min(row_end, w_row0 + 16 * COLS) - 1] : -1;
   // Stages whose keys all precede the wave's first row need no causal mask.
   const int w_kmin = w_row0 < row_end ? positions[w_row0] : -1;
-  int pos[2];
-  bf16x8_t qf[2][4];
+  int pos[COLS];
+  bf16x8_t qf[COLS][4];
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
+  for (int c = 0; c < COLS; ++c) {
     const int row = min(w_row0 + 16 * c + c16, row_end - 1);
     pos[c] = positions[row];
     const bf16_t* qp = q + ((int64_t)row * Hq + h) * HD + j4 * 8;
@@ -348,24 +350,32 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void attn_prefill_kernel(
       qf[c][t] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(qp + t * 32));
   }
 
-  // Wave wv stages block st*4 + wv (clamped to the last block: a repeat that
-  // the causal mask hides) into LDS.
+  // The stage's 4 blocks (clamped to the last block: a repeat that the
+  // causal mask hides) x {K, V} tiles are 8 tiles of four 1 KB pieces;
+  // wave wv stages tiles wv, wv + WAVES, ... into LDS.
   auto issue = [&](int st, int buf) {
-    const int blk = min(st * kPfBlk + wv, n_blk - 1);
-    const int64_t tile_off = ((int64_t)bt[blk] * Hkv + g) * kTileElems + lane * 8;
 #pragma unroll
-    for (int pc = 0; pc < 4; ++pc) {
-      __builtin_amdgcn_global_load_lds(k_cache + tile_off + pc * 512,
-                                       (lds_void_t*)&kv[buf][0][wv][pc * 512], 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(v_cache + tile_off + pc * 512,
-                                       (lds_void_t*)&kv[buf][1][wv][pc * 512], 16, 0, 0);
+    for (int tt = wv; tt < 2 * kPfBlk; tt += WAVES) {
+      const int kvsel = tt / kPfBlk, bi = tt % kPfBlk;
+      const int blk = min(st * kPfBlk + bi, n_blk - 1);
+      const bf16_t* src = (kvsel ? v_cache : k_cache) +
+                          ((int64_t)bt[blk] * Hkv + g) * kTileElems + lane * 8;
+#pragma unroll
+      for (int pc = 0; pc < 4; ++pc)
+        __builtin_amdgcn_global_load_lds(src + pc * 512,
+                                         (lds_void_t*)&kv[buf][kvsel][bi][pc * 512], 16, 0, 0);
     }
   };
 
-  float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.f, 0.f};
-  f32x4_t acc[2][8];
+  float m[COLS], l[COLS];
+  f32x4_t acc[COLS][8];
 #pragma unroll
-  for (int c = 0; c < 2; ++c)
+  for (int c = 0; c < COLS; ++c) {
+    m[c] = -INFINITY;
+    l[c] = 0.f;
+  }
+#pragma unroll
+  for (int c = 0; c < COLS; ++c)
 #pragma unroll
     for (int n = 0; n < 8; ++n) acc[c][n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
@@ -379,7 +389,7 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void attn_prefill_kernel(
       const bf16_t* vl = &kv[buf][1][0][lane * 8];
       // Scores of the stage's 4 blocks for both column tiles; the next
       // block's K fragments are read while the current block's MFMAs run.
-      f32x4_t sc[2][kPfBlk];
+      f32x4_t sc[COLS][kPfBlk];
       u32x4_t kfr[2][4];
 #pragma unroll
       for (int pc = 0; pc < 4; ++pc) kfr[0][pc] = *(const u32x4_t*)(kl + pc * 512);
@@ -391,7 +401,7 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void attn_prefill_kernel(
             kfr[(i + 1) & 1][pc] = *(const u32x4_t*)(kl + (i + 1) * kTileElems + pc * 512);
         }
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
+        for (int c = 0; c < COLS; ++c) {
           f32x4_t a = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int pc = 0; pc < 4; ++pc)
@@ -410,9 +420,9 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void attn_prefill_kernel(
       }
       // Online softmax, once per 64 keys (log2 domain: p = 2^(s*scale - m)),
       // P^T packed as two 32-key operands.
-      u32x4_t pk[2][2];
+      u32x4_t pk[COLS][2];
 #pragma unroll
-      for (int c = 0; c < 2; ++c) {
+      for (int c = 0; c < COLS; ++c) {
         float mx = -INFINITY;
         if (unmasked) {
 #pragma unroll
@@ -470,7 +480,7 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void attn_prefill_kernel(
           const bf16x8_t va = __builtin_bit_cast(bf16x8_t, u32x4_t{v0.x, v0.y, v1.x, v1.y});
           const bf16x8_t vb = __builtin_bit_cast(bf16x8_t, u32x4_t{v0.z, v0.w, v1.z, v1.w});
 #pragma unroll
-          for (int c = 0; c < 2; ++c) {
+          for (int c = 0; c < COLS; ++c) {
             const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, pk[c][pp]);
             acc[c][2 * pc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb, acc[c][2 * pc], 0, 0, 0);
             acc[c][2 * pc + 1] =
@@ -483,7 +493,7 @@ __global__ __launch_bounds__(kPfWaves * 64, 2) void attn_prefill_kernel(
   }
 
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
+  for (int c = 0; c < COLS; ++c) {
     const int row = w_row0 + 16 * c + c16;
     const float inv = 1.0f / col_sum4(l[c]);
     if (row < row_end) {
@@ -597,7 +607,8 @@ hipError_t launch_attn_prefill_bf16(const uint16_t* q, const uint16_t* k_cache,
   // tile return at once.
   const int64_t tiles = (n_rows + kPfRows - 1) / kPfRows + n_seqs;
   if (tiles * Hq > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(attn_prefill_kernel, dim3((unsigned)(tiles * Hq)), dim3(kPfWaves * 64), 0, st, q,
+  hipLaunchKernelGGL((attn_prefill_kernel<kPfLaunchWaves, 8 / kPfLaunchWaves>),
+                     dim3((unsigned)(tiles * Hq)), dim3(kPfLaunchWaves * 64), 0, st, q,
                      k_cache, v_cache, block_table, max_blocks, ctx_lens, positions, seq_starts,
                      n_seqs, Hq, Hkv, scale_log2, o);
   return hipGetLastError();
