@@ -135,20 +135,35 @@ hipError_t launch_gather_rmsnorm(const T* src, const int32_t* row_idx, int M, in
 }
 
 // ----------------------------------------------------------------------------
-// QKV epilogue: one wave per (row, head). Reduce the split-K partials, rotate
-// query and key heads to the row's absolute position (rotate-half RoPE,
-// angles in fp64), store queries, append the rotated key and the value to
-// the sequence's cache slot.
+// QKV epilogue: one wave per (row, head), kEpiHeads heads per workgroup.
+// Reduce the split-K partials, rotate query and key heads to the row's
+// absolute position (rotate-half RoPE; the angles' cos/sin in fp64, computed
+// once per workgroup into LDS), store queries, append the rotated key and the
+// value to the sequence's cache slot.
 // ----------------------------------------------------------------------------
+constexpr int kEpiHeads = 8;
+
 template <typename T, int S>
-__global__ __launch_bounds__(kWave) void qkv_epilogue_kernel(
+__global__ __launch_bounds__(kEpiHeads * kWave) void qkv_epilogue_kernel(
     const float* __restrict__ part, int M, int Hq, int Hkv, int hd,
     const int32_t* __restrict__ positions, const int32_t* __restrict__ seq_starts, int n_seqs,
     const int32_t* __restrict__ block_table, int max_blocks, const double* __restrict__ inv_freq,
     T* __restrict__ q_out, T* __restrict__ k_cache, T* __restrict__ v_cache,
     const int32_t* __restrict__ ctx_lens, int32_t* __restrict__ split_off) {
-  const int h = blockIdx.x, i = blockIdx.y, lane = threadIdx.x;
-  if (split_off != nullptr && h == 0 && i == 0) {
+  __shared__ float rot[2][128];  // cos, sin of the row's angles (hd / 2 <= 128)
+  const int i = blockIdx.y, lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+  const int h = blockIdx.x * kEpiHeads + wv;
+  const int half = hd >> 1;
+  const int pos = positions[i];
+  // The row's rotation angles in fp64, once for all the heads of the block.
+  for (int j = threadIdx.x; j < half; j += kEpiHeads * kWave) {
+    double sn, cn;
+    sincos((double)pos * inv_freq[j], &sn, &cn);
+    rot[0][j] = (float)cn;
+    rot[1][j] = (float)sn;
+  }
+  __syncthreads();
+  if (split_off != nullptr && blockIdx.x == 0 && i == 0 && wv == 0) {
     // Decode attention work list: exclusive prefix sum of ceil(ctx / 256).
     int run = 0;
     if (lane == 0) split_off[0] = 0;
@@ -164,11 +179,10 @@ __global__ __launch_bounds__(kWave) void qkv_epilogue_kernel(
       run += __shfl(v, kWave - 1, kWave);
     }
   }
-  const int half = hd >> 1;
+  if (h >= Hq + 2 * Hkv) return;
   const int N = (Hq + 2 * Hkv) * hd;
   const int64_t pstride = (int64_t)M * N;
   const float* p = part + (int64_t)i * N + (int64_t)h * hd;
-  const int pos = positions[i];
   int64_t blk = 0;
   int slot = 0;
   if (h >= Hq) {
@@ -179,9 +193,7 @@ __global__ __launch_bounds__(kWave) void qkv_epilogue_kernel(
   if (h < Hq + Hkv) {
     for (int j = lane; j < half; j += kWave) {
       const float lo = sum_parts1<S>(p + j, pstride), hi = sum_parts1<S>(p + j + half, pstride);
-      double sn, cn;
-      sincos((double)pos * inv_freq[j], &sn, &cn);
-      const float c = (float)cn, s = (float)sn;
+      const float c = rot[0][j], s = rot[1][j];
       const float rlo = lo * c - hi * s, rhi = hi * c + lo * s;
       if (h < Hq) {
         T* dst = q_out + ((int64_t)i * Hq + h) * hd;
@@ -219,8 +231,10 @@ hipError_t launch_qkv_epilogue(const float* part, int S, int M, int Hq, int Hkv,
                                const double* inv_freq, T* q_out, T* k_cache, T* v_cache,
                                const int32_t* ctx_lens, int32_t* split_off, hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  const dim3 grid(Hq + 2 * Hkv, M);
-  COCO_SWITCH_S(S, hipLaunchKernelGGL((qkv_epilogue_kernel<T, S_>), grid, dim3(kWave), 0, st,
+  if (hd > 256) return hipErrorInvalidValue;
+  const dim3 grid((Hq + 2 * Hkv + kEpiHeads - 1) / kEpiHeads, M);
+  COCO_SWITCH_S(S, hipLaunchKernelGGL((qkv_epilogue_kernel<T, S_>), grid,
+                                      dim3(kEpiHeads * kWave), 0, st,
                                       part, M, Hq, Hkv, hd, positions, seq_starts, n_seqs,
                                       block_table, max_blocks, inv_freq, q_out, k_cache,
                                       v_cache, ctx_lens, split_off));
