@@ -71,7 +71,8 @@ struct DecItem {
 };
 
 __device__ __forceinline__ DecItem decode_item(int w, int Hkv, const int32_t* split_off,
-                                               const int32_t* ctx_lens, int n_seqs) {
+                                               const int32_t* ctx_lens, int n_seqs,
+                                               int max_blocks) {
   DecItem it;
   const int item = w / Hkv;
   it.g = w - item * Hkv;
@@ -83,7 +84,8 @@ __device__ __forceinline__ DecItem decode_item(int w, int Hkv, const int32_t* sp
   it.s = lo;
   it.sp = item - split_off[lo];
   const int t0 = it.sp * kDecodeSplit;
-  it.t1 = min(ctx_lens[lo], t0 + kDecodeSplit);
+  // Capped at the block table's width (only invalid lengths reach the cap).
+  it.t1 = min(min(ctx_lens[lo], t0 + kDecodeSplit), max_blocks * kBlockTokens);
   it.b_first = t0 / kBlockTokens;
   it.b_last = (it.t1 - 1) / kBlockTokens;
   return it;
@@ -132,7 +134,7 @@ __global__ __launch_bounds__(kDecWaves * 64, 4) void attn_decode_kernel(
   int w = blockIdx.x;
   DecItem cur{};
   if (w < total) {
-    cur = decode_item(w, Hkv, split_off, ctx_lens, n_seqs);
+    cur = decode_item(w, Hkv, split_off, ctx_lens, n_seqs, max_blocks);
     issue(cur);
   }
   for (; w < total; w += gridDim.x) {
@@ -196,7 +198,8 @@ __global__ __launch_bounds__(kDecWaves * 64, 4) void attn_decode_kernel(
     // The registers are free: start the next item's reads now (past the
     // last item, a repeat of the last one that is never used).
     const DecItem it = cur;
-    cur = decode_item(min(w + (int)gridDim.x, total - 1), Hkv, split_off, ctx_lens, n_seqs);
+    cur = decode_item(min(w + (int)gridDim.x, total - 1), Hkv, split_off, ctx_lens, n_seqs,
+                      max_blocks);
     issue(cur);
     __syncthreads();
 
@@ -225,7 +228,12 @@ __global__ __launch_bounds__(kDecWaves * 64, 4) void attn_decode_kernel(
 
 // Merge the partitions of one (sequence, query head) in partition order.
 // Partition weights exp2(m_sp - max) are computed once into LDS (dynamic,
-// 2 * max_splits floats); each thread then owns one head dimension.
+// 2 * max_splits floats); each thread then owns one head dimension. The
+// first kPre partitions' values are loaded together with the (max, sum)
+// pairs, so a sequence of up to kPre * 256 tokens needs one memory round
+// trip after its length.
+constexpr int kPre = 8;
+
 __global__ __launch_bounds__(HD) void attn_combine_kernel(const float* __restrict__ part_o,
                                                           const float* __restrict__ part_ml,
                                                           const int32_t* __restrict__ ctx_lens,
@@ -234,8 +242,12 @@ __global__ __launch_bounds__(HD) void attn_combine_kernel(const float* __restric
   extern __shared__ float sm[];  // [0, max_splits): weights; [max_splits, 2*max_splits): l
   __shared__ float red[HD / kWave];
   const int h = blockIdx.x, s = blockIdx.y, dim = threadIdx.x;
-  const int nsp = (ctx_lens[s] + kDecodeSplit - 1) / kDecodeSplit;
+  const int nsp = min((ctx_lens[s] + kDecodeSplit - 1) / kDecodeSplit, max_splits);
   const int64_t base = ((int64_t)s * Hq + h) * max_splits;
+  const float* po = part_o + base * HD + dim;
+  float pre[kPre];
+#pragma unroll
+  for (int k = 0; k < kPre; ++k) pre[k] = k < nsp ? po[k * HD] : 0.f;
   float mx = -INFINITY;
   for (int sp = dim; sp < nsp; sp += HD) {
     const float m = part_ml[(base + sp) * 2];
@@ -250,8 +262,10 @@ __global__ __launch_bounds__(HD) void attn_combine_kernel(const float* __restric
   for (int sp = dim; sp < nsp; sp += HD) sm[sp] = exp2f(sm[sp] - mx);
   __syncthreads();
   float acc = 0.f, L = 0.f;
-  const float* po = part_o + base * HD + dim;
-  int sp = 0;
+#pragma unroll
+  for (int k = 0; k < kPre; ++k)
+    if (k < nsp) acc += sm[k] * pre[k];
+  int sp = kPre;
   for (; sp + 4 <= nsp; sp += 4) {
     const float a0 = po[(sp + 0) * HD], a1 = po[(sp + 1) * HD];
     const float a2 = po[(sp + 2) * HD], a3 = po[(sp + 3) * HD];

@@ -151,6 +151,11 @@ int coco_layer_init(const coco_layer_config* cfg, const coco_layer_weights* laye
         !w.k_cache || !w.v_cache)
       return fail(COCO_EINVAL, "layer %d has a NULL weight or cache pointer", l);
     if (w.num_blocks <= 0) return fail(COCO_EINVAL, "layer %d: num_blocks must be > 0", l);
+    // The kernels read weights, gains and cache tiles with 16-byte vector loads.
+    const void* ptrs[8] = {w.w_qkv, w.w_o, w.w_gate_up, w.w_down, w.gamma_attn, w.gamma_mlp,
+                           w.k_cache, w.v_cache};
+    for (const void* ptr : ptrs)
+      if ((uintptr_t)ptr % 16) return fail(COCO_EINVAL, "layer %d: a weight or cache pointer is not 16-byte aligned", l);
   }
 
   int dev = 0, cus = 0;
@@ -495,7 +500,7 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
                                         (seq_starts == nullptr && c.dtype == COCO_BF16)
                                             ? H->split_off
                                             : nullptr,
-                                        st)));
+                                        H->max_splits, st)));
     // Attention over the paged cache.
     if ((rc = attention<T>(H, w, M, positions, seq_starts, n_seqs, bt, ctx, st))) return rc;
     // O projection + residual + RMSNorm_2.
@@ -543,6 +548,7 @@ int check_batch(coco_layer* H, int first, int nl, const void* hidden, int64_t hi
   if (!hidden || !row_idx || !positions || !bt || !ctx)
     return fail(COCO_EINVAL, "NULL batch pointer");
   if (hidden_rows < 1) return fail(COCO_EINVAL, "hidden_rows must be >= 1");
+  if ((uintptr_t)hidden % 16) return fail(COCO_EINVAL, "hidden is not 16-byte aligned");
   if (n_seqs < 1 || n_seqs > c.max_seqs)
     return fail(COCO_EINVAL, "n_seqs = %d outside [1, max_seqs = %d]", n_seqs, c.max_seqs);
   if (!seq_starts) {

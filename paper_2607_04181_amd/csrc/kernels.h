@@ -17,13 +17,14 @@ hipError_t launch_gather_rmsnorm(const T* src, const int32_t* row_idx, int M, in
 // Sum of S split-K partials of the QKV projection, RoPE on query and key
 // heads, queries to q_out [M][Hq*hd], keys/values into the paged cache.
 // With split_off non-null (decode), one workgroup also writes the decode
-// attention's partition offsets from ctx_lens.
+// attention's partition offsets from ctx_lens (counts capped at max_splits).
 template <typename T>
 hipError_t launch_qkv_epilogue(const float* part, int S, int M, int Hq, int Hkv, int hd,
                                const int32_t* positions, const int32_t* seq_starts,
                                int n_seqs, const int32_t* block_table, int max_blocks,
                                const double* inv_freq, T* q_out, T* k_cache, T* v_cache,
-                               const int32_t* ctx_lens, int32_t* split_off, hipStream_t st);
+                               const int32_t* ctx_lens, int32_t* split_off, int max_splits,
+                               hipStream_t st);
 
 // x1 = x + sum_s part[s]  (fp32);  h2 = RMSNorm(x1) * gamma.
 template <typename T>

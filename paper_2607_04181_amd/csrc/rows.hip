@@ -93,13 +93,22 @@ __global__ __launch_bounds__(kRowThreads) void gather_rmsnorm_kernel<bf16_t>(
   const int64_t r = row_idx ? (int64_t)row_idx[i] : (int64_t)i;
   const int nv = d / 8;
   const u32x4_t* x = (const u32x4_t*)(src + r * d);
-  u32x4_t xv[kMaxVec];
-  float ss = 0.f;
+  const u32x4_t* g = (const u32x4_t*)gamma;
+  // The gains are loaded together with the row: one memory round trip.
+  u32x4_t xv[kMaxVec], gv[kMaxVec];
 #pragma unroll
   for (int u = 0; u < kMaxVec; ++u) {
     const int v = threadIdx.x + u * kRowThreads;
     if (v < nv) {
       xv[u] = x[v];
+      gv[u] = g[v];
+    }
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int u = 0; u < kMaxVec; ++u) {
+    const int v = threadIdx.x + u * kRowThreads;
+    if (v < nv) {
       float f[8];
       unpack_bf16x8(xv[u], f);
 #pragma unroll
@@ -109,14 +118,13 @@ __global__ __launch_bounds__(kRowThreads) void gather_rmsnorm_kernel<bf16_t>(
   }
   ss = block_sum<kRowThreads>(ss, red);
   const float inv = 1.0f / sqrtf(ss / (float)d + eps);
-  const u32x4_t* g = (const u32x4_t*)gamma;
 #pragma unroll
   for (int u = 0; u < kMaxVec; ++u) {
     const int v = threadIdx.x + u * kRowThreads;
     if (v < nv) {
       float f[8], gf[8];
       unpack_bf16x8(xv[u], f);
-      unpack_bf16x8(g[v], gf);
+      unpack_bf16x8(gv[u], gf);
 #pragma unroll
       for (int e = 0; e < 8; ++e) f[e] = f[e] * inv * gf[e];
       ((u32x4_t*)(h_out + (int64_t)i * d))[v] = pack_bf16x8(f);
@@ -139,7 +147,9 @@ hipError_t launch_gather_rmsnorm(const T* src, const int32_t* row_idx, int M, in
 // Reduce the split-K partials, rotate query and key heads to the row's
 // absolute position (rotate-half RoPE; the angles' cos/sin in fp64, computed
 // once per workgroup into LDS), store queries, append the rotated key and the
-// value to the sequence's cache slot.
+// value to the sequence's cache slot. The partial loads, which depend on
+// nothing, are issued first; the cache slot lookup and the angles overlap
+// them. In decode, one wave also writes the attention's partition offsets.
 // ----------------------------------------------------------------------------
 constexpr int kEpiHeads = 8;
 
@@ -149,12 +159,45 @@ __global__ __launch_bounds__(kEpiHeads * kWave) void qkv_epilogue_kernel(
     const int32_t* __restrict__ positions, const int32_t* __restrict__ seq_starts, int n_seqs,
     const int32_t* __restrict__ block_table, int max_blocks, const double* __restrict__ inv_freq,
     T* __restrict__ q_out, T* __restrict__ k_cache, T* __restrict__ v_cache,
-    const int32_t* __restrict__ ctx_lens, int32_t* __restrict__ split_off) {
+    const int32_t* __restrict__ ctx_lens, int32_t* __restrict__ split_off, int max_splits) {
   __shared__ float rot[2][128];  // cos, sin of the row's angles (hd / 2 <= 128)
   const int i = blockIdx.y, lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+  const int nh = Hq + 2 * Hkv;
   const int h = blockIdx.x * kEpiHeads + wv;
+  const bool live = h < nh;
   const int half = hd >> 1;
+  const int N = nh * hd;
+  const int64_t pstride = (int64_t)M * N;
+  const float* p = part + (int64_t)i * N + (int64_t)(live ? h : 0) * hd;
+  // Query/key heads: val[2t], val[2t+1] = dims j, j + hd/2 for j = lane + 64t;
+  // value heads: val[t] = dim lane + 64t.
+  float val[4] = {0.f, 0.f, 0.f, 0.f};
+  if (live) {
+    if (h < Hq + Hkv) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int j = lane + kWave * t;
+        if (j < half) {
+          val[2 * t] = sum_parts1<S>(p + j, pstride);
+          val[2 * t + 1] = sum_parts1<S>(p + j + half, pstride);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int e = lane + kWave * t;
+        if (e < hd) val[t] = sum_parts1<S>(p + e, pstride);
+      }
+    }
+  }
   const int pos = positions[i];
+  int64_t blk = 0;
+  int slot = 0;
+  if (live && h >= Hq) {
+    const int seq = row_to_seq(seq_starts, n_seqs, i);
+    blk = block_table[(int64_t)seq * max_blocks + pos / kBlockTokens];
+    slot = pos % kBlockTokens;
+  }
   // The row's rotation angles in fp64, once for all the heads of the block.
   for (int j = threadIdx.x; j < half; j += kEpiHeads * kWave) {
     double sn, cn;
@@ -164,12 +207,13 @@ __global__ __launch_bounds__(kEpiHeads * kWave) void qkv_epilogue_kernel(
   }
   __syncthreads();
   if (split_off != nullptr && blockIdx.x == 0 && i == 0 && wv == 0) {
-    // Decode attention work list: exclusive prefix sum of ceil(ctx / 256).
+    // Decode attention work list: exclusive prefix sum of ceil(ctx / 256),
+    // capped at max_splits (only invalid lengths reach the cap).
     int run = 0;
     if (lane == 0) split_off[0] = 0;
     for (int base = 0; base < n_seqs; base += kWave) {
       const int s = base + lane;
-      int v = s < n_seqs ? (ctx_lens[s] + kDecodeSplit - 1) / kDecodeSplit : 0;
+      int v = s < n_seqs ? min((ctx_lens[s] + kDecodeSplit - 1) / kDecodeSplit, max_splits) : 0;
 #pragma unroll
       for (int o = 1; o < kWave; o <<= 1) {
         const int t = __shfl_up(v, o, kWave);
@@ -179,37 +223,33 @@ __global__ __launch_bounds__(kEpiHeads * kWave) void qkv_epilogue_kernel(
       run += __shfl(v, kWave - 1, kWave);
     }
   }
-  if (h >= Hq + 2 * Hkv) return;
-  const int N = (Hq + 2 * Hkv) * hd;
-  const int64_t pstride = (int64_t)M * N;
-  const float* p = part + (int64_t)i * N + (int64_t)h * hd;
-  int64_t blk = 0;
-  int slot = 0;
-  if (h >= Hq) {
-    const int seq = row_to_seq(seq_starts, n_seqs, i);
-    blk = block_table[(int64_t)seq * max_blocks + pos / kBlockTokens];
-    slot = pos % kBlockTokens;
-  }
+  if (!live) return;
   if (h < Hq + Hkv) {
-    for (int j = lane; j < half; j += kWave) {
-      const float lo = sum_parts1<S>(p + j, pstride), hi = sum_parts1<S>(p + j + half, pstride);
-      const float c = rot[0][j], s = rot[1][j];
-      const float rlo = lo * c - hi * s, rhi = hi * c + lo * s;
-      if (h < Hq) {
-        T* dst = q_out + ((int64_t)i * Hq + h) * hd;
-        Elem<T>::store(dst + j, rlo);
-        Elem<T>::store(dst + j + half, rhi);
-      } else {
-        T* tile = k_cache + (blk * Hkv + (h - Hq)) * kBlockTokens * hd;
-        Elem<T>::store(tile + k_tile_offset(slot, j), rlo);
-        Elem<T>::store(tile + k_tile_offset(slot, j + half), rhi);
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int j = lane + kWave * t;
+      if (j < half) {
+        const float lo = val[2 * t], hi = val[2 * t + 1];
+        const float c = rot[0][j], sn = rot[1][j];
+        const float rlo = lo * c - hi * sn, rhi = hi * c + lo * sn;
+        if (h < Hq) {
+          T* dst = q_out + ((int64_t)i * Hq + h) * hd;
+          Elem<T>::store(dst + j, rlo);
+          Elem<T>::store(dst + j + half, rhi);
+        } else {
+          T* tile = k_cache + (blk * Hkv + (h - Hq)) * kBlockTokens * hd;
+          Elem<T>::store(tile + k_tile_offset(slot, j), rlo);
+          Elem<T>::store(tile + k_tile_offset(slot, j + half), rhi);
+        }
       }
     }
   } else {
-    const int kh = h - Hq - Hkv;
-    T* tile = v_cache + (blk * Hkv + kh) * kBlockTokens * hd;
-    for (int e = lane; e < hd; e += kWave)
-      Elem<T>::store(tile + v_tile_offset(slot, e), sum_parts1<S>(p + e, pstride));
+    T* tile = v_cache + (blk * Hkv + (h - Hq - Hkv)) * kBlockTokens * hd;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int e = lane + kWave * t;
+      if (e < hd) Elem<T>::store(tile + v_tile_offset(slot, e), val[t]);
+    }
   }
 }
 
@@ -229,15 +269,16 @@ hipError_t launch_qkv_epilogue(const float* part, int S, int M, int Hq, int Hkv,
                                const int32_t* positions, const int32_t* seq_starts,
                                int n_seqs, const int32_t* block_table, int max_blocks,
                                const double* inv_freq, T* q_out, T* k_cache, T* v_cache,
-                               const int32_t* ctx_lens, int32_t* split_off, hipStream_t st) {
+                               const int32_t* ctx_lens, int32_t* split_off, int max_splits,
+                               hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  if (hd > 256) return hipErrorInvalidValue;
+  if (hd > 256 || hd % 2 != 0) return hipErrorInvalidValue;
   const dim3 grid((Hq + 2 * Hkv + kEpiHeads - 1) / kEpiHeads, M);
   COCO_SWITCH_S(S, hipLaunchKernelGGL((qkv_epilogue_kernel<T, S_>), grid,
                                       dim3(kEpiHeads * kWave), 0, st,
                                       part, M, Hq, Hkv, hd, positions, seq_starts, n_seqs,
                                       block_table, max_blocks, inv_freq, q_out, k_cache,
-                                      v_cache, ctx_lens, split_off));
+                                      v_cache, ctx_lens, split_off, max_splits));
   return hipGetLastError();
 }
 
@@ -245,6 +286,17 @@ hipError_t launch_qkv_epilogue(const float* part, int S, int M, int Hq, int Hkv,
 // O-projection epilogue: residual add (kept in fp32) fused with RMSNorm_2.
 // One 1024-thread workgroup per row; every thread owns 4-column vectors.
 // ----------------------------------------------------------------------------
+template <typename T>
+__device__ __forceinline__ f32x4_t load4(const T* p);
+template <>
+__device__ __forceinline__ f32x4_t load4<float>(const float* p) { return *(const f32x4_t*)p; }
+template <>
+__device__ __forceinline__ f32x4_t load4<bf16_t>(const bf16_t* p) {
+  const u32x2_t u = *(const u32x2_t*)p;
+  return f32x4_t{__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u),
+                 __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xFFFF0000u)};
+}
+
 template <typename T, int S>
 __global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_kernel(
     const float* __restrict__ part, int M, int d, const T* __restrict__ x,
@@ -254,20 +306,29 @@ __global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_kernel(
   const int i = blockIdx.x;
   const int64_t pstride = (int64_t)M * d;
   const int nv = d / 4;
-  f32x4_t a[kMaxVec];
-  float ss = 0.f;
+  // Partials, residual and gains in one memory round trip.
+  f32x4_t a[kMaxVec], xr[kMaxVec], g[kMaxVec];
 #pragma unroll
   for (int u = 0; u < kMaxVec; ++u) {
     const int v = threadIdx.x + u * kNormThreads;
     if (v < nv) {
       const int c = 4 * v;
       a[u] = sum_parts4<S>(part + (int64_t)i * d + c, pstride);
+      xr[u] = load4<T>(x + (int64_t)i * d + c);
+      g[u] = load4<T>(gamma + c);
+    }
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int u = 0; u < kMaxVec; ++u) {
+    const int v = threadIdx.x + u * kNormThreads;
+    if (v < nv) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        a[u][e] += Elem<T>::load(x + (int64_t)i * d + c + e);
+        a[u][e] += xr[u][e];
         ss += a[u][e] * a[u][e];
       }
-      *(f32x4_t*)(x1 + (int64_t)i * d + c) = a[u];
+      *(f32x4_t*)(x1 + (int64_t)i * d + 4 * v) = a[u];
     }
   }
   ss = block_sum<kNormThreads>(ss, red);
@@ -279,7 +340,7 @@ __global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_kernel(
       const int c = 4 * v;
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        Elem<T>::store(h2 + (int64_t)i * d + c + e, a[u][e] * inv * Elem<T>::load(gamma + c + e));
+        Elem<T>::store(h2 + (int64_t)i * d + c + e, a[u][e] * inv * g[u][e]);
     }
   }
 }
@@ -393,7 +454,7 @@ hipError_t launch_kv_append(const T* k, const T* v, const int32_t* seq_idx,
   template hipError_t launch_qkv_epilogue<T>(const float*, int, int, int, int, int,          \
                                              const int32_t*, const int32_t*, int,            \
                                              const int32_t*, int, const double*, T*, T*, T*, \
-                                             const int32_t*, int32_t*, hipStream_t);         \
+                                             const int32_t*, int32_t*, int, hipStream_t);    \
   template hipError_t launch_residual_rmsnorm<T>(const float*, int, int, int, const T*,      \
                                                  const T*, float, float*, T*, hipStream_t);  \
   template hipError_t launch_swiglu<T>(const float*, int, int, int, T*, hipStream_t);        \

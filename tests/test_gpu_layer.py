@@ -152,6 +152,33 @@ def test_decode_split_batch_is_bit_identical():
             assert np.array_equal(k1, k2) and np.array_equal(v1, v2)
 
 
+def test_decode_of_many_sequences_matches_oracle_and_splits():
+    """300 decode sequences (the attention's partition offsets are a prefix
+    sum over 64 sequences at a time) with lengths on block and partition
+    edges: sampled rows against the oracle, the whole batch bit-identical to
+    two uneven halves."""
+    shape = small_bf16_shape()
+    edges = [0, 1, 15, 254, 255, 256, 257, 510, 511, 512, 700, 16]
+    priors = [edges[i % len(edges)] for i in range(300)]
+    b = ragged_decode_batch(9, priors, max_ctx=1025, hidden_rows=320,
+                            row_idx=np.random.default_rng(9).permutation(320)[:300])
+    rep = Replica.for_batch(shape, "s9", 1, b)
+    hidden = WD.hidden_tensor(shape, "s9", b.hidden_rows)
+    h0 = to64(hidden)
+    whole = hidden.clone()
+    rep.forward(0, whole, WD.batch_tensors(b))
+    torch.cuda.synchronize()
+    rows = [0, 5, 63, 64, 130, 255, 256, 257, 270, 299]
+    ref, _, _ = oracle_decode_rows(shape, "s9", 0, b, rows, h0)
+    got = to64(whole)[b.row_idx[rows]]
+    _check_rows("300-sequence decode", got, ref, h0[b.row_idx[rows]])
+    split = hidden.clone()
+    for part in (np.arange(0, 97), np.arange(97, 300)):
+        rep.forward(0, split, WD.batch_tensors(b.select(part)))
+    torch.cuda.synchronize()
+    assert torch.equal(split.view(torch.int16), whole.view(torch.int16))
+
+
 def test_prefill_request_aligned_split_is_bit_identical():
     shape = small_bf16_shape()
     b = ragged_prefill_batch(4, priors=[0, 5, 30, 200], lens=[70, 1, 33, 64], max_ctx=512,
