@@ -228,10 +228,10 @@ __global__ __launch_bounds__(kDecWaves * 64, 4) void attn_decode_kernel(
 
 // Merge the partitions of one (sequence, query head) in partition order.
 // Partition weights exp2(m_sp - max) are computed once into LDS (dynamic,
-// 2 * max_splits floats); each thread then owns one head dimension. The
-// first kPre partitions' values are loaded together with the (max, sum)
-// pairs, so a sequence of up to kPre * 256 tokens needs one memory round
-// trip after its length.
+// 2 * max_splits floats); each thread then owns one head dimension. Loads
+// that do not depend on the sequence's length go out together with it (the
+// first kPre partitions' values and the thread's own (max, sum) pair), so a
+// sequence of up to kPre * 256 tokens needs one memory round trip.
 constexpr int kPre = 8;
 
 __global__ __launch_bounds__(HD) void attn_combine_kernel(const float* __restrict__ part_o,
@@ -242,14 +242,26 @@ __global__ __launch_bounds__(HD) void attn_combine_kernel(const float* __restric
   extern __shared__ float sm[];  // [0, max_splits): weights; [max_splits, 2*max_splits): l
   __shared__ float red[HD / kWave];
   const int h = blockIdx.x, s = blockIdx.y, dim = threadIdx.x;
-  const int nsp = min((ctx_lens[s] + kDecodeSplit - 1) / kDecodeSplit, max_splits);
   const int64_t base = ((int64_t)s * Hq + h) * max_splits;
   const float* po = part_o + base * HD + dim;
+  // Slots past the sequence's partition count hold stale values; they are
+  // loaded (inside the workspace) but never used.
   float pre[kPre];
 #pragma unroll
-  for (int k = 0; k < kPre; ++k) pre[k] = k < nsp ? po[k * HD] : 0.f;
+  for (int k = 0; k < kPre; ++k) pre[k] = k < max_splits ? po[k * HD] : 0.f;
+  float m_own = -INFINITY, l_own = 0.f;
+  if (dim < max_splits) {
+    m_own = part_ml[(base + dim) * 2];
+    l_own = part_ml[(base + dim) * 2 + 1];
+  }
+  const int nsp = min((ctx_lens[s] + kDecodeSplit - 1) / kDecodeSplit, max_splits);
   float mx = -INFINITY;
-  for (int sp = dim; sp < nsp; sp += HD) {
+  if (dim < nsp) {
+    sm[dim] = m_own;
+    sm[max_splits + dim] = l_own;
+    mx = m_own;
+  }
+  for (int sp = dim + HD; sp < nsp; sp += HD) {
     const float m = part_ml[(base + sp) * 2];
     sm[sp] = m;
     sm[max_splits + sp] = part_ml[(base + sp) * 2 + 1];

@@ -146,7 +146,8 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
           if (c16 < 8 && m < M)
             H[(int64_t)m * (N / 2) + o0 + c16] = (bf16_t)f32_to_bf16(g / (1.0f + expf(-g)) * u);
         } else if (m < M) {
-          out[(int64_t)m * N + n_col] = acc[mt][r];
+          // Non-temporal: the partials are read once, by the next kernel.
+          __builtin_nontemporal_store(acc[mt][r], out + (int64_t)m * N + n_col);
         }
       }
     }

@@ -6,13 +6,17 @@
 //   * a 512-thread workgroup computes a 256 x 256 tile; each of its eight
 //     waves owns a 128 x 64 sub-tile as 4 x 2 v_mfma_f32_32x32x16_bf16
 //     accumulators, two waves per SIMD so that one wave's MFMAs issue while
-//     the other waits on LDS or the barrier (measured 20-25% faster than four
-//     waves of 128 x 128 on the large shapes, with identical bits);
-//   * 64-deep K stages of A and W tiles are staged through LDS (2 x 64 KB,
-//     double-buffered) with 16-byte chunks XOR-swizzled by row pair, so the
-//     rows a wave reads per MFMA operand fall in distinct banks; the next
-//     stage's global loads are in flight while the current stage is
-//     multiplied;
+//     the other waits on LDS or the barrier;
+//   * 32-deep K stages of the A and W tiles go straight from global memory
+//     to LDS (global_load_lds, 16 bytes per lane, no register staging) into
+//     a ring of four buffers, three stages in flight. Each wave fills 32 rows
+//     of both tiles with four 1 KB loads per stage. 16-byte chunks are
+//     XOR-swizzled by row quad (chunk ^ (r / 4) % 4), so the 16 rows a
+//     fragment read touches per 16-lane group fall on distinct banks;
+//   * one barrier per stage: the barrier at the top of stage st publishes
+//     stage st + 1, so the first fragments of the next stage are read while
+//     the second half of this stage's MFMAs runs, and the stage that the
+//     next loads overwrite (st - 1) has been fully read by every wave;
 //   * workgroups are remapped so that the tiles sharing a W column slab run
 //     on the same XCD (blockIdx % 8) back to back and hit its L2;
 //   * narrow outputs with a long K are split into K-slices (tile_splits, a
@@ -29,31 +33,57 @@ namespace coco {
 
 namespace {
 
-constexpr int kTM = 256, kTN = 256, kTK = 64;
+constexpr int kTM = 256, kTN = 256, kTK = 32;
+constexpr int kTBuf = 4;        // LDS ring depth (stages)
 constexpr int kTThreads = 512;  // 8 waves, two per SIMD
 constexpr int kXCDs = 8;
 
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void lds_void_t;
 
-// LDS element offset of 16-byte chunk c (0..7) of row r in a [256][64] tile.
-// A 16-lane group of a 16-byte-per-lane LDS access covers 256 bytes (all 64
-// banks) = two 128-byte rows; XOR-ing the chunk with (r / 2) % 8 gives the
-// 16 consecutive rows a fragment read touches, and the two rows a store
-// group writes, 16 distinct 4-bank slots.
-__device__ __forceinline__ int swz(int r, int c) { return r * kTK + ((c ^ ((r >> 1) & 7)) << 3); }
+// LDS element offset of 16-byte chunk c (0..3) of row r in a [256][32] tile.
+// A 16-lane group of a 16-byte-per-lane access covers 256 bytes (all 64
+// banks) = four 64-byte rows; XOR-ing the chunk with (r / 4) % 4 spreads the
+// 16 consecutive rows a fragment read touches over 16 distinct 4-bank slots.
+__device__ __forceinline__ int swz(int r, int c) { return r * kTK + ((c ^ ((r >> 2) & 3)) << 3); }
+
+// Waits until at most N vector-memory operations of this wave are in flight
+// (vmcnt only; the direct-to-LDS loads count there).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// Workgroup barrier that keeps the compiler from moving memory operations
+// across it and adds no waits of its own: the direct-to-LDS loads of later
+// stages stay in flight through it (a __syncthreads() fence would drain them).
+__device__ __forceinline__ void stage_barrier() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// One LDS object per ring slot, so the compiler tracks each slot's pending
+// direct loads on its own and never drains the ring before a fragment read.
+__shared__ __attribute__((aligned(16))) bf16_t g_ta0[kTM * kTK], g_ta1[kTM * kTK],
+    g_ta2[kTM * kTK], g_ta3[kTM * kTK];
+__shared__ __attribute__((aligned(16))) bf16_t g_tw0[kTN * kTK], g_tw1[kTN * kTK],
+    g_tw2[kTN * kTK], g_tw3[kTN * kTK];
 
 // FUSE: W is the [2F][K] gate/up matrix; each 32-column half of a wave's
 // 64 columns holds gate rows and the other the matching up rows, so each lane
 // owns both factors of its outputs and the epilogue writes h = silu(gate) *
 // up in bf16 to the [M][F] buffer `H` (N = 2F, one K-slice). Otherwise C is
-// the fp32 partial.
+// the fp32 partial. k_slice is a multiple of kTK * kTBuf.
 template <bool FUSE>
 __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __restrict__ A,
                                                                  const bf16_t* __restrict__ W,
                                                                  float* __restrict__ C,
                                                                  bf16_t* __restrict__ H, int M,
                                                                  int N, int K, int k_slice) {
-  __shared__ __attribute__((aligned(16))) bf16_t lds[2][2][kTM * kTK];  // [buf][A|W]
+  bf16_t* const ta[kTBuf] = {g_ta0, g_ta1, g_ta2, g_ta3};
+  bf16_t* const tw[kTBuf] = {g_tw0, g_tw1, g_tw2, g_tw3};
 
   const int tiles_m = (M + kTM - 1) / kTM;
   const int nb = gridDim.x;
@@ -66,7 +96,8 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
   C += (int64_t)blockIdx.y * M * N;
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wv = tid >> 6;
+  const int lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wv & 1, wn = wv >> 1;  // 128-row half, 64-column quarter
   const int l32 = lane & 31, hi = lane >> 5;
 
@@ -79,26 +110,31 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
     return (j ? F : 0) + o0 + 32 * w + i;
   };
 
-  u32x4_t ra[4], rw[4];
+  // This lane's sources: wave wv fills rows 32 wv .. 32 wv + 31 of both tiles,
+  // 16 rows (1 KB) per load; lane l lands at row + l / 4, slot l % 4, which
+  // holds logical chunk (l % 4) ^ (row / 4) % 4. Rows past M repeat row M - 1
+  // (never stored).
   const int stages = k_slice / kTK;
-  auto load = [&](int st) {
-    const int k0 = kb + min(st, stages - 1) * kTK;
+  const bf16_t* src_a[2];
+  const bf16_t* src_w[2];
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int q = tid + v * kTThreads;
-      const int r = q >> 3, c = q & 7;
-      const int m = min(m0 + r, M - 1), n = w_row(r);
-      ra[v] = *(const u32x4_t*)(A + (int64_t)m * K + k0 + c * 8);
-      rw[v] = *(const u32x4_t*)(W + (int64_t)n * K + k0 + c * 8);
-    }
-  };
-  auto store = [&](int buf) {
+  for (int h = 0; h < 2; ++h) {
+    const int r = 32 * wv + 16 * h + (lane >> 2);
+    const int c = (lane & 3) ^ ((r >> 2) & 3);
+    src_a[h] = A + (int64_t)min(m0 + r, M - 1) * K + kb + c * 8;
+    src_w[h] = W + (int64_t)w_row(r) * K + kb + c * 8;
+  }
+  // Loads past the slice repeat its last stage (never multiplied).
+  auto issue = [&](int st, int slot) {
+    const int ko = min(st, stages - 1) * kTK;
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int q = tid + v * kTThreads;
-      const int r = q >> 3, c = q & 7;
-      *(u32x4_t*)(&lds[buf][0][swz(r, c)]) = ra[v];
-      *(u32x4_t*)(&lds[buf][1][swz(r, c)]) = rw[v];
+    for (int h = 0; h < 2; ++h) {
+      __builtin_amdgcn_global_load_lds(src_a[h] + ko,
+                                       (lds_void_t*)(ta[slot] + (32 * wv + 16 * h) * kTK), 16,
+                                       0, 0);
+      __builtin_amdgcn_global_load_lds(src_w[h] + ko,
+                                       (lds_void_t*)(tw[slot] + (32 * wv + 16 * h) * kTK), 16,
+                                       0, 0);
     }
   };
 
@@ -121,46 +157,41 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
       w[j] = __builtin_bit_cast(
           bf16x8_t, *(const u32x4_t*)(&lw[swz(wn * 64 + j * 32 + l32, c)]));
   };
-
-  load(0);
-  store(0);
-  __syncthreads();
-  load(1);
-
-  for (int st = 0; st < stages; ++st) {
-    const int buf = st & 1;
-    const bf16_t* la = lds[buf][0];
-    const bf16_t* lw = lds[buf][1];
-    bf16x8_t a[2][4], w[2][2];
-    read_frags(la, lw, 0, a[0], w[0]);
+  auto mfma_step = [&](const bf16x8_t* a, const bf16x8_t* w) {
 #pragma unroll
-    for (int kk = 0; kk < kTK / 16; ++kk) {
-      const int cur = kk & 1;
-      if (kk + 1 < kTK / 16) read_frags(la, lw, kk + 1, a[cur ^ 1], w[cur ^ 1]);
-      if (kk == 1) store(buf ^ 1);
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] =
-              __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[cur][i], w[cur][j], acc[i][j], 0, 0, 0);
-      if (kk == 1) load(st + 2);
-      if (kk + 1 < kTK / 16) {
-        for (int g = 0; g < 6; ++g) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-      }
-      if (kk == 1) {
-        for (int g = 0; g < 8; ++g) {
-          __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // DS write
-          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read
-        }
-      }
+      for (int j = 0; j < 2; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], w[j], acc[i][j], 0, 0, 0);
+    // Interleave the six fragment reads issued next to these MFMAs.
+    for (int g = 0; g < 6; ++g) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
     }
-    __syncthreads();
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+  };
+
+  issue(0, 0);
+  issue(1, 1);
+  issue(2, 2);
+  wait_vmcnt<8>();  // this wave's stage-0 loads are in LDS
+  stage_barrier();  // ... and every wave's
+  bf16x8_t a0[4], w0[2], a1[4], w1[2];
+  read_frags(ta[0], tw[0], 0, a0, w0);
+  for (int st0 = 0; st0 < stages; st0 += kTBuf) {
+#pragma unroll
+    for (int u = 0; u < kTBuf; ++u) {
+      const int st = st0 + u;
+      wait_vmcnt<4>();  // this wave's loads of stage st + 1 are in LDS
+      stage_barrier();  // every wave's: stage st + 1 published, stage st - 1 read
+      issue(st + 3, (u + 3) % kTBuf);
+      read_frags(ta[u], tw[u], 1, a1, w1);
+      mfma_step(a0, w0);
+      read_frags(ta[(u + 1) % kTBuf], tw[(u + 1) % kTBuf], 0, a0, w0);
+      mfma_step(a1, w1);
+    }
   }
+  wait_vmcnt<0>();  // no direct load outlives the workgroup
 
   if (FUSE) {
 #pragma unroll
@@ -203,14 +234,14 @@ int tile_splits(int N, int K) {
   int S = (K + 4096) / 8192;
   if (S < 1) S = 1;
   if (S > 4) S = 4;
-  while (S > 1 && (K / kTK) % S != 0) --S;
+  while (S > 1 && (K / (kTK * kTBuf)) % S != 0) --S;
   return S;  // 1..4: the split counts the epilogues are built for
 }
 
 hipError_t launch_gemm_tile_bf16(const uint16_t* A, const uint16_t* W, float* C, int M, int N,
                                  int K, int S, hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  if (S < 1 || K % (kTK * S) != 0) return hipErrorInvalidValue;
+  if (S < 1 || K % (kTK * kTBuf * S) != 0) return hipErrorInvalidValue;
   const int tiles = ((M + kTM - 1) / kTM) * ((N + kTN - 1) / kTN);
   hipLaunchKernelGGL(gemm_tile_kernel<false>, dim3(tiles, S), dim3(kTThreads), 0, st, A, W, C,
                      nullptr, M, N, K, K / S);
@@ -220,7 +251,7 @@ hipError_t launch_gemm_tile_bf16(const uint16_t* A, const uint16_t* W, float* C,
 hipError_t launch_gemm_tile_swiglu_bf16(const uint16_t* A, const uint16_t* W_gate_up,
                                         uint16_t* H, int M, int F, int K, hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  if (F % (kTN / 2) != 0 || K % kTK != 0 || tile_splits(2 * F, K) != 1)
+  if (F % (kTN / 2) != 0 || K % (kTK * kTBuf) != 0 || tile_splits(2 * F, K) != 1)
     return hipErrorInvalidValue;
   const int tiles = ((M + kTM - 1) / kTM) * (2 * F / kTN);
   hipLaunchKernelGGL(gemm_tile_kernel<true>, dim3(tiles, 1), dim3(kTThreads), 0, st, A,
