@@ -185,8 +185,12 @@ int coco_layer_span_forward(coco_layer_t h, int32_t first_layer, int32_t n_layer
  * row i holds call row i of the last layer run. Copies min(dst_bytes, buffer
  * size) bytes on `stream`. */
 enum {
-  COCO_WS_X = 0,  /* layer input rows, [max_rows][d], dtype */
-  COCO_WS_H = 1,  /* RMSNorm_1 output, [max_rows][d], dtype */
+  COCO_WS_X = 0,  /* layer input rows, [max_rows][d], dtype (written by the
+                     first layer of prefill and fp32 calls, and for every
+                     later layer of a span) */
+  COCO_WS_H = 1,  /* RMSNorm_1 output, [max_rows][d], dtype (prefill and
+                     fp32 calls; bf16 decode folds RMSNorm_1 into the QKV
+                     projection and never writes it) */
   COCO_WS_Q = 2,  /* rotated queries, [max_rows][Hq*hd], dtype */
   COCO_WS_O = 3,  /* attention output, [max_rows][Hq*hd], dtype */
   COCO_WS_X1 = 4, /* residual after the O projection, [max_rows][d], fp32 */

@@ -47,6 +47,7 @@ struct coco_layer {
   // workspace carve-out
   void *x = nullptr, *h = nullptr, *q = nullptr, *o = nullptr, *h2 = nullptr, *u = nullptr;
   float *x1 = nullptr, *part = nullptr, *attn_o = nullptr, *attn_ml = nullptr;
+  float* ss = nullptr;  // per-slice row sums of squares (decode QKV with RMSNorm_1 folded in)
   double* inv_freq = nullptr;
   int32_t* split_off = nullptr;  // decode attention work list offsets
   size_t act_rows_bytes[7] = {};
@@ -183,8 +184,8 @@ int coco_layer_init(const coco_layer_config* cfg, const coco_layer_weights* laye
   H->dec_rows = c.max_rows < c.max_seqs ? c.max_rows : c.max_seqs;
 
   size_t off = 0;
-  size_t offs[12];
-  const size_t sizes[12] = {
+  size_t offs[13];
+  const size_t sizes[13] = {
       align256(R * d * eb),          // x
       align256(R * d * eb),          // h
       align256(R * qd * eb),         // q
@@ -196,8 +197,9 @@ int coco_layer_init(const coco_layer_config* cfg, const coco_layer_weights* laye
       c.dtype == COCO_BF16 ? align256((size_t)H->dec_rows * c.n_q_heads * H->max_splits * 128 * 4) : 0,
       c.dtype == COCO_BF16 ? align256((size_t)H->dec_rows * c.n_q_heads * H->max_splits * 2 * 4) : 0,
       align256((size_t)(c.head_dim / 2) * 8),  // inv_freq
-      align256((size_t)(H->dec_rows + 1) * 4)};  // split_off
-  for (int i = 0; i < 12; ++i) {
+      align256((size_t)(H->dec_rows + 1) * 4),  // split_off
+      align256((size_t)16 * R * 4)};  // ss: at most 16 K-slices
+  for (int i = 0; i < 13; ++i) {
     offs[i] = off;
     off += sizes[i];
   }
@@ -219,6 +221,7 @@ int coco_layer_init(const coco_layer_config* cfg, const coco_layer_weights* laye
   H->attn_ml = (float*)(H->ws + offs[9]);
   H->inv_freq = (double*)(H->ws + offs[10]);
   H->split_off = (int32_t*)(H->ws + offs[11]);
+  H->ss = (float*)(H->ws + offs[12]);
   H->act_rows_bytes[COCO_WS_X] = R * d * eb;
   H->act_rows_bytes[COCO_WS_H] = R * d * eb;
   H->act_rows_bytes[COCO_WS_Q] = R * qd * eb;
@@ -486,13 +489,31 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
   for (int l = first; l < first + nl; ++l) {
     const coco_layer_weights& w = H->layers[l];
     const bool first_l = l == first, last_l = l == first + nl - 1;
-    // Gather (first layer of the segment) + RMSNorm_1.
-    TIMED(COCO_K_GATHER_NORM,
-          HIPCHK(launch_gather_rmsnorm<T>(first_l ? hidden : x, first_l ? row_idx : nullptr, M,
-                                          d, (const T*)w.gamma_attn, c.rms_eps,
-                                          first_l ? x : nullptr, h, st)));
+    // Decode (bf16) folds the gather and RMSNorm_1 into the QKV projection:
+    // it stages bf16(x * gamma) straight from the input rows and the QKV
+    // epilogue applies each row's 1/rms. Otherwise a gather + RMSNorm_1
+    // kernel writes x and h first.
+    const bool fold_norm = !pre && std::is_same<T, bf16_t>::value;
+    const T* x_src = first_l ? hidden : x;                     // this layer's input rows
+    const int32_t* x_idx = first_l ? row_idx : nullptr;
+    if (!fold_norm)
+      TIMED(COCO_K_GATHER_NORM,
+            HIPCHK(launch_gather_rmsnorm<T>(first_l ? hidden : x, first_l ? row_idx : nullptr, M,
+                                            d, (const T*)w.gamma_attn, c.rms_eps,
+                                            first_l ? x : nullptr, h, st)));
     // QKV projection, RoPE, local cache append.
-    TIMED(COCO_K_GEMM_QKV, if ((rc = gemm<T>(H, h, (const T*)w.w_qkv, M, nqkv, d, pre, &S, st))) return rc);
+    if (fold_norm) {
+      const SkinnyPlan plan = skinny_plan(nqkv, d);
+      if (plan.waves == 0) return fail(COCO_EINVAL, "no GEMM plan for N=%d K=%d", nqkv, d);
+      S = plan.S;
+      TIMED(COCO_K_GEMM_QKV,
+            HIPCHK(launch_gemm_skinny_norm_bf16((const bf16_t*)x_src, x_idx,
+                                                (const bf16_t*)w.gamma_attn,
+                                                (const bf16_t*)w.w_qkv, H->part, H->ss, M, nqkv, d,
+                                                plan, st)));
+    } else {
+      TIMED(COCO_K_GEMM_QKV, if ((rc = gemm<T>(H, h, (const T*)w.w_qkv, M, nqkv, d, pre, &S, st))) return rc);
+    }
     TIMED(COCO_K_QKV_EPILOGUE,
           HIPCHK(launch_qkv_epilogue<T>(H->part, S, M, Hq, Hkv, hd, positions, seq_starts,
                                         n_seqs, bt, c.max_blocks_per_seq, H->inv_freq, q,
@@ -500,13 +521,15 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
                                         (seq_starts == nullptr && c.dtype == COCO_BF16)
                                             ? H->split_off
                                             : nullptr,
-                                        H->max_splits, st)));
+                                        H->max_splits, fold_norm ? H->ss : nullptr, d, c.rms_eps,
+                                        st)));
     // Attention over the paged cache.
     if ((rc = attention<T>(H, w, M, positions, seq_starts, n_seqs, bt, ctx, st))) return rc;
     // O projection + residual + RMSNorm_2.
     TIMED(COCO_K_GEMM_O, if ((rc = gemm<T>(H, o, (const T*)w.w_o, M, d, Hq * hd, pre, &S, st))) return rc);
     TIMED(COCO_K_RESIDUAL_NORM,
-          HIPCHK(launch_residual_rmsnorm<T>(H->part, S, M, d, x, (const T*)w.gamma_mlp,
+          HIPCHK(launch_residual_rmsnorm<T>(H->part, S, M, d, fold_norm ? x_src : x,
+                                            fold_norm ? x_idx : nullptr, (const T*)w.gamma_mlp,
                                             c.rms_eps, H->x1, h2, st)));
     // SwiGLU MLP (prefill: SwiGLU in the gate/up GEMM's epilogue when the
     // GEMM is not split along K).

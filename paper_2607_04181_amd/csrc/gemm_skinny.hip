@@ -16,6 +16,11 @@
 //     16-rows-per-instruction fragment reads hit distinct banks;
 //   * each 16x16 output tile is accumulated with v_mfma_f32_16x16x32_bf16 in
 //     ascending k.
+// The NORM variant (decode QKV projection) folds the row gather and the
+// first RMSNorm into the activation staging: it reads the layer input rows
+// x[row_idx[m]] directly, stages bf16(x * gamma), and writes each row's sum
+// of x^2 over its K-slice; the 1/rms factor of a row is a scalar that the
+// consumer applies to the summed partials.
 // The plan (WAVES, split count S) is chosen from (N, K) alone (skinny_plan);
 // every output element is
 // summed in the same k order for any M, so a row's result does not depend on
@@ -40,10 +45,16 @@ __device__ __forceinline__ int a_swz(int r, int c) { return r * kBK + ((c ^ (r &
 // c16 < 8 of a wave stream gate rows o0..o0+7 and lanes c16 >= 8 the
 // matching up rows, so the epilogue pairs lanes c16 and c16+8 and writes
 // h = silu(gate) * up in bf16 to H[M][F] instead of fp32 partials.
-template <int WAVES, int MT, int PF, bool FUSE>
+// NORM: A holds the layer input rows, row m of the call at A[row_idx[m]]
+// (row_idx null: row m); the staged operand is bf16(A * gamma) and
+// ss[blockIdx.y][m] receives the row's sum of squares over the K-slice
+// (row m by the workgroup of the slice with blockIdx.x == m % gridDim.x).
+template <int WAVES, int MT, int PF, bool FUSE, bool NORM>
 __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
     const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, float* __restrict__ part,
-    bf16_t* __restrict__ H, int M, int N, int K, int k_slice) {
+    bf16_t* __restrict__ H, int M, int N, int K, int k_slice,
+    const int32_t* __restrict__ row_idx, const bf16_t* __restrict__ gamma,
+    float* __restrict__ ss) {
   constexpr int NT = WAVES * 64;
   constexpr int kChunks = MT * 16 * (kBK / 8);  // 16-byte A chunks per stage
   constexpr int kPerT = (kChunks + NT - 1) / NT;
@@ -85,28 +96,70 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
     // Activation ring: stage x lives in register slot x % 2 from the start of
     // stage x-2 until it is copied to LDS buffer x % 2 at the end of stage
     // x-1, so its L2 latency is hidden behind two stages of weight streaming.
+    // A thread stages the same (row, 16-byte chunk column) of every stage:
+    // rows (tid + v * NT) / 16 and chunk column tid % 16 (NT is a multiple of
+    // 16), so under NORM it needs one gain chunk per stage and keeps one sum
+    // of squares per row it stages.
     u32x4_t areg[2][kPerT];
+    u32x4_t greg[2];
+    int arow[kPerT];  // source row of each staged chunk (32-bit to spare registers)
+#pragma unroll
+    for (int v = 0; v < kPerT; ++v) {
+      const int q = min(tid + v * NT, kChunks - 1);
+      const int m = min(m0 + (q >> 4), M - 1);
+      arow[v] = (NORM && row_idx) ? row_idx[m] : m;
+    }
+    const bf16_t* a_col = A + k_begin + (tid & 15) * 8;  // NT % 16 == 0: column tid % 16
     auto load_a = [&](int st, int slot) {
       const int sc = min(st, stages - 1);
 #pragma unroll
-      for (int v = 0; v < kPerT; ++v) {
-        const int q = min(tid + v * NT, kChunks - 1);
-        const int m = min(m0 + (q >> 4), M - 1);
-        areg[slot][v] = *(const u32x4_t*)(A + (int64_t)m * K + k_begin + sc * kBK + (q & 15) * 8);
-      }
+      for (int v = 0; v < kPerT; ++v)
+        areg[slot][v] = *(const u32x4_t*)(a_col + (int64_t)arow[v] * K + sc * kBK);
+      if (NORM) greg[slot] = *(const u32x4_t*)(gamma + k_begin + sc * kBK + (tid & 15) * 8);
     };
     auto store_a = [&](int st, int slot, int buf) {
 #pragma unroll
       for (int v = 0; v < kPerT; ++v) {
         const int q = tid + v * NT;
         const bool live = st < stages && m0 + (q >> 4) < M;
-        const u32x4_t val = live ? areg[slot][v] : u32x4_t{0u, 0u, 0u, 0u};
+        u32x4_t val = live ? areg[slot][v] : u32x4_t{0u, 0u, 0u, 0u};
+        if (NORM) {
+          // x * gamma in fp32, rounded to bf16.
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float lo = __uint_as_float(val[e] << 16), hi = __uint_as_float(val[e] & 0xFFFF0000u);
+            const float glo = __uint_as_float(greg[slot][e] << 16);
+            const float ghi = __uint_as_float(greg[slot][e] & 0xFFFF0000u);
+            val[e] = pack_bf16x2(lo * glo, hi * ghi);
+          }
+        }
         if (q < kChunks) *(u32x4_t*)(&lds[buf][a_swz(q >> 4, q & 15)]) = val;
       }
     };
 
     load_a(0, 0);
     load_a(1, 1);
+    if (NORM && wv == 0) {
+      // Sums of squares of this K-slice for rows m0 + blockIdx.x, + gridDim.x,
+      // ... (each row by one workgroup of the slice), while the first weight
+      // stages are in flight: per lane in chunk order, then a fixed butterfly.
+      for (int r = m0 + blockIdx.x; r < min(M, m0 + MT * 16); r += gridDim.x) {
+        const bf16_t* xr =
+            A + (int64_t)((row_idx != nullptr) ? row_idx[r] : r) * K + k_begin;
+        float t = 0.f;
+        for (int c = lane; c < k_slice / 8; c += 64) {
+          const u32x4_t u = *(const u32x4_t*)(xr + c * 8);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float lo = __uint_as_float(u[e] << 16), hi = __uint_as_float(u[e] & 0xFFFF0000u);
+            t = fmaf(lo, lo, t);
+            t = fmaf(hi, hi, t);
+          }
+        }
+        t = wave_sum(t);
+        if (lane == 0) ss[(int64_t)blockIdx.y * M + r] = t;
+      }
+    }
     store_a(0, 0, 0);
     __syncthreads();
 
@@ -154,34 +207,41 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
   }
 }
 
-template <int WAVES, int MT, bool FUSE>
+struct NormArgs {
+  const int32_t* row_idx = nullptr;
+  const uint16_t* gamma = nullptr;
+  float* ss = nullptr;
+};
+
+template <int WAVES, int MT, bool FUSE, bool NORM>
 hipError_t launch_plan(const uint16_t* A, const uint16_t* W, float* part, uint16_t* H, int M,
-                       int N, int K, int S, hipStream_t st) {
+                       int N, int K, int S, NormArgs na, hipStream_t st) {
   // Two stages of weights in flight per wave (~56 KB per CU at 7 waves) is
   // enough to cover HBM latency; deeper rings measured slower (more requests
   // queued behind each other) and cost registers.
   constexpr int PF = 2;
-  hipLaunchKernelGGL((gemm_skinny_kernel<WAVES, MT, PF, FUSE>), dim3(N / (16 * WAVES), S),
-                     dim3(WAVES * 64), 0, st, A, W, part, H, M, N, K, K / S);
+  hipLaunchKernelGGL((gemm_skinny_kernel<WAVES, MT, PF, FUSE, NORM>), dim3(N / (16 * WAVES), S),
+                     dim3(WAVES * 64), 0, st, A, W, part, H, M, N, K, K / S, na.row_idx,
+                     (const bf16_t*)na.gamma, na.ss);
   return hipGetLastError();
 }
 
-template <int WAVES, bool FUSE>
+template <int WAVES, bool FUSE, bool NORM>
 hipError_t launch_waves(const uint16_t* A, const uint16_t* W, float* part, uint16_t* H, int M,
-                        int N, int K, int S, hipStream_t st) {
-  return M <= 64 ? launch_plan<WAVES, 4, FUSE>(A, W, part, H, M, N, K, S, st)
-                 : launch_plan<WAVES, 8, FUSE>(A, W, part, H, M, N, K, S, st);
+                        int N, int K, int S, NormArgs na, hipStream_t st) {
+  return M <= 64 ? launch_plan<WAVES, 4, FUSE, NORM>(A, W, part, H, M, N, K, S, na, st)
+                 : launch_plan<WAVES, 8, FUSE, NORM>(A, W, part, H, M, N, K, S, na, st);
 }
 
-template <bool FUSE>
+template <bool FUSE, bool NORM>
 hipError_t launch_any(const uint16_t* A, const uint16_t* W, float* part, uint16_t* H, int M,
-                      int N, int K, SkinnyPlan plan, hipStream_t st) {
+                      int N, int K, SkinnyPlan plan, NormArgs na, hipStream_t st) {
   switch (plan.waves) {
-    case 4: return launch_waves<4, FUSE>(A, W, part, H, M, N, K, plan.S, st);
-    case 5: return launch_waves<5, FUSE>(A, W, part, H, M, N, K, plan.S, st);
-    case 6: return launch_waves<6, FUSE>(A, W, part, H, M, N, K, plan.S, st);
-    case 7: return launch_waves<7, FUSE>(A, W, part, H, M, N, K, plan.S, st);
-    default: return launch_waves<8, FUSE>(A, W, part, H, M, N, K, plan.S, st);
+    case 4: return launch_waves<4, FUSE, NORM>(A, W, part, H, M, N, K, plan.S, na, st);
+    case 5: return launch_waves<5, FUSE, NORM>(A, W, part, H, M, N, K, plan.S, na, st);
+    case 6: return launch_waves<6, FUSE, NORM>(A, W, part, H, M, N, K, plan.S, na, st);
+    case 7: return launch_waves<7, FUSE, NORM>(A, W, part, H, M, N, K, plan.S, na, st);
+    default: return launch_waves<8, FUSE, NORM>(A, W, part, H, M, N, K, plan.S, na, st);
   }
 }
 
@@ -226,7 +286,22 @@ hipError_t launch_gemm_skinny_bf16(const uint16_t* A, const uint16_t* W, float* 
   if (plan.waves < 4 || plan.waves > 8 || N % (16 * plan.waves) != 0 ||
       K % (plan.S * kBK) != 0)
     return hipErrorInvalidValue;
-  return launch_any<false>(A, W, part, nullptr, M, N, K, plan, st);
+  return launch_any<false, false>(A, W, part, nullptr, M, N, K, plan, NormArgs{}, st);
+}
+
+hipError_t launch_gemm_skinny_norm_bf16(const uint16_t* X, const int32_t* row_idx,
+                                        const uint16_t* gamma, const uint16_t* W, float* part,
+                                        float* ss, int M, int N, int K, SkinnyPlan plan,
+                                        hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  if (plan.waves < 4 || plan.waves > 8 || N % (16 * plan.waves) != 0 ||
+      K % (plan.S * kBK) != 0)
+    return hipErrorInvalidValue;
+  NormArgs na;
+  na.row_idx = row_idx;
+  na.gamma = gamma;
+  na.ss = ss;
+  return launch_any<false, true>(X, W, part, nullptr, M, N, K, plan, na, st);
 }
 
 hipError_t launch_gemm_skinny_swiglu_bf16(const uint16_t* A, const uint16_t* W_gate_up,
@@ -236,7 +311,7 @@ hipError_t launch_gemm_skinny_swiglu_bf16(const uint16_t* A, const uint16_t* W_g
   if (plan.S != 1 || plan.waves < 4 || plan.waves > 8 || (2 * F) % (16 * plan.waves) != 0 ||
       K % kBK != 0)
     return hipErrorInvalidValue;
-  return launch_any<true>(A, W_gate_up, nullptr, H, M, 2 * F, K, plan, st);
+  return launch_any<true, false>(A, W_gate_up, nullptr, H, M, 2 * F, K, plan, NormArgs{}, st);
 }
 
 // ----------------------------------------------------------------------------

@@ -16,6 +16,8 @@ hipError_t launch_gather_rmsnorm(const T* src, const int32_t* row_idx, int M, in
 
 // Sum of S split-K partials of the QKV projection, RoPE on query and key
 // heads, queries to q_out [M][Hq*hd], keys/values into the paged cache.
+// With ss non-null (decode, RMSNorm_1 folded into the projection), each row's
+// sums are first scaled by 1 / sqrt(sum_s ss[s][row] / d + eps).
 // With split_off non-null (decode), one workgroup also writes the decode
 // attention's partition offsets from ctx_lens (counts capped at max_splits).
 template <typename T>
@@ -24,13 +26,14 @@ hipError_t launch_qkv_epilogue(const float* part, int S, int M, int Hq, int Hkv,
                                int n_seqs, const int32_t* block_table, int max_blocks,
                                const double* inv_freq, T* q_out, T* k_cache, T* v_cache,
                                const int32_t* ctx_lens, int32_t* split_off, int max_splits,
-                               hipStream_t st);
+                               const float* ss, int d, float eps, hipStream_t st);
 
-// x1 = x + sum_s part[s]  (fp32);  h2 = RMSNorm(x1) * gamma.
+// x1 = x + sum_s part[s]  (fp32);  h2 = RMSNorm(x1) * gamma. Row i of x is
+// x[row_idx ? row_idx[i] : i].
 template <typename T>
 hipError_t launch_residual_rmsnorm(const float* part, int S, int M, int d, const T* x,
-                                   const T* gamma, float eps, float* x1, T* h2,
-                                   hipStream_t st);
+                                   const int32_t* row_idx, const T* gamma, float eps, float* x1,
+                                   T* h2, hipStream_t st);
 
 // u = silu(sum_s gate) * sum_s up, part rows [2F] = gate then up.
 template <typename T>
@@ -59,6 +62,13 @@ struct SkinnyPlan {
 SkinnyPlan skinny_plan(int N, int K);
 hipError_t launch_gemm_skinny_bf16(const uint16_t* A, const uint16_t* W, float* part, int M,
                                    int N, int K, SkinnyPlan plan, hipStream_t st);
+// Same with the gather and RMSNorm_1 folded in: the operand of row m is
+// bf16(X[row_idx ? row_idx[m] : m] * gamma), and ss[s][m] = sum of X^2 over
+// K-slice s (the consumer scales row m's sums by its 1/rms).
+hipError_t launch_gemm_skinny_norm_bf16(const uint16_t* X, const int32_t* row_idx,
+                                        const uint16_t* gamma, const uint16_t* W, float* part,
+                                        float* ss, int M, int N, int K, SkinnyPlan plan,
+                                        hipStream_t st);
 // Decode gate/up GEMM with the SwiGLU epilogue: H[M][F] = bf16(silu(A W_g^T) *
 // (A W_u^T)), W_gate_up = [W_g; W_u] [2F][K]; plan = skinny_plan(2F, K) with S == 1.
 hipError_t launch_gemm_skinny_swiglu_bf16(const uint16_t* A, const uint16_t* W_gate_up,

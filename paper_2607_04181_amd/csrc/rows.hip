@@ -159,7 +159,8 @@ __global__ __launch_bounds__(kEpiHeads * kWave) void qkv_epilogue_kernel(
     const int32_t* __restrict__ positions, const int32_t* __restrict__ seq_starts, int n_seqs,
     const int32_t* __restrict__ block_table, int max_blocks, const double* __restrict__ inv_freq,
     T* __restrict__ q_out, T* __restrict__ k_cache, T* __restrict__ v_cache,
-    const int32_t* __restrict__ ctx_lens, int32_t* __restrict__ split_off, int max_splits) {
+    const int32_t* __restrict__ ctx_lens, int32_t* __restrict__ split_off, int max_splits,
+    const float* __restrict__ ss, int d, float eps) {
   __shared__ float rot[2][128];  // cos, sin of the row's angles (hd / 2 <= 128)
   const int i = blockIdx.y, lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
   const int nh = Hq + 2 * Hkv;
@@ -189,6 +190,13 @@ __global__ __launch_bounds__(kEpiHeads * kWave) void qkv_epilogue_kernel(
         if (e < hd) val[t] = sum_parts1<S>(p + e, pstride);
       }
     }
+  }
+  // RMSNorm_1 folded into the projection: this row's 1/rms from the
+  // per-slice sums of squares, added in slice order.
+  float rscale = 1.f;
+  if (ss != nullptr) {
+    const float t = sum_parts1<S>(ss + i, M);
+    rscale = 1.0f / sqrtf(t / (float)d + eps);
   }
   const int pos = positions[i];
   int64_t blk = 0;
@@ -224,6 +232,8 @@ __global__ __launch_bounds__(kEpiHeads * kWave) void qkv_epilogue_kernel(
     }
   }
   if (!live) return;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) val[t] *= rscale;
   if (h < Hq + Hkv) {
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
@@ -270,7 +280,7 @@ hipError_t launch_qkv_epilogue(const float* part, int S, int M, int Hq, int Hkv,
                                int n_seqs, const int32_t* block_table, int max_blocks,
                                const double* inv_freq, T* q_out, T* k_cache, T* v_cache,
                                const int32_t* ctx_lens, int32_t* split_off, int max_splits,
-                               hipStream_t st) {
+                               const float* ss, int d, float eps, hipStream_t st) {
   if (M <= 0) return hipSuccess;
   if (hd > 256 || hd % 2 != 0) return hipErrorInvalidValue;
   const dim3 grid((Hq + 2 * Hkv + kEpiHeads - 1) / kEpiHeads, M);
@@ -278,7 +288,7 @@ hipError_t launch_qkv_epilogue(const float* part, int S, int M, int Hq, int Hkv,
                                       dim3(kEpiHeads * kWave), 0, st,
                                       part, M, Hq, Hkv, hd, positions, seq_starts, n_seqs,
                                       block_table, max_blocks, inv_freq, q_out, k_cache,
-                                      v_cache, ctx_lens, split_off, max_splits));
+                                      v_cache, ctx_lens, split_off, max_splits, ss, d, eps));
   return hipGetLastError();
 }
 
@@ -300,10 +310,12 @@ __device__ __forceinline__ f32x4_t load4<bf16_t>(const bf16_t* p) {
 template <typename T, int S>
 __global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_kernel(
     const float* __restrict__ part, int M, int d, const T* __restrict__ x,
-    const T* __restrict__ gamma, float eps, float* __restrict__ x1, T* __restrict__ h2) {
+    const int32_t* __restrict__ row_idx, const T* __restrict__ gamma, float eps,
+    float* __restrict__ x1, T* __restrict__ h2) {
   __shared__ float red[kNormThreads / kWave];
   constexpr int kMaxVec = 4;  // d <= 16384
   const int i = blockIdx.x;
+  const int64_t xr_row = row_idx ? (int64_t)row_idx[i] : (int64_t)i;
   const int64_t pstride = (int64_t)M * d;
   const int nv = d / 4;
   // Partials, residual and gains in one memory round trip.
@@ -314,7 +326,7 @@ __global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_kernel(
     if (v < nv) {
       const int c = 4 * v;
       a[u] = sum_parts4<S>(part + (int64_t)i * d + c, pstride);
-      xr[u] = load4<T>(x + (int64_t)i * d + c);
+      xr[u] = load4<T>(x + xr_row * d + c);
       g[u] = load4<T>(gamma + c);
     }
   }
@@ -347,13 +359,13 @@ __global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_kernel(
 
 template <typename T>
 hipError_t launch_residual_rmsnorm(const float* part, int S, int M, int d, const T* x,
-                                   const T* gamma, float eps, float* x1, T* h2,
-                                   hipStream_t st) {
+                                   const int32_t* row_idx, const T* gamma, float eps, float* x1,
+                                   T* h2, hipStream_t st) {
   if (M <= 0) return hipSuccess;
   if (d % 4 != 0 || d > 4 * 4 * kNormThreads) return hipErrorInvalidValue;
   COCO_SWITCH_S(S, hipLaunchKernelGGL((residual_rmsnorm_kernel<T, S_>), dim3(M),
-                                      dim3(kNormThreads), 0, st, part, M, d, x, gamma, eps, x1,
-                                      h2));
+                                      dim3(kNormThreads), 0, st, part, M, d, x, row_idx, gamma,
+                                      eps, x1, h2));
   return hipGetLastError();
 }
 
@@ -454,9 +466,11 @@ hipError_t launch_kv_append(const T* k, const T* v, const int32_t* seq_idx,
   template hipError_t launch_qkv_epilogue<T>(const float*, int, int, int, int, int,          \
                                              const int32_t*, const int32_t*, int,            \
                                              const int32_t*, int, const double*, T*, T*, T*, \
-                                             const int32_t*, int32_t*, int, hipStream_t);    \
+                                             const int32_t*, int32_t*, int, const float*,    \
+                                             int, float, hipStream_t);                       \
   template hipError_t launch_residual_rmsnorm<T>(const float*, int, int, int, const T*,      \
-                                                 const T*, float, float*, T*, hipStream_t);  \
+                                                 const int32_t*, const T*, float, float*, T*, \
+                                                 hipStream_t);                               \
   template hipError_t launch_swiglu<T>(const float*, int, int, int, T*, hipStream_t);        \
   template hipError_t launch_residual_scatter<T>(const float*, int, int, int, const float*,  \
                                                  T*, const int32_t*, hipStream_t);           \
