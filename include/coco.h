@@ -185,9 +185,9 @@ int coco_layer_span_forward(coco_layer_t h, int32_t first_layer, int32_t n_layer
  * row i holds call row i of the last layer run. Copies min(dst_bytes, buffer
  * size) bytes on `stream`. */
 enum {
-  COCO_WS_X = 0,  /* layer input rows, [max_rows][d], dtype (written by the
-                     first layer of prefill and fp32 calls, and for every
-                     later layer of a span) */
+  COCO_WS_X = 0,  /* layer input rows, [max_rows][d], dtype (written for the
+                     second and later layers of a span; the first layer reads
+                     its rows from the hidden buffer) */
   COCO_WS_H = 1,  /* RMSNorm_1 output, [max_rows][d], dtype (prefill and
                      fp32 calls; bf16 decode folds RMSNorm_1 into the QKV
                      projection and never writes it) */

@@ -492,7 +492,9 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
     // Decode (bf16) folds the gather and RMSNorm_1 into the QKV projection:
     // it stages bf16(x * gamma) straight from the input rows and the QKV
     // epilogue applies each row's 1/rms. Otherwise a gather + RMSNorm_1
-    // kernel writes x and h first.
+    // kernel writes h first. The residual reads the input rows where they
+    // are (hidden[row_idx] in the first layer of the call), so no copy of
+    // them is made.
     const bool fold_norm = !pre && std::is_same<T, bf16_t>::value;
     const T* x_src = first_l ? hidden : x;                     // this layer's input rows
     const int32_t* x_idx = first_l ? row_idx : nullptr;
@@ -500,7 +502,7 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
       TIMED(COCO_K_GATHER_NORM,
             HIPCHK(launch_gather_rmsnorm<T>(first_l ? hidden : x, first_l ? row_idx : nullptr, M,
                                             d, (const T*)w.gamma_attn, c.rms_eps,
-                                            first_l ? x : nullptr, h, st)));
+                                            nullptr, h, st)));
     // QKV projection, RoPE, local cache append.
     if (fold_norm) {
       const SkinnyPlan plan = skinny_plan(nqkv, d);
@@ -528,8 +530,7 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
     // O projection + residual + RMSNorm_2.
     TIMED(COCO_K_GEMM_O, if ((rc = gemm<T>(H, o, (const T*)w.w_o, M, d, Hq * hd, pre, &S, st))) return rc);
     TIMED(COCO_K_RESIDUAL_NORM,
-          HIPCHK(launch_residual_rmsnorm<T>(H->part, S, M, d, fold_norm ? x_src : x,
-                                            fold_norm ? x_idx : nullptr, (const T*)w.gamma_mlp,
+          HIPCHK(launch_residual_rmsnorm<T>(H->part, S, M, d, x_src, x_idx, (const T*)w.gamma_mlp,
                                             c.rms_eps, H->x1, h2, st)));
     // SwiGLU MLP (prefill: SwiGLU in the gate/up GEMM's epilogue when the
     // GEMM is not split along K).
