@@ -327,3 +327,54 @@ def test_init_rejects_unsupported_shapes():
     t = WD.layer_tensors(small_bf16_shape(), "x", 0, 4)
     with pytest.raises(coco.CocoError, match="head_dim"):
         coco.coco_layer_init(bad, [t])
+
+
+def test_single_request_decode_with_a_full_block_table_matches_oracle():
+    """Degenerate and maximal cases in one call: a batch of one request whose
+    context fills its block table exactly (ctx = max_blocks * 16 = 1024), so
+    the last partition and the last block end at the table's edge."""
+    shape = small_bf16_shape()
+    b = ragged_decode_batch(8, [1023], max_ctx=1024, hidden_rows=5, row_idx=np.array([3]))
+    assert int(b.ctx_lens[0]) == b.block_table.shape[1] * W.BLOCK_SIZE
+    rep = Replica.for_batch(shape, "s8", 1, b)
+    hidden = WD.hidden_tensor(shape, "s8", b.hidden_rows)
+    h0 = to64(hidden)
+    rep.forward(0, hidden, WD.batch_tensors(b))
+    torch.cuda.synchronize()
+    ref, _, _ = oracle_decode_rows(shape, "s8", 0, b, range(b.n_rows), h0)
+    got = to64(hidden)
+    y, x = got[b.row_idx], h0[b.row_idx]
+    e = normwise_err(y, ref)
+    assert e < TOL, e
+    # One row: the branch y - x is ~15x smaller than y itself, so the bf16
+    # rounding of the stored output (half an ulp, 2^-9 |y|) alone is several
+    # percent of the branch. The branch bound is widened by exactly that
+    # rounding budget.
+    ed = normwise_err(y - x, ref - x)
+    budget = 2.0 ** -8 * np.max(np.abs(ref)) / np.max(np.abs(ref - x))
+    log(f"single full-table decode: output err {e:.2e}, branch err {ed:.2e} (rounding budget {budget:.2e})")
+    assert ed < DELTA_TOL + budget, (ed, budget)
+    others = sorted(set(range(b.hidden_rows)) - set(b.row_idx.tolist()))
+    assert np.array_equal(got[others], h0[others])
+
+
+def test_one_token_prefill_chunks_match_oracle_and_split():
+    """The smallest prefill chunks: each request brings one token (one at
+    position 0, so it attends only to itself). The rows match the oracle, and
+    one request called alone gives the bits it gets inside the batch."""
+    shape = small_bf16_shape()
+    priors = [0, 17, 300]
+    p = ragged_prefill_batch(9, priors=priors, lens=[1, 1, 1], max_ctx=512, hidden_rows=6)
+    rep = Replica.for_batch(shape, "s9", 1, p)
+    hidden = WD.hidden_tensor(shape, "s9", p.hidden_rows)
+    h0 = to64(hidden)
+    whole = hidden.clone()
+    rep.forward(0, whole, WD.batch_tensors(p))
+    torch.cuda.synchronize()
+    ref, _, _, _ = oracle_prefill_seqs(shape, "s9", 0, p, range(p.n_seqs), h0)
+    _check_rows("one-token prefill", to64(whole)[p.row_idx], ref, h0[p.row_idx])
+    alone = hidden.clone()
+    rep.forward(0, alone, WD.batch_tensors(p.select_seqs([1])))
+    torch.cuda.synchronize()
+    r = int(p.row_idx[1])
+    assert torch.equal(alone[r].view(torch.int16), whole[r].view(torch.int16))
