@@ -18,7 +18,10 @@
  *   weights and caches for the handle's lifetime and the rest for the call.
  *   The only memory the library owns is its workspace, allocated once in
  *   coco_layer_init and sized by the config (the paper's persistent memory
- *   pool with fixed addresses, Sec. 5.2, CUDA-graph compatibility).
+ *   pool with fixed addresses, Sec. 5.2, CUDA-graph compatibility): per-row
+ *   activations and split-K partials for max_rows rows, the decode attention
+ *   partials, and (bf16) a RoPE cos/sin table of max_blocks_per_seq * 16
+ *   positions * head_dim * 4 bytes.
  * Streams. `stream` is a hipStream_t (NULL = the null stream). Work is
  *   enqueued on it; calls return without synchronising, never allocate, and
  *   keep every address fixed, so a call can be captured in a HIP graph --

@@ -49,6 +49,9 @@ struct coco_layer {
   float *x1 = nullptr, *part = nullptr, *attn_o = nullptr, *attn_ml = nullptr;
   float* ss = nullptr;  // per-slice row sums of squares (decode QKV with RMSNorm_1 folded in)
   double* inv_freq = nullptr;
+  float* rope = nullptr;  // RoPE table [rope_rows][head_dim / 2] (cos, sin)
+  int rope_rows = 0;      // positions the configuration admits
+  int32_t* row_info = nullptr;  // prefill row slots [max_rows][2] (position, cache block)
   int32_t* split_off = nullptr;  // decode attention work list offsets
   size_t act_rows_bytes[7] = {};
   int max_splits = 0;
@@ -183,9 +186,11 @@ int coco_layer_init(const coco_layer_config* cfg, const coco_layer_weights* laye
   H->max_splits = decode_max_splits(c.max_blocks_per_seq);
   H->dec_rows = c.max_rows < c.max_seqs ? c.max_rows : c.max_seqs;
 
+  // RoPE table for the fused prefill QKV epilogue (bf16 only).
+  H->rope_rows = c.dtype == COCO_BF16 ? c.max_blocks_per_seq * kBlockTokens : 0;
   size_t off = 0;
-  size_t offs[13];
-  const size_t sizes[13] = {
+  size_t offs[15];
+  const size_t sizes[15] = {
       align256(R * d * eb),          // x
       align256(R * d * eb),          // h
       align256(R * qd * eb),         // q
@@ -198,8 +203,10 @@ int coco_layer_init(const coco_layer_config* cfg, const coco_layer_weights* laye
       c.dtype == COCO_BF16 ? align256((size_t)H->dec_rows * c.n_q_heads * H->max_splits * 2 * 4) : 0,
       align256((size_t)(c.head_dim / 2) * 8),  // inv_freq
       align256((size_t)(H->dec_rows + 1) * 4),  // split_off
-      align256((size_t)16 * R * 4)};  // ss: at most 16 K-slices
-  for (int i = 0; i < 13; ++i) {
+      align256((size_t)16 * R * 4),  // ss: at most 16 K-slices
+      align256((size_t)H->rope_rows * (c.head_dim / 2) * 8),  // RoPE table
+      align256(R * 8)};  // row_info
+  for (int i = 0; i < 15; ++i) {
     offs[i] = off;
     off += sizes[i];
   }
@@ -222,6 +229,8 @@ int coco_layer_init(const coco_layer_config* cfg, const coco_layer_weights* laye
   H->inv_freq = (double*)(H->ws + offs[10]);
   H->split_off = (int32_t*)(H->ws + offs[11]);
   H->ss = (float*)(H->ws + offs[12]);
+  H->rope = (float*)(H->ws + offs[13]);
+  H->row_info = (int32_t*)(H->ws + offs[14]);
   H->act_rows_bytes[COCO_WS_X] = R * d * eb;
   H->act_rows_bytes[COCO_WS_H] = R * d * eb;
   H->act_rows_bytes[COCO_WS_Q] = R * qd * eb;
@@ -235,7 +244,11 @@ int coco_layer_init(const coco_layer_config* cfg, const coco_layer_weights* laye
   for (int j = 0; j < c.head_dim / 2; ++j)
     inv[j] = pow((double)c.rope_theta, -2.0 * j / (double)c.head_dim);
   if (hipMemcpy(H->inv_freq, inv.data(), inv.size() * 8, hipMemcpyHostToDevice) != hipSuccess ||
-      hipMemset(H->ws, 0, offs[10]) != hipSuccess) {
+      hipMemset(H->ws, 0, offs[10]) != hipSuccess ||
+      (H->rope_rows > 0 &&
+       (launch_rope_table(H->inv_freq, c.head_dim / 2, H->rope_rows, H->rope, nullptr) !=
+            hipSuccess ||
+        hipDeviceSynchronize() != hipSuccess))) {
     (void)hipGetLastError();
     (void)hipFree(H->ws);
     delete H;
@@ -496,13 +509,26 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
     // are (hidden[row_idx] in the first layer of the call), so no copy of
     // them is made.
     const bool fold_norm = !pre && std::is_same<T, bf16_t>::value;
+    const bool fuse_qkv = pre && std::is_same<T, bf16_t>::value && tile_qkv_fusable(Hq, Hkv, d);
     const T* x_src = first_l ? hidden : x;                     // this layer's input rows
     const int32_t* x_idx = first_l ? row_idx : nullptr;
+    // The fused prefill QKV epilogue reads each row's (position, cache block),
+    // written once per call by the first layer's gather.
+    RowSlotArgs rs;
+    if (fuse_qkv && first_l) {
+      rs.positions = positions;
+      rs.seq_starts = seq_starts;
+      rs.block_table = bt;
+      rs.row_info = H->row_info;
+      rs.n_seqs = n_seqs;
+      rs.max_blocks = c.max_blocks_per_seq;
+      rs.rope_rows = H->rope_rows;
+    }
     if (!fold_norm)
       TIMED(COCO_K_GATHER_NORM,
             HIPCHK(launch_gather_rmsnorm<T>(first_l ? hidden : x, first_l ? row_idx : nullptr, M,
                                             d, (const T*)w.gamma_attn, c.rms_eps,
-                                            nullptr, h, st)));
+                                            nullptr, h, rs, st)));
     // QKV projection, RoPE, local cache append.
     if (fold_norm) {
       const SkinnyPlan plan = skinny_plan(nqkv, d);
@@ -513,18 +539,33 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
                                                 (const bf16_t*)w.gamma_attn,
                                                 (const bf16_t*)w.w_qkv, H->part, H->ss, M, nqkv, d,
                                                 plan, st)));
+    } else if (fuse_qkv) {
+      // Prefill (bf16, QKV projection not split along K): RoPE and the cache
+      // append run in the GEMM's epilogue.
+      TileQkvArgs qa;
+      qa.row_info = H->row_info;
+      qa.rope = H->rope;
+      qa.q_out = (uint16_t*)q;
+      qa.k_cache = (uint16_t*)w.k_cache;
+      qa.v_cache = (uint16_t*)w.v_cache;
+      qa.Hq = Hq;
+      qa.Hkv = Hkv;
+      TIMED(COCO_K_GEMM_QKV,
+            HIPCHK(launch_gemm_tile_qkv_bf16((const uint16_t*)h, (const uint16_t*)w.w_qkv, M, d,
+                                             qa, st)));
     } else {
       TIMED(COCO_K_GEMM_QKV, if ((rc = gemm<T>(H, h, (const T*)w.w_qkv, M, nqkv, d, pre, &S, st))) return rc);
     }
-    TIMED(COCO_K_QKV_EPILOGUE,
-          HIPCHK(launch_qkv_epilogue<T>(H->part, S, M, Hq, Hkv, hd, positions, seq_starts,
-                                        n_seqs, bt, c.max_blocks_per_seq, H->inv_freq, q,
-                                        (T*)w.k_cache, (T*)w.v_cache, ctx,
-                                        (seq_starts == nullptr && c.dtype == COCO_BF16)
-                                            ? H->split_off
-                                            : nullptr,
-                                        H->max_splits, fold_norm ? H->ss : nullptr, d, c.rms_eps,
-                                        st)));
+    if (!fuse_qkv)
+      TIMED(COCO_K_QKV_EPILOGUE,
+            HIPCHK(launch_qkv_epilogue<T>(H->part, S, M, Hq, Hkv, hd, positions, seq_starts,
+                                          n_seqs, bt, c.max_blocks_per_seq, H->inv_freq, q,
+                                          (T*)w.k_cache, (T*)w.v_cache, ctx,
+                                          (seq_starts == nullptr && c.dtype == COCO_BF16)
+                                              ? H->split_off
+                                              : nullptr,
+                                          H->max_splits, fold_norm ? H->ss : nullptr, d,
+                                          c.rms_eps, st)));
     // Attention over the paged cache.
     if ((rc = attention<T>(H, w, M, positions, seq_starts, n_seqs, bt, ctx, st))) return rc;
     // O projection + residual + RMSNorm_2.

@@ -22,7 +22,10 @@
 //   * narrow outputs with a long K are split into K-slices (tile_splits, a
 //     function of (N, K) only) so the grid covers the CUs;
 //   * for the gate/up projection a variant pairs gate and up columns inside
-//     each wave and writes silu(gate) * up directly in bf16.
+//     each wave and writes silu(gate) * up directly in bf16;
+//   * for the QKV projection (unsplit) a variant orders each head's columns so
+//     that a lane holds both dims j and j + 64 of its rows, applies RoPE in
+//     registers and writes queries and the cache tiles directly in bf16.
 // Every output element is summed over k in ascending 16-steps within its
 // slice, independent of M and of the tile it falls in, so request-aligned
 // prefill splits give identical bits.
@@ -70,18 +73,28 @@ __shared__ __attribute__((aligned(16))) bf16_t g_ta0[kTM * kTK], g_ta1[kTM * kTK
     g_ta2[kTM * kTK], g_ta3[kTM * kTK];
 __shared__ __attribute__((aligned(16))) bf16_t g_tw0[kTN * kTK], g_tw1[kTN * kTK],
     g_tw2[kTN * kTK], g_tw3[kTN * kTK];
+// QKV epilogue: position (clamped to the RoPE table) and cache block of each
+// row of the tile.
+__shared__ int g_row_pos[kTM], g_row_blk[kTM];
 
-// FUSE: W is the [2F][K] gate/up matrix; each 32-column half of a wave's
-// 64 columns holds gate rows and the other the matching up rows, so each lane
-// owns both factors of its outputs and the epilogue writes h = silu(gate) *
-// up in bf16 to the [M][F] buffer `H` (N = 2F, one K-slice). Otherwise C is
-// the fp32 partial. k_slice is a multiple of kTK * kTBuf.
-template <bool FUSE>
+enum { kTilePartial = 0, kTileSwiglu = 1, kTileQkv = 2 };
+
+// kTilePartial: C is the fp32 partial of K-slice blockIdx.y.
+// kTileSwiglu: W is the [2F][K] gate/up matrix; each 32-column half of a
+// wave's 64 columns holds gate rows and the other the matching up rows, so
+// each lane owns both factors of its outputs and the epilogue writes
+// h = silu(gate) * up in bf16 to the [M][F] buffer `H` (N = 2F, one K-slice).
+// kTileQkv: W is the [(Hq + 2 Hkv) * 128][K] QKV matrix, N a multiple of 256
+// (two heads per tile), one K-slice; see the epilogue.
+// k_slice is a multiple of kTK * kTBuf.
+template <int MODE>
 __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __restrict__ A,
                                                                  const bf16_t* __restrict__ W,
                                                                  float* __restrict__ C,
                                                                  bf16_t* __restrict__ H, int M,
-                                                                 int N, int K, int k_slice) {
+                                                                 int N, int K, int k_slice,
+                                                                 TileQkvArgs qa) {
+  constexpr bool FUSE = MODE == kTileSwiglu;
   bf16_t* const ta[kTBuf] = {g_ta0, g_ta1, g_ta2, g_ta3};
   bf16_t* const tw[kTBuf] = {g_tw0, g_tw1, g_tw2, g_tw3};
 
@@ -103,8 +116,13 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
 
   // Fused tile of 128 outputs o0 .. o0+127: tile rows 64w + 32j + i hold gate
   // row o0 + 32w + i for j = 0 and up row F + o0 + 32w + i for j = 1.
+  // QKV tile of heads n0/128 and n0/128 + 1: tile rows 64w + 32j + i hold
+  // dim 32(w % 2) + 64j + i of head n0/128 + w/2, so wave column quarter w
+  // gets dims jd and jd + 64 (jd = 32(w % 2) + i) of one head in its two
+  // 32-column halves.
   const int F = N / 2, o0 = n0 / 2;
   auto w_row = [&](int r) {
+    if (MODE == kTileQkv) return n0 + (r & 0x80) + ((r >> 6) & 1) * 32 + ((r >> 5) & 1) * 64 + (r & 31);
     if (!FUSE) return min(n0 + r, N - 1);
     const int w = r >> 6, j = (r >> 5) & 1, i = r & 31;
     return (j ? F : 0) + o0 + 32 * w + i;
@@ -171,6 +189,12 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
     __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
   };
 
+  // QKV epilogue: this thread's tile row slot (position, cache block), loaded
+  // ahead of the ring so the stage waits below also cover it.
+  u32x2_t rinfo = {0u, 0u};
+  if constexpr (MODE == kTileQkv)
+    if (tid < kTM) rinfo = *(const u32x2_t*)(qa.row_info + 2 * min(m0 + tid, M - 1));
+
   issue(0, 0);
   issue(1, 1);
   issue(2, 2);
@@ -193,6 +217,86 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
   }
   wait_vmcnt<0>();  // no direct load outlives the workgroup
 
+  if constexpr (MODE == kTileQkv) {
+    // The tile rows' slots (position clamped to the RoPE table, cache block)
+    // and, when a head of the tile is rotated, the RoPE table rows of their
+    // positions, staged by direct loads into the now idle ring (row lr at
+    // ring object lr / 32, 512 bytes per row), so the stores below wait on
+    // no load.
+    constexpr int kHd = 128, kTile = kBlockTokens * kHd;
+    if (tid < kTM) {
+      g_row_pos[tid] = (int)rinfo.x;
+      g_row_blk[tid] = (int)rinfo.y;
+    }
+    __syncthreads();
+    const int hh0 = n0 >> 7;
+    auto ring = [](int k) -> bf16_t* {  // k wave-uniform
+      switch (k) {
+        case 0: return g_ta0;
+        case 1: return g_ta1;
+        case 2: return g_ta2;
+        case 3: return g_ta3;
+        case 4: return g_tw0;
+        case 5: return g_tw1;
+        case 6: return g_tw2;
+        default: return g_tw3;
+      }
+    };
+    if (hh0 < qa.Hq + qa.Hkv) {
+#pragma unroll
+      for (int c = 0; c < 16; ++c) {
+        const int row = 32 * wv + 2 * c + hi;
+        __builtin_amdgcn_global_load_lds(
+            qa.rope + ((int64_t)g_row_pos[row] * (kHd / 2) + 2 * l32) * 2,
+            (lds_void_t*)(ring(wv) + c * 512), 16, 0, 0);
+      }
+      wait_vmcnt<0>();
+      __syncthreads();
+    }
+    // Rotate-half RoPE on query and key heads: this lane holds dims jd and
+    // jd + 64 of head hh for its 64 rows. Queries go to q_out [M][Hq][128];
+    // keys (rotated) and values to their cache slot (block, position % 16).
+    const int hh = hh0 + (wn >> 1);
+    const int jd = (wn & 1) * 32 + l32;
+    const int kind = hh < qa.Hq ? 0 : (hh < qa.Hq + qa.Hkv ? 1 : 2);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int lr = wm * 128 + i * 32 + 8 * jj + 4 * hi + r;
+          const int m = m0 + lr;
+          if (m >= M) continue;
+          float lo = acc[i][0][4 * jj + r], up = acc[i][1][4 * jj + r];
+          const int pos = g_row_pos[lr];
+          if (kind != 2) {
+            const f32x2_t cs =
+                ((const f32x2_t*)ring(wm * 4 + i))[(8 * jj + 4 * hi + r) * (kHd / 2) + jd];
+            const float rlo = lo * cs.x - up * cs.y, rup = up * cs.x + lo * cs.y;
+            lo = rlo;
+            up = rup;
+          }
+          if (kind == 0) {
+            bf16_t* dst = qa.q_out + ((int64_t)m * qa.Hq + hh) * kHd;
+            dst[jd] = (bf16_t)f32_to_bf16(lo);
+            dst[jd + 64] = (bf16_t)f32_to_bf16(up);
+          } else {
+            const int slot = pos % kBlockTokens;
+            const int g = hh - qa.Hq - (kind == 2 ? qa.Hkv : 0);
+            bf16_t* tile = (kind == 1 ? qa.k_cache : qa.v_cache) +
+                           ((int64_t)g_row_blk[lr] * qa.Hkv + g) * kTile;
+            if (kind == 1) {
+              tile[k_tile_offset(slot, jd)] = (bf16_t)f32_to_bf16(lo);
+              tile[k_tile_offset(slot, jd + 64)] = (bf16_t)f32_to_bf16(up);
+            } else {
+              tile[v_tile_offset(slot, jd)] = (bf16_t)f32_to_bf16(lo);
+              tile[v_tile_offset(slot, jd + 64)] = (bf16_t)f32_to_bf16(up);
+            }
+          }
+        }
+    return;
+  }
   if (FUSE) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -243,8 +347,8 @@ hipError_t launch_gemm_tile_bf16(const uint16_t* A, const uint16_t* W, float* C,
   if (M <= 0) return hipSuccess;
   if (S < 1 || K % (kTK * kTBuf * S) != 0) return hipErrorInvalidValue;
   const int tiles = ((M + kTM - 1) / kTM) * ((N + kTN - 1) / kTN);
-  hipLaunchKernelGGL(gemm_tile_kernel<false>, dim3(tiles, S), dim3(kTThreads), 0, st, A, W, C,
-                     nullptr, M, N, K, K / S);
+  hipLaunchKernelGGL(gemm_tile_kernel<kTilePartial>, dim3(tiles, S), dim3(kTThreads), 0, st, A,
+                     W, C, nullptr, M, N, K, K / S, TileQkvArgs{});
   return hipGetLastError();
 }
 
@@ -254,8 +358,24 @@ hipError_t launch_gemm_tile_swiglu_bf16(const uint16_t* A, const uint16_t* W_gat
   if (F % (kTN / 2) != 0 || K % (kTK * kTBuf) != 0 || tile_splits(2 * F, K) != 1)
     return hipErrorInvalidValue;
   const int tiles = ((M + kTM - 1) / kTM) * (2 * F / kTN);
-  hipLaunchKernelGGL(gemm_tile_kernel<true>, dim3(tiles, 1), dim3(kTThreads), 0, st, A,
-                     W_gate_up, nullptr, H, M, 2 * F, K, K);
+  hipLaunchKernelGGL(gemm_tile_kernel<kTileSwiglu>, dim3(tiles, 1), dim3(kTThreads), 0, st, A,
+                     W_gate_up, nullptr, H, M, 2 * F, K, K, TileQkvArgs{});
+  return hipGetLastError();
+}
+
+bool tile_qkv_fusable(int Hq, int Hkv, int K) {
+  const int N = (Hq + 2 * Hkv) * 128;
+  return N % kTN == 0 && K % (kTK * kTBuf) == 0 && tile_splits(N, K) == 1;
+}
+
+hipError_t launch_gemm_tile_qkv_bf16(const uint16_t* A, const uint16_t* W_qkv, int M, int K,
+                                     const TileQkvArgs& qa, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  if (!tile_qkv_fusable(qa.Hq, qa.Hkv, K) || !qa.row_info || !qa.rope) return hipErrorInvalidValue;
+  const int N = (qa.Hq + 2 * qa.Hkv) * 128;
+  const int tiles = ((M + kTM - 1) / kTM) * (N / kTN);
+  hipLaunchKernelGGL(gemm_tile_kernel<kTileQkv>, dim3(tiles, 1), dim3(kTThreads), 0, st, A,
+                     W_qkv, nullptr, nullptr, M, N, K, K, qa);
   return hipGetLastError();
 }
 

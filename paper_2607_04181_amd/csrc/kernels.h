@@ -7,12 +7,29 @@
 namespace coco {
 
 // ---------------------------------------------------------------- row kernels
+// Prefill row slots (optional output of the gather kernel): row_info[2i] =
+// positions[i] clamped to [0, rope_rows), row_info[2i + 1] = the cache block
+// of that position in row i's sequence (rows of a sequence contiguous).
+struct RowSlotArgs {
+  const int32_t* positions = nullptr;
+  const int32_t* seq_starts = nullptr;
+  const int32_t* block_table = nullptr;
+  int32_t* row_info = nullptr;  // null: not written
+  int n_seqs = 0, max_blocks = 0, rope_rows = 0;
+};
+
 // x_out[i] = src[row_idx ? row_idx[i] : i];  h_out[i] = RMSNorm(x) * gamma.
 // x_out may be null (span layers after the first read x in place).
 template <typename T>
 hipError_t launch_gather_rmsnorm(const T* src, const int32_t* row_idx, int M, int d,
                                  const T* gamma, float eps, T* x_out, T* h_out,
-                                 hipStream_t st);
+                                 const RowSlotArgs& rs, hipStream_t st);
+
+// RoPE table rope[p][j] = (cos, sin)(p * inv_freq[j]) for p < n_pos and
+// j < half, angle and both functions in fp64 (as the QKV epilogue computes
+// them), stored as fp32 pairs.
+hipError_t launch_rope_table(const double* inv_freq, int half, int n_pos, float* rope,
+                             hipStream_t st);
 
 // Sum of S split-K partials of the QKV projection, RoPE on query and key
 // heads, queries to q_out [M][Hq*hd], keys/values into the paged cache.
@@ -85,6 +102,21 @@ hipError_t launch_gemm_tile_bf16(const uint16_t* A, const uint16_t* W, float* C,
 // where W_gate_up = [W_g; W_u] is [2F][K]; only for tile_splits(2F, K) == 1.
 hipError_t launch_gemm_tile_swiglu_bf16(const uint16_t* A, const uint16_t* W_gate_up,
                                         uint16_t* H, int M, int F, int K, hipStream_t st);
+// Prefill QKV projection with the QKV epilogue in the GEMM's own epilogue
+// (head_dim 128): RoPE on query and key heads with the rotations of the RoPE
+// table, queries to q_out [M][Hq*128] in bf16, keys and values into the
+// paged cache tiles; no fp32 partials. Only when tile_qkv_fusable(Hq, Hkv, K).
+struct TileQkvArgs {
+  const int32_t* row_info;  // [M][2] row slots from the gather kernel
+  const float* rope;        // [rope_rows][64] (cos, sin) pairs
+  uint16_t* q_out;
+  uint16_t* k_cache;
+  uint16_t* v_cache;
+  int Hq, Hkv;
+};
+bool tile_qkv_fusable(int Hq, int Hkv, int K);
+hipError_t launch_gemm_tile_qkv_bf16(const uint16_t* A, const uint16_t* W_qkv, int M, int K,
+                                     const TileQkvArgs& qa, hipStream_t st);
 
 // part[0][m][n] = sum_k A[m][k] * W[n][k], fp32 (tiny fp32 configurations).
 hipError_t launch_gemm_f32(const float* A, const float* W, float* part, int M, int N, int K,

@@ -60,12 +60,29 @@ __device__ __forceinline__ u32x4_t pack_bf16x8(const float* f) {
 // ----------------------------------------------------------------------------
 // Segment-boundary gather of the sub-batch rows, fused with the first RMSNorm.
 // ----------------------------------------------------------------------------
+// Prefill row slots: row_info[i] = (position clamped to the RoPE table,
+// cache block of the position), for the QKV projection's fused epilogue.
+__device__ __forceinline__ void write_row_slot(const RowSlotArgs& rs, int i) {
+  const int pos = rs.positions[i];
+  int lo = 0, hi = rs.n_seqs - 1;  // the s with seq_starts[s] <= i < seq_starts[s + 1]
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (rs.seq_starts[mid] <= i) lo = mid; else hi = mid - 1;
+  }
+  const int blk = rs.block_table[(int64_t)lo * rs.max_blocks +
+                                 min(max(pos, 0) / kBlockTokens, rs.max_blocks - 1)];
+  rs.row_info[2 * i] = min(max(pos, 0), rs.rope_rows - 1);
+  rs.row_info[2 * i + 1] = blk;
+}
+
 template <typename T>
 __global__ __launch_bounds__(kRowThreads) void gather_rmsnorm_kernel(
     const T* __restrict__ src, const int32_t* __restrict__ row_idx, int d,
-    const T* __restrict__ gamma, float eps, T* __restrict__ x_out, T* __restrict__ h_out) {
+    const T* __restrict__ gamma, float eps, T* __restrict__ x_out, T* __restrict__ h_out,
+    RowSlotArgs rs) {
   __shared__ float red[kRowThreads / kWave];
   const int i = blockIdx.x;
+  if (rs.row_info != nullptr && threadIdx.x == 0) write_row_slot(rs, i);
   const int64_t r = row_idx ? (int64_t)row_idx[i] : (int64_t)i;
   const T* x = src + r * d;
   float ss = 0.f;
@@ -86,10 +103,11 @@ template <>
 __global__ __launch_bounds__(kRowThreads) void gather_rmsnorm_kernel<bf16_t>(
     const bf16_t* __restrict__ src, const int32_t* __restrict__ row_idx, int d,
     const bf16_t* __restrict__ gamma, float eps, bf16_t* __restrict__ x_out,
-    bf16_t* __restrict__ h_out) {
+    bf16_t* __restrict__ h_out, RowSlotArgs rs) {
   __shared__ float red[kRowThreads / kWave];
   constexpr int kMaxVec = 8;  // d <= 16384
   const int i = blockIdx.x;
+  if (rs.row_info != nullptr && threadIdx.x == 0) write_row_slot(rs, i);
   const int64_t r = row_idx ? (int64_t)row_idx[i] : (int64_t)i;
   const int nv = d / 8;
   const u32x4_t* x = (const u32x4_t*)(src + r * d);
@@ -135,10 +153,39 @@ __global__ __launch_bounds__(kRowThreads) void gather_rmsnorm_kernel<bf16_t>(
 template <typename T>
 hipError_t launch_gather_rmsnorm(const T* src, const int32_t* row_idx, int M, int d,
                                  const T* gamma, float eps, T* x_out, T* h_out,
-                                 hipStream_t st) {
+                                 const RowSlotArgs& rs, hipStream_t st) {
   if (M <= 0) return hipSuccess;
+  if (rs.row_info != nullptr && (rs.n_seqs < 1 || rs.max_blocks < 1 || rs.rope_rows < 1))
+    return hipErrorInvalidValue;
   hipLaunchKernelGGL(gather_rmsnorm_kernel<T>, dim3(M), dim3(kRowThreads), 0, st, src, row_idx,
-                     d, gamma, eps, x_out, h_out);
+                     d, gamma, eps, x_out, h_out, rs);
+  return hipGetLastError();
+}
+
+// ----------------------------------------------------------------------------
+// RoPE table: rope[p][j] = (cos, sin)(p * inv_freq[j]), the angle and its
+// cosine and sine evaluated in fp64 and rounded to fp32 exactly as the QKV
+// epilogue below does, for every position p < n_pos the configuration
+// admits. Built once at init for the prefill QKV projection's fused epilogue.
+// ----------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void rope_table_kernel(const double* __restrict__ inv_freq,
+                                                         int half, int n_pos,
+                                                         float* __restrict__ rope) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e >= (int64_t)n_pos * half) return;
+  const int p = (int)(e / half), j = (int)(e - (int64_t)p * half);
+  double sn, cn;
+  sincos((double)p * inv_freq[j], &sn, &cn);
+  rope[2 * e] = (float)cn;
+  rope[2 * e + 1] = (float)sn;
+}
+
+hipError_t launch_rope_table(const double* inv_freq, int half, int n_pos, float* rope,
+                             hipStream_t st) {
+  const int64_t n = (int64_t)n_pos * half;
+  if (n <= 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(rope_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
+                     inv_freq, half, n_pos, rope);
   return hipGetLastError();
 }
 
@@ -149,7 +196,8 @@ hipError_t launch_gather_rmsnorm(const T* src, const int32_t* row_idx, int M, in
 // once per workgroup into LDS), store queries, append the rotated key and the
 // value to the sequence's cache slot. The partial loads, which depend on
 // nothing, are issued first; the cache slot lookup and the angles overlap
-// them. In decode, one wave also writes the attention's partition offsets.
+// them (a dependent load of the RoPE table measured slower here). In decode,
+// one wave also writes the attention's partition offsets.
 // ----------------------------------------------------------------------------
 constexpr int kEpiHeads = 8;
 
@@ -462,7 +510,8 @@ hipError_t launch_kv_append(const T* k, const T* v, const int32_t* seq_idx,
 
 #define COCO_INSTANTIATE(T)                                                                   \
   template hipError_t launch_gather_rmsnorm<T>(const T*, const int32_t*, int, int, const T*, \
-                                               float, T*, T*, hipStream_t);                  \
+                                               float, T*, T*, const RowSlotArgs&,            \
+                                               hipStream_t);                                 \
   template hipError_t launch_qkv_epilogue<T>(const float*, int, int, int, int, int,          \
                                              const int32_t*, const int32_t*, int,            \
                                              const int32_t*, int, const double*, T*, T*, T*, \

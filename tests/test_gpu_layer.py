@@ -253,6 +253,56 @@ def test_span_equals_successive_layers_bit_exactly():
     assert torch.equal(a.view(torch.int16), c.view(torch.int16))
 
 
+def test_prefill_span_equals_successive_layers_bit_exactly():
+    """A prefill span reuses the per-row cache slots its first layer computes;
+    every layer's output rows and appended cache bytes equal those of one-layer
+    calls."""
+    shape = small_bf16_shape()
+    b = ragged_prefill_batch(12, priors=[0, 21, 300, 7], lens=[40, 3, 90, 33], max_ctx=512,
+                             hidden_rows=200)
+    L = 3
+    rep = Replica.for_batch(shape, "s10", L, b)
+    pools0 = [{k: t[k].clone() for k in ("k_cache", "v_cache")} for t in rep.layers]
+    hidden = WD.hidden_tensor(shape, "s10", b.hidden_rows)
+    bt = WD.batch_tensors(b)
+    a = hidden.clone()
+    rep.span(0, L, a, bt)
+    torch.cuda.synchronize()
+    pools_span = [{k: t[k].clone() for k in ("k_cache", "v_cache")} for t in rep.layers]
+    for t, p in zip(rep.layers, pools0):
+        for k in p:
+            t[k].copy_(p[k])
+    c = hidden.clone()
+    for l in range(L):
+        rep.forward(l, c, bt)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), c.view(torch.int16))
+    for t, p in zip(rep.layers, pools_span):
+        for k in p:
+            assert torch.equal(t[k].view(torch.int16), p[k].view(torch.int16)), k
+
+
+def test_prefill_with_an_odd_head_count_matches_oracle():
+    """Five query heads and one KV head: the QKV width (7 heads) is not a
+    multiple of the prefill GEMM's two-head tile, so the projection writes fp32
+    partials and the separate QKV epilogue applies RoPE and the cache append."""
+    shape = small_bf16_shape(d=512, hq=5, hkv=1, ffn=768)
+    b = ragged_prefill_batch(13, priors=[0, 50, 17], lens=[30, 70, 16], max_ctx=256,
+                             hidden_rows=150)
+    rep = Replica.for_batch(shape, "s11", 1, b)
+    hidden = WD.hidden_tensor(shape, "s11", b.hidden_rows)
+    h0 = to64(hidden)
+    rep.forward(0, hidden, WD.batch_tensors(b))
+    torch.cuda.synchronize()
+    ref, _, cache, _ = oracle_prefill_seqs(shape, "s11", 0, b, range(b.n_seqs), h0)
+    _check_rows("odd-head prefill", to64(hidden)[b.row_idx], ref, h0[b.row_idx])
+    for s in range(b.n_seqs):
+        t0, t1 = int(b.prior_lens[s]), int(b.ctx_lens[s])
+        K, V = gpu_cache_tokens(rep.layers[0], b, s, t0, t1)
+        assert normwise_err(K, cache.K[s][t0:t1]) < TOL
+        assert normwise_err(V, cache.V[s][t0:t1]) < TOL
+
+
 def test_empty_call_is_a_no_op():
     shape, b = _small_decode(8)
     rep = Replica.for_batch(shape, "s8", 1, b)
