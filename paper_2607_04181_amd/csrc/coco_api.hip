@@ -47,7 +47,9 @@ struct coco_layer {
   // workspace carve-out
   void *x = nullptr, *h = nullptr, *q = nullptr, *o = nullptr, *h2 = nullptr, *u = nullptr;
   float *x1 = nullptr, *part = nullptr, *attn_o = nullptr, *attn_ml = nullptr;
-  float* ss = nullptr;  // per-slice row sums of squares (decode QKV with RMSNorm_1 folded in)
+  // Row sums of squares: per K-slice (decode QKV with RMSNorm_1 folded in) or
+  // per 256-column tile (prefill O projection with RMSNorm_2 folded in).
+  float* ss = nullptr;
   double* inv_freq = nullptr;
   float* rope = nullptr;  // RoPE table [rope_rows][head_dim / 2] (cos, sin)
   int rope_rows = 0;      // positions the configuration admits
@@ -203,7 +205,9 @@ int coco_layer_init(const coco_layer_config* cfg, const coco_layer_weights* laye
       c.dtype == COCO_BF16 ? align256((size_t)H->dec_rows * c.n_q_heads * H->max_splits * 2 * 4) : 0,
       align256((size_t)(c.head_dim / 2) * 8),  // inv_freq
       align256((size_t)(H->dec_rows + 1) * 4),  // split_off
-      align256((size_t)16 * R * 4),  // ss: at most 16 K-slices
+      // ss: per-slice row sums of squares (decode QKV, at most 16 K-slices)
+      // or per-256-column-tile ones (prefill O projection)
+      align256((size_t)(c.d_model / 256 > 16 ? c.d_model / 256 : 16) * R * 4),
       align256((size_t)H->rope_rows * (c.head_dim / 2) * 8),  // RoPE table
       align256(R * 8)};  // row_info
   for (int i = 0; i < 15; ++i) {
@@ -510,6 +514,8 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
     // them is made.
     const bool fold_norm = !pre && std::is_same<T, bf16_t>::value;
     const bool fuse_qkv = pre && std::is_same<T, bf16_t>::value && tile_qkv_fusable(Hq, Hkv, d);
+    const bool fold_norm2 =
+        pre && std::is_same<T, bf16_t>::value && tile_norm2_foldable(d, Hq * hd, F);
     const T* x_src = first_l ? hidden : x;                     // this layer's input rows
     const int32_t* x_idx = first_l ? row_idx : nullptr;
     // The fused prefill QKV epilogue reads each row's (position, cache block),
@@ -542,7 +548,7 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
     } else if (fuse_qkv) {
       // Prefill (bf16, QKV projection not split along K): RoPE and the cache
       // append run in the GEMM's epilogue.
-      TileQkvArgs qa;
+      TileEpiArgs qa;
       qa.row_info = H->row_info;
       qa.rope = H->rope;
       qa.q_out = (uint16_t*)q;
@@ -568,18 +574,30 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
                                           c.rms_eps, st)));
     // Attention over the paged cache.
     if ((rc = attention<T>(H, w, M, positions, seq_starts, n_seqs, bt, ctx, st))) return rc;
-    // O projection + residual + RMSNorm_2.
-    TIMED(COCO_K_GEMM_O, if ((rc = gemm<T>(H, o, (const T*)w.w_o, M, d, Hq * hd, pre, &S, st))) return rc);
-    TIMED(COCO_K_RESIDUAL_NORM,
-          HIPCHK(launch_residual_rmsnorm<T>(H->part, S, M, d, x_src, x_idx, (const T*)w.gamma_mlp,
-                                            c.rms_eps, H->x1, h2, st)));
+    // O projection + residual + RMSNorm_2. Prefill (bf16, unsplit O and
+    // gate/up projections): the O projection's epilogue adds the residual and
+    // writes bf16(x1 * gamma_2) with per-tile sums of x1^2; the gate/up
+    // epilogue applies each row's 1/rms, so no separate norm kernel runs.
+    if (fold_norm2) {
+      TIMED(COCO_K_GEMM_O,
+            HIPCHK(launch_gemm_tile_resid_bf16((const uint16_t*)o, (const uint16_t*)w.w_o, M, d,
+                                               Hq * hd, (const uint16_t*)x_src, x_idx,
+                                               (const uint16_t*)w.gamma_mlp, H->x1,
+                                               (uint16_t*)h2, H->ss, st)));
+    } else {
+      TIMED(COCO_K_GEMM_O, if ((rc = gemm<T>(H, o, (const T*)w.w_o, M, d, Hq * hd, pre, &S, st))) return rc);
+      TIMED(COCO_K_RESIDUAL_NORM,
+            HIPCHK(launch_residual_rmsnorm<T>(H->part, S, M, d, x_src, x_idx,
+                                              (const T*)w.gamma_mlp, c.rms_eps, H->x1, h2, st)));
+    }
     // SwiGLU MLP (prefill: SwiGLU in the gate/up GEMM's epilogue when the
     // GEMM is not split along K).
     if (fused_swiglu<T>(pre, F, d)) {
       if (pre) {
         TIMED(COCO_K_GEMM_GATE_UP,
               HIPCHK(launch_gemm_tile_swiglu_bf16((const bf16_t*)h2, (const bf16_t*)w.w_gate_up,
-                                                  (bf16_t*)u, M, F, d, st)));
+                                                  (bf16_t*)u, M, F, d,
+                                                  fold_norm2 ? H->ss : nullptr, c.rms_eps, st)));
       } else {
         TIMED(COCO_K_GEMM_GATE_UP,
               HIPCHK(launch_gemm_skinny_swiglu_bf16((const bf16_t*)h2,

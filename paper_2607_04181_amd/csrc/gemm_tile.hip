@@ -25,7 +25,10 @@
 //     each wave and writes silu(gate) * up directly in bf16;
 //   * for the QKV projection (unsplit) a variant orders each head's columns so
 //     that a lane holds both dims j and j + 64 of its rows, applies RoPE in
-//     registers and writes queries and the cache tiles directly in bf16.
+//     registers and writes queries and the cache tiles directly in bf16;
+//   * for the O projection (unsplit) a variant adds the residual and writes
+//     the RMSNorm_2 operand bf16(x1 * gamma) with per-tile row sums of x1^2,
+//     which the gate/up variant turns into each row's 1/rms.
 // Every output element is summed over k in ascending 16-steps within its
 // slice, independent of M and of the tile it falls in, so request-aligned
 // prefill splits give identical bits.
@@ -73,11 +76,13 @@ __shared__ __attribute__((aligned(16))) bf16_t g_ta0[kTM * kTK], g_ta1[kTM * kTK
     g_ta2[kTM * kTK], g_ta3[kTM * kTK];
 __shared__ __attribute__((aligned(16))) bf16_t g_tw0[kTN * kTK], g_tw1[kTN * kTK],
     g_tw2[kTN * kTK], g_tw3[kTN * kTK];
-// QKV epilogue: position (clamped to the RoPE table) and cache block of each
-// row of the tile.
+// Per-row values of the tile for the epilogues: QKV: position (clamped to the
+// RoPE table) and cache block; residual: source row of the residual; SwiGLU
+// with RMSNorm_2 folded in: the row's 1/rms (bits of a float).
 __shared__ int g_row_pos[kTM], g_row_blk[kTM];
 
-enum { kTilePartial = 0, kTileSwiglu = 1, kTileQkv = 2 };
+enum { kTilePartial = 0, kTileSwiglu = 1, kTileQkv = 2, kTileResid = 3 };
+constexpr int kMaxNormTiles = 32;  // d <= 32 * 256 for the folded RMSNorm_2
 
 // kTilePartial: C is the fp32 partial of K-slice blockIdx.y.
 // kTileSwiglu: W is the [2F][K] gate/up matrix; each 32-column half of a
@@ -86,6 +91,11 @@ enum { kTilePartial = 0, kTileSwiglu = 1, kTileQkv = 2 };
 // h = silu(gate) * up in bf16 to the [M][F] buffer `H` (N = 2F, one K-slice).
 // kTileQkv: W is the [(Hq + 2 Hkv) * 128][K] QKV matrix, N a multiple of 256
 // (two heads per tile), one K-slice; see the epilogue.
+// kTileResid: one K-slice, N a multiple of 256; C = x1 = A W^T + residual
+// (fp32), H = bf16(x1 * gamma) and ea.ss_part[n0 / 256][m] = sum over the
+// tile's columns of x1^2.
+// kTileSwiglu with ea.ss_in: gate and up of row m are first scaled by
+// 1 / sqrt(sum_t ss_in[t][m] / ea.d + ea.eps), t < ea.n_ss, in tile order.
 // k_slice is a multiple of kTK * kTBuf.
 template <int MODE>
 __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __restrict__ A,
@@ -93,7 +103,7 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
                                                                  float* __restrict__ C,
                                                                  bf16_t* __restrict__ H, int M,
                                                                  int N, int K, int k_slice,
-                                                                 TileQkvArgs qa) {
+                                                                 TileEpiArgs ea) {
   constexpr bool FUSE = MODE == kTileSwiglu;
   bf16_t* const ta[kTBuf] = {g_ta0, g_ta1, g_ta2, g_ta3};
   bf16_t* const tw[kTBuf] = {g_tw0, g_tw1, g_tw2, g_tw3};
@@ -189,15 +199,36 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
     __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
   };
 
-  // QKV epilogue: this thread's tile row slot (position, cache block), loaded
-  // ahead of the ring so the stage waits below also cover it.
+  // Per-row inputs of the epilogues, loaded ahead of the ring so the stage
+  // waits below also cover them: QKV row slot (position, cache block);
+  // residual source row; the per-tile sums of squares of the row.
   u32x2_t rinfo = {0u, 0u};
-  if constexpr (MODE == kTileQkv)
-    if (tid < kTM) rinfo = *(const u32x2_t*)(qa.row_info + 2 * min(m0 + tid, M - 1));
+  int rrow = 0;
+  float ssv[kMaxNormTiles];
+  const bool fold_norm = MODE == kTileSwiglu && ea.ss_in != nullptr;
+  if (tid < kTM) {
+    const int m = min(m0 + tid, M - 1);
+    if constexpr (MODE == kTileQkv) rinfo = *(const u32x2_t*)(ea.row_info + 2 * m);
+    if constexpr (MODE == kTileResid) rrow = ea.res_idx ? ea.res_idx[m] : m;
+    if (fold_norm) {
+#pragma unroll
+      for (int t = 0; t < kMaxNormTiles; ++t)
+        ssv[t] = t < ea.n_ss ? ea.ss_in[(int64_t)t * M + m] : 0.f;
+    }
+  }
 
   issue(0, 0);
   issue(1, 1);
   issue(2, 2);
+  // The row's 1/rms (sums in tile order), once the loads above are in.
+  float rnorm = 1.f;
+  if (fold_norm && tid < kTM) {
+    float t2 = 0.f;
+#pragma unroll
+    for (int t = 0; t < kMaxNormTiles; ++t)
+      if (t < ea.n_ss) t2 += ssv[t];
+    rnorm = 1.0f / sqrtf(t2 / (float)ea.d + ea.eps);
+  }
   wait_vmcnt<8>();  // this wave's stage-0 loads are in LDS
   stage_barrier();  // ... and every wave's
   bf16x8_t a0[4], w0[2], a1[4], w1[2];
@@ -242,12 +273,12 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
         default: return g_tw3;
       }
     };
-    if (hh0 < qa.Hq + qa.Hkv) {
+    if (hh0 < ea.Hq + ea.Hkv) {
 #pragma unroll
       for (int c = 0; c < 16; ++c) {
         const int row = 32 * wv + 2 * c + hi;
         __builtin_amdgcn_global_load_lds(
-            qa.rope + ((int64_t)g_row_pos[row] * (kHd / 2) + 2 * l32) * 2,
+            ea.rope + ((int64_t)g_row_pos[row] * (kHd / 2) + 2 * l32) * 2,
             (lds_void_t*)(ring(wv) + c * 512), 16, 0, 0);
       }
       wait_vmcnt<0>();
@@ -258,7 +289,7 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
     // keys (rotated) and values to their cache slot (block, position % 16).
     const int hh = hh0 + (wn >> 1);
     const int jd = (wn & 1) * 32 + l32;
-    const int kind = hh < qa.Hq ? 0 : (hh < qa.Hq + qa.Hkv ? 1 : 2);
+    const int kind = hh < ea.Hq ? 0 : (hh < ea.Hq + ea.Hkv ? 1 : 2);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -278,14 +309,14 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
             up = rup;
           }
           if (kind == 0) {
-            bf16_t* dst = qa.q_out + ((int64_t)m * qa.Hq + hh) * kHd;
+            bf16_t* dst = ea.q_out + ((int64_t)m * ea.Hq + hh) * kHd;
             dst[jd] = (bf16_t)f32_to_bf16(lo);
             dst[jd + 64] = (bf16_t)f32_to_bf16(up);
           } else {
             const int slot = pos % kBlockTokens;
-            const int g = hh - qa.Hq - (kind == 2 ? qa.Hkv : 0);
-            bf16_t* tile = (kind == 1 ? qa.k_cache : qa.v_cache) +
-                           ((int64_t)g_row_blk[lr] * qa.Hkv + g) * kTile;
+            const int g = hh - ea.Hq - (kind == 2 ? ea.Hkv : 0);
+            bf16_t* tile = (kind == 1 ? ea.k_cache : ea.v_cache) +
+                           ((int64_t)g_row_blk[lr] * ea.Hkv + g) * kTile;
             if (kind == 1) {
               tile[k_tile_offset(slot, jd)] = (bf16_t)f32_to_bf16(lo);
               tile[k_tile_offset(slot, jd + 64)] = (bf16_t)f32_to_bf16(up);
@@ -297,7 +328,85 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
         }
     return;
   }
+  if constexpr (MODE == kTileResid) {
+    // x1 = acc + residual row (bf16 [*][N], row ea.res_idx[m] or m), staged by
+    // direct loads into the idle ring (tile row lr at ring object lr / 32,
+    // 512 bytes per row); H = bf16(x1 * gamma). Each lane's x1^2 over its two
+    // columns goes back into the ring as [lr][128] with the 4-byte
+    // slot k = 32 wn + l32 stored at k ^ (lr % 32) (conflict-free reads),
+    // and thread t < 256 sums row t's 128 slots in slot order.
+    if (tid < kTM) g_row_pos[tid] = rrow;
+    __syncthreads();
+    auto ring = [](int k) -> bf16_t* {  // k wave-uniform
+      switch (k) {
+        case 0: return g_ta0;
+        case 1: return g_ta1;
+        case 2: return g_ta2;
+        case 3: return g_ta3;
+        case 4: return g_tw0;
+        case 5: return g_tw1;
+        case 6: return g_tw2;
+        default: return g_tw3;
+      }
+    };
+#pragma unroll
+    for (int c = 0; c < 16; ++c) {
+      const int row = 32 * wv + 2 * c + hi;
+      __builtin_amdgcn_global_load_lds(ea.res_x + (int64_t)g_row_pos[row] * N + n0 + 8 * l32,
+                                       (lds_void_t*)(ring(wv) + c * 512), 16, 0, 0);
+    }
+    float gam[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) gam[j] = bf16_to_f32(ea.gamma[n0 + wn * 64 + j * 32 + l32]);
+    wait_vmcnt<0>();
+    __syncthreads();
+    float v[4][4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int lr = wm * 128 + i * 32 + 8 * jj + 4 * hi + r;
+          const int m = m0 + lr;
+          const bf16_t* xrow = ring(wm * 4 + i) + (8 * jj + 4 * hi + r) * 256;
+          float sq = 0.f;
+#pragma unroll
+          for (int j = 0; j < 2; ++j) {
+            const int col = wn * 64 + j * 32 + l32;
+            const float x1 = acc[i][j][4 * jj + r] + bf16_to_f32(xrow[col]);
+            sq += x1 * x1;
+            if (m < M) {
+              C[(int64_t)m * N + n0 + col] = x1;
+              H[(int64_t)m * N + n0 + col] = (bf16_t)f32_to_bf16(x1 * gam[j]);
+            }
+          }
+          v[i][jj][r] = sq;
+        }
+    __syncthreads();  // every wave is done with the residual tile
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int rr = 8 * jj + 4 * hi + r;  // row within ring object wm * 4 + i
+          ((float*)ring(wm * 4 + i))[rr * 128 + ((wn * 32 + l32) ^ rr)] = v[i][jj][r];
+        }
+    __syncthreads();
+    if (tid < kTM && m0 + tid < M) {
+      const float* sr = (const float*)ring(tid >> 5) + (tid & 31) * 128;
+      float t2 = 0.f;
+      for (int k = 0; k < 128; ++k) t2 += sr[k ^ (tid & 31)];
+      ea.ss_part[(int64_t)(n0 / kTN) * M + m0 + tid] = t2;
+    }
+    return;
+  }
   if (FUSE) {
+    if (fold_norm) {
+      if (tid < kTM) g_row_pos[tid] = __float_as_int(rnorm);
+      __syncthreads();
+    }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int o = o0 + 32 * wn + l32;
@@ -305,8 +414,14 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
       for (int jj = 0; jj < 4; ++jj)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int m = m0 + wm * 128 + i * 32 + 8 * jj + 4 * hi + r;
-          const float g = acc[i][0][4 * jj + r], u = acc[i][1][4 * jj + r];
+          const int lr = wm * 128 + i * 32 + 8 * jj + 4 * hi + r;
+          const int m = m0 + lr;
+          float g = acc[i][0][4 * jj + r], u = acc[i][1][4 * jj + r];
+          if (fold_norm) {
+            const float rs = __int_as_float(g_row_pos[lr]);
+            g *= rs;
+            u *= rs;
+          }
           if (m < M) H[(int64_t)m * F + o] = (bf16_t)f32_to_bf16(g / (1.0f + expf(-g)) * u);
         }
     }
@@ -348,18 +463,51 @@ hipError_t launch_gemm_tile_bf16(const uint16_t* A, const uint16_t* W, float* C,
   if (S < 1 || K % (kTK * kTBuf * S) != 0) return hipErrorInvalidValue;
   const int tiles = ((M + kTM - 1) / kTM) * ((N + kTN - 1) / kTN);
   hipLaunchKernelGGL(gemm_tile_kernel<kTilePartial>, dim3(tiles, S), dim3(kTThreads), 0, st, A,
-                     W, C, nullptr, M, N, K, K / S, TileQkvArgs{});
+                     W, C, nullptr, M, N, K, K / S, TileEpiArgs{});
   return hipGetLastError();
 }
 
 hipError_t launch_gemm_tile_swiglu_bf16(const uint16_t* A, const uint16_t* W_gate_up,
-                                        uint16_t* H, int M, int F, int K, hipStream_t st) {
+                                        uint16_t* H, int M, int F, int K, const float* ss_in,
+                                        float eps, hipStream_t st) {
   if (M <= 0) return hipSuccess;
   if (F % (kTN / 2) != 0 || K % (kTK * kTBuf) != 0 || tile_splits(2 * F, K) != 1)
     return hipErrorInvalidValue;
+  TileEpiArgs ea{};
+  if (ss_in) {
+    if (K % kTN != 0 || K / kTN > kMaxNormTiles) return hipErrorInvalidValue;
+    ea.ss_in = ss_in;
+    ea.n_ss = K / kTN;
+    ea.d = K;
+    ea.eps = eps;
+  }
   const int tiles = ((M + kTM - 1) / kTM) * (2 * F / kTN);
   hipLaunchKernelGGL(gemm_tile_kernel<kTileSwiglu>, dim3(tiles, 1), dim3(kTThreads), 0, st, A,
-                     W_gate_up, nullptr, H, M, 2 * F, K, K, TileQkvArgs{});
+                     W_gate_up, nullptr, H, M, 2 * F, K, K, ea);
+  return hipGetLastError();
+}
+
+bool tile_norm2_foldable(int d, int qdim, int F) {
+  return d % kTN == 0 && d / kTN <= kMaxNormTiles && qdim % (kTK * kTBuf) == 0 &&
+         tile_splits(d, qdim) == 1 && F % (kTN / 2) == 0 && tile_splits(2 * F, d) == 1;
+}
+
+hipError_t launch_gemm_tile_resid_bf16(const uint16_t* A, const uint16_t* W, int M, int N, int K,
+                                       const uint16_t* res_x, const int32_t* res_idx,
+                                       const uint16_t* gamma, float* x1, uint16_t* h,
+                                       float* ss_part, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  if (N % kTN != 0 || N / kTN > kMaxNormTiles || K % (kTK * kTBuf) != 0 ||
+      tile_splits(N, K) != 1 || !res_x || !gamma || !x1 || !h || !ss_part)
+    return hipErrorInvalidValue;
+  TileEpiArgs ea{};
+  ea.res_x = res_x;
+  ea.res_idx = res_idx;
+  ea.gamma = gamma;
+  ea.ss_part = ss_part;
+  const int tiles = ((M + kTM - 1) / kTM) * (N / kTN);
+  hipLaunchKernelGGL(gemm_tile_kernel<kTileResid>, dim3(tiles, 1), dim3(kTThreads), 0, st, A, W,
+                     x1, h, M, N, K, K, ea);
   return hipGetLastError();
 }
 
@@ -369,13 +517,13 @@ bool tile_qkv_fusable(int Hq, int Hkv, int K) {
 }
 
 hipError_t launch_gemm_tile_qkv_bf16(const uint16_t* A, const uint16_t* W_qkv, int M, int K,
-                                     const TileQkvArgs& qa, hipStream_t st) {
+                                     const TileEpiArgs& ea, hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  if (!tile_qkv_fusable(qa.Hq, qa.Hkv, K) || !qa.row_info || !qa.rope) return hipErrorInvalidValue;
-  const int N = (qa.Hq + 2 * qa.Hkv) * 128;
+  if (!tile_qkv_fusable(ea.Hq, ea.Hkv, K) || !ea.row_info || !ea.rope) return hipErrorInvalidValue;
+  const int N = (ea.Hq + 2 * ea.Hkv) * 128;
   const int tiles = ((M + kTM - 1) / kTM) * (N / kTN);
   hipLaunchKernelGGL(gemm_tile_kernel<kTileQkv>, dim3(tiles, 1), dim3(kTThreads), 0, st, A,
-                     W_qkv, nullptr, nullptr, M, N, K, K, qa);
+                     W_qkv, nullptr, nullptr, M, N, K, K, ea);
   return hipGetLastError();
 }
 

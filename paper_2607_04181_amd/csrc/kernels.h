@@ -98,25 +98,51 @@ hipError_t launch_gemm_skinny_swiglu_bf16(const uint16_t* A, const uint16_t* W_g
 int tile_splits(int N, int K);
 hipError_t launch_gemm_tile_bf16(const uint16_t* A, const uint16_t* W, float* C, int M, int N,
                                  int K, int S, hipStream_t st);
+// Epilogue inputs of the tile GEMM variants below (unused fields zero).
+struct TileEpiArgs {
+  // QKV variant
+  const int32_t* row_info = nullptr;  // [M][2] row slots from the gather kernel
+  const float* rope = nullptr;        // [rope_rows][64] (cos, sin) pairs
+  uint16_t* q_out = nullptr;
+  uint16_t* k_cache = nullptr;
+  uint16_t* v_cache = nullptr;
+  int Hq = 0, Hkv = 0;
+  // residual variant
+  const uint16_t* res_x = nullptr;    // residual rows [*][N] (bf16)
+  const int32_t* res_idx = nullptr;   // row m's residual row (null: m)
+  const uint16_t* gamma = nullptr;    // RMSNorm_2 gains [N]
+  float* ss_part = nullptr;           // [N / 256][M] per-tile row sums of x1^2
+  // SwiGLU variant with RMSNorm_2 folded in
+  const float* ss_in = nullptr;       // [n_ss][M] from the residual variant
+  int n_ss = 0, d = 0;
+  float eps = 0.f;
+};
+
 // Gate/up GEMM with the SwiGLU epilogue: H[M][F] = bf16(silu(A W_g^T) * (A W_u^T))
 // where W_gate_up = [W_g; W_u] is [2F][K]; only for tile_splits(2F, K) == 1.
+// With ss_in non-null (RMSNorm_2 folded in: A = bf16(x1 * gamma)), gate and
+// up of row m are first scaled by 1 / sqrt(sum_t ss_in[t][m] / K + eps),
+// t < K / 256 in order.
 hipError_t launch_gemm_tile_swiglu_bf16(const uint16_t* A, const uint16_t* W_gate_up,
-                                        uint16_t* H, int M, int F, int K, hipStream_t st);
+                                        uint16_t* H, int M, int F, int K, const float* ss_in,
+                                        float eps, hipStream_t st);
 // Prefill QKV projection with the QKV epilogue in the GEMM's own epilogue
 // (head_dim 128): RoPE on query and key heads with the rotations of the RoPE
 // table, queries to q_out [M][Hq*128] in bf16, keys and values into the
 // paged cache tiles; no fp32 partials. Only when tile_qkv_fusable(Hq, Hkv, K).
-struct TileQkvArgs {
-  const int32_t* row_info;  // [M][2] row slots from the gather kernel
-  const float* rope;        // [rope_rows][64] (cos, sin) pairs
-  uint16_t* q_out;
-  uint16_t* k_cache;
-  uint16_t* v_cache;
-  int Hq, Hkv;
-};
 bool tile_qkv_fusable(int Hq, int Hkv, int K);
 hipError_t launch_gemm_tile_qkv_bf16(const uint16_t* A, const uint16_t* W_qkv, int M, int K,
-                                     const TileQkvArgs& qa, hipStream_t st);
+                                     const TileEpiArgs& ea, hipStream_t st);
+// Prefill O projection with the residual and the first half of RMSNorm_2 in
+// its epilogue: x1[m] = A W^T + res_x[res_idx ? res_idx[m] : m] (fp32),
+// h[m] = bf16(x1 * gamma), ss_part[t][m] = sum of x1^2 over columns
+// 256t .. 256t + 255. With tile_norm2_foldable(d, qdim, F), the O projection
+// (N = d, K = qdim) and the gate/up projection take this path.
+bool tile_norm2_foldable(int d, int qdim, int F);
+hipError_t launch_gemm_tile_resid_bf16(const uint16_t* A, const uint16_t* W, int M, int N, int K,
+                                       const uint16_t* res_x, const int32_t* res_idx,
+                                       const uint16_t* gamma, float* x1, uint16_t* h,
+                                       float* ss_part, hipStream_t st);
 
 // part[0][m][n] = sum_k A[m][k] * W[n][k], fp32 (tiny fp32 configurations).
 hipError_t launch_gemm_f32(const float* A, const float* W, float* part, int M, int N, int K,

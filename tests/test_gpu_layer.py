@@ -283,10 +283,11 @@ def test_prefill_span_equals_successive_layers_bit_exactly():
 
 
 def test_prefill_with_an_odd_head_count_matches_oracle():
-    """Five query heads and one KV head: the QKV width (7 heads) is not a
-    multiple of the prefill GEMM's two-head tile, so the projection writes fp32
-    partials and the separate QKV epilogue applies RoPE and the cache append."""
-    shape = small_bf16_shape(d=512, hq=5, hkv=1, ffn=768)
+    """Five query heads, one KV head and d = 384: neither the QKV width (7
+    heads) nor d is a multiple of the prefill GEMM's 256-column tile, so the
+    projections write fp32 partials, the separate QKV epilogue applies RoPE
+    and the cache append, and the separate residual + RMSNorm_2 kernel runs."""
+    shape = small_bf16_shape(d=384, hq=5, hkv=1, ffn=768)
     b = ragged_prefill_batch(13, priors=[0, 50, 17], lens=[30, 70, 16], max_ctx=256,
                              hidden_rows=150)
     rep = Replica.for_batch(shape, "s11", 1, b)
