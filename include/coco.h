@@ -197,7 +197,9 @@ enum {
   COCO_WS_Q = 2,  /* rotated queries, [max_rows][Hq*hd], dtype */
   COCO_WS_O = 3,  /* attention output, [max_rows][Hq*hd], dtype */
   COCO_WS_X1 = 4, /* residual after the O projection, [max_rows][d], fp32 */
-  COCO_WS_H2 = 5, /* RMSNorm_2 output, [max_rows][d], dtype */
+  COCO_WS_H2 = 5, /* RMSNorm_2 output, [max_rows][d], dtype (bf16 prefill
+                     with d a multiple of 256 folds the row's 1/rms into the
+                     gate/up projection and holds x1 * gamma_2 here) */
   COCO_WS_U = 6   /* SwiGLU activation, [max_rows][F], dtype */
 };
 int coco_layer_workspace(coco_layer_t h, int32_t which, void* dst, int64_t dst_bytes,
