@@ -445,7 +445,8 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_prefill_kernel(
         vfr[1][pc] = *(const u32x4_t*)(vl + kTileElems + pc * 512);
       }
       // Online softmax, once per 64 keys (log2 domain: p = 2^(s*scale - m)),
-      // P^T packed as two 32-key operands.
+      // P^T packed as two 32-key operands. Stages wholly before the wave's
+      // first row skip the causal mask.
       u32x4_t pk[COLS][2];
 #pragma unroll
       for (int c = 0; c < COLS; ++c) {
@@ -460,8 +461,11 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_prefill_kernel(
           for (int i = 0; i < kPfBlk; ++i) {
             const int tok0 = (st * kPfBlk + i) * kBlockTokens + j4 * 4;
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-              if (tok0 + r <= pos[c]) mx = fmaxf(mx, sc[c][i][r]);
+            for (int r = 0; r < 4; ++r) {
+              // Keys after the row's position score -inf: 2^-inf = 0 below.
+              if (tok0 + r > pos[c]) sc[c][i][r] = -INFINITY;
+              mx = fmaxf(mx, sc[c][i][r]);
+            }
           }
         }
         mx = col_max4(mx) * scale_log2;
@@ -471,21 +475,22 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_prefill_kernel(
         uint32_t pw[kPfBlk][2];
 #pragma unroll
         for (int i = 0; i < kPfBlk; ++i) {
-          const int tok0 = (st * kPfBlk + i) * kBlockTokens + j4 * 4;
           float pr[4];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float e = __builtin_amdgcn_exp2f(fmaf(sc[c][i][r], scale_log2, -m_new));
-            pr[r] = unmasked || tok0 + r <= pos[c] ? e : 0.f;
-          }
+          for (int r = 0; r < 4; ++r)
+            pr[r] = __builtin_amdgcn_exp2f(fmaf(sc[c][i][r], scale_log2, -m_new));
           ps += (pr[0] + pr[1]) + (pr[2] + pr[3]);
           pw[i][0] = pack_bf16x2(pr[0], pr[1]);
           pw[i][1] = pack_bf16x2(pr[2], pr[3]);
         }
         l[c] = l[c] * alpha + ps;
         m[c] = m_new;
+        // alpha is exactly 1 for a column whose max did not move: rescale only
+        // when some column's did (multiplying by 1 would change nothing).
+        if (__ballot(alpha != 1.f) != 0) {
 #pragma unroll
-        for (int n = 0; n < 8; ++n) acc[c][n] = acc[c][n] * alpha;
+          for (int n = 0; n < 8; ++n) acc[c][n] = acc[c][n] * alpha;
+        }
 #pragma unroll
         for (int pp = 0; pp < 2; ++pp)
           pk[c][pp] = u32x4_t{pw[2 * pp][0], pw[2 * pp][1], pw[2 * pp + 1][0], pw[2 * pp + 1][1]};
