@@ -100,7 +100,7 @@ typedef struct {
   int32_t block_size;         /* must be 16 */
   int32_t max_rows;           /* largest n_rows of any call (decode rows or prefill tokens) */
   int32_t max_seqs;           /* largest n_seqs of any call */
-  int32_t max_blocks_per_seq; /* row stride of block_table */
+  int32_t max_blocks_per_seq; /* row stride of block_table (<= 2^24) */
   float rope_theta;           /* RoPE base theta */
   float rms_eps;              /* RMSNorm epsilon */
 } coco_layer_config;

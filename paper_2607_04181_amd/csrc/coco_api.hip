@@ -114,6 +114,8 @@ int check_config(const coco_layer_config* c) {
       c->max_blocks_per_seq <= 0)
     return fail(COCO_EINVAL, "config sizes must be positive");
   if (c->block_size != kBlockTokens) return fail(COCO_EINVAL, "block_size must be 16");
+  if (c->max_blocks_per_seq > (1 << 24))
+    return fail(COCO_EINVAL, "max_blocks_per_seq must be <= 2^24 (positions fit in int32)");
   if (c->n_q_heads % c->n_kv_heads) return fail(COCO_EINVAL, "n_q_heads %% n_kv_heads != 0");
   if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.f))
     return fail(COCO_EINVAL, "rms_eps must be >= 0 and rope_theta > 0");

@@ -56,3 +56,8 @@ def test_init_rejects_bad_config_without_a_gpu():
     assert "n_kv_heads" in _lib.coco_last_error()
     assert _lib.raw_call("coco_layer_forward", None, 0, None, 0, None, 0, None, None, 0, None,
                          None, None) == _lib.COCO_EINVAL
+    # Positions (max_blocks_per_seq * 16) must fit the int32 RoPE table index.
+    cfg = _lib.make_config(512, 8, 2, 128, 768, 1, "bf16", 8, 8, (1 << 24) + 1, 1e4, 1e-5)
+    rc = _lib.raw_call("coco_layer_init", ctypes.byref(cfg), w, ctypes.byref(h))
+    assert rc == _lib.COCO_EINVAL
+    assert "max_blocks_per_seq" in _lib.coco_last_error()
