@@ -216,7 +216,8 @@ def main():
         graph = {"ms_per_step": round(gms, 4)}
         del g
 
-    # Per-kernel durations: every launch bracketed by HIP events on the stream.
+    # Per-kernel durations: every launch carries a pair of HIP events that the
+    # runtime timestamps at the kernel's start and end on its stream.
     coco.coco_layer_set_timing(handle, True)
     per_kernel = {}
     for _ in range(args.steps):

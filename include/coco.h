@@ -207,9 +207,11 @@ int coco_layer_workspace(coco_layer_t h, int32_t which, void* dst, int64_t dst_b
 
 /* Per-kernel timing for benchmarks (calls of any handle are unaffected while
  * it is off). When on, every kernel launched by coco_layer_forward /
- * coco_layer_span_forward on this handle is bracketed by a pair of HIP events
- * recorded on the call's stream, from a pool of events created here (so
- * switching it on allocates; timed calls themselves do not). */
+ * coco_layer_span_forward on this handle is launched with a pair of HIP events
+ * (hipExtLaunchKernelGGL) that the runtime timestamps at the kernel's own
+ * start and end, from a pool of events created here (so switching it on
+ * allocates; timed calls themselves do not). Switch it off before capturing
+ * calls into a HIP graph. */
 enum {
   COCO_K_GATHER_NORM = 0,    /* gather + RMSNorm_1 (or RMSNorm_1 inside a span) */
   COCO_K_GEMM_QKV = 1,       /* QKV projection */

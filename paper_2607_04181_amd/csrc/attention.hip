@@ -610,7 +610,7 @@ hipError_t launch_attn_decode_bf16(const uint16_t* q, const uint16_t* k_cache,
   // of LDS each): a persistent grid of two per CU, never more than the work.
   const int64_t work_bound = (int64_t)n_seqs * max_splits * Hkv;
   const int grid = (int)(work_bound < 2 * num_cus ? work_bound : 2 * num_cus);
-  hipLaunchKernelGGL(attn_decode_kernel, dim3(grid), dim3(kDecWaves * 64), 0, st, q, k_cache,
+  COCO_LAUNCH(attn_decode_kernel, dim3(grid), dim3(kDecWaves * 64), 0, st, q, k_cache,
                      v_cache, block_table, max_blocks, ctx_lens, split_off, n_seqs, Hq, Hkv,
                      part_o, part_ml, max_splits, scale_log2);
   return hipGetLastError();
@@ -620,7 +620,7 @@ hipError_t launch_attn_combine_bf16(const float* part_o, const float* part_ml,
                                     const int32_t* ctx_lens, int n_seqs, int Hq, int max_splits,
                                     uint16_t* o, hipStream_t st) {
   if (n_seqs <= 0) return hipSuccess;
-  hipLaunchKernelGGL(attn_combine_kernel, dim3(Hq, n_seqs), dim3(HD),
+  COCO_LAUNCH(attn_combine_kernel, dim3(Hq, n_seqs), dim3(HD),
                      2 * max_splits * sizeof(float), st, part_o, part_ml, ctx_lens, Hq,
                      max_splits, o);
   return hipGetLastError();
@@ -638,7 +638,7 @@ hipError_t launch_attn_prefill_bf16(const uint16_t* q, const uint16_t* k_cache,
   // tile return at once.
   const int64_t tiles = (n_rows + kPfRows - 1) / kPfRows + n_seqs;
   if (tiles * Hq > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((attn_prefill_kernel<kPfLaunchWaves, 8 / kPfLaunchWaves>),
+  COCO_LAUNCH((attn_prefill_kernel<kPfLaunchWaves, 8 / kPfLaunchWaves>),
                      dim3((unsigned)(tiles * Hq)), dim3(kPfLaunchWaves * 64), 0, st, q,
                      k_cache, v_cache, block_table, max_blocks, ctx_lens, positions, seq_starts,
                      n_seqs, Hq, Hkv, scale_log2, o);
@@ -650,7 +650,7 @@ hipError_t launch_attn_f32(const float* q, const float* k_cache, const float* v_
                            const int32_t* positions, const int32_t* seq_starts, int n_seqs,
                            int n_rows, int Hq, int Hkv, int hd, float* o, hipStream_t st) {
   if (n_rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(attn_f32_kernel, dim3(n_rows, Hq), dim3(64), 0, st, q, k_cache, v_cache,
+  COCO_LAUNCH(attn_f32_kernel, dim3(n_rows, Hq), dim3(64), 0, st, q, k_cache, v_cache,
                      block_table, max_blocks, ctx_lens, positions, seq_starts, n_seqs, Hq, Hkv,
                      hd, o);
   return hipGetLastError();

@@ -66,11 +66,20 @@ struct coco_layer {
   hipStream_t ev_stream = nullptr;
 };
 
+namespace coco {
+LaunchEvents& launch_events() {
+  thread_local LaunchEvents le;
+  return le;
+}
+}  // namespace coco
+
 namespace {
 
 constexpr int kTimingPairs = 4096;
 
-// Brackets one kernel launch with events when timing is on.
+// Times the one kernel launched in its scope when timing is on: the launch
+// timestamps the event pair at the kernel's own start and end. A scope that
+// launches nothing (empty work) records an empty interval.
 struct KernelTimer {
   coco_layer* H;
   int kind;
@@ -85,10 +94,16 @@ struct KernelTimer {
     pair = n;
     H->ev_kind.push_back(kind);
     H->ev_stream = st;
-    (void)hipEventRecord(H->ev[2 * pair], st);
+    coco::launch_events() = coco::LaunchEvents{H->ev[2 * pair], H->ev[2 * pair + 1]};
   }
   ~KernelTimer() {
-    if (pair >= 0) (void)hipEventRecord(H->ev[2 * pair + 1], H->ev_stream);
+    if (pair < 0) return;
+    coco::LaunchEvents& le = coco::launch_events();
+    if (le.start != nullptr) {
+      (void)hipEventRecord(le.start, H->ev_stream);
+      (void)hipEventRecord(le.stop, H->ev_stream);
+      le = coco::LaunchEvents{};
+    }
   }
 };
 

@@ -220,7 +220,7 @@ hipError_t launch_plan(const uint16_t* A, const uint16_t* W, float* part, uint16
   // enough to cover HBM latency; deeper rings measured slower (more requests
   // queued behind each other) and cost registers.
   constexpr int PF = 2;
-  hipLaunchKernelGGL((gemm_skinny_kernel<WAVES, MT, PF, FUSE, NORM>), dim3(N / (16 * WAVES), S),
+  COCO_LAUNCH((gemm_skinny_kernel<WAVES, MT, PF, FUSE, NORM>), dim3(N / (16 * WAVES), S),
                      dim3(WAVES * 64), 0, st, A, W, part, H, M, N, K, K / S, na.row_idx,
                      (const bf16_t*)na.gamma, na.ss);
   return hipGetLastError();
@@ -354,7 +354,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 hipError_t launch_gemm_f32(const float* A, const float* W, float* part, int M, int N, int K,
                            hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  hipLaunchKernelGGL(gemm_f32_kernel, dim3((N + 15) / 16, (M + 15) / 16), dim3(256), 0, st, A,
+  COCO_LAUNCH(gemm_f32_kernel, dim3((N + 15) / 16, (M + 15) / 16), dim3(256), 0, st, A,
                      W, part, M, N, K);
   return hipGetLastError();
 }

@@ -462,7 +462,7 @@ hipError_t launch_gemm_tile_bf16(const uint16_t* A, const uint16_t* W, float* C,
   if (M <= 0) return hipSuccess;
   if (S < 1 || K % (kTK * kTBuf * S) != 0) return hipErrorInvalidValue;
   const int tiles = ((M + kTM - 1) / kTM) * ((N + kTN - 1) / kTN);
-  hipLaunchKernelGGL(gemm_tile_kernel<kTilePartial>, dim3(tiles, S), dim3(kTThreads), 0, st, A,
+  COCO_LAUNCH(gemm_tile_kernel<kTilePartial>, dim3(tiles, S), dim3(kTThreads), 0, st, A,
                      W, C, nullptr, M, N, K, K / S, TileEpiArgs{});
   return hipGetLastError();
 }
@@ -482,7 +482,7 @@ hipError_t launch_gemm_tile_swiglu_bf16(const uint16_t* A, const uint16_t* W_gat
     ea.eps = eps;
   }
   const int tiles = ((M + kTM - 1) / kTM) * (2 * F / kTN);
-  hipLaunchKernelGGL(gemm_tile_kernel<kTileSwiglu>, dim3(tiles, 1), dim3(kTThreads), 0, st, A,
+  COCO_LAUNCH(gemm_tile_kernel<kTileSwiglu>, dim3(tiles, 1), dim3(kTThreads), 0, st, A,
                      W_gate_up, nullptr, H, M, 2 * F, K, K, ea);
   return hipGetLastError();
 }
@@ -506,7 +506,7 @@ hipError_t launch_gemm_tile_resid_bf16(const uint16_t* A, const uint16_t* W, int
   ea.gamma = gamma;
   ea.ss_part = ss_part;
   const int tiles = ((M + kTM - 1) / kTM) * (N / kTN);
-  hipLaunchKernelGGL(gemm_tile_kernel<kTileResid>, dim3(tiles, 1), dim3(kTThreads), 0, st, A, W,
+  COCO_LAUNCH(gemm_tile_kernel<kTileResid>, dim3(tiles, 1), dim3(kTThreads), 0, st, A, W,
                      x1, h, M, N, K, K, ea);
   return hipGetLastError();
 }
@@ -522,7 +522,7 @@ hipError_t launch_gemm_tile_qkv_bf16(const uint16_t* A, const uint16_t* W_qkv, i
   if (!tile_qkv_fusable(ea.Hq, ea.Hkv, K) || !ea.row_info || !ea.rope) return hipErrorInvalidValue;
   const int N = (ea.Hq + 2 * ea.Hkv) * 128;
   const int tiles = ((M + kTM - 1) / kTM) * (N / kTN);
-  hipLaunchKernelGGL(gemm_tile_kernel<kTileQkv>, dim3(tiles, 1), dim3(kTThreads), 0, st, A,
+  COCO_LAUNCH(gemm_tile_kernel<kTileQkv>, dim3(tiles, 1), dim3(kTThreads), 0, st, A,
                      W_qkv, nullptr, nullptr, M, N, K, K, ea);
   return hipGetLastError();
 }

@@ -1,10 +1,27 @@
 // Host-side launchers of the gfx950 kernels (internal to libcoco).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace coco {
+
+// Per-kernel timing (benchmark mode): events that the next kernel launch of
+// this thread passes to hipExtLaunchKernelGGL, which timestamps them at the
+// kernel's own start and end, then clears. Null events: a plain launch.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+LaunchEvents& launch_events();
+
+#define COCO_LAUNCH(kernel, grid, block, shmem, stream, ...)                                  \
+  do {                                                                                        \
+    ::coco::LaunchEvents& le_ = ::coco::launch_events();                                      \
+    hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, le_.start, le_.stop, 0,         \
+                          __VA_ARGS__);                                                       \
+    le_ = ::coco::LaunchEvents{};                                                             \
+  } while (0)
 
 // ---------------------------------------------------------------- row kernels
 // Prefill row slots (optional output of the gather kernel): row_info[2i] =

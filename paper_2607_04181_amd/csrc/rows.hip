@@ -157,7 +157,7 @@ hipError_t launch_gather_rmsnorm(const T* src, const int32_t* row_idx, int M, in
   if (M <= 0) return hipSuccess;
   if (rs.row_info != nullptr && (rs.n_seqs < 1 || rs.max_blocks < 1 || rs.rope_rows < 1))
     return hipErrorInvalidValue;
-  hipLaunchKernelGGL(gather_rmsnorm_kernel<T>, dim3(M), dim3(kRowThreads), 0, st, src, row_idx,
+  COCO_LAUNCH(gather_rmsnorm_kernel<T>, dim3(M), dim3(kRowThreads), 0, st, src, row_idx,
                      d, gamma, eps, x_out, h_out, rs);
   return hipGetLastError();
 }
@@ -184,7 +184,7 @@ hipError_t launch_rope_table(const double* inv_freq, int half, int n_pos, float*
                              hipStream_t st) {
   const int64_t n = (int64_t)n_pos * half;
   if (n <= 0) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(rope_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
+  COCO_LAUNCH(rope_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
                      inv_freq, half, n_pos, rope);
   return hipGetLastError();
 }
@@ -332,7 +332,7 @@ hipError_t launch_qkv_epilogue(const float* part, int S, int M, int Hq, int Hkv,
   if (M <= 0) return hipSuccess;
   if (hd > 256 || hd % 2 != 0) return hipErrorInvalidValue;
   const dim3 grid((Hq + 2 * Hkv + kEpiHeads - 1) / kEpiHeads, M);
-  COCO_SWITCH_S(S, hipLaunchKernelGGL((qkv_epilogue_kernel<T, S_>), grid,
+  COCO_SWITCH_S(S, COCO_LAUNCH((qkv_epilogue_kernel<T, S_>), grid,
                                       dim3(kEpiHeads * kWave), 0, st,
                                       part, M, Hq, Hkv, hd, positions, seq_starts, n_seqs,
                                       block_table, max_blocks, inv_freq, q_out, k_cache,
@@ -411,7 +411,7 @@ hipError_t launch_residual_rmsnorm(const float* part, int S, int M, int d, const
                                    T* h2, hipStream_t st) {
   if (M <= 0) return hipSuccess;
   if (d % 4 != 0 || d > 4 * 4 * kNormThreads) return hipErrorInvalidValue;
-  COCO_SWITCH_S(S, hipLaunchKernelGGL((residual_rmsnorm_kernel<T, S_>), dim3(M),
+  COCO_SWITCH_S(S, COCO_LAUNCH((residual_rmsnorm_kernel<T, S_>), dim3(M),
                                       dim3(kNormThreads), 0, st, part, M, d, x, row_idx, gamma,
                                       eps, x1, h2));
   return hipGetLastError();
@@ -441,7 +441,7 @@ hipError_t launch_swiglu(const float* part, int S, int M, int F, T* u, hipStream
   if (M <= 0) return hipSuccess;
   if (F % 4 != 0) return hipErrorInvalidValue;
   const dim3 grid((F / 4 + kRowThreads - 1) / kRowThreads, M);
-  COCO_SWITCH_S(S, hipLaunchKernelGGL((swiglu_kernel<T, S_>), grid, dim3(kRowThreads), 0, st,
+  COCO_SWITCH_S(S, COCO_LAUNCH((swiglu_kernel<T, S_>), grid, dim3(kRowThreads), 0, st,
                                       part, M, F, u));
   return hipGetLastError();
 }
@@ -470,7 +470,7 @@ hipError_t launch_residual_scatter(const float* part, int S, int M, int d, const
   if (M <= 0) return hipSuccess;
   if (d % 4 != 0) return hipErrorInvalidValue;
   const dim3 grid((d / 4 + kRowThreads - 1) / kRowThreads, M);
-  COCO_SWITCH_S(S, hipLaunchKernelGGL((residual_scatter_kernel<T, S_>), grid, dim3(kRowThreads),
+  COCO_SWITCH_S(S, COCO_LAUNCH((residual_scatter_kernel<T, S_>), grid, dim3(kRowThreads),
                                       0, st, part, M, d, x1, out, row_idx));
   return hipGetLastError();
 }
@@ -503,7 +503,7 @@ hipError_t launch_kv_append(const T* k, const T* v, const int32_t* seq_idx,
                             const int32_t* block_table, int max_blocks, T* k_cache,
                             T* v_cache, hipStream_t st) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(kv_append_kernel<T>, dim3(n), dim3(kRowThreads), 0, st, k, v, seq_idx,
+  COCO_LAUNCH(kv_append_kernel<T>, dim3(n), dim3(kRowThreads), 0, st, k, v, seq_idx,
                      positions, Hkv, hd, block_table, max_blocks, k_cache, v_cache);
   return hipGetLastError();
 }
