@@ -304,6 +304,28 @@ def test_prefill_with_an_odd_head_count_matches_oracle():
         assert normwise_err(V, cache.V[s][t0:t1]) < TOL
 
 
+def test_prefill_at_high_positions_matches_oracle():
+    """A chunk at positions near 30,000: far rows of the prefill RoPE table and
+    the cache slots of a long sequence, against the oracle (prior cache bits
+    read from the device pools, which the generator test pins to the CPU ones)."""
+    shape = small_bf16_shape()
+    b = ragged_prefill_batch(14, priors=[30000, 5], lens=[40, 20], max_ctx=32768,
+                             hidden_rows=80)
+    rep = Replica.for_batch(shape, "s12", 1, b)
+    hidden = WD.hidden_tensor(shape, "s12", b.hidden_rows)
+    h0 = to64(hidden)
+    rep.forward(0, hidden, WD.batch_tensors(b))
+    torch.cuda.synchronize()
+    ref, _, cache, _ = oracle_prefill_seqs(shape, "s12", 0, b, range(b.n_seqs), h0,
+                                           source="device", dev_layer=rep.layers[0])
+    _check_rows("high-position prefill", to64(hidden)[b.row_idx], ref, h0[b.row_idx])
+    for s in range(b.n_seqs):
+        t0, t1 = int(b.prior_lens[s]), int(b.ctx_lens[s])
+        K, V = gpu_cache_tokens(rep.layers[0], b, s, t0, t1)
+        assert normwise_err(K, cache.K[s][t0:t1]) < TOL
+        assert normwise_err(V, cache.V[s][t0:t1]) < TOL
+
+
 def test_empty_call_is_a_no_op():
     shape, b = _small_decode(8)
     rep = Replica.for_batch(shape, "s8", 1, b)
