@@ -216,10 +216,12 @@ struct NormArgs {
 template <int WAVES, int MT, bool FUSE, bool NORM>
 hipError_t launch_plan(const uint16_t* A, const uint16_t* W, float* part, uint16_t* H, int M,
                        int N, int K, int S, NormArgs na, hipStream_t st) {
-  // Two stages of weights in flight per wave (~56 KB per CU at 7 waves) is
-  // enough to cover HBM latency; deeper rings measured slower (more requests
-  // queued behind each other) and cost registers.
-  constexpr int PF = 2;
+  // Two stages of weights in flight per wave (~56 KB per CU at 7 waves) cover
+  // HBM latency for 64-row tiles; deeper rings measured slower there (more
+  // requests queued behind each other) and cost registers. With 128-row tiles
+  // and 8 waves, four stages measured faster (70B O and down shapes), and no
+  // worse on the 32B gate/up shape (the NORM variant would spill with four).
+  constexpr int PF = (MT == 8 && WAVES == 8 && !NORM) ? 4 : 2;
   COCO_LAUNCH((gemm_skinny_kernel<WAVES, MT, PF, FUSE, NORM>), dim3(N / (16 * WAVES), S),
                      dim3(WAVES * 64), 0, st, A, W, part, H, M, N, K, K / S, na.row_idx,
                      (const bf16_t*)na.gamma, na.ss);
