@@ -34,6 +34,8 @@ def parse():
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--workload", default="c2",
                    choices=["c2", "c3", "c3full", "c4p", "c4d", "c5"])
+    p.add_argument("--batch", type=int, default=64,
+                   help="decode rows of the 8B workload (c2): one replica's share of the batch")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="target duration of the oracle CPU baseline (0 = skip)")
     p.add_argument("--no-graph", action="store_true",
@@ -99,11 +101,13 @@ def load_traffic(kernel_kind, workload_name, src_sha):
     return float(m_b.group(1))
 
 
-def build_workload(name):
+def build_workload(name, batch=64):
     import numpy as np
     import workloads as W
     if name == "c2":
-        wl = W.c2_llama8b_decode()
+        wl = W.c2_llama8b_decode(batch)
+        if batch != 64:
+            wl.name = f"llama8b_decode_b{batch}"
         return wl, wl.batch, 1
     if name == "c3":
         wl = W.c3_llama8b_skewed()
@@ -145,9 +149,15 @@ def main():
     import workloads as W
     from workloads import device as WD
 
+    if args.batch != 64 and args.workload != "c2":
+        print(json.dumps({"error": "--batch applies to the 8B decode workload (c2) only"}))
+        sys.exit(2)
+    if args.batch < 1:
+        print(json.dumps({"error": "--batch must be >= 1"}))
+        sys.exit(2)
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
-    wl, batch, n_layers = build_workload(args.workload)
+    wl, batch, n_layers = build_workload(args.workload, args.batch)
     shape = wl.shape
     t0 = time.time()
     layers = [WD.layer_tensors(shape, wl.tag, l, batch.num_blocks) for l in range(n_layers)]
