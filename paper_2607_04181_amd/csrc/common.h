@@ -43,6 +43,23 @@ template <> struct Elem<float> {
   static __device__ __forceinline__ void store(float* p, float v) { *p = v; }
 };
 
+// Waits until at most N vector-memory operations of this wave are in flight
+// (vmcnt only; direct global-to-LDS loads count there).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// Workgroup barrier that keeps the compiler from moving memory operations
+// across it and adds no waits of its own: the direct-to-LDS loads of later
+// stages stay in flight through it (a __syncthreads() fence would drain them).
+__device__ __forceinline__ void stage_barrier() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);

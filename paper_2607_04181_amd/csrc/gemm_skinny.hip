@@ -16,6 +16,11 @@
 //     16-rows-per-instruction fragment reads hit distinct banks;
 //   * each 16x16 output tile is accumulated with v_mfma_f32_16x16x32_bf16 in
 //     ascending k.
+// A pass covers up to 128 rows. Plans of 7 or 8 waves without the folded
+// norm take a row-split variant with passes of 256 rows for larger batches
+// (gemm_skinny_rows_kernel below): there the weight tile of a stage goes to
+// LDS and the row tiles are dealt to the waves, since every wave reading the
+// whole activation tile from LDS costs more LDS time at that size.
 // The NORM variant (decode QKV projection) folds the row gather and the
 // first RMSNorm into the activation staging: it reads the layer input rows
 // x[row_idx[m]] directly, stages bf16(x * gamma), and writes each row's sum
@@ -27,6 +32,8 @@
 // the other rows in the call (batch invariance). Partials of the S slices
 // are added in slice order by the consumer epilogue.
 #include <math.h>
+
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -40,6 +47,46 @@ constexpr int kCUs = 256;
 
 // LDS element offset of 16-byte chunk c (0..15) of activation row r.
 __device__ __forceinline__ int a_swz(int r, int c) { return r * kBK + ((c ^ (r & 15)) << 3); }
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// NORM row sums, by one wave: ss[blockIdx.y][r] = sum of x^2 over the K-slice
+// for rows r = r_first, r_first + gridDim.x, ... below r_end (each row of a
+// pass by one workgroup of the slice), per lane in chunk order, then a fixed
+// butterfly. Both decode GEMM kernels use it, so a row's sum never depends
+// on the batch.
+__device__ __forceinline__ void norm_row_sums(const bf16_t* __restrict__ A,
+                                              const int32_t* __restrict__ row_idx, int M, int K,
+                                              int k_begin, int k_slice, int r_first, int r_end,
+                                              float* __restrict__ ss, int lane) {
+  for (int r = r_first; r < r_end; r += gridDim.x) {
+    const bf16_t* xr = A + (int64_t)((row_idx != nullptr) ? row_idx[r] : r) * K + k_begin;
+    float t = 0.f;
+    for (int c = lane; c < k_slice / 8; c += 64) {
+      const u32x4_t u = *(const u32x4_t*)(xr + c * 8);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float lo = __uint_as_float(u[e] << 16), hi = __uint_as_float(u[e] & 0xFFFF0000u);
+        t = fmaf(lo, lo, t);
+        t = fmaf(hi, hi, t);
+      }
+    }
+    t = wave_sum(t);
+    if (lane == 0) ss[(int64_t)blockIdx.y * M + r] = t;
+  }
+}
+
+// bf16(x * gamma) of eight packed elements, the product in fp32.
+__device__ __forceinline__ u32x4_t scale_bf16x8(u32x4_t x, u32x4_t g) {
+  u32x4_t y;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float lo = __uint_as_float(x[e] << 16), hi = __uint_as_float(x[e] & 0xFFFF0000u);
+    const float glo = __uint_as_float(g[e] << 16), ghi = __uint_as_float(g[e] & 0xFFFF0000u);
+    y[e] = pack_bf16x2(lo * glo, hi * ghi);
+  }
+  return y;
+}
 
 // FUSE: W is the [2F][K] gate/up matrix (N = 2F, one K-slice). Lanes
 // c16 < 8 of a wave stream gate rows o0..o0+7 and lanes c16 >= 8 the
@@ -123,43 +170,17 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
         const int q = tid + v * NT;
         const bool live = st < stages && m0 + (q >> 4) < M;
         u32x4_t val = live ? areg[slot][v] : u32x4_t{0u, 0u, 0u, 0u};
-        if (NORM) {
-          // x * gamma in fp32, rounded to bf16.
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float lo = __uint_as_float(val[e] << 16), hi = __uint_as_float(val[e] & 0xFFFF0000u);
-            const float glo = __uint_as_float(greg[slot][e] << 16);
-            const float ghi = __uint_as_float(greg[slot][e] & 0xFFFF0000u);
-            val[e] = pack_bf16x2(lo * glo, hi * ghi);
-          }
-        }
+        if (NORM) val = scale_bf16x8(val, greg[slot]);  // x * gamma in fp32, rounded to bf16
         if (q < kChunks) *(u32x4_t*)(&lds[buf][a_swz(q >> 4, q & 15)]) = val;
       }
     };
 
     load_a(0, 0);
     load_a(1, 1);
-    if (NORM && wv == 0) {
-      // Sums of squares of this K-slice for rows m0 + blockIdx.x, + gridDim.x,
-      // ... (each row by one workgroup of the slice), while the first weight
-      // stages are in flight: per lane in chunk order, then a fixed butterfly.
-      for (int r = m0 + blockIdx.x; r < min(M, m0 + MT * 16); r += gridDim.x) {
-        const bf16_t* xr =
-            A + (int64_t)((row_idx != nullptr) ? row_idx[r] : r) * K + k_begin;
-        float t = 0.f;
-        for (int c = lane; c < k_slice / 8; c += 64) {
-          const u32x4_t u = *(const u32x4_t*)(xr + c * 8);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float lo = __uint_as_float(u[e] << 16), hi = __uint_as_float(u[e] & 0xFFFF0000u);
-            t = fmaf(lo, lo, t);
-            t = fmaf(hi, hi, t);
-          }
-        }
-        t = wave_sum(t);
-        if (lane == 0) ss[(int64_t)blockIdx.y * M + r] = t;
-      }
-    }
+    // Row sums of squares of this pass while the first weight stages are in flight.
+    if (NORM && wv == 0)
+      norm_row_sums(A, row_idx, M, K, k_begin, k_slice, m0 + blockIdx.x, min(M, m0 + MT * 16),
+                    ss, lane);
     store_a(0, 0, 0);
     __syncthreads();
 
@@ -207,6 +228,210 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
   }
 }
 
+// Row-split variant for passes of 256 rows (16 row tiles). Same outputs, bit
+// for bit, as gemm_skinny_kernel: every 16x16 output tile is the same chain of
+// v_mfma_f32_16x16x32_bf16 (activation fragment as the A operand, weight
+// fragment as B) in ascending k.
+//   * the workgroup's 16*WAVES weight rows of a 64-k stage go straight to LDS
+//     (global_load_lds, 16 bytes per lane; wave w fills rows 16w .. 16w + 15
+//     as two 1 KB loads of eight rows) into a ring of six slots, four stages
+//     in flight (as many weight bytes per CU as the other kernel's two 128-k
+//     register stages); 16-byte chunks are swizzled as chunk ^ (row / 2) % 8,
+//     so the 16 rows a fragment read touches per 16-lane group cover every
+//     bank once;
+//   * row tile t of the pass (rows 16t .. 16t + 15) belongs to wave t % WAVES;
+//     a wave loads its tiles' activation fragments from memory straight into
+//     registers, three stages deep (stage st + 3 once stage st has been
+//     multiplied), and multiplies them with all 16*WAVES weight rows (LDS
+//     reads per stage: WAVES * 2 KB per wave);
+//   * one barrier per stage: the wait before it covers this wave's direct
+//     loads of the stage; after it, every wave's are in LDS and the slot the
+//     stage's new loads overwrite was read by every wave two stages ago.
+constexpr int kRowTiles = 16;  // row tiles per pass
+constexpr int kRK = 64;        // k per stage
+constexpr int kRSlots = 6;     // weight ring slots
+constexpr int kRAhead = 4;     // weight stages in flight
+constexpr int kRAst = 3;       // activation stages in registers
+
+// LDS element offset of 16-byte chunk c (0..7) of row r of a [rows][64] tile.
+__device__ __forceinline__ int w_swz(int r, int c) { return r * kRK + ((c ^ ((r >> 1) & 7)) << 3); }
+
+template <int WAVES, bool FUSE>
+__global__ __launch_bounds__(WAVES * 64) void gemm_skinny_rows_kernel(
+    const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, float* __restrict__ part,
+    bf16_t* __restrict__ H, int M, int N, int K, int k_slice) {
+  constexpr int TPW = (kRowTiles + WAVES - 1) / WAVES;  // row tiles per wave
+  constexpr int NR = 16 * WAVES;                         // weight rows per workgroup
+  constexpr int kDLoads = 2;                             // direct loads per stage
+  constexpr int kALoads = 2 * TPW;                       // activation loads per stage
+  // One LDS object per slot, so the compiler tracks each slot's direct loads.
+  __shared__ __attribute__((aligned(16))) bf16_t w0[NR * kRK], w1[NR * kRK], w2[NR * kRK],
+      w3[NR * kRK], w4[NR * kRK], w5[NR * kRK];
+  bf16_t* const ring[kRSlots] = {w0, w1, w2, w3, w4, w5};
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int c16 = lane & 15, j4 = lane >> 4;
+  const int k_begin = blockIdx.y * k_slice;
+  const int stages = k_slice / kRK;
+  float* out = FUSE ? nullptr : part + (int64_t)blockIdx.y * M * N;
+
+  // Weight row of workgroup row rho = 16 j + c (column tile j, column c of
+  // it): the rows wave j of gemm_skinny_kernel streams.
+  auto w_row = [&](int rho) -> int {
+    const int j = rho >> 4, c = rho & 15;
+    if (FUSE) {
+      const int o = (blockIdx.x * WAVES + j) * 8;
+      return c < 8 ? o + c : N / 2 + o + c - 8;
+    }
+    return blockIdx.x * NR + rho;
+  };
+  // Direct load q of this wave: rows 16 wv + 8q .. + 7; lane l lands at row
+  // 16 wv + 8q + l / 8, slot l % 8, which holds chunk (l % 8) ^ (row / 2) % 8.
+  const bf16_t* wsrc[kDLoads];
+#pragma unroll
+  for (int q = 0; q < kDLoads; ++q) {
+    const int rho = 16 * wv + 8 * q + (lane >> 3);
+    const int c = (lane & 7) ^ ((rho >> 1) & 7);
+    wsrc[q] = W + (int64_t)w_row(rho) * K + k_begin + c * 8;
+  }
+  // Stages past the slice repeat its last stage (never multiplied).
+  auto issue_w = [&](int st, int slot) {
+    const int ko = min(st, stages - 1) * kRK;
+#pragma unroll
+    for (int q = 0; q < kDLoads; ++q)
+      __builtin_amdgcn_global_load_lds(wsrc[q] + ko,
+                                       (lds_void_t*)(ring[slot] + (16 * wv + 8 * q) * kRK), 16,
+                                       0, 0);
+  };
+
+  for (int m0 = 0; m0 < M; m0 += kRowTiles * 16) {
+    // Activation fragments: lane (c16, j4) of row tile i holds, for k-step t,
+    // elements 32t + 8j4 .. + 7 of the stage of row m0 + 16 tile + c16 (rows
+    // past M repeat row M - 1 and are never stored).
+    const bf16_t* asrc[TPW];
+#pragma unroll
+    for (int i = 0; i < TPW; ++i) {
+      const int m = min(m0 + (wv + i * WAVES) * 16 + c16, M - 1);
+      asrc[i] = A + (int64_t)m * K + k_begin + j4 * 8;
+    }
+    u32x4_t areg[kRAst][TPW][2];
+    auto load_a = [&](int st, int slot) {
+      const int ko = min(st, stages - 1) * kRK;
+#pragma unroll
+      for (int i = 0; i < TPW; ++i)
+#pragma unroll
+        for (int t = 0; t < 2; ++t) areg[slot][i][t] = *(const u32x4_t*)(asrc[i] + ko + t * 32);
+    };
+
+    f32x4_t acc[TPW][WAVES];
+#pragma unroll
+    for (int i = 0; i < TPW; ++i)
+#pragma unroll
+      for (int j = 0; j < WAVES; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    // Issue order: weights of stage x + 4 at the top of stage x, activations
+    // of x + 3 at its end, so that after the weights of stage x come exactly
+    // four activation groups and three weight groups (stage 0: one
+    // activation group fewer, hence its own wait).
+    issue_w(0, 0);
+    issue_w(1, 1);
+    load_a(0, 0);
+    issue_w(2, 2);
+    load_a(1, 1);
+    issue_w(3, 3);
+    load_a(2, 2);
+    wait_vmcnt<3 * kALoads + 3 * kDLoads>();
+
+    // Stage st: ring slot st % 6, activation slot st % 3. A wave whose last
+    // row tile is past the pass multiplies that tile too (wave-uniform
+    // branches around the MFMAs would break up the schedule); it is never
+    // stored.
+    auto stage = [&](int st, auto slot_c) {
+      constexpr int u = decltype(slot_c)::value;
+      constexpr int as = u % kRAst;
+      wait_vmcnt<4 * kALoads + 3 * kDLoads>();
+      stage_barrier();
+      issue_w(st + kRAhead, (u + kRAhead) % kRSlots);
+      const bf16_t* lw = ring[u];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+#pragma unroll
+        for (int j = 0; j < WAVES; ++j) {
+          const bf16x8_t b = __builtin_bit_cast(
+              bf16x8_t, *(const u32x4_t*)(&lw[w_swz(16 * j + c16, t * 4 + j4)]));
+#pragma unroll
+          for (int i = 0; i < TPW; ++i)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8_t, areg[as][i][t]), b, acc[i][j], 0, 0, 0);
+        }
+      }
+      // Weight fragments two reads ahead of their MFMAs, not all at once.
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // DS read
+      for (int x = 0; x < 2 * WAVES - 2; ++x) {
+        __builtin_amdgcn_sched_group_barrier(0x008, TPW, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 2 * TPW, 0);
+      // Refill this activation slot (read above) with stage st + 3; the
+      // scheduler may not hoist these loads above the MFMAs (that would hold
+      // a fourth activation stage in registers).
+      __builtin_amdgcn_sched_barrier(0);
+      load_a(st + kRAst, as);
+    };
+    using S0 = std::integral_constant<int, 0>;
+    using S1 = std::integral_constant<int, 1>;
+    using S2 = std::integral_constant<int, 2>;
+    using S3 = std::integral_constant<int, 3>;
+    using S4 = std::integral_constant<int, 4>;
+    using S5 = std::integral_constant<int, 5>;
+    // Whole groups of six stages branch-free, then the rest.
+    const int full = stages / kRSlots, rem = stages % kRSlots;
+    for (int g = 0; g < full; ++g) {
+      const int st = g * kRSlots;
+      stage(st, S0{});
+      stage(st + 1, S1{});
+      stage(st + 2, S2{});
+      stage(st + 3, S3{});
+      stage(st + 4, S4{});
+      stage(st + 5, S5{});
+    }
+    const int st = full * kRSlots;
+    if (rem > 0) stage(st, S0{});
+    if (rem > 1) stage(st + 1, S1{});
+    if (rem > 2) stage(st + 2, S2{});
+    if (rem > 3) stage(st + 3, S3{});
+    if (rem > 4) stage(st + 4, S4{});
+    wait_vmcnt<0>();  // no direct load outlives the pass
+    __syncthreads();  // every wave is done with the ring
+
+    // D layout: lane holds rows 4*j4 + r of column c16 of each 16x16 tile.
+#pragma unroll
+    for (int i = 0; i < TPW; ++i) {
+      const int tile = wv + i * WAVES;
+      if (tile >= kRowTiles) continue;  // wave-uniform
+#pragma unroll
+      for (int j = 0; j < WAVES; ++j) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = m0 + tile * 16 + j4 * 4 + r;
+          if (FUSE) {
+            const float u = __shfl_down(acc[i][j][r], 8, 16);
+            const float g = acc[i][j][r];
+            const int o = (blockIdx.x * WAVES + j) * 8;
+            if (c16 < 8 && m < M)
+              H[(int64_t)m * (N / 2) + o + c16] = (bf16_t)f32_to_bf16(g / (1.0f + expf(-g)) * u);
+          } else if (m < M) {
+            __builtin_nontemporal_store(acc[i][j][r],
+                                        out + (int64_t)m * N + blockIdx.x * NR + 16 * j + c16);
+          }
+        }
+      }
+    }
+  }
+}
+
 struct NormArgs {
   const int32_t* row_idx = nullptr;
   const uint16_t* gamma = nullptr;
@@ -231,8 +456,18 @@ hipError_t launch_plan(const uint16_t* A, const uint16_t* W, float* part, uint16
 template <int WAVES, bool FUSE, bool NORM>
 hipError_t launch_waves(const uint16_t* A, const uint16_t* W, float* part, uint16_t* H, int M,
                         int N, int K, int S, NormArgs na, hipStream_t st) {
-  return M <= 64 ? launch_plan<WAVES, 4, FUSE, NORM>(A, W, part, H, M, N, K, S, na, st)
-                 : launch_plan<WAVES, 8, FUSE, NORM>(A, W, part, H, M, N, K, S, na, st);
+  if (M <= 64) return launch_plan<WAVES, 4, FUSE, NORM>(A, W, part, H, M, N, K, S, na, st);
+  // Above 128 rows, the row-split kernel where it measured faster than
+  // 128-row passes (8B gate/up and down shapes at 256 rows: 113 -> 99 us and
+  // 64 -> 48 us); with fewer waves or the folded norm it measured slower.
+  if constexpr (WAVES >= 7 && !NORM) {
+    if (M > 128) {
+      COCO_LAUNCH((gemm_skinny_rows_kernel<WAVES, FUSE>), dim3(N / (16 * WAVES), S),
+                  dim3(WAVES * 64), 0, st, A, W, part, H, M, N, K, K / S);
+      return hipGetLastError();
+    }
+  }
+  return launch_plan<WAVES, 8, FUSE, NORM>(A, W, part, H, M, N, K, S, na, st);
 }
 
 template <bool FUSE, bool NORM>

@@ -53,23 +53,6 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 // 16 consecutive rows a fragment read touches over 16 distinct 4-bank slots.
 __device__ __forceinline__ int swz(int r, int c) { return r * kTK + ((c ^ ((r >> 2) & 3)) << 3); }
 
-// Waits until at most N vector-memory operations of this wave are in flight
-// (vmcnt only; the direct-to-LDS loads count there).
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
-
-// Workgroup barrier that keeps the compiler from moving memory operations
-// across it and adds no waits of its own: the direct-to-LDS loads of later
-// stages stay in flight through it (a __syncthreads() fence would drain them).
-__device__ __forceinline__ void stage_barrier() {
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_s_barrier();
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-}
-
 // One LDS object per ring slot, so the compiler tracks each slot's pending
 // direct loads on its own and never drains the ring before a fragment read.
 __shared__ __attribute__((aligned(16))) bf16_t g_ta0[kTM * kTK], g_ta1[kTM * kTK],
