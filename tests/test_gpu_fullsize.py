@@ -75,6 +75,32 @@ def test_c2_llama8b_decode_batch64_sampled_rows():
         assert normwise_err(K[0], cache.K[j][p]) < TOL and normwise_err(V[0], cache.V[j][p]) < TOL
 
 
+def test_llama8b_decode_300_rows_matches_oracle_and_splits():
+    """300 decode rows of the 8B layer: the gate/up and down projections
+    (7- and 8-wave plans) take the row-split GEMM in two passes (256 rows,
+    then 44), QKV and O three 128-row passes. Sampled rows of both passes
+    against the oracle; the whole batch bit-identical to a 200/100 split
+    (one row-split pass, then the 128-row kernel)."""
+    wl = W.c2_llama8b_decode(300)
+    b, shape = wl.batch, wl.shape
+    rep = Replica.for_batch(shape, wl.tag, 1, b)
+    hidden = WD.hidden_tensor(shape, wl.tag, b.hidden_rows)
+    h0 = to64(hidden)
+    whole = hidden.clone()
+    rep.forward(0, whole, WD.batch_tensors(b))
+    torch.cuda.synchronize()
+    split = hidden.clone()
+    for part in (np.arange(0, 200), np.arange(200, 300)):
+        rep.forward(0, split, WD.batch_tensors(b.select(part)))
+    torch.cuda.synchronize()
+    assert torch.equal(split.view(torch.int16), whole.view(torch.int16))
+    rows = sorted(set(sample_rows(b, 3, seed=5)) | {130, 255, 256, 299})
+    ref, _, _ = oracle_decode_rows(shape, wl.tag, 0, b, rows, h0, source="device",
+                                   dev_layer=rep.layers[0])
+    check("300-row decode sampled rows", to64(whole)[b.row_idx[rows]], ref,
+          h0[b.row_idx[rows]])
+
+
 def _kv_new_tokens(layer_t, b: W.Batch, seqs):
     out = []
     for s in seqs:
