@@ -44,11 +44,20 @@ template <> struct Elem<float> {
 };
 
 // Waits until at most N vector-memory operations of this wave are in flight
-// (vmcnt only; direct global-to-LDS loads count there).
+// (vmcnt only; direct global-to-LDS loads count there). N counts the loads
+// issued before this point in program order, so no memory operation may move
+// across it: the fences and scheduling barriers pin it (the waitcnt builtin
+// alone lets the compiler sink earlier loads below it, which would make the
+// wait release too early). ALU and MFMA instructions may still cross.
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
+  constexpr int kMayCross = 0x1 | 0x2 | 0x4 | 0x8 | 0x400;  // ALU, VALU, SALU, MFMA, transcendental
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_sched_barrier(kMayCross);
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+  __builtin_amdgcn_sched_barrier(kMayCross);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
 // Workgroup barrier that keeps the compiler from moving memory operations

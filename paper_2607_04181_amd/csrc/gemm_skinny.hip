@@ -234,27 +234,36 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
 // fragment as B) in ascending k.
 //   * the workgroup's 16*WAVES weight rows of a 64-k stage go straight to LDS
 //     (global_load_lds, 16 bytes per lane; wave w fills rows 16w .. 16w + 15
-//     as two 1 KB loads of eight rows) into a ring of six slots, four stages
-//     in flight (as many weight bytes per CU as the other kernel's two 128-k
-//     register stages); 16-byte chunks are swizzled as chunk ^ (row / 2) % 8,
+//     as two 1 KB loads of eight rows) into a ring of four slots, three stages
+//     in flight; 16-byte chunks are swizzled as chunk ^ (row / 2) % 8,
 //     so the 16 rows a fragment read touches per 16-lane group cover every
 //     bank once;
 //   * row tile t of the pass (rows 16t .. 16t + 15) belongs to wave t % WAVES;
 //     a wave loads its tiles' activation fragments from memory straight into
-//     registers, three stages deep (stage st + 3 once stage st has been
+//     registers, two stages deep (stage st + 2 once stage st has been
 //     multiplied), and multiplies them with all 16*WAVES weight rows (LDS
 //     reads per stage: WAVES * 2 KB per wave);
 //   * one barrier per stage: the wait before it covers this wave's direct
 //     loads of the stage; after it, every wave's are in LDS and the slot the
-//     stage's new loads overwrite was read by every wave two stages ago.
+//     stage's new loads overwrite was read by every wave in the stage before.
+// The stage loop is unrolled by four (ring and activation slots then known at
+// compile time); the stage counts of the 7- and 8-wave decode shapes are
+// multiples of four, and other counts finish with up to three guarded stages.
 constexpr int kRowTiles = 16;  // row tiles per pass
 constexpr int kRK = 64;        // k per stage
-constexpr int kRSlots = 6;     // weight ring slots
-constexpr int kRAhead = 4;     // weight stages in flight
-constexpr int kRAst = 3;       // activation stages in registers
+constexpr int kRSlots = 4;     // weight ring slots
+constexpr int kRAhead = 3;     // weight stages in flight
+constexpr int kRAst = 2;       // activation stages in registers
 
 // LDS element offset of 16-byte chunk c (0..7) of row r of a [rows][64] tile.
 __device__ __forceinline__ int w_swz(int r, int c) { return r * kRK + ((c ^ ((r >> 1) & 7)) << 3); }
+
+// Weight ring of the row-split kernel, one LDS object per slot (sized for 8
+// waves), so the compiler tracks each slot's pending direct loads on its own
+// and an LDS read waits only for the loads into its slot.
+constexpr int kRMaxRows = 16 * 8;
+__shared__ __attribute__((aligned(16))) bf16_t g_rw0[kRMaxRows * kRK], g_rw1[kRMaxRows * kRK],
+    g_rw2[kRMaxRows * kRK], g_rw3[kRMaxRows * kRK];
 
 template <int WAVES, bool FUSE>
 __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_rows_kernel(
@@ -264,10 +273,8 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_rows_kernel(
   constexpr int NR = 16 * WAVES;                         // weight rows per workgroup
   constexpr int kDLoads = 2;                             // direct loads per stage
   constexpr int kALoads = 2 * TPW;                       // activation loads per stage
-  // One LDS object per slot, so the compiler tracks each slot's direct loads.
-  __shared__ __attribute__((aligned(16))) bf16_t w0[NR * kRK], w1[NR * kRK], w2[NR * kRK],
-      w3[NR * kRK], w4[NR * kRK], w5[NR * kRK];
-  bf16_t* const ring[kRSlots] = {w0, w1, w2, w3, w4, w5};
+  static_assert(NR <= kRMaxRows, "weight ring sized for 8 waves");
+  bf16_t* const ring[kRSlots] = {g_rw0, g_rw1, g_rw2, g_rw3};
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -289,19 +296,23 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_rows_kernel(
   };
   // Direct load q of this wave: rows 16 wv + 8q .. + 7; lane l lands at row
   // 16 wv + 8q + l / 8, slot l % 8, which holds chunk (l % 8) ^ (row / 2) % 8.
-  const bf16_t* wsrc[kDLoads];
+  // Addresses are a uniform base (advanced per stage) plus a fixed 32-bit byte
+  // offset per lane, so no address register is rewritten inside the loop (a
+  // rewrite of a register that a pending load shares would wait for it).
+  const char* wbase = (const char*)(W + k_begin);
+  uint32_t woff[kDLoads];
 #pragma unroll
   for (int q = 0; q < kDLoads; ++q) {
     const int rho = 16 * wv + 8 * q + (lane >> 3);
     const int c = (lane & 7) ^ ((rho >> 1) & 7);
-    wsrc[q] = W + (int64_t)w_row(rho) * K + k_begin + c * 8;
+    woff[q] = ((uint32_t)w_row(rho) * (uint32_t)K + (uint32_t)(c * 8)) * 2u;
   }
   // Stages past the slice repeat its last stage (never multiplied).
   auto issue_w = [&](int st, int slot) {
-    const int ko = min(st, stages - 1) * kRK;
+    const char* b = wbase + (size_t)min(st, stages - 1) * (kRK * 2);
 #pragma unroll
     for (int q = 0; q < kDLoads; ++q)
-      __builtin_amdgcn_global_load_lds(wsrc[q] + ko,
+      __builtin_amdgcn_global_load_lds((const void*)(b + woff[q]),
                                        (lds_void_t*)(ring[slot] + (16 * wv + 8 * q) * kRK), 16,
                                        0, 0);
   };
@@ -310,19 +321,20 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_rows_kernel(
     // Activation fragments: lane (c16, j4) of row tile i holds, for k-step t,
     // elements 32t + 8j4 .. + 7 of the stage of row m0 + 16 tile + c16 (rows
     // past M repeat row M - 1 and are never stored).
-    const bf16_t* asrc[TPW];
+    const char* abase = (const char*)(A + k_begin);
+    uint32_t aoff[TPW];
 #pragma unroll
     for (int i = 0; i < TPW; ++i) {
       const int m = min(m0 + (wv + i * WAVES) * 16 + c16, M - 1);
-      asrc[i] = A + (int64_t)m * K + k_begin + j4 * 8;
+      aoff[i] = ((uint32_t)m * (uint32_t)K + (uint32_t)(j4 * 8)) * 2u;
     }
     u32x4_t areg[kRAst][TPW][2];
     auto load_a = [&](int st, int slot) {
-      const int ko = min(st, stages - 1) * kRK;
+      const char* b = abase + (size_t)min(st, stages - 1) * (kRK * 2);
 #pragma unroll
       for (int i = 0; i < TPW; ++i)
 #pragma unroll
-        for (int t = 0; t < 2; ++t) areg[slot][i][t] = *(const u32x4_t*)(asrc[i] + ko + t * 32);
+        for (int t = 0; t < 2; ++t) areg[slot][i][t] = *(const u32x4_t*)(b + aoff[i] + t * 64);
     };
 
     f32x4_t acc[TPW][WAVES];
@@ -331,28 +343,31 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_rows_kernel(
 #pragma unroll
       for (int j = 0; j < WAVES; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    // Issue order: weights of stage x + 4 at the top of stage x, activations
-    // of x + 3 at its end, so that after the weights of stage x come exactly
-    // four activation groups and three weight groups (stage 0: one
-    // activation group fewer, hence its own wait).
+    // Issue order: weights of stage x + 3 at the top of stage x, activations
+    // of x + 2 at its end, so that after the weights of stage x come exactly
+    // three activation groups and two weight groups (stage 0: one activation
+    // group fewer, hence its own wait), and after the activations of stage x
+    // one weight group and one activation group.
     issue_w(0, 0);
     issue_w(1, 1);
     load_a(0, 0);
     issue_w(2, 2);
     load_a(1, 1);
-    issue_w(3, 3);
-    load_a(2, 2);
-    wait_vmcnt<3 * kALoads + 3 * kDLoads>();
+    wait_vmcnt<2 * kALoads + 2 * kDLoads>();
 
-    // Stage st: ring slot st % 6, activation slot st % 3. A wave whose last
+    // Stage st: ring slot st % 4, activation slot st % 2. A wave whose last
     // row tile is past the pass multiplies that tile too (wave-uniform
     // branches around the MFMAs would break up the schedule); it is never
     // stored.
     auto stage = [&](int st, auto slot_c) {
       constexpr int u = decltype(slot_c)::value;
       constexpr int as = u % kRAst;
-      wait_vmcnt<4 * kALoads + 3 * kDLoads>();
+      wait_vmcnt<3 * kALoads + 2 * kDLoads>();
       stage_barrier();
+      // This stage's activations before its MFMAs, stated here: the compiler
+      // does not count direct and register loads in one queue and would wait
+      // for all of them.
+      wait_vmcnt<kALoads + kDLoads>();
       issue_w(st + kRAhead, (u + kRAhead) % kRSlots);
       const bf16_t* lw = ring[u];
 #pragma unroll
@@ -374,9 +389,9 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_rows_kernel(
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
       __builtin_amdgcn_sched_group_barrier(0x008, 2 * TPW, 0);
-      // Refill this activation slot (read above) with stage st + 3; the
+      // Refill this activation slot (read above) with stage st + 2; the
       // scheduler may not hoist these loads above the MFMAs (that would hold
-      // a fourth activation stage in registers).
+      // a third activation stage in registers).
       __builtin_amdgcn_sched_barrier(0);
       load_a(st + kRAst, as);
     };
@@ -384,9 +399,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_rows_kernel(
     using S1 = std::integral_constant<int, 1>;
     using S2 = std::integral_constant<int, 2>;
     using S3 = std::integral_constant<int, 3>;
-    using S4 = std::integral_constant<int, 4>;
-    using S5 = std::integral_constant<int, 5>;
-    // Whole groups of six stages branch-free, then the rest.
+    // Whole groups of four stages branch-free, then the rest.
     const int full = stages / kRSlots, rem = stages % kRSlots;
     for (int g = 0; g < full; ++g) {
       const int st = g * kRSlots;
@@ -394,15 +407,11 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_rows_kernel(
       stage(st + 1, S1{});
       stage(st + 2, S2{});
       stage(st + 3, S3{});
-      stage(st + 4, S4{});
-      stage(st + 5, S5{});
     }
     const int st = full * kRSlots;
     if (rem > 0) stage(st, S0{});
     if (rem > 1) stage(st + 1, S1{});
     if (rem > 2) stage(st + 2, S2{});
-    if (rem > 3) stage(st + 3, S3{});
-    if (rem > 4) stage(st + 4, S4{});
     wait_vmcnt<0>();  // no direct load outlives the pass
     __syncthreads();  // every wave is done with the ring
 
@@ -461,7 +470,9 @@ hipError_t launch_waves(const uint16_t* A, const uint16_t* W, float* part, uint1
   // 128-row passes (8B gate/up and down shapes at 256 rows: 113 -> 99 us and
   // 64 -> 48 us); with fewer waves or the folded norm it measured slower.
   if constexpr (WAVES >= 7 && !NORM) {
-    if (M > 128) {
+    // Its per-lane byte offsets are 32-bit: both operands under 4 GB.
+    if (M > 128 && (int64_t)N * K * 2 < (int64_t(1) << 32) &&
+        (int64_t)M * K * 2 < (int64_t(1) << 32)) {
       COCO_LAUNCH((gemm_skinny_rows_kernel<WAVES, FUSE>), dim3(N / (16 * WAVES), S),
                   dim3(WAVES * 64), 0, st, A, W, part, H, M, N, K, K / S);
       return hipGetLastError();
