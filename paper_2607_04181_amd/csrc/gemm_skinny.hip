@@ -249,11 +249,9 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
 // The stage loop is unrolled by four (ring and activation slots then known at
 // compile time); the stage counts of the 7- and 8-wave decode shapes are
 // multiples of four, and other counts finish with up to three guarded stages.
-constexpr int kRowTiles = 16;  // row tiles per pass
 constexpr int kRK = 64;        // k per stage
 constexpr int kRSlots = 4;     // weight ring slots
 constexpr int kRAhead = 3;     // weight stages in flight
-constexpr int kRAst = 2;       // activation stages in registers
 
 // LDS element offset of 16-byte chunk c (0..7) of row r of a [rows][64] tile.
 __device__ __forceinline__ int w_swz(int r, int c) { return r * kRK + ((c ^ ((r >> 1) & 7)) << 3); }
@@ -265,10 +263,15 @@ constexpr int kRMaxRows = 16 * 8;
 __shared__ __attribute__((aligned(16))) bf16_t g_rw0[kRMaxRows * kRK], g_rw1[kRMaxRows * kRK],
     g_rw2[kRMaxRows * kRK], g_rw3[kRMaxRows * kRK];
 
-template <int WAVES, bool FUSE>
+// ROWT: row tiles per pass (16 or 8). AST: activation stages in registers
+// (2 or 4; stage st + AST is loaded after stage st's MFMAs).
+template <int WAVES, bool FUSE, int ROWT, int AST>
 __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_rows_kernel(
     const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, float* __restrict__ part,
     bf16_t* __restrict__ H, int M, int N, int K, int k_slice) {
+  static_assert(kRSlots % AST == 0, "activation slots must follow the unrolled stages");
+  constexpr int kRowTiles = ROWT;
+  constexpr int kRAst = AST;
   constexpr int TPW = (kRowTiles + WAVES - 1) / WAVES;  // row tiles per wave
   constexpr int NR = 16 * WAVES;                         // weight rows per workgroup
   constexpr int kDLoads = 2;                             // direct loads per stage
@@ -344,16 +347,20 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_rows_kernel(
       for (int j = 0; j < WAVES; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
     // Issue order: weights of stage x + 3 at the top of stage x, activations
-    // of x + 2 at its end, so that after the weights of stage x come exactly
-    // three activation groups and two weight groups (stage 0: one activation
-    // group fewer, hence its own wait), and after the activations of stage x
-    // one weight group and one activation group.
-    issue_w(0, 0);
-    issue_w(1, 1);
-    load_a(0, 0);
-    issue_w(2, 2);
-    load_a(1, 1);
-    wait_vmcnt<2 * kALoads + 2 * kDLoads>();
+    // of x + AST at its end, so that after the weights of stage x come
+    // exactly three activation groups and two weight groups, and after the
+    // activations of stage x AST - 1 weight groups and as many activation
+    // groups. The prologue issues the same sequence for stages -3 .. -1
+    // (activations of stages below 0 do not exist: with AST = 2 stage 0's
+    // weights are followed by one activation group fewer, hence its own wait).
+#pragma unroll
+    for (int j = 0; j < AST - 3; ++j) load_a(j, j);
+#pragma unroll
+    for (int x = 0; x < 3; ++x) {
+      issue_w(x, x);
+      if (x + AST - 3 >= 0) load_a(x + AST - 3, (x + AST - 3) % AST);
+    }
+    if constexpr (AST < 3) wait_vmcnt<AST * kALoads + 2 * kDLoads>();
 
     // Stage st: ring slot st % 4, activation slot st % 2. A wave whose last
     // row tile is past the pass multiplies that tile too (wave-uniform
@@ -367,7 +374,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_rows_kernel(
       // This stage's activations before its MFMAs, stated here: the compiler
       // does not count direct and register loads in one queue and would wait
       // for all of them.
-      wait_vmcnt<kALoads + kDLoads>();
+      wait_vmcnt<(AST - 1) * (kALoads + kDLoads)>();
       issue_w(st + kRAhead, (u + kRAhead) % kRSlots);
       const bf16_t* lw = ring[u];
 #pragma unroll
@@ -389,9 +396,9 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_rows_kernel(
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
       __builtin_amdgcn_sched_group_barrier(0x008, 2 * TPW, 0);
-      // Refill this activation slot (read above) with stage st + 2; the
+      // Refill this activation slot (read above) with stage st + AST; the
       // scheduler may not hoist these loads above the MFMAs (that would hold
-      // a third activation stage in registers).
+      // one more activation stage in registers).
       __builtin_amdgcn_sched_barrier(0);
       load_a(st + kRAst, as);
     };
@@ -466,15 +473,23 @@ template <int WAVES, bool FUSE, bool NORM>
 hipError_t launch_waves(const uint16_t* A, const uint16_t* W, float* part, uint16_t* H, int M,
                         int N, int K, int S, NormArgs na, hipStream_t st) {
   if (M <= 64) return launch_plan<WAVES, 4, FUSE, NORM>(A, W, part, H, M, N, K, S, na, st);
-  // Above 128 rows, the row-split kernel where it measured faster than
-  // 128-row passes (8B gate/up and down shapes at 256 rows: 113 -> 99 us and
-  // 64 -> 48 us); with fewer waves or the folded norm it measured slower.
+  // The row-split kernel where it measured faster: above 128 rows for 7- and
+  // 8-wave plans (8B gate/up and down at 256 rows: 113 -> 89 us and
+  // 64 -> 46 us against two 128-row passes; with fewer waves or the folded
+  // norm it measured slower), and 128-row passes of 8-wave plans.
   if constexpr (WAVES >= 7 && !NORM) {
     // Its per-lane byte offsets are 32-bit: both operands under 4 GB.
-    if (M > 128 && (int64_t)N * K * 2 < (int64_t(1) << 32) &&
-        (int64_t)M * K * 2 < (int64_t(1) << 32)) {
-      COCO_LAUNCH((gemm_skinny_rows_kernel<WAVES, FUSE>), dim3(N / (16 * WAVES), S),
-                  dim3(WAVES * 64), 0, st, A, W, part, H, M, N, K, K / S);
+    const bool fits = (int64_t)N * K * 2 < (int64_t(1) << 32) &&
+                      (int64_t)M * K * 2 < (int64_t(1) << 32);
+    if (fits && M > 128) {
+      COCO_LAUNCH((gemm_skinny_rows_kernel<WAVES, FUSE, 16, WAVES == 8 ? 4 : 2>),
+                  dim3(N / (16 * WAVES), S), dim3(WAVES * 64), 0, st, A, W, part, H, M, N, K,
+                  K / S);
+      return hipGetLastError();
+    }
+    if (fits && WAVES == 8 && M > 64) {
+      COCO_LAUNCH((gemm_skinny_rows_kernel<8, FUSE, 8, 4>), dim3(N / 128, S), dim3(512), 0, st,
+                  A, W, part, H, M, N, K, K / S);
       return hipGetLastError();
     }
   }
