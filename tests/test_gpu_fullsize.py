@@ -101,6 +101,32 @@ def test_llama8b_decode_300_rows_matches_oracle_and_splits():
           h0[b.row_idx[rows]])
 
 
+def test_llama8b_decode_129_rows_across_gemm_row_limits():
+    """129 decode rows of the 8B layer split at the decode GEMMs' row limits:
+    the whole batch (gate/up and down: one 256-row pass of the row-split
+    GEMM, mostly past M), 65 rows (down: a 128-row pass of it), 64 rows
+    (the 64-row kernel) give identical bits; sampled rows against the
+    oracle."""
+    wl = W.c2_llama8b_decode(129)
+    b, shape = wl.batch, wl.shape
+    rep = Replica.for_batch(shape, wl.tag, 1, b)
+    hidden = WD.hidden_tensor(shape, wl.tag, b.hidden_rows)
+    h0 = to64(hidden)
+    whole = hidden.clone()
+    rep.forward(0, whole, WD.batch_tensors(b))
+    torch.cuda.synchronize()
+    split = hidden.clone()
+    for part in (np.arange(0, 65), np.arange(65, 129)):
+        rep.forward(0, split, WD.batch_tensors(b.select(part)))
+    torch.cuda.synchronize()
+    assert torch.equal(split.view(torch.int16), whole.view(torch.int16))
+    rows = sorted(set(sample_rows(b, 2, seed=7)) | {0, 64, 128})
+    ref, _, _ = oracle_decode_rows(shape, wl.tag, 0, b, rows, h0, source="device",
+                                   dev_layer=rep.layers[0])
+    check("129-row decode sampled rows", to64(whole)[b.row_idx[rows]], ref,
+          h0[b.row_idx[rows]])
+
+
 def _kv_new_tokens(layer_t, b: W.Batch, seqs):
     out = []
     for s in seqs:
