@@ -476,8 +476,9 @@ hipError_t launch_waves(const uint16_t* A, const uint16_t* W, float* part, uint1
   // The row-split kernel where it measured faster: above 128 rows for 7- and
   // 8-wave plans (8B gate/up and down at 256 rows: 113 -> 89 us and
   // 64 -> 46 us against two 128-row passes; with fewer waves or the folded
-  // norm it measured slower), and 128-row passes of 8-wave plans.
-  if constexpr (WAVES >= 7 && !NORM) {
+  // norm it measured slower), and 128-row passes of 8-wave plans. (No decode
+  // shape here has an unfused 7-wave plan; those keep the 128-row kernel.)
+  if constexpr ((WAVES == 8 || (WAVES == 7 && FUSE)) && !NORM) {
     // Its per-lane byte offsets are 32-bit: both operands under 4 GB.
     const bool fits = (int64_t)N * K * 2 < (int64_t(1) << 32) &&
                       (int64_t)M * K * 2 < (int64_t(1) << 32);

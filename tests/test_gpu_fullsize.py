@@ -216,8 +216,14 @@ def test_c4_qwen32b_prefill_then_decode():
     # and sampled decode-only requests.
     dh = WD.hidden_tensor(shape, wl.tag + "dec", dec.hidden_rows)
     d0 = to64(dh)
+    halves = dh.clone()
     rep.forward(0, dh, WD.batch_tensors(dec))
+    # Two 64-row halves (the 64-row GEMM kernels) give the bits of the whole
+    # batch (the 8-wave gate/up plan's 128-row pass of the row-split kernel).
+    for part in (np.arange(0, 64), np.arange(64, 128)):
+        rep.forward(0, halves, WD.batch_tensors(dec.select(part)))
     torch.cuda.synchronize()
+    assert torch.equal(halves.view(torch.int16), dh.view(torch.int16))
     got = to64(dh)
     sample = [0] + sample_rows(dec.select(range(4, 128)), 3, seed=4)
     sample = [0] + [s + 4 for s in sample[1:]]
