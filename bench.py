@@ -133,9 +133,9 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "single-GPU build: the replica runs on one MI355X; "
-                          "multi-GPU sharding of the row subsets is described in DESIGN.md "
-                          "and not run", "n_gpus": args.gpus}))
+        print(json.dumps({"error": "bench.py runs one replica's share on one MI355X; "
+                          "sharding the row subsets over several GPUs is not implemented",
+                          "n_gpus": args.gpus}))
         sys.exit(2)
 
     if args.copy_calibration:

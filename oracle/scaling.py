@@ -14,7 +14,7 @@ generalisation) and the scaling algorithm of Sec. 4.4:
 * distance, scale_candidates: the L1 transition distance and the candidate
                    ranking of the unified scaling algorithm.
 
-Readings (the paper is silent or inconsistent; each is listed in the design doc):
+Readings (where the paper is silent or inconsistent):
 * T(P) and T(v) are printed without bytes per element; `elem_bytes` makes it
   explicit (2 for bf16). T(v) is printed without the sequence length l; the
   same factor as in T(P) is applied.
