@@ -51,14 +51,18 @@ def log(msg):
 
 
 def kernel_source_sha():
-    """Digest of every kernel source: a counter summary is only valid for the
-    sources it was taken with."""
+    """Digest of every kernel source without its comments and whitespace: a
+    counter summary is only valid for the code it was taken with."""
     csrc = os.path.join(ROOT, "paper_2607_04181_amd", "csrc")
     h = hashlib.sha256()
     for f in sorted(os.listdir(csrc)):
         if f.endswith((".hip", ".h")):
-            with open(os.path.join(csrc, f), "rb") as fh:
-                h.update(f.encode() + b"\0" + fh.read())
+            with open(os.path.join(csrc, f), encoding="utf-8") as fh:
+                code = fh.read()
+            code = re.sub(r"/\*.*?\*/", " ", code, flags=re.S)
+            code = re.sub(r"//[^\n]*", " ", code)
+            code = " ".join(code.split())
+            h.update(f.encode() + b"\0" + code.encode())
     return h.hexdigest()[:16]
 
 

@@ -16,11 +16,12 @@
 //     16-rows-per-instruction fragment reads hit distinct banks;
 //   * each 16x16 output tile is accumulated with v_mfma_f32_16x16x32_bf16 in
 //     ascending k.
-// A pass covers up to 128 rows. Plans of 7 or 8 waves without the folded
-// norm take a row-split variant with passes of 256 rows for larger batches
-// (gemm_skinny_rows_kernel below): there the weight tile of a stage goes to
-// LDS and the row tiles are dealt to the waves, since every wave reading the
-// whole activation tile from LDS costs more LDS time at that size.
+// A pass covers up to 128 rows. For batches of more than 128 rows (8-wave
+// and fused 7-wave plans) and of 65-128 rows (8-wave plans), a row-split
+// variant takes over (gemm_skinny_rows_kernel below): there the weight tile
+// of a stage goes to LDS and the row tiles are dealt to the waves, since every
+// wave reading the whole activation tile from LDS costs more LDS time as the
+// batch grows.
 // The NORM variant (decode QKV projection) folds the row gather and the
 // first RMSNorm into the activation staging: it reads the layer input rows
 // x[row_idx[m]] directly, stages bf16(x * gamma), and writes each row's sum
@@ -228,8 +229,8 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
   }
 }
 
-// Row-split variant for passes of 256 rows (16 row tiles). Same outputs, bit
-// for bit, as gemm_skinny_kernel: every 16x16 output tile is the same chain of
+// Row-split variant for passes of 256 or 128 rows (16 or 8 row tiles). Same
+// outputs, bit for bit, as gemm_skinny_kernel: every 16x16 output tile is the same chain of
 // v_mfma_f32_16x16x32_bf16 (activation fragment as the A operand, weight
 // fragment as B) in ascending k.
 //   * the workgroup's 16*WAVES weight rows of a 64-k stage go straight to LDS
@@ -240,7 +241,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
 //     bank once;
 //   * row tile t of the pass (rows 16t .. 16t + 15) belongs to wave t % WAVES;
 //     a wave loads its tiles' activation fragments from memory straight into
-//     registers, two stages deep (stage st + 2 once stage st has been
+//     registers, AST stages deep (stage st + AST once stage st has been
 //     multiplied), and multiplies them with all 16*WAVES weight rows (LDS
 //     reads per stage: WAVES * 2 KB per wave);
 //   * one barrier per stage: the wait before it covers this wave's direct
