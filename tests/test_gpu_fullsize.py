@@ -127,6 +127,34 @@ def test_llama8b_decode_129_rows_across_gemm_row_limits():
           h0[b.row_idx[rows]])
 
 
+def test_qwen32b_decode_192_rows_row_split_gate_up():
+    """192 decode rows of the 32B layer: its 8-wave gate/up plan takes the
+    row-split GEMM's 256-row pass with the SwiGLU epilogue; two 96-row
+    halves (its 128-row pass) give identical bits, and sampled rows match
+    the oracle."""
+    shape = W.QWEN32B
+    rng = np.random.default_rng(192)
+    prior = np.clip(np.exp(rng.normal(np.log(1024), 0.8, 192)).astype(np.int64), 16, 4096)
+    b = W.decode_batch(rng, prior, max_ctx=4097)
+    tag = "c4x"
+    rep = Replica.for_batch(shape, tag, 1, b)
+    hidden = WD.hidden_tensor(shape, tag, b.hidden_rows)
+    h0 = to64(hidden)
+    whole = hidden.clone()
+    rep.forward(0, whole, WD.batch_tensors(b))
+    torch.cuda.synchronize()
+    halves = hidden.clone()
+    for part in (np.arange(0, 96), np.arange(96, 192)):
+        rep.forward(0, halves, WD.batch_tensors(b.select(part)))
+    torch.cuda.synchronize()
+    assert torch.equal(halves.view(torch.int16), whole.view(torch.int16))
+    rows = sorted(set(sample_rows(b, 2, seed=9)) | {0, 191})
+    ref, _, _ = oracle_decode_rows(shape, tag, 0, b, rows, h0, source="device",
+                                   dev_layer=rep.layers[0])
+    check("32B 192-row decode sampled rows", to64(whole)[b.row_idx[rows]], ref,
+          h0[b.row_idx[rows]])
+
+
 def _kv_new_tokens(layer_t, b: W.Batch, seqs):
     out = []
     for s in seqs:
