@@ -54,8 +54,7 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 // NORM row sums, by one wave: ss[blockIdx.y][r] = sum of x^2 over the K-slice
 // for rows r = r_first, r_first + gridDim.x, ... below r_end (each row of a
 // pass by one workgroup of the slice), per lane in chunk order, then a fixed
-// butterfly. Both decode GEMM kernels use it, so a row's sum never depends
-// on the batch.
+// butterfly: a row's sum never depends on the batch.
 __device__ __forceinline__ void norm_row_sums(const bf16_t* __restrict__ A,
                                               const int32_t* __restrict__ row_idx, int M, int K,
                                               int k_begin, int k_slice, int r_first, int r_end,
