@@ -3,9 +3,16 @@
 
 One step = one pass of the whole path (gather, RMSNorm, QKV, RoPE + cache
 append, paged attention, O projection + residual, RMSNorm, SwiGLU MLP +
-residual, scatter) over one batch, through the C ABI. Default workload: the
-Llama-3-8B-shaped layer, bf16 decode of a 64-request batch with lognormal
-contexts (metric: decode layer-steps/s). Other workloads via --workload.
+residual, scatter) over one batch, through the C ABI. The default run measures
+both halves of the metric:
+  * the headline: the Llama-3-8B-shaped layer, bf16 decode of a 64-request
+    batch with lognormal contexts (decode layer-steps/s, HBM roofline);
+  * under "prefill": the Qwen-32B-shaped layer, a 2048-token chunked prefill
+    over four requests (tokens/s per layer, MFMA roofline).
+--workload runs one workload alone. Each workload reports the mean of K hot
+back-to-back steps (the value), the median of at least 30 steps each after a
+1 GiB cache-flushing write, a HIP-graph replay, per-kernel event timings, and
+fractions of the published peaks and of the peaks measured on this GPU.
 
 Prints one JSON line on stdout; per-kernel timings go to stderr. Inputs are
 synthetic (seeded) and resident in HBM before the timed region.
@@ -25,6 +32,7 @@ METRIC = "decode layer-steps/s & prefill tokens/s per layer; % HBM / MFMA peak"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s
 XGMI_LINK_BPS = 153e9           # one MI355X xGMI link, bytes/s (boundary transfers)
+FLUSH_BYTES = 1 << 30           # written between flushed steps: 4x the 256 MB MALL
 
 
 def parse():
@@ -32,14 +40,18 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=5)
-    p.add_argument("--workload", default="c2",
-                   choices=["c2", "c3", "c3full", "c4p", "c4d", "c5"])
+    p.add_argument("--workload", default=None,
+                   choices=["c2", "c3", "c3full", "c4p", "c4d", "c5"],
+                   help="one workload only (default: the 8B batch-64 decode step as the "
+                        "headline, plus the 32B 2048-token prefill under \"prefill\")")
     p.add_argument("--batch", type=int, default=64,
                    help="decode rows of the 8B workload (c2): one replica's share of the batch")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="target duration of the oracle CPU baseline (0 = skip)")
     p.add_argument("--no-graph", action="store_true",
                    help="skip the HIP-graph replay measurement of the same step")
+    p.add_argument("--no-peaks", action="store_true",
+                   help="skip the measured-peak probes (read stream, copy, MFMA loop)")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only time a plain 1 GiB device copy (the reference kernel that "
                         "scales the FETCH_SIZE / WRITE_SIZE counters to bytes)")
@@ -133,35 +145,64 @@ def build_workload(name, batch=64):
     raise ValueError(name)
 
 
-def main():
-    args = parse()
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "bench.py runs one replica's share on one MI355X; "
-                          "sharding the row subsets over several GPUs is not implemented",
-                          "n_gpus": args.gpus}))
-        sys.exit(2)
+def measure_peaks(num_cus):
+    """What this GPU sustains, measured here: a read stream over 2 GiB (the
+    library's read probe), a 1 GiB device copy (torch's copy kernel, read +
+    write) and a loop of bf16 MFMAs (the library's MFMA probe). Medians of 10
+    timed launches after 2 warm-ups."""
+    import torch
+    import paper_2607_04181_amd as coco
+    stream = torch.cuda.current_stream()
 
-    if args.copy_calibration:
-        copy_calibration()
-        return
+    def timed(fn, reps=10, warm=2):
+        for _ in range(warm):
+            fn()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(reps)]
+        for a, b in ev:
+            a.record(stream)
+            fn()
+            b.record(stream)
+        torch.cuda.synchronize()
+        t = sorted(a.elapsed_time(b) for a, b in ev)
+        return t[len(t) // 2]
 
+    nbytes = 2 << 30
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    buf.random_(0, 255)
+    blocks = 8 * num_cus
+    out = torch.empty(blocks, dtype=torch.int32, device="cuda")
+    ms_read = timed(lambda: coco.coco_probe_read(buf, out, blocks, stream))
+    x = buf[: nbytes // 2]
+    y = torch.empty_like(x)
+    ms_copy = timed(lambda: y.copy_(x))
+    del buf, x, y
+    mblocks = 2 * num_cus  # two 4-wave workgroups per CU: two waves per SIMD
+    mout = torch.empty(4 * mblocks, dtype=torch.float32, device="cuda")
+    flops = [0.0]
+
+    def mfma():
+        flops[0] = coco.coco_probe_mfma_bf16(2000, mout, mblocks, stream)
+    ms_mfma = timed(mfma)
+    torch.cuda.empty_cache()
+    return {"read_GBps": round(nbytes / (ms_read * 1e-3) / 1e9, 1),
+            "copy_GBps": round(nbytes / (ms_copy * 1e-3) / 1e9, 1),
+            "mfma_bf16_TFLOPs": round(flops[0] / (ms_mfma * 1e-3) / 1e12, 1),
+            "method": "median of 10 launches: read probe over 2 GiB, 1 GiB device copy "
+                      "(bytes read + written), bf16 MFMA probe (4 chains/wave, 2 waves/SIMD)"}
+
+
+def run_workload(name, batch_rows, args, peaks, flush):
+    """One workload: hot K-step timing (the contract's value), a cache-flushed
+    median, a HIP-graph replay, per-kernel event timings, rooflines, and the
+    oracle's CPU baseline. Frees its device memory before returning."""
     import numpy as np
     import torch
 
     import paper_2607_04181_amd as coco
-    import workloads as W
     from workloads import device as WD
 
-    if args.batch != 64 and args.workload != "c2":
-        print(json.dumps({"error": "--batch applies to the 8B decode workload (c2) only"}))
-        sys.exit(2)
-    if args.batch < 1:
-        print(json.dumps({"error": "--batch must be >= 1"}))
-        sys.exit(2)
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    torch.cuda.set_device(0)
-    wl, batch, n_layers = build_workload(args.workload, args.batch)
+    wl, batch, n_layers = build_workload(name, batch_rows)
     shape = wl.shape
     t0 = time.time()
     layers = [WD.layer_tensors(shape, wl.tag, l, batch.num_blocks) for l in range(n_layers)]
@@ -203,6 +244,20 @@ def main():
     e1.record(stream)
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / args.steps
+
+    # Cache-flushed steps: before each, a kernel writes the 1 GiB flush buffer
+    # (four times the 256 MB last-level cache), outside the timed interval.
+    reps = max(30, args.steps)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(reps)]
+    for r, (a, b) in enumerate(evs):
+        flush.fill_(float(r))
+        a.record(stream)
+        step()
+        b.record(stream)
+    torch.cuda.synchronize()
+    flushed = sorted(a.elapsed_time(b) for a, b in evs)
+    fms = flushed[len(flushed) // 2]
 
     # The same step captured once as a HIP graph and replayed (the forward
     # only enqueues kernels on fixed buffers, so it is capturable as is).
@@ -272,6 +327,7 @@ def main():
             rows.append((k, tot / n, n, tot))
     rows.sort(key=lambda r: -r[3])
     tot_all = sum(r[3] for r in rows)
+    log(f"{wl.name}: hot {ms:.4f} ms/step, flushed median {fms:.4f} ms ({reps} reps)")
     log(f"{'kernel':18s} {'avg us':>9s} {'share':>6s} {'GB/s':>8s} {'TFLOP/s':>8s}")
     for k, avg, n, tot in rows:
         gbs = alg_bytes.get(k, 0) / (avg * 1e-3) / 1e9 if k in alg_bytes else float("nan")
@@ -282,32 +338,49 @@ def main():
     dom, dom_avg, dom_n, _ = cand[0]
     bound = "hbm" if is_decode else "mfma"
     src_sha = kernel_source_sha()
-    if bound == "hbm":
-        achieved = alg_bytes[dom] / (dom_avg * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
-    else:
-        achieved = alg_flops[dom] / (dom_avg * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4)}
-    roof["traffic"] = load_traffic(dom, wl.name, src_sha)
-    roof["kernel"] = dom
-    roof["avg_launch_us"] = round(dom_avg * 1e3, 2)
-    roof["algorithmic_per_launch"] = alg_bytes[dom] if bound == "hbm" else alg_flops[dom]
-
-    if is_decode:
-        value = n_layers * 1000.0 / ms
-        unit = "layer-steps/s"
-    else:
-        value = M * 1000.0 / ms
-        unit = "tokens/s per layer"
-    if graph is not None:
-        graph["value"] = round((n_layers * 1000.0 if is_decode else M * 1000.0) / graph["ms_per_step"], 2)
     whole = {"step_hbm_bytes": step_bytes, "step_flops": step_flops,
              "step_GBps": round(step_bytes / (ms * 1e-3) / 1e9, 1),
              "step_TFLOPs": round(step_flops / (ms * 1e-3) / 1e12, 2)}
     whole["step_frac_hbm"] = round(whole["step_GBps"] / HBM_PEAK_GBS, 4)
     whole["step_frac_mfma"] = round(whole["step_TFLOPs"] / MFMA_BF16_PEAK_TFLOPS, 4)
+    if bound == "hbm":
+        achieved = alg_bytes[dom] / (dom_avg * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
+        step_frac = whole["step_frac_hbm"]
+        meas_peak = peaks.get("read_GBps") if peaks else None
+        step_meas = whole["step_GBps"]
+    else:
+        achieved = alg_flops[dom] / (dom_avg * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4)}
+        step_frac = whole["step_frac_mfma"]
+        meas_peak = peaks.get("mfma_bf16_TFLOPs") if peaks else None
+        step_meas = whole["step_TFLOPs"]
+    roof["traffic"] = load_traffic(dom, wl.name, src_sha)
+    roof["kernel"] = dom
+    roof["avg_launch_us"] = round(dom_avg * 1e3, 2)
+    roof["algorithmic_per_launch"] = alg_bytes[dom] if bound == "hbm" else alg_flops[dom]
+    # The whole step (every kernel and the gaps between them) against the same
+    # peak: the layer's own fraction of the roofline.
+    roof["step_frac"] = step_frac
+    if meas_peak:
+        roof["peak_measured"] = meas_peak
+        roof["frac_measured"] = round(achieved / meas_peak, 4)
+        roof["step_frac_measured"] = round(step_meas / meas_peak, 4)
+
+    per_unit = n_layers * 1000.0 if is_decode else M * 1000.0
+    value = per_unit / ms
+    unit = "layer-steps/s" if is_decode else "tokens/s per layer"
+    if graph is not None:
+        graph["value"] = round(per_unit / graph["ms_per_step"], 2)
+    flushed_out = {"median_ms": round(fms, 4), "reps": reps,
+                   "min_ms": round(flushed[0], 4), "max_ms": round(flushed[-1], 4),
+                   "value": round(per_unit / fms, 2), "flush_bytes": flush.numel() * 4,
+                   "step_frac": round((step_bytes / (fms * 1e-3) / 1e9 / HBM_PEAK_GBS)
+                                      if is_decode else
+                                      (step_flops / (fms * 1e-3) / 1e12 /
+                                       MFMA_BF16_PEAK_TFLOPS), 4)}
 
     # The paper's speedup model (Sec. 4.2) fed with this measured per-layer
     # time: boundary rows over one xGMI link, bf16 hidden states.
@@ -327,23 +400,78 @@ def main():
                    "S": {f"N={N},P={P}": round(coco.coco_speedup(sm, N, P), 4)
                          for N in (L // 4, L // 2, L) for P in (2, 4)}}
 
+    del handle, layers, hidden, bt
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
     cpu = None
     if cpu_inputs is not None:
         cpu = cpu_baseline(wl, batch, cpu_inputs, args.cpu_seconds, n_layers, is_decode)
+        del cpu_inputs
+
+    config = {"workload": wl.name, "d_model": d, "n_q_heads": Hq, "n_kv_heads": Hkv,
+              "head_dim": hd, "d_ffn": F, "layers": n_layers, "rows": M,
+              "hidden_rows": batch.hidden_rows, "sum_ctx": sum_ctx,
+              "mode": "decode" if is_decode else "prefill", "kv_block": 16,
+              "parallelism": "single GPU (one replica's share)"}
+    return {"value": round(value, 2), "unit": unit, "ms_per_step": round(ms, 4),
+            "dtype": shape.dtype, "config": config, "roofline": roof, "whole_step": whole,
+            "flushed": flushed_out, "graph_replay": graph, "scaling_model": scaling,
+            "cpu_baseline": cpu}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "bench.py runs one replica's share on one MI355X; "
+                          "sharding the row subsets over several GPUs is not implemented",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    if args.copy_calibration:
+        copy_calibration()
+        return
+
+    if args.batch != 64 and args.workload not in (None, "c2"):
+        print(json.dumps({"error": "--batch applies to the 8B decode workload (c2) only"}))
+        sys.exit(2)
+    if args.batch < 1:
+        print(json.dumps({"error": "--batch must be >= 1"}))
+        sys.exit(2)
+
+    import torch
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    num_cus = torch.cuda.get_device_properties(0).multi_processor_count
+    peaks = None if args.no_peaks else measure_peaks(num_cus)
+    if peaks:
+        log(f"measured peaks: {peaks}")
+    flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device="cuda")
+
+    if args.workload is None:
+        # The metric's two halves: the 8B decode step (headline value) and the
+        # 32B 2048-token chunked prefill (under "prefill").
+        dec = run_workload("c2", args.batch, args, peaks, flush)
+        pre = None if args.batch != 64 else run_workload("c4p", 64, args, peaks, flush)
+    else:
+        dec = run_workload(args.workload, args.batch, args, peaks, flush)
+        pre = None
 
     out = {
-        "metric": METRIC, "value": round(value, 2), "unit": unit, "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "metric": METRIC, "value": dec["value"], "unit": dec["unit"], "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": dec["ms_per_step"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": shape.dtype, "data": "synthetic (seeded counter-based generator)",
-        "config": {"workload": wl.name, "d_model": d, "n_q_heads": Hq, "n_kv_heads": Hkv,
-                   "head_dim": hd, "d_ffn": F, "layers": n_layers, "rows": M,
-                   "hidden_rows": batch.hidden_rows, "sum_ctx": sum_ctx,
-                   "mode": "decode" if is_decode else "prefill", "kv_block": 16,
-                   "parallelism": "single GPU (one replica's share)"},
-        "roofline": roof, "whole_step": whole, "graph_replay": graph,
-        "scaling_model": scaling, "cpu_baseline": cpu,
+        "dtype": dec["dtype"], "data": "synthetic (seeded counter-based generator)",
+        "config": dec["config"], "roofline": dec["roofline"], "whole_step": dec["whole_step"],
+        "flushed": dec["flushed"], "graph_replay": dec["graph_replay"],
+        "peaks_measured": peaks, "scaling_model": dec["scaling_model"],
+        "cpu_baseline": dec["cpu_baseline"],
     }
+    if pre is not None:
+        out["prefill"] = {k: pre[k] for k in ("value", "unit", "ms_per_step", "config",
+                                               "roofline", "whole_step", "flushed",
+                                               "graph_replay", "cpu_baseline")}
     print(json.dumps(out), flush=True)
 
 

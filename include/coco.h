@@ -63,9 +63,11 @@
  *                          (then n_seqs == n_rows).
  *   block_table[n_seqs][max_blocks_per_seq]   physical block ids, -1 unused
  *   ctx_lens[n_seqs]       cached tokens of sequence s once this call's tokens
- *                          are appended (decode: positions[i] + 1)
+ *                          are appended (decode, normally positions[i] + 1)
  * Every token attends to the cached keys of its own sequence at positions
- * 0 .. its own position (causal), its own key included.
+ * 0 .. its own position (causal), its own key included: a decode row i
+ * attends min(ctx_lens[i], positions[i] + 1) keys, so cached tokens past its
+ * position (positions[i] < ctx_lens[i] - 1) are not read.
  */
 #ifndef COCO_H
 #define COCO_H
@@ -100,7 +102,8 @@ typedef struct {
   int32_t block_size;         /* must be 16 */
   int32_t max_rows;           /* largest n_rows of any call (decode rows or prefill tokens) */
   int32_t max_seqs;           /* largest n_seqs of any call */
-  int32_t max_blocks_per_seq; /* row stride of block_table (<= 2^24) */
+  int32_t max_blocks_per_seq; /* row stride of block_table (<= 2^24; bf16: <= 130944,
+                                 the decode partition merge's limit) */
   float rope_theta;           /* RoPE base theta */
   float rms_eps;              /* RMSNorm epsilon */
 } coco_layer_config;
@@ -126,8 +129,11 @@ typedef struct {
 int coco_layer_init(const coco_layer_config* cfg, const coco_layer_weights* layers,
                     coco_layer_t* out);
 
-/* Release the workspace and the handle. Waits for work on the device first.
- * NULL is ignored. */
+/* Release the workspace and the handle. First waits for the handle's last
+ * call made outside graph capture to finish (an event recorded behind the
+ * last kernel of every such call; calls on one handle are ordered, since they
+ * share the workspace), not for other work on the device. A graph captured
+ * from the handle's calls must not run after this. NULL is ignored. */
 void coco_layer_destroy(coco_layer_t h);
 
 /* Message of the last failed call on this thread ("" if none). */
@@ -234,6 +240,26 @@ int coco_layer_set_timing(coco_layer_t h, int32_t on);
  * the recorded events, then resets the sums. Returns COCO_ESTATE if more
  * launches were made than the pool holds (4096 per read). */
 int coco_layer_read_timing(coco_layer_t h, double* ms, int64_t* launches, int32_t n_kinds);
+
+/* Peak probes for benchmarks (not part of the layer): the rates this GPU
+ * sustains, against which measured kernels are quoted next to the published
+ * peaks. Both enqueue one kernel on `stream` and return COCO_EINVAL for bad
+ * arguments or COCO_EHIP for a failed launch (without a coco_last_error
+ * message); the caller times them with events on the same stream.
+ *
+ * coco_probe_read: reads `bytes` (a multiple of 16, 16-byte aligned) of device
+ * memory at `buf` once, as 16-byte vector loads spread over `blocks`
+ * 256-thread workgroups; writes one 32-bit word per workgroup to `out`
+ * (device, >= 4 * blocks bytes).
+ *
+ * coco_probe_mfma_bf16: `blocks` workgroups of four waves, each wave running
+ * `iters` rounds of four independent v_mfma_f32_32x32x16_bf16 chains on
+ * register operands; writes one float per wave to `out` (device, >= 16 *
+ * blocks bytes) and the dense flop count of the launch to *flops (host). */
+int coco_probe_read(const void* buf, int64_t bytes, void* out, int32_t blocks,
+                    coco_stream_t stream);
+int coco_probe_mfma_bf16(int64_t iters, void* out, int32_t blocks, double* flops,
+                         coco_stream_t stream);
 
 #ifdef __cplusplus
 }

@@ -10,7 +10,7 @@ from ._lib import (  # noqa: F401
     COCO_WS_X1, CocoError, Handle, LIB_PATH, coco_kv_append, coco_last_error, coco_layer_destroy,
     coco_layer_forward, coco_layer_init, coco_layer_set_validate, coco_layer_span_forward,
     coco_layer_workspace, coco_version, make_config, coco_layer_set_timing,
-    coco_layer_read_timing, KERNEL_KINDS,
+    coco_layer_read_timing, KERNEL_KINDS, coco_probe_read, coco_probe_mfma_bf16,
     make_scale_model, coco_split_batch, coco_comm_time, coco_speedup, coco_cost_mem,
     coco_cost_comp, coco_speedup_vec, coco_scale_candidates,
 )

@@ -23,7 +23,7 @@ COCO_WS_X, COCO_WS_H, COCO_WS_Q, COCO_WS_O, COCO_WS_X1, COCO_WS_H2, COCO_WS_U = 
 EXPORTS = ["coco_layer_init", "coco_layer_destroy", "coco_last_error", "coco_version",
            "coco_layer_set_validate", "coco_kv_append", "coco_layer_forward",
            "coco_layer_span_forward", "coco_layer_workspace", "coco_layer_set_timing",
-           "coco_layer_read_timing",
+           "coco_layer_read_timing", "coco_probe_read", "coco_probe_mfma_bf16",
            # include/coco_scaling.h: host arithmetic of the speedup/cost model
            "coco_split_batch", "coco_comm_time", "coco_speedup", "coco_cost_mem",
            "coco_cost_comp", "coco_speedup_vec", "coco_scale_candidates"]
@@ -84,6 +84,9 @@ def _load():
         "coco_layer_set_timing": (ctypes.c_int, [vp, i32]),
         "coco_layer_read_timing": (ctypes.c_int, [vp, ctypes.POINTER(ctypes.c_double),
                                                   ctypes.POINTER(i64), i32]),
+        "coco_probe_read": (ctypes.c_int, [vp, i64, vp, i32, vp]),
+        "coco_probe_mfma_bf16": (ctypes.c_int, [i64, vp, i32, ctypes.POINTER(ctypes.c_double),
+                                                vp]),
         "coco_split_batch": (ctypes.c_int, [i64, i32, ctypes.POINTER(i64)]),
         "coco_comm_time": (ctypes.c_double, [ctypes.POINTER(coco_scale_model), i32]),
         "coco_speedup": (ctypes.c_double, [ctypes.POINTER(coco_scale_model), i32, i32]),
@@ -191,8 +194,58 @@ def coco_layer_set_validate(h: Handle, on: bool) -> None:
     _check(_lib.coco_layer_set_validate(h.raw, 1 if on else 0))
 
 
+def _elem_dtype(cfg):
+    return torch.bfloat16 if cfg.dtype == COCO_BF16 else torch.float32
+
+
+def _shape_check(cond: bool, msg: str):
+    if not cond:
+        raise ValueError(msg)
+
+
+def _check_batch(h: Handle, hidden, row_idx, positions, seq_starts, block_table, ctx_lens):
+    """Shapes and dtypes against the handle's config, before any call: the
+    library takes plain pointers and uses the config for every stride."""
+    cfg = h.cfg
+    for name, t in (("hidden", hidden), ("row_idx", row_idx), ("positions", positions),
+                    ("block_table", block_table), ("ctx_lens", ctx_lens)):
+        if not isinstance(t, torch.Tensor):
+            raise TypeError(f"{name} must be a torch tensor")
+    if hidden.dtype != _elem_dtype(cfg):
+        raise TypeError(f"hidden must be {_elem_dtype(cfg)}, got {hidden.dtype}")
+    _shape_check(hidden.dim() == 2 and hidden.shape[1] == cfg.d_model,
+                 f"hidden must be [rows, {cfg.d_model}], got {tuple(hidden.shape)}")
+    n = row_idx.numel()
+    _shape_check(row_idx.dim() == 1, "row_idx must be 1-D")
+    _shape_check(positions.numel() == n,
+                 f"positions has {positions.numel()} entries for {n} rows")
+    n_seqs = ctx_lens.numel()
+    if seq_starts is None:
+        _shape_check(n_seqs == n, f"decode: ctx_lens has {n_seqs} entries for {n} rows")
+    else:
+        _shape_check(isinstance(seq_starts, torch.Tensor) and seq_starts.numel() == n_seqs + 1,
+                     f"seq_starts must have n_seqs + 1 = {n_seqs + 1} entries")
+    _shape_check(block_table.dim() == 2 and block_table.shape[1] == cfg.max_blocks_per_seq,
+                 f"block_table must be [n_seqs, {cfg.max_blocks_per_seq}], "
+                 f"got {tuple(block_table.shape)}")
+    _shape_check(block_table.shape[0] >= n_seqs,
+                 f"block_table has {block_table.shape[0]} rows for {n_seqs} sequences")
+
+
 def coco_kv_append(h: Handle, layer: int, k, v, seq_idx, positions, block_table, stream=None):
     i32 = torch.int32
+    cfg = h.cfg
+    n_tok = int(positions.numel())
+    per_tok = cfg.n_kv_heads * cfg.head_dim
+    for name, t in (("k", k), ("v", v)):
+        if t.dtype != _elem_dtype(cfg):
+            raise TypeError(f"{name} must be {_elem_dtype(cfg)}, got {t.dtype}")
+        _shape_check(t.numel() == n_tok * per_tok,
+                     f"{name} must hold [{n_tok}, {cfg.n_kv_heads}, {cfg.head_dim}] elements")
+    _shape_check(seq_idx.numel() == n_tok, f"seq_idx has {seq_idx.numel()} entries for {n_tok} tokens")
+    _shape_check(block_table.dim() == 2 and block_table.shape[1] == cfg.max_blocks_per_seq,
+                 f"block_table must be [n_seqs, {cfg.max_blocks_per_seq}], "
+                 f"got {tuple(block_table.shape)}")
     _check(_lib.coco_kv_append(h.raw, layer, _ptr(k, what="k"), _ptr(v, what="v"),
                                _ptr(seq_idx, i32, "seq_idx"), _ptr(positions, i32, "positions"),
                                int(positions.numel()), _ptr(block_table, i32, "block_table"),
@@ -202,6 +255,7 @@ def coco_kv_append(h: Handle, layer: int, k, v, seq_idx, positions, block_table,
 def coco_layer_forward(h: Handle, layer: int, hidden, row_idx, positions, seq_starts,
                        block_table, ctx_lens, stream=None):
     i32 = torch.int32
+    _check_batch(h, hidden, row_idx, positions, seq_starts, block_table, ctx_lens)
     n_seqs = int(ctx_lens.numel())
     _check(_lib.coco_layer_forward(
         h.raw, layer, _ptr(hidden, what="hidden"), int(hidden.shape[0]),
@@ -213,6 +267,7 @@ def coco_layer_forward(h: Handle, layer: int, hidden, row_idx, positions, seq_st
 def coco_layer_span_forward(h: Handle, first_layer: int, n_layers: int, hidden, row_idx,
                             positions, seq_starts, block_table, ctx_lens, stream=None):
     i32 = torch.int32
+    _check_batch(h, hidden, row_idx, positions, seq_starts, block_table, ctx_lens)
     n_seqs = int(ctx_lens.numel())
     _check(_lib.coco_layer_span_forward(
         h.raw, first_layer, n_layers, _ptr(hidden, what="hidden"), int(hidden.shape[0]),
@@ -237,6 +292,23 @@ def coco_layer_read_timing(h: Handle) -> dict:
     cnt = (ctypes.c_int64 * n)()
     _check(_lib.coco_layer_read_timing(h.raw, ms, cnt, n))
     return {k: (ms[i], cnt[i]) for i, k in enumerate(KERNEL_KINDS)}
+
+
+def coco_probe_read(buf, out, blocks: int, stream=None) -> None:
+    """One read pass over the whole of `buf` (device tensor); `out` holds at
+    least `blocks` int32 words."""
+    nbytes = buf.numel() * buf.element_size()
+    _check(_lib.coco_probe_read(_ptr(buf, what="buf"), nbytes, _ptr(out, what="out"), blocks,
+                                _stream(stream)))
+
+
+def coco_probe_mfma_bf16(iters: int, out, blocks: int, stream=None) -> float:
+    """Enqueues the MFMA loop; returns its dense flop count. `out` holds at
+    least 4 * blocks floats."""
+    flops = ctypes.c_double()
+    _check(_lib.coco_probe_mfma_bf16(iters, _ptr(out, what="out"), blocks, ctypes.byref(flops),
+                                     _stream(stream)))
+    return flops.value
 
 
 def raw_call(name: str, *args) -> int:

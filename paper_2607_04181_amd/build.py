@@ -24,7 +24,7 @@ FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-Wall",
          "-Wno-unused-function", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          f"-I{os.path.join(ROOT, 'include')}"]
 SOURCES = ["rows.hip", "gemm_skinny.hip", "gemm_tile.hip", "attention.hip", "coco_api.hip",
-           "scaling.cpp"]
+           "probe.hip", "scaling.cpp"]
 
 
 def build(verbose: bool = False, jobs: int = 8) -> str:

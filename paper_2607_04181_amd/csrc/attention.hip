@@ -70,8 +70,16 @@ struct DecItem {
   int s, g, sp, t1, b_first, b_last;
 };
 
+// Keys a decode row attends: positions 0 .. its own position, within the
+// cached length (min(ctx_lens[s], positions[s] + 1), never negative).
+__device__ __forceinline__ int decode_keys(const int32_t* ctx_lens, const int32_t* positions,
+                                           int s) {
+  return max(0, min(ctx_lens[s], positions[s] + 1));
+}
+
 __device__ __forceinline__ DecItem decode_item(int w, int Hkv, const int32_t* split_off,
-                                               const int32_t* ctx_lens, int n_seqs,
+                                               const int32_t* ctx_lens,
+                                               const int32_t* positions, int n_seqs,
                                                int max_blocks) {
   DecItem it;
   const int item = w / Hkv;
@@ -85,7 +93,8 @@ __device__ __forceinline__ DecItem decode_item(int w, int Hkv, const int32_t* sp
   it.sp = item - split_off[lo];
   const int t0 = it.sp * kDecodeSplit;
   // Capped at the block table's width (only invalid lengths reach the cap).
-  it.t1 = min(min(ctx_lens[lo], t0 + kDecodeSplit), max_blocks * kBlockTokens);
+  it.t1 = min(min(decode_keys(ctx_lens, positions, lo), t0 + kDecodeSplit),
+              max_blocks * kBlockTokens);
   it.b_first = t0 / kBlockTokens;
   it.b_last = (it.t1 - 1) / kBlockTokens;
   return it;
@@ -94,9 +103,9 @@ __device__ __forceinline__ DecItem decode_item(int w, int Hkv, const int32_t* sp
 __global__ __launch_bounds__(kDecWaves * 64, 4) void attn_decode_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k_cache,
     const bf16_t* __restrict__ v_cache, const int32_t* __restrict__ block_table, int max_blocks,
-    const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ split_off, int n_seqs,
-    int Hq, int Hkv, float* __restrict__ part_o, float* __restrict__ part_ml, int max_splits,
-    float scale_log2) {
+    const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ positions,
+    const int32_t* __restrict__ split_off, int n_seqs, int Hq, int Hkv,
+    float* __restrict__ part_o, float* __restrict__ part_ml, int max_splits, float scale_log2) {
   __shared__ float sm_m[kDecWaves][16], sm_l[kDecWaves][16];
   __shared__ float sm_o[kDecWaves][16][HD + 4];
 
@@ -134,7 +143,7 @@ __global__ __launch_bounds__(kDecWaves * 64, 4) void attn_decode_kernel(
   int w = blockIdx.x;
   DecItem cur{};
   if (w < total) {
-    cur = decode_item(w, Hkv, split_off, ctx_lens, n_seqs, max_blocks);
+    cur = decode_item(w, Hkv, split_off, ctx_lens, positions, n_seqs, max_blocks);
     issue(cur);
   }
   for (; w < total; w += gridDim.x) {
@@ -198,8 +207,8 @@ __global__ __launch_bounds__(kDecWaves * 64, 4) void attn_decode_kernel(
     // The registers are free: start the next item's reads now (past the
     // last item, a repeat of the last one that is never used).
     const DecItem it = cur;
-    cur = decode_item(min(w + (int)gridDim.x, total - 1), Hkv, split_off, ctx_lens, n_seqs,
-                      max_blocks);
+    cur = decode_item(min(w + (int)gridDim.x, total - 1), Hkv, split_off, ctx_lens, positions,
+                      n_seqs, max_blocks);
     issue(cur);
     __syncthreads();
 
@@ -237,6 +246,7 @@ constexpr int kPre = 8;
 __global__ __launch_bounds__(HD) void attn_combine_kernel(const float* __restrict__ part_o,
                                                           const float* __restrict__ part_ml,
                                                           const int32_t* __restrict__ ctx_lens,
+                                                          const int32_t* __restrict__ positions,
                                                           int Hq, int max_splits,
                                                           bf16_t* __restrict__ o) {
   extern __shared__ float sm[];  // [0, max_splits): weights; [max_splits, 2*max_splits): l
@@ -254,7 +264,8 @@ __global__ __launch_bounds__(HD) void attn_combine_kernel(const float* __restric
     m_own = part_ml[(base + dim) * 2];
     l_own = part_ml[(base + dim) * 2 + 1];
   }
-  const int nsp = min((ctx_lens[s] + kDecodeSplit - 1) / kDecodeSplit, max_splits);
+  const int nsp =
+      min((decode_keys(ctx_lens, positions, s) + kDecodeSplit - 1) / kDecodeSplit, max_splits);
   float mx = -INFINITY;
   if (dim < nsp) {
     sm[dim] = m_own;
@@ -597,12 +608,18 @@ int decode_max_splits(int max_blocks_per_seq) {
   return (max_blocks_per_seq * kBlockTokens + kDecodeSplit - 1) / kDecodeSplit;
 }
 
+// The merge kernel keeps two floats per partition in dynamic LDS, within the
+// 64 KB a launch gets without an opt-in (its static LDS is 8 bytes).
+bool attn_combine_fits(int max_splits) {
+  return max_splits >= 1 && (int64_t)max_splits * 2 * sizeof(float) <= 65536 - 64;
+}
+
 hipError_t launch_attn_decode_bf16(const uint16_t* q, const uint16_t* k_cache,
                                    const uint16_t* v_cache, const int32_t* block_table,
                                    int max_blocks, const int32_t* ctx_lens,
-                                   const int32_t* split_off, int n_seqs, int Hq, int Hkv,
-                                   float* part_o, float* part_ml, int max_splits,
-                                   int num_cus, hipStream_t st) {
+                                   const int32_t* positions, const int32_t* split_off,
+                                   int n_seqs, int Hq, int Hkv, float* part_o, float* part_ml,
+                                   int max_splits, int num_cus, hipStream_t st) {
   if (n_seqs <= 0) return hipSuccess;
   if (num_cus <= 0) return hipErrorInvalidValue;
   const float scale_log2 = kLog2e / sqrtf((float)HD);
@@ -611,18 +628,19 @@ hipError_t launch_attn_decode_bf16(const uint16_t* q, const uint16_t* k_cache,
   const int64_t work_bound = (int64_t)n_seqs * max_splits * Hkv;
   const int grid = (int)(work_bound < 2 * num_cus ? work_bound : 2 * num_cus);
   COCO_LAUNCH(attn_decode_kernel, dim3(grid), dim3(kDecWaves * 64), 0, st, q, k_cache,
-                     v_cache, block_table, max_blocks, ctx_lens, split_off, n_seqs, Hq, Hkv,
-                     part_o, part_ml, max_splits, scale_log2);
+                     v_cache, block_table, max_blocks, ctx_lens, positions, split_off, n_seqs,
+                     Hq, Hkv, part_o, part_ml, max_splits, scale_log2);
   return hipGetLastError();
 }
 
 hipError_t launch_attn_combine_bf16(const float* part_o, const float* part_ml,
-                                    const int32_t* ctx_lens, int n_seqs, int Hq, int max_splits,
-                                    uint16_t* o, hipStream_t st) {
+                                    const int32_t* ctx_lens, const int32_t* positions,
+                                    int n_seqs, int Hq, int max_splits, uint16_t* o,
+                                    hipStream_t st) {
   if (n_seqs <= 0) return hipSuccess;
   COCO_LAUNCH(attn_combine_kernel, dim3(Hq, n_seqs), dim3(HD),
-                     2 * max_splits * sizeof(float), st, part_o, part_ml, ctx_lens, Hq,
-                     max_splits, o);
+                     2 * max_splits * sizeof(float), st, part_o, part_ml, ctx_lens, positions,
+                     Hq, max_splits, o);
   return hipGetLastError();
 }
 

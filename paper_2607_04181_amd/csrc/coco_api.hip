@@ -64,6 +64,8 @@ struct coco_layer {
   std::vector<int> ev_kind;    // kind of each recorded pair
   bool ev_overflow = false;
   hipStream_t ev_stream = nullptr;
+  // Recorded at the end of every call made outside graph capture.
+  hipEvent_t done = nullptr;
 };
 
 namespace coco {
@@ -141,6 +143,13 @@ int check_config(const coco_layer_config* c) {
     if (c->d_model % 128 || c->d_ffn % 128)
       return fail(COCO_EINVAL, "bf16 path needs d_model and d_ffn multiples of 128");
     if (c->d_model > 16384) return fail(COCO_EINVAL, "bf16 path needs d_model <= 16384");
+    // The decode partition merge keeps two floats per 256-token partition in LDS.
+    if (!attn_combine_fits(decode_max_splits(c->max_blocks_per_seq)))
+      return fail(COCO_EINVAL,
+                  "max_blocks_per_seq = %d: its %d decode partitions exceed what the partition "
+                  "merge holds in LDS (max_blocks_per_seq <= %d)",
+                  c->max_blocks_per_seq, decode_max_splits(c->max_blocks_per_seq),
+                  (65536 - 64) / 8 * (kDecodeSplit / kBlockTokens));
   } else if (c->dtype == COCO_F32) {
     if (c->head_dim % 32 || c->head_dim > 256)
       return fail(COCO_EINVAL, "fp32 path needs head_dim a multiple of 32, <= 256");
@@ -266,11 +275,13 @@ int coco_layer_init(const coco_layer_config* cfg, const coco_layer_weights* laye
     inv[j] = pow((double)c.rope_theta, -2.0 * j / (double)c.head_dim);
   if (hipMemcpy(H->inv_freq, inv.data(), inv.size() * 8, hipMemcpyHostToDevice) != hipSuccess ||
       hipMemset(H->ws, 0, offs[10]) != hipSuccess ||
+      hipEventCreateWithFlags(&H->done, hipEventDisableTiming) != hipSuccess ||
       (H->rope_rows > 0 &&
        (launch_rope_table(H->inv_freq, c.head_dim / 2, H->rope_rows, H->rope, nullptr) !=
             hipSuccess ||
         hipDeviceSynchronize() != hipSuccess))) {
     (void)hipGetLastError();
+    if (H->done) (void)hipEventDestroy(H->done);
     (void)hipFree(H->ws);
     delete H;
     return fail(COCO_EHIP, "workspace initialisation failed");
@@ -284,7 +295,13 @@ void coco_layer_destroy(coco_layer_t H) {
   int cur = 0;
   (void)hipGetDevice(&cur);
   (void)hipSetDevice(H->device);
-  (void)hipDeviceSynchronize();
+  // The handle's last call outside graph capture recorded `done` after its
+  // last kernel; calls on one handle are ordered (they share the workspace),
+  // so this waits for all of its enqueued work and nothing else.
+  if (H->done) {
+    (void)hipEventSynchronize(H->done);
+    (void)hipEventDestroy(H->done);
+  }
   for (auto& e : H->ev) (void)hipEventDestroy(e);
   (void)hipFree(H->ws);
   (void)hipSetDevice(cur);
@@ -472,11 +489,11 @@ int attention<bf16_t>(coco_layer* H, const coco_layer_weights& w, int M,
       KernelTimer t(H, COCO_K_ATTENTION, st);
       HIPCHK(launch_attn_decode_bf16((const bf16_t*)H->q, (const bf16_t*)w.k_cache,
                                      (const bf16_t*)w.v_cache, bt, c.max_blocks_per_seq, ctx,
-                                     H->split_off, n_seqs, c.n_q_heads, c.n_kv_heads, H->attn_o,
-                                     H->attn_ml, H->max_splits, H->num_cus, st));
+                                     positions, H->split_off, n_seqs, c.n_q_heads, c.n_kv_heads,
+                                     H->attn_o, H->attn_ml, H->max_splits, H->num_cus, st));
     }
     KernelTimer t(H, COCO_K_ATTN_COMBINE, st);
-    HIPCHK(launch_attn_combine_bf16(H->attn_o, H->attn_ml, ctx, n_seqs, c.n_q_heads,
+    HIPCHK(launch_attn_combine_bf16(H->attn_o, H->attn_ml, ctx, positions, n_seqs, c.n_q_heads,
                                     H->max_splits, (bf16_t*)H->o, st));
   } else {
     KernelTimer t(H, COCO_K_ATTENTION, st);
@@ -662,6 +679,16 @@ int check_batch(coco_layer* H, int first, int nl, const void* hidden, int64_t hi
   return COCO_OK;
 }
 
+// Records the handle's completion event behind the call's last kernel, unless
+// the stream is being captured into a graph (the event would then only fire
+// on replays).
+int mark_done(coco_layer* H, hipStream_t st) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  HIPCHK(hipStreamIsCapturing(st, &cs));
+  if (cs == hipStreamCaptureStatusNone) HIPCHK(hipEventRecord(H->done, st));
+  return COCO_OK;
+}
+
 int forward_impl(coco_layer* H, int first, int nl, void* hidden, int64_t hidden_rows,
                  const int32_t* row_idx, int n_rows, const int32_t* positions,
                  const int32_t* seq_starts, int n_seqs, const int32_t* bt, const int32_t* ctx,
@@ -677,10 +704,13 @@ int forward_impl(coco_layer* H, int first, int nl, void* hidden, int64_t hidden_
                            ctx, first, nl, st)))
     return rc;
   if (H->cfg.dtype == COCO_BF16)
-    return run_span<bf16_t>(H, first, nl, (bf16_t*)hidden, row_idx, n_rows, positions,
-                            seq_starts, n_seqs, bt, ctx, st);
-  return run_span<float>(H, first, nl, (float*)hidden, row_idx, n_rows, positions, seq_starts,
+    rc = run_span<bf16_t>(H, first, nl, (bf16_t*)hidden, row_idx, n_rows, positions, seq_starts,
+                          n_seqs, bt, ctx, st);
+  else
+    rc = run_span<float>(H, first, nl, (float*)hidden, row_idx, n_rows, positions, seq_starts,
                          n_seqs, bt, ctx, st);
+  if (rc) return rc;
+  return mark_done(H, st);
 }
 
 }  // namespace
@@ -741,7 +771,7 @@ int coco_kv_append(coco_layer_t H, int32_t layer, const void* k, const void* v,
     HIPCHK(launch_kv_append<float>((const float*)k, (const float*)v, seq_idx, positions, n_tok,
                                    c.n_kv_heads, c.head_dim, block_table, c.max_blocks_per_seq,
                                    (float*)w.k_cache, (float*)w.v_cache, st));
-  return COCO_OK;
+  return mark_done(H, st);
 }
 
 }  // extern "C"

@@ -53,7 +53,8 @@ hipError_t launch_rope_table(const double* inv_freq, int half, int n_pos, float*
 // With ss non-null (decode, RMSNorm_1 folded into the projection), each row's
 // sums are first scaled by 1 / sqrt(sum_s ss[s][row] / d + eps).
 // With split_off non-null (decode), one workgroup also writes the decode
-// attention's partition offsets from ctx_lens (counts capped at max_splits).
+// attention's partition offsets from the keys each row attends,
+// min(ctx_lens, positions + 1) (counts capped at max_splits).
 template <typename T>
 hipError_t launch_qkv_epilogue(const float* part, int S, int M, int Hq, int Hkv, int hd,
                                const int32_t* positions, const int32_t* seq_starts,
@@ -168,18 +169,21 @@ hipError_t launch_gemm_f32(const float* A, const float* W, float* part, int M, i
 // ---------------------------------------------------------------- attention
 constexpr int kDecodeSplit = 256;  // tokens per split-KV partition
 int decode_max_splits(int max_blocks_per_seq);
+bool attn_combine_fits(int max_splits);
 
 // split_off[n_seqs + 1]: exclusive prefix sum of each sequence's partition
 // count (written by the QKV epilogue of the same call).
+// Decode row s attends min(ctx_lens[s], positions[s] + 1) keys.
 hipError_t launch_attn_decode_bf16(const uint16_t* q, const uint16_t* k_cache,
                                    const uint16_t* v_cache, const int32_t* block_table,
                                    int max_blocks, const int32_t* ctx_lens,
-                                   const int32_t* split_off, int n_seqs, int Hq, int Hkv,
-                                   float* part_o, float* part_ml, int max_splits,
-                                   int num_cus, hipStream_t st);
+                                   const int32_t* positions, const int32_t* split_off,
+                                   int n_seqs, int Hq, int Hkv, float* part_o, float* part_ml,
+                                   int max_splits, int num_cus, hipStream_t st);
 hipError_t launch_attn_combine_bf16(const float* part_o, const float* part_ml,
-                                    const int32_t* ctx_lens, int n_seqs, int Hq, int max_splits,
-                                    uint16_t* o, hipStream_t st);
+                                    const int32_t* ctx_lens, const int32_t* positions,
+                                    int n_seqs, int Hq, int max_splits, uint16_t* o,
+                                    hipStream_t st);
 
 hipError_t launch_attn_prefill_bf16(const uint16_t* q, const uint16_t* k_cache,
                                     const uint16_t* v_cache, const int32_t* block_table,

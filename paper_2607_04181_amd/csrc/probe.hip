@@ -1,0 +1,104 @@
+// Peak probes for benchmarks: what this GPU sustains on a plain HBM read
+// stream and on a loop of bf16 MFMAs, so that measured kernels can be quoted
+// against measured ceilings as well as against the published ones. Neither
+// kernel is on the layer's path.
+#include "../../include/coco.h"
+#include "common.h"
+#include "kernels.h"
+
+namespace coco {
+namespace {
+
+constexpr int kProbeThreads = 256;
+
+// Every thread reads 16-byte vectors with a grid-wide stride (consecutive
+// lanes on consecutive vectors) and folds them into one word; each block
+// writes one word so the loads cannot be dropped.
+__global__ __launch_bounds__(kProbeThreads) void probe_read_kernel(const u32x4_t* __restrict__ buf,
+                                                                   int64_t n_vec,
+                                                                   uint32_t* __restrict__ out) {
+  const int64_t stride = (int64_t)gridDim.x * kProbeThreads;
+  uint32_t acc = 0;
+  int64_t i = (int64_t)blockIdx.x * kProbeThreads + threadIdx.x;
+  // Four independent loads in flight per thread per iteration.
+  for (; i + 3 * stride < n_vec; i += 4 * stride) {
+    const u32x4_t a = buf[i], b = buf[i + stride], c = buf[i + 2 * stride],
+                  d = buf[i + 3 * stride];
+    acc ^= (a.x ^ a.y ^ a.z ^ a.w) ^ (b.x ^ b.y ^ b.z ^ b.w) ^ (c.x ^ c.y ^ c.z ^ c.w) ^
+           (d.x ^ d.y ^ d.z ^ d.w);
+  }
+  for (; i < n_vec; i += stride) {
+    const u32x4_t a = buf[i];
+    acc ^= a.x ^ a.y ^ a.z ^ a.w;
+  }
+  __shared__ uint32_t red[kProbeThreads / kWave];
+  for (int o = 32; o > 0; o >>= 1) acc ^= __shfl_xor(acc, o, kWave);
+  if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t t = 0;
+    for (int w = 0; w < kProbeThreads / kWave; ++w) t ^= red[w];
+    out[blockIdx.x] = t;
+  }
+}
+
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+// Four independent chains of v_mfma_f32_32x32x16_bf16 per wave (32*32*16*2
+// flops each), operands held in registers; lane 0 of each wave writes one
+// element of every chain so the chains cannot be dropped.
+constexpr int kMfmaChains = 4;
+
+__global__ __launch_bounds__(kProbeThreads) void probe_mfma_kernel(int64_t iters,
+                                                                   float* __restrict__ out) {
+  const int lane = threadIdx.x & (kWave - 1);
+  bf16x8_t a, b;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    a[e] = (__bf16)(0.001f * (float)(lane + e));
+    b[e] = (__bf16)(0.002f * (float)(lane - e));
+  }
+  f32x16_t acc[kMfmaChains];
+#pragma unroll
+  for (int c = 0; c < kMfmaChains; ++c)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[c][e] = 0.f;
+  for (int64_t it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int c = 0; c < kMfmaChains; ++c)
+      acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[c], 0, 0, 0);
+  }
+  if (lane == 0) {
+    float t = 0.f;
+#pragma unroll
+    for (int c = 0; c < kMfmaChains; ++c) t += acc[c][0];
+    out[(int64_t)blockIdx.x * (kProbeThreads / kWave) + threadIdx.x / kWave] = t;
+  }
+}
+
+}  // namespace
+}  // namespace coco
+
+using namespace coco;
+
+extern "C" {
+
+int coco_probe_read(const void* buf, int64_t bytes, void* out, int32_t blocks,
+                    coco_stream_t stream) {
+  if (!buf || !out || bytes < 16 || bytes % 16 || (uintptr_t)buf % 16 || blocks < 1)
+    return COCO_EINVAL;
+  COCO_LAUNCH(probe_read_kernel, dim3(blocks), dim3(kProbeThreads), 0, (hipStream_t)stream,
+              (const u32x4_t*)buf, bytes / 16, (uint32_t*)out);
+  return hipGetLastError() == hipSuccess ? COCO_OK : COCO_EHIP;
+}
+
+int coco_probe_mfma_bf16(int64_t iters, void* out, int32_t blocks, double* flops,
+                         coco_stream_t stream) {
+  if (!out || !flops || iters < 1 || blocks < 1) return COCO_EINVAL;
+  *flops = 2.0 * 32 * 32 * 16 * kMfmaChains * (double)iters * blocks * (kProbeThreads / kWave);
+  COCO_LAUNCH(probe_mfma_kernel, dim3(blocks), dim3(kProbeThreads), 0, (hipStream_t)stream,
+              iters, (float*)out);
+  return hipGetLastError() == hipSuccess ? COCO_OK : COCO_EHIP;
+}
+
+}  // extern "C"

@@ -263,13 +263,15 @@ __global__ __launch_bounds__(kEpiHeads * kWave) void qkv_epilogue_kernel(
   }
   __syncthreads();
   if (split_off != nullptr && blockIdx.x == 0 && i == 0 && wv == 0) {
-    // Decode attention work list: exclusive prefix sum of ceil(ctx / 256),
-    // capped at max_splits (only invalid lengths reach the cap).
+    // Decode attention work list: exclusive prefix sum of ceil(n / 256) for
+    // the n = min(ctx_lens[s], positions[s] + 1) keys row s attends, capped
+    // at max_splits (only invalid lengths reach the cap).
     int run = 0;
     if (lane == 0) split_off[0] = 0;
     for (int base = 0; base < n_seqs; base += kWave) {
       const int s = base + lane;
-      int v = s < n_seqs ? min((ctx_lens[s] + kDecodeSplit - 1) / kDecodeSplit, max_splits) : 0;
+      const int n = s < n_seqs ? max(0, min(ctx_lens[s], positions[s] + 1)) : 0;
+      int v = min((n + kDecodeSplit - 1) / kDecodeSplit, max_splits);
 #pragma unroll
       for (int o = 1; o < kWave; o <<= 1) {
         const int t = __shfl_up(v, o, kWave);

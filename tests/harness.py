@@ -1,11 +1,15 @@
 """Glue shared by the GPU tests and smoke(): build a replica on the GPU from a
 workload, run the oracle on chosen rows, compare.
 
-Oracle inputs are generated on the CPU by the counter-based generator
-(``source="cpu"``) or copied from the tensors the same generator produced on
-the GPU (``source="device"``, used for the largest layers); the two are
-bit-identical, which test_gpu_inputs checks. Nothing the oracle reads comes
-out of the library.
+Oracle inputs come from the counter-based generator, never from memory the
+library writes:
+  * prior cache tokens are always regenerated on the CPU, block by block
+    (``W.kv_pool(..., blocks=...)``), so a kernel that overwrote an earlier
+    token's slot cannot feed that value to the oracle too;
+  * weights are generated on the CPU (``source="cpu"``) or, for the largest
+    layers, copied from the weight tensors the same generator produced on the
+    GPU (``source="device"``); the library only reads weights, and
+    test_generator_is_identical_on_cpu_and_gpu shows the two are bit-identical.
 """
 from __future__ import annotations
 
@@ -39,6 +43,17 @@ def normwise_err(got, ref) -> float:
     got = np.asarray(got, np.float64).reshape(ref.shape)
     den = np.max(np.abs(ref))
     return float(np.max(np.abs(got - ref)) / (den if den > 0 else 1.0))
+
+
+def elementwise_err(got, ref) -> float:
+    """max_i |got_i - ref_i| / max(|ref_i|, rms(ref)): an elementwise relative
+    error whose denominator never drops below the tensor's rms (reported next
+    to the normwise bound, not bound itself)."""
+    ref = np.asarray(ref, np.float64)
+    got = np.asarray(got, np.float64).reshape(ref.shape)
+    rms = float(np.sqrt(np.mean(ref * ref))) if ref.size else 0.0
+    den = np.maximum(np.abs(ref), rms if rms > 0 else 1.0)
+    return float(np.max(np.abs(got - ref) / den)) if ref.size else 0.0
 
 
 class Replica:
@@ -82,23 +97,19 @@ def oracle_weights(shape, tag, layer, source="cpu", dev_layer=None) -> dict:
     return {k: to64(v) for k, v in t.items()}
 
 
-def oracle_cache(shape, tag, layer, batch: W.Batch, seqs, num_blocks, source="cpu",
-                 dev_layer=None) -> oracle.KVCache:
-    """Logical caches of call-sequences `seqs`: the prior tokens from the pool,
-    room up to ctx_lens for the tokens the call appends."""
+def oracle_cache(shape, tag, layer, batch: W.Batch, seqs, num_blocks) -> oracle.KVCache:
+    """Logical caches of call-sequences `seqs`: the prior tokens regenerated on
+    the CPU from the pool's generator stream (never read back from the GPU
+    pools, which the library writes), room up to ctx_lens for the tokens the
+    call appends."""
     Ks, Vs = [], []
     Hkv, hd = shape.n_kv_heads, shape.head_dim
     for s in seqs:
         prior, ctx = int(batch.prior_lens[s]), int(batch.ctx_lens[s])
         nb = -(-prior // W.BLOCK_SIZE)
         blocks = batch.block_table[s, :nb]
-        if source == "device":
-            idx = torch.from_numpy(blocks.astype(np.int64)).cuda()
-            kb = to64(dev_layer["k_cache"].index_select(0, idx))
-            vb = to64(dev_layer["v_cache"].index_select(0, idx))
-        else:
-            kb = to64(W.kv_pool(shape, tag, layer, num_blocks, "k", blocks=blocks))
-            vb = to64(W.kv_pool(shape, tag, layer, num_blocks, "v", blocks=blocks))
+        kb = to64(W.kv_pool(shape, tag, layer, num_blocks, "k", blocks=blocks))
+        vb = to64(W.kv_pool(shape, tag, layer, num_blocks, "v", blocks=blocks))
         K = np.zeros((ctx, Hkv, hd))
         V = np.zeros((ctx, Hkv, hd))
         if prior:
@@ -113,8 +124,7 @@ def oracle_decode_rows(shape, tag, layer, batch: W.Batch, call_rows, hidden64, s
     """Oracle output rows (in call-row order) of a decode batch's call rows."""
     sub = batch.select(call_rows)
     w64 = w64 if w64 is not None else oracle_weights(shape, tag, layer, source, dev_layer)
-    cache = oracle_cache(shape, tag, layer, sub, range(sub.n_seqs), batch.num_blocks, source,
-                         dev_layer)
+    cache = oracle_cache(shape, tag, layer, sub, range(sub.n_seqs), batch.num_blocks)
     out, rec = oracle.layer_forward(w64, shape, hidden64, sub.row_idx, sub.positions, None,
                                     sub.ctx_lens, cache, record=record)
     return out[sub.row_idx], rec, cache
@@ -124,8 +134,7 @@ def oracle_prefill_seqs(shape, tag, layer, batch: W.Batch, seqs, hidden64, sourc
                         dev_layer=None, w64=None, record=False):
     sub = batch.select_seqs(seqs)
     w64 = w64 if w64 is not None else oracle_weights(shape, tag, layer, source, dev_layer)
-    cache = oracle_cache(shape, tag, layer, sub, range(sub.n_seqs), batch.num_blocks, source,
-                         dev_layer)
+    cache = oracle_cache(shape, tag, layer, sub, range(sub.n_seqs), batch.num_blocks)
     out, rec = oracle.layer_forward(w64, shape, hidden64, sub.row_idx, sub.positions,
                                     sub.seq_starts, sub.ctx_lens, cache, record=record)
     return out[sub.row_idx], rec, cache, sub
@@ -182,9 +191,39 @@ def expected_attention_flops(batch: W.Batch, shape) -> float:
 
 def isclose_report(name, got, ref, tol=TOL):
     e = normwise_err(got, ref)
-    log(f"{name}: normwise err {e:.3e} (bound {tol:g})")
+    log(f"{name}: normwise err {e:.3e} (bound {tol:g}), elementwise (rms floor) "
+        f"{elementwise_err(got, ref):.3e}")
     return e
 
 
+def pool_blocks_of_new_tokens(batch: W.Batch) -> np.ndarray:
+    """Physical blocks that hold the tokens a call appends (positions
+    prior_lens .. ctx_lens - 1 of each of its sequences)."""
+    out = set()
+    for s in range(batch.n_seqs):
+        p0, p1 = int(batch.prior_lens[s]), int(batch.ctx_lens[s])
+        if p1 > p0:
+            out.update(int(b) for b in batch.block_table[s, p0 // W.BLOCK_SIZE:
+                                                         (p1 - 1) // W.BLOCK_SIZE + 1])
+    return np.array(sorted(out), np.int64)
+
+
+class PoolSnapshot:
+    """Saved contents of chosen physical blocks of a layer's pools, to put the
+    cache back into its state before a call (so a later call that skipped or
+    misplaced its append cannot pass on the bytes an earlier call wrote)."""
+
+    def __init__(self, layer_t: dict, blocks: np.ndarray):
+        self.layer_t = layer_t
+        self.idx = torch.from_numpy(np.asarray(blocks, np.int64)).cuda()
+        self.saved = {k: layer_t[k][self.idx].clone() for k in ("k_cache", "v_cache")}
+
+    def restore(self):
+        for k, v in self.saved.items():
+            self.layer_t[k][self.idx] = v
+        torch.cuda.synchronize()
+
+
 __all__ = ["Replica", "oracle_weights", "oracle_cache", "oracle_decode_rows",
-           "oracle_prefill_seqs", "normwise_err", "to64", "TOL", "log", "math"]
+           "oracle_prefill_seqs", "normwise_err", "elementwise_err", "to64", "TOL", "log",
+           "math", "PoolSnapshot", "pool_blocks_of_new_tokens"]

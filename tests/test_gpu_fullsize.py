@@ -1,12 +1,14 @@
 """Full-size configurations, in the launch configuration bench.py times.
 
 The GPU runs the whole batch; the oracle recomputes sampled output rows one
-by one (decode rows are independent; prefill samples whole requests), and
-properties that hold at any size (split-batch bit identity) are checked on
-the whole batch. Weights of the largest layers reach the oracle as host
-copies of the tensors the counter-based generator produced on the GPU;
-test_generator_is_identical_on_cpu_and_gpu shows these are the bits the CPU
-generator gives.
+by one (decode rows are independent; prefill checks whole requests), and
+properties that hold at any size (split-batch bit identity of output rows and
+appended cache bytes) are checked on the whole batch, each split run starting
+from the cache state before the first run. Prior cache tokens reach the
+oracle regenerated on the CPU; weights of the largest layers as host copies
+of the tensors the counter-based generator produced on the GPU (the library
+only reads them; test_generator_is_identical_on_cpu_and_gpu shows these are
+the bits the CPU generator gives).
 """
 import numpy as np
 import pytest
@@ -14,8 +16,9 @@ import torch
 
 import oracle
 import workloads as W
-from harness import (TOL, Replica, gpu_cache_tokens, log, normwise_err, oracle_cache,
-                     oracle_decode_rows, oracle_prefill_seqs, oracle_weights, to64)
+from harness import (TOL, PoolSnapshot, Replica, elementwise_err, gpu_cache_tokens, log,
+                     normwise_err, oracle_cache, oracle_decode_rows, oracle_prefill_seqs,
+                     oracle_weights, pool_blocks_of_new_tokens, to64)
 from workloads import device as WD
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
@@ -37,8 +40,22 @@ def sample_rows(b: W.Batch, k: int, seed: int = 0):
 def check(name, got, ref, x):
     e = normwise_err(got, ref)
     ed = normwise_err(got - x, ref - x)
-    log(f"{name}: output err {e:.2e}, branch err {ed:.2e}")
+    log(f"{name}: output err {e:.2e}, branch err {ed:.2e}, elementwise (rms floor) "
+        f"{elementwise_err(got, ref):.2e}")
     assert e < TOL and ed < TOL, (name, e, ed)
+
+
+def _kv_new_tokens(layer_t, b: W.Batch, seqs):
+    out = []
+    for s in seqs:
+        K, V = gpu_cache_tokens(layer_t, b, s, int(b.prior_lens[s]), int(b.ctx_lens[s]))
+        out.append((K, V))
+    return out
+
+
+def _same_kv(a, b):
+    return all(np.array_equal(k1, k2) and np.array_equal(v1, v2)
+               for (k1, v1), (k2, v2) in zip(a, b))
 
 
 def test_generator_is_identical_on_cpu_and_gpu():
@@ -86,14 +103,18 @@ def test_llama8b_decode_300_rows_matches_oracle_and_splits():
     rep = Replica.for_batch(shape, wl.tag, 1, b)
     hidden = WD.hidden_tensor(shape, wl.tag, b.hidden_rows)
     h0 = to64(hidden)
+    snap = PoolSnapshot(rep.layers[0], pool_blocks_of_new_tokens(b))
     whole = hidden.clone()
     rep.forward(0, whole, WD.batch_tensors(b))
     torch.cuda.synchronize()
+    kv_whole = _kv_new_tokens(rep.layers[0], b, range(b.n_seqs))
+    snap.restore()
     split = hidden.clone()
     for part in (np.arange(0, 200), np.arange(200, 300)):
         rep.forward(0, split, WD.batch_tensors(b.select(part)))
     torch.cuda.synchronize()
     assert torch.equal(split.view(torch.int16), whole.view(torch.int16))
+    assert _same_kv(_kv_new_tokens(rep.layers[0], b, range(b.n_seqs)), kv_whole)
     rows = sorted(set(sample_rows(b, 3, seed=5)) | {130, 255, 256, 299})
     ref, _, _ = oracle_decode_rows(shape, wl.tag, 0, b, rows, h0, source="device",
                                    dev_layer=rep.layers[0])
@@ -112,14 +133,18 @@ def test_llama8b_decode_129_rows_across_gemm_row_limits():
     rep = Replica.for_batch(shape, wl.tag, 1, b)
     hidden = WD.hidden_tensor(shape, wl.tag, b.hidden_rows)
     h0 = to64(hidden)
+    snap = PoolSnapshot(rep.layers[0], pool_blocks_of_new_tokens(b))
     whole = hidden.clone()
     rep.forward(0, whole, WD.batch_tensors(b))
     torch.cuda.synchronize()
+    kv_whole = _kv_new_tokens(rep.layers[0], b, range(b.n_seqs))
+    snap.restore()
     split = hidden.clone()
     for part in (np.arange(0, 65), np.arange(65, 129)):
         rep.forward(0, split, WD.batch_tensors(b.select(part)))
     torch.cuda.synchronize()
     assert torch.equal(split.view(torch.int16), whole.view(torch.int16))
+    assert _same_kv(_kv_new_tokens(rep.layers[0], b, range(b.n_seqs)), kv_whole)
     rows = sorted(set(sample_rows(b, 2, seed=7)) | {0, 64, 128})
     ref, _, _ = oracle_decode_rows(shape, wl.tag, 0, b, rows, h0, source="device",
                                    dev_layer=rep.layers[0])
@@ -140,27 +165,23 @@ def test_qwen32b_decode_192_rows_row_split_gate_up():
     rep = Replica.for_batch(shape, tag, 1, b)
     hidden = WD.hidden_tensor(shape, tag, b.hidden_rows)
     h0 = to64(hidden)
+    snap = PoolSnapshot(rep.layers[0], pool_blocks_of_new_tokens(b))
     whole = hidden.clone()
     rep.forward(0, whole, WD.batch_tensors(b))
     torch.cuda.synchronize()
+    kv_whole = _kv_new_tokens(rep.layers[0], b, range(b.n_seqs))
+    snap.restore()
     halves = hidden.clone()
     for part in (np.arange(0, 96), np.arange(96, 192)):
         rep.forward(0, halves, WD.batch_tensors(b.select(part)))
     torch.cuda.synchronize()
     assert torch.equal(halves.view(torch.int16), whole.view(torch.int16))
+    assert _same_kv(_kv_new_tokens(rep.layers[0], b, range(b.n_seqs)), kv_whole)
     rows = sorted(set(sample_rows(b, 2, seed=9)) | {0, 191})
     ref, _, _ = oracle_decode_rows(shape, tag, 0, b, rows, h0, source="device",
                                    dev_layer=rep.layers[0])
     check("32B 192-row decode sampled rows", to64(whole)[b.row_idx[rows]], ref,
           h0[b.row_idx[rows]])
-
-
-def _kv_new_tokens(layer_t, b: W.Batch, seqs):
-    out = []
-    for s in seqs:
-        K, V = gpu_cache_tokens(layer_t, b, s, int(b.prior_lens[s]), int(b.ctx_lens[s]))
-        out.append((K, V))
-    return out
 
 
 def test_c3_skewed_split_is_bit_identical_and_matches_oracle():
@@ -172,15 +193,9 @@ def test_c3_skewed_split_is_bit_identical_and_matches_oracle():
     rep = Replica.for_batch(shape, wl.tag, 1, full, max_rows=full.n_rows, max_seqs=full.n_seqs)
     hidden = WD.hidden_tensor(shape, wl.tag, full.hidden_rows)
     h0 = to64(hidden)
-    # Blocks holding the new tokens of the 96 requests, to restore between runs.
-    new_blocks = np.unique([sub.block_table[s, int(sub.prior_lens[s]) // 16]
-                            for s in range(sub.n_seqs)])
-    idx = torch.from_numpy(new_blocks.astype(np.int64)).cuda()
-    saved = {k: rep.layers[0][k][idx].clone() for k in ("k_cache", "v_cache")}
-
-    def restore():
-        for k in saved:
-            rep.layers[0][k][idx] = saved[k]
+    # Blocks holding the new tokens of all 256 requests, restored between runs.
+    snap = PoolSnapshot(rep.layers[0], pool_blocks_of_new_tokens(full))
+    restore = snap.restore
 
     whole = hidden.clone()
     rep.forward(0, whole, WD.batch_tensors(full))
@@ -214,56 +229,78 @@ def test_c3_skewed_split_is_bit_identical_and_matches_oracle():
 
 
 def test_c4_qwen32b_prefill_then_decode():
+    """The 32B chunked prefill (4 x 512 tokens after {0, 512, 1024, 4096}
+    cached), then the batch-128 decode on the same cache.
+      * prefill: a request-aligned split, run from the cache state before the
+        whole batch, gives the whole batch's output rows and appended cache
+        bytes; every request's rows and appended keys/values against the
+        oracle;
+      * decode: two 64-row halves, run from the cache state before the whole
+        batch, give its bits; the four prefilled requests (keys from the
+        oracle's own prefill) and sampled decode-only requests against the
+        oracle."""
     wl = W.c4_qwen32b()
     pre, dec, shape = wl.batch, wl.decode_after, wl.shape
     rep = Replica.for_batch(shape, wl.tag, 1, pre, max_rows=pre.n_rows, max_seqs=dec.n_seqs)
     w64 = oracle_weights(shape, wl.tag, 0, "device", rep.layers[0])
     hidden = WD.hidden_tensor(shape, wl.tag, pre.hidden_rows)
     h0 = to64(hidden)
-    # Request-aligned split first (fresh cache state is not needed: the
-    # prefill rewrites the same slots with the same values).
-    split = hidden.clone()
-    for seqs in ([2, 0], [3, 1]):
-        rep.forward(0, split, WD.batch_tensors(pre.select_seqs(seqs)))
+    lay = rep.layers[0]
+    snap = PoolSnapshot(lay, pool_blocks_of_new_tokens(pre))
     whole = hidden.clone()
     rep.forward(0, whole, WD.batch_tensors(pre))
     torch.cuda.synchronize()
+    kv_whole = _kv_new_tokens(lay, pre, range(pre.n_seqs))
+    snap.restore()
+    split = hidden.clone()
+    for seqs in ([2, 0], [3, 1]):
+        rep.forward(0, split, WD.batch_tensors(pre.select_seqs(seqs)))
+    torch.cuda.synchronize()
     assert torch.equal(split.view(torch.int16), whole.view(torch.int16))
-    # Oracle on request 1 (512 new tokens after 512 cached).
-    ref, _, cache, sub = oracle_prefill_seqs(shape, wl.tag, 0, pre, [1], h0, source="device",
-                                             dev_layer=rep.layers[0], w64=w64)
-    rows = sub.row_idx.astype(np.int64)
-    check("c4 prefill request 1", to64(whole)[rows], ref, h0[rows])
-    # Request 0 (no cached context): its keys/values feed the decode check.
-    ref0, _, cache0, sub0 = oracle_prefill_seqs(shape, wl.tag, 0, pre, [0], h0, source="device",
-                                                dev_layer=rep.layers[0], w64=w64)
-    rows0 = sub0.row_idx.astype(np.int64)
-    check("c4 prefill request 0", to64(whole)[rows0], ref0, h0[rows0])
+    assert _same_kv(_kv_new_tokens(lay, pre, range(pre.n_seqs)), kv_whole)
+    got = to64(whole)
+    caches = []
+    for s in range(pre.n_seqs):
+        ref, _, cache, sub = oracle_prefill_seqs(shape, wl.tag, 0, pre, [s], h0, w64=w64)
+        rows = sub.row_idx.astype(np.int64)
+        check(f"c4 prefill request {s} (prior {int(pre.prior_lens[s])})", got[rows], ref, h0[rows])
+        t0, t1 = int(pre.prior_lens[s]), int(pre.ctx_lens[s])
+        K, V = kv_whole[s]
+        assert normwise_err(K, cache.K[0][t0:t1]) < TOL and normwise_err(V, cache.V[0][t0:t1]) < TOL
+        caches.append(cache)
+        log(f"c4 prefill request {s}: appended keys/values match the oracle")
 
-    # Batch-128 decode on the same cache: request 0 (keys from the prefill)
-    # and sampled decode-only requests.
+    # Batch-128 decode on the same cache.
     dh = WD.hidden_tensor(shape, wl.tag + "dec", dec.hidden_rows)
     d0 = to64(dh)
-    halves = dh.clone()
+    dsnap = PoolSnapshot(lay, pool_blocks_of_new_tokens(dec))
     rep.forward(0, dh, WD.batch_tensors(dec))
+    torch.cuda.synchronize()
+    kv_dec = _kv_new_tokens(lay, dec, range(dec.n_seqs))
+    dsnap.restore()
     # Two 64-row halves (the 64-row GEMM kernels) give the bits of the whole
     # batch (the 8-wave gate/up plan's 128-row pass of the row-split kernel).
+    halves = WD.hidden_tensor(shape, wl.tag + "dec", dec.hidden_rows)
     for part in (np.arange(0, 64), np.arange(64, 128)):
         rep.forward(0, halves, WD.batch_tensors(dec.select(part)))
     torch.cuda.synchronize()
     assert torch.equal(halves.view(torch.int16), dh.view(torch.int16))
+    assert _same_kv(_kv_new_tokens(lay, dec, range(dec.n_seqs)), kv_dec)
     got = to64(dh)
-    sample = [0] + sample_rows(dec.select(range(4, 128)), 3, seed=4)
-    sample = [0] + [s + 4 for s in sample[1:]]
+    sample = [0, 1, 2, 3] + [s + 4 for s in sample_rows(dec.select(range(4, 128)), 3, seed=4)]
     for r in sample:
         sb = dec.select([r])
-        if r == 0:
-            K = np.zeros((int(sb.ctx_lens[0]), shape.n_kv_heads, shape.head_dim))
+        if r < pre.n_seqs:
+            # Prefilled request: its keys/values up to the prefill's end from the
+            # oracle's own prefill of it.
+            ctx = int(sb.ctx_lens[0])
+            K = np.zeros((ctx, shape.n_kv_heads, shape.head_dim))
             V = np.zeros_like(K)
-            K[:512], V[:512] = cache0.K[0][:512], cache0.V[0][:512]
+            n = int(pre.ctx_lens[r])
+            K[:n], V[:n] = caches[r].K[0][:n], caches[r].V[0][:n]
             c = oracle.KVCache([K], [V])
         else:
-            c = oracle_cache(shape, wl.tag, 0, sb, [0], dec.num_blocks, "cpu")
+            c = oracle_cache(shape, wl.tag, 0, sb, [0], dec.num_blocks)
         out, _ = oracle.layer_forward(w64, shape, d0, sb.row_idx, sb.positions, None,
                                       sb.ctx_lens, c)
         check(f"c4 decode row {r}", got[sb.row_idx], out[sb.row_idx], d0[sb.row_idx])
@@ -282,8 +319,7 @@ def test_c5_llama70b_span8_sampled_rows():
     x = h0.copy()
     for l in range(wl.n_layers):
         w64 = oracle_weights(shape, wl.tag, l, "device", rep.layers[l])
-        c = oracle_cache(shape, wl.tag, l, sub, range(sub.n_seqs), b.num_blocks, "device",
-                         rep.layers[l])
+        c = oracle_cache(shape, wl.tag, l, sub, range(sub.n_seqs), b.num_blocks)
         x, _ = oracle.layer_forward(w64, shape, x, sub.row_idx, sub.positions, None,
                                     sub.ctx_lens, c)
         del w64

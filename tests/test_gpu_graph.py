@@ -12,7 +12,8 @@ import pytest
 import torch
 
 import workloads as W
-from harness import Replica, log, ragged_decode_batch, ragged_prefill_batch, small_bf16_shape
+from harness import (PoolSnapshot, Replica, log, pool_blocks_of_new_tokens, ragged_decode_batch,
+                     ragged_prefill_batch, small_bf16_shape)
 from workloads import device as WD
 
 pytestmark = pytest.mark.gpu
@@ -44,11 +45,18 @@ def _capture(fn):
     return g
 
 
-def _replay_and_check(g, static_hidden, hidden, ref, rep, ref_pools, eager_noise):
+def _restore(rep, pools):
+    for t, p in zip(rep.layers, pools):
+        for k in p:
+            t[k].copy_(p[k])
+
+
+def _replay_and_check(g, static_hidden, hidden, ref, rep, ref_pools, eager_noise, init_pools):
     for r in range(REPLAYS):
         static_hidden.copy_(hidden)   # eager input reset between replays
         eager_noise()                 # unrelated eager work on the same buffers' device
-        torch.cuda.synchronize()
+        _restore(rep, init_pools)     # the cache as before the eager run: every
+        torch.cuda.synchronize()      # appended byte must come from the replay
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(static_hidden.view(torch.int16), ref.view(torch.int16)), r
@@ -64,6 +72,7 @@ def test_graph_replay_of_decode_span_is_bit_identical():
     rep = Replica.for_batch(shape, "g1", L, b)
     bt = WD.batch_tensors(b)
     hidden = WD.hidden_tensor(shape, "g1", b.hidden_rows)
+    init_pools = _pools(rep)
 
     ref = hidden.clone()
     rep.span(0, L, ref, bt)
@@ -78,7 +87,7 @@ def test_graph_replay_of_decode_span_is_bit_identical():
         scratch.normal_()
         torch.mm(scratch[:4096].view(64, 64), scratch[4096:8192].view(64, 64))
 
-    _replay_and_check(g, static_hidden, hidden, ref, rep, ref_pools, noise)
+    _replay_and_check(g, static_hidden, hidden, ref, rep, ref_pools, noise, init_pools)
 
 
 def test_graph_replay_of_prefill_is_bit_identical():
@@ -88,6 +97,7 @@ def test_graph_replay_of_prefill_is_bit_identical():
     rep = Replica.for_batch(shape, "g2", 1, b)
     bt = WD.batch_tensors(b)
     hidden = WD.hidden_tensor(shape, "g2", b.hidden_rows)
+    init_pools = _pools(rep)
 
     ref = hidden.clone()
     rep.forward(0, ref, bt)
@@ -102,7 +112,7 @@ def test_graph_replay_of_prefill_is_bit_identical():
         other.copy_(hidden)
         rep.forward(0, other, bt)
 
-    _replay_and_check(g, static_hidden, hidden, ref, rep, ref_pools, noise)
+    _replay_and_check(g, static_hidden, hidden, ref, rep, ref_pools, noise, init_pools)
 
 
 @pytest.mark.slow
@@ -114,19 +124,20 @@ def test_graph_replay_of_llama8b_decode_step_is_bit_identical():
     bt = WD.batch_tensors(b)
     hidden = WD.hidden_tensor(shape, wl.tag, b.hidden_rows)
 
+    # Only the new tokens' blocks change; compare those, and put them back
+    # into their state before the eager run ahead of every replay.
+    snap = PoolSnapshot(rep.layers[0], pool_blocks_of_new_tokens(b))
+    idx = snap.idx
     ref = hidden.clone()
     rep.forward(0, ref, bt)
     torch.cuda.synchronize()
-    # Only the new tokens' blocks change; compare those.
-    new_blocks = np.unique([b.block_table[s, int(b.positions[s]) // 16] for s in range(b.n_seqs)])
-    idx = torch.from_numpy(new_blocks.astype(np.int64)).cuda()
     ref_kv = [rep.layers[0][k][idx].clone() for k in ("k_cache", "v_cache")]
 
     static_hidden = hidden.clone()
     g = _capture(lambda: rep.forward(0, static_hidden, bt))
     for r in range(REPLAYS):
         static_hidden.copy_(hidden)
-        torch.cuda.synchronize()
+        snap.restore()
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(static_hidden.view(torch.int16), ref.view(torch.int16)), r

@@ -11,8 +11,9 @@ import torch
 
 import paper_2607_04181_amd as coco
 import workloads as W
-from harness import (TOL, Replica, gpu_cache_tokens, log, normwise_err, oracle_decode_rows,
-                     oracle_prefill_seqs, ragged_decode_batch, ragged_prefill_batch,
+from harness import (TOL, PoolSnapshot, Replica, elementwise_err, gpu_cache_tokens, log,
+                     normwise_err, oracle_decode_rows, oracle_prefill_seqs,
+                     pool_blocks_of_new_tokens, ragged_decode_batch, ragged_prefill_batch,
                      small_bf16_shape, to64)
 from workloads import device as WD
 
@@ -37,7 +38,8 @@ def _small_decode(seed=0, shape=None, priors=DECODE_PRIORS, hidden_rows=24):
 def _check_rows(name, got, ref, x):
     e = normwise_err(got, ref)
     ed = normwise_err(got - x, ref - x)
-    log(f"{name}: output err {e:.2e}, branch err {ed:.2e}")
+    log(f"{name}: output err {e:.2e}, branch err {ed:.2e}, elementwise (rms floor) "
+        f"{elementwise_err(got, ref):.2e}")
     assert e < TOL, f"{name}: output error {e} exceeds {TOL}"
     assert ed < DELTA_TOL, f"{name}: branch error {ed} exceeds {DELTA_TOL}"
 
@@ -132,17 +134,21 @@ def _kv_snapshot(rep, b):
 
 def test_decode_split_batch_is_bit_identical():
     """Any partition of a decode batch into replica shares gives the same
-    output rows and cache bytes as the whole batch (uneven shares too)."""
+    output rows and cache bytes as the whole batch (uneven shares too). Each
+    partition runs from the cache state before the whole batch, so a share
+    that skipped or misplaced its append would read the old slot and fail."""
     shape, b = _small_decode(3)
     bt = WD.batch_tensors(b)
     rep = Replica.for_batch(shape, "s3", 1, b)
     hidden = WD.hidden_tensor(shape, "s3", b.hidden_rows)
+    snap = PoolSnapshot(rep.layers[0], pool_blocks_of_new_tokens(b))
     whole = hidden.clone()
     rep.forward(0, whole, bt)
     torch.cuda.synchronize()
     kv_whole = _kv_snapshot(rep, b)
     for parts in (W.even_partition(b.n_rows, 2), W.even_partition(b.n_rows, 5),
                   [np.array([i]) for i in range(b.n_rows)]):
+        snap.restore()
         split = hidden.clone()
         for p in parts:
             sub = b.select(p)
@@ -167,33 +173,46 @@ def test_decode_of_many_sequences_matches_oracle_and_splits():
     rep = Replica.for_batch(shape, "s9", 1, b)
     hidden = WD.hidden_tensor(shape, "s9", b.hidden_rows)
     h0 = to64(hidden)
+    snap = PoolSnapshot(rep.layers[0], pool_blocks_of_new_tokens(b))
     whole = hidden.clone()
     rep.forward(0, whole, WD.batch_tensors(b))
     torch.cuda.synchronize()
+    kv_whole = _kv_snapshot(rep, b)
     rows = [0, 5, 63, 64, 130, 255, 256, 257, 270, 299]
     ref, _, _ = oracle_decode_rows(shape, "s9", 0, b, rows, h0)
     got = to64(whole)[b.row_idx[rows]]
     _check_rows("300-sequence decode", got, ref, h0[b.row_idx[rows]])
+    snap.restore()
     split = hidden.clone()
     for part in (np.arange(0, 97), np.arange(97, 300)):
         rep.forward(0, split, WD.batch_tensors(b.select(part)))
     torch.cuda.synchronize()
     assert torch.equal(split.view(torch.int16), whole.view(torch.int16))
+    for (k1, v1), (k2, v2) in zip(_kv_snapshot(rep, b), kv_whole):
+        assert np.array_equal(k1, k2) and np.array_equal(v1, v2)
 
 
 def test_prefill_request_aligned_split_is_bit_identical():
+    """Request-aligned shares of a prefill batch, run from the cache state
+    before the whole batch, give its output rows and appended cache bytes."""
     shape = small_bf16_shape()
     b = ragged_prefill_batch(4, priors=[0, 5, 30, 200], lens=[70, 1, 33, 64], max_ctx=512,
                              hidden_rows=200)
     rep = Replica.for_batch(shape, "s4", 1, b)
     hidden = WD.hidden_tensor(shape, "s4", b.hidden_rows)
+    snap = PoolSnapshot(rep.layers[0], pool_blocks_of_new_tokens(b))
     whole = hidden.clone()
     rep.forward(0, whole, WD.batch_tensors(b))
+    torch.cuda.synchronize()
+    kv_whole = _kv_snapshot(rep, b)
+    snap.restore()
     split = hidden.clone()
     for seqs in ([2, 0], [3], [1]):
         rep.forward(0, split, WD.batch_tensors(b.select_seqs(seqs)))
     torch.cuda.synchronize()
     assert torch.equal(split.view(torch.int16), whole.view(torch.int16))
+    for (k1, v1), (k2, v2) in zip(_kv_snapshot(rep, b), kv_whole):
+        assert np.array_equal(k1, k2) and np.array_equal(v1, v2)
 
 
 def test_zero_output_projections_give_identity_bit_exactly():
@@ -306,8 +325,8 @@ def test_prefill_with_an_odd_head_count_matches_oracle():
 
 def test_prefill_at_high_positions_matches_oracle():
     """A chunk at positions near 30,000: far rows of the prefill RoPE table and
-    the cache slots of a long sequence, against the oracle (prior cache bits
-    read from the device pools, which the generator test pins to the CPU ones)."""
+    the cache slots of a long sequence, against the oracle (its 30,000 prior
+    tokens regenerated on the CPU)."""
     shape = small_bf16_shape()
     b = ragged_prefill_batch(14, priors=[30000, 5], lens=[40, 20], max_ctx=32768,
                              hidden_rows=80)
@@ -316,8 +335,7 @@ def test_prefill_at_high_positions_matches_oracle():
     h0 = to64(hidden)
     rep.forward(0, hidden, WD.batch_tensors(b))
     torch.cuda.synchronize()
-    ref, _, cache, _ = oracle_prefill_seqs(shape, "s12", 0, b, range(b.n_seqs), h0,
-                                           source="device", dev_layer=rep.layers[0])
+    ref, _, cache, _ = oracle_prefill_seqs(shape, "s12", 0, b, range(b.n_seqs), h0)
     _check_rows("high-position prefill", to64(hidden)[b.row_idx], ref, h0[b.row_idx])
     for s in range(b.n_seqs):
         t0, t1 = int(b.prior_lens[s]), int(b.ctx_lens[s])
@@ -441,13 +459,45 @@ def test_one_token_prefill_chunks_match_oracle_and_split():
     rep = Replica.for_batch(shape, "s9", 1, p)
     hidden = WD.hidden_tensor(shape, "s9", p.hidden_rows)
     h0 = to64(hidden)
+    snap = PoolSnapshot(rep.layers[0], pool_blocks_of_new_tokens(p))
     whole = hidden.clone()
     rep.forward(0, whole, WD.batch_tensors(p))
     torch.cuda.synchronize()
     ref, _, _, _ = oracle_prefill_seqs(shape, "s9", 0, p, range(p.n_seqs), h0)
     _check_rows("one-token prefill", to64(whole)[p.row_idx], ref, h0[p.row_idx])
+    snap.restore()
     alone = hidden.clone()
     rep.forward(0, alone, WD.batch_tensors(p.select_seqs([1])))
     torch.cuda.synchronize()
     r = int(p.row_idx[1])
     assert torch.equal(alone[r].view(torch.int16), whole[r].view(torch.int16))
+
+
+def test_decode_row_before_the_cached_end_attends_up_to_its_position():
+    """A decode row whose position lies before its sequence's cached end
+    (positions[i] < ctx_lens[i] - 1, e.g. a rewound request) rewrites the slot
+    of its position and attends keys 0 .. position only: the cached tokens past
+    it are not read. Lengths cross block and 256-token partition edges (600
+    cached, attending 301 keys; 256 cached, attending 256), a row at position 0
+    attends only itself. Against the oracle, which takes
+    min(ctx_lens, position + 1) keys."""
+    shape = small_bf16_shape()
+    priors = np.array([600, 256, 17, 1000, 40, 300], np.int64)
+    back = np.array([300, 1, 17, 0, 24, 44], np.int64)   # position = prior - back
+    base = ragged_decode_batch(21, priors, max_ctx=1025, hidden_rows=10,
+                               row_idx=np.random.default_rng(21).permutation(10)[:6])
+    b = W.Batch(base.hidden_rows, base.row_idx, (priors - back).astype(np.int32), None,
+                base.prior_lens, base.ctx_lens, base.block_table, base.num_blocks)
+    assert int(np.sum(b.positions < b.ctx_lens - 1)) == 5
+    rep = Replica.for_batch(shape, "s21", 1, b)
+    coco.coco_layer_set_validate(rep.h, True)  # the rows are valid input
+    hidden = WD.hidden_tensor(shape, "s21", b.hidden_rows)
+    h0 = to64(hidden)
+    rep.forward(0, hidden, WD.batch_tensors(b))
+    torch.cuda.synchronize()
+    ref, _, cache = oracle_decode_rows(shape, "s21", 0, b, range(b.n_rows), h0)
+    _check_rows("decode before the cached end", to64(hidden)[b.row_idx], ref, h0[b.row_idx])
+    for s in range(b.n_seqs):
+        p = int(b.positions[s])
+        K, V = gpu_cache_tokens(rep.layers[0], b, s, p, p + 1)
+        assert normwise_err(K[0], cache.K[s][p]) < TOL and normwise_err(V[0], cache.V[s][p]) < TOL
