@@ -189,6 +189,30 @@ int coco_layer_span_forward(coco_layer_t h, int32_t first_layer, int32_t n_layer
                             const int32_t* block_table, const int32_t* ctx_lens,
                             coco_stream_t stream);
 
+/* For callers that cannot allocate device memory at call time (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same call as coco_layer_forward, with the same results bit for bit, but
+ * its per-call buffers (activations, split-K partials, decode attention
+ * partials and work list) come from a static array of 64 MiB that every GPU
+ * the library runs on holds from module load until the process ends, sized
+ * for this call's rows instead of the handle's max_rows. The call itself
+ * allocates nothing, host or device. Its address is looked up once per
+ * device by coco_layer_init. Returns COCO_EINVAL, before anything is
+ * enqueued, when the call's buffers exceed 64 MiB (a batch-64 decode of the
+ * 8B-shaped layer with 8k-token block tables takes about 49 MB; a
+ * 2048-token prefill of the 32B-shaped layer does not fit). All such calls
+ * on one GPU share the
+ * array, whatever their handle: calls that overlap on one GPU (other
+ * streams, other threads, other handles) race on it. The array keeps the
+ * last call's contents; no part of it needs to start at zero. Validation
+ * mode is not run by this entry point, and coco_layer_workspace shows the
+ * handle's own workspace, not this array. */
+int coco_layer_forward_noalloc(coco_layer_t h, int32_t layer, void* hidden, int64_t hidden_rows,
+                               const int32_t* row_idx, int32_t n_rows, const int32_t* positions,
+                               const int32_t* seq_starts, int32_t n_seqs,
+                               const int32_t* block_table, const int32_t* ctx_lens,
+                               coco_stream_t stream);
+
 /* Copy an intermediate buffer of the last call into `dst` (device memory of
  * at least dst_bytes bytes), for inspection by tests. which = COCO_WS_*;
  * row i holds call row i of the last layer run. Copies min(dst_bytes, buffer

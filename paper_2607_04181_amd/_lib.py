@@ -22,7 +22,8 @@ COCO_WS_X, COCO_WS_H, COCO_WS_Q, COCO_WS_O, COCO_WS_X1, COCO_WS_H2, COCO_WS_U = 
 
 EXPORTS = ["coco_layer_init", "coco_layer_destroy", "coco_last_error", "coco_version",
            "coco_layer_set_validate", "coco_kv_append", "coco_layer_forward",
-           "coco_layer_span_forward", "coco_layer_workspace", "coco_layer_set_timing",
+           "coco_layer_span_forward", "coco_layer_forward_noalloc", "coco_layer_workspace",
+           "coco_layer_set_timing",
            "coco_layer_read_timing", "coco_probe_read", "coco_probe_mfma_bf16",
            # include/coco_scaling.h: host arithmetic of the speedup/cost model
            "coco_split_batch", "coco_comm_time", "coco_speedup", "coco_cost_mem",
@@ -80,6 +81,8 @@ def _load():
                                               vp]),
         "coco_layer_span_forward": (ctypes.c_int, [vp, i32, i32, vp, i64, vp, i32, vp, vp, i32,
                                                    vp, vp, vp]),
+        "coco_layer_forward_noalloc": (ctypes.c_int, [vp, i32, vp, i64, vp, i32, vp, vp, i32,
+                                                      vp, vp, vp]),
         "coco_layer_workspace": (ctypes.c_int, [vp, i32, vp, i64, vp]),
         "coco_layer_set_timing": (ctypes.c_int, [vp, i32]),
         "coco_layer_read_timing": (ctypes.c_int, [vp, ctypes.POINTER(ctypes.c_double),
@@ -258,6 +261,18 @@ def coco_layer_forward(h: Handle, layer: int, hidden, row_idx, positions, seq_st
     _check_batch(h, hidden, row_idx, positions, seq_starts, block_table, ctx_lens)
     n_seqs = int(ctx_lens.numel())
     _check(_lib.coco_layer_forward(
+        h.raw, layer, _ptr(hidden, what="hidden"), int(hidden.shape[0]),
+        _ptr(row_idx, i32, "row_idx"), int(row_idx.numel()), _ptr(positions, i32, "positions"),
+        _ptr(seq_starts, i32, "seq_starts"), n_seqs, _ptr(block_table, i32, "block_table"),
+        _ptr(ctx_lens, i32, "ctx_lens"), _stream(stream)))
+
+
+def coco_layer_forward_noalloc(h: Handle, layer: int, hidden, row_idx, positions, seq_starts,
+                               block_table, ctx_lens, stream=None):
+    i32 = torch.int32
+    _check_batch(h, hidden, row_idx, positions, seq_starts, block_table, ctx_lens)
+    n_seqs = int(ctx_lens.numel())
+    _check(_lib.coco_layer_forward_noalloc(
         h.raw, layer, _ptr(hidden, what="hidden"), int(hidden.shape[0]),
         _ptr(row_idx, i32, "row_idx"), int(row_idx.numel()), _ptr(positions, i32, "positions"),
         _ptr(seq_starts, i32, "seq_starts"), n_seqs, _ptr(block_table, i32, "block_table"),

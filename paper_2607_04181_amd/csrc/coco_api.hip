@@ -5,7 +5,7 @@
 #include <stdio.h>
 #include <type_traits>
 
-#include <string>
+#include <mutex>
 #include <vector>
 
 #include "../../include/coco.h"
@@ -16,15 +16,15 @@ using namespace coco;
 
 namespace {
 
-thread_local std::string g_err;
+// Message of the last failure on this thread (a fixed buffer: reporting an
+// error allocates nothing).
+thread_local char g_err[512];
 
 int fail(int code, const char* fmt, ...) {
-  char buf[512];
   va_list ap;
   va_start(ap, fmt);
-  vsnprintf(buf, sizeof buf, fmt, ap);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
   va_end(ap);
-  g_err = buf;
   return code;
 }
 
@@ -36,6 +36,19 @@ int fail(int code, const char* fmt, ...) {
 
 }  // namespace
 
+// Per-call buffers of the launch sequence, carved out of one region (the
+// handle's workspace, or the static scratch array of the no-alloc entry
+// point).
+struct Work {
+  void *x = nullptr, *h = nullptr, *q = nullptr, *o = nullptr, *h2 = nullptr, *u = nullptr;
+  float *x1 = nullptr, *part = nullptr, *attn_o = nullptr, *attn_ml = nullptr;
+  // Row sums of squares: per K-slice (decode QKV with RMSNorm_1 folded in) or
+  // per 256-column tile (prefill O projection with RMSNorm_2 folded in).
+  float* ss = nullptr;
+  int32_t* split_off = nullptr;  // decode attention work list offsets
+  int32_t* row_info = nullptr;   // prefill row slots [rows][2] (position, cache block)
+};
+
 struct coco_layer {
   coco_layer_config cfg;
   std::vector<coco_layer_weights> layers;
@@ -44,17 +57,10 @@ struct coco_layer {
   bool validate = false;
   char* ws = nullptr;
   size_t ws_bytes = 0;
-  // workspace carve-out
-  void *x = nullptr, *h = nullptr, *q = nullptr, *o = nullptr, *h2 = nullptr, *u = nullptr;
-  float *x1 = nullptr, *part = nullptr, *attn_o = nullptr, *attn_ml = nullptr;
-  // Row sums of squares: per K-slice (decode QKV with RMSNorm_1 folded in) or
-  // per 256-column tile (prefill O projection with RMSNorm_2 folded in).
-  float* ss = nullptr;
+  Work w;  // the workspace's per-call buffers, sized for max_rows
   double* inv_freq = nullptr;
   float* rope = nullptr;  // RoPE table [rope_rows][head_dim / 2] (cos, sin)
   int rope_rows = 0;      // positions the configuration admits
-  int32_t* row_info = nullptr;  // prefill row slots [max_rows][2] (position, cache block)
-  int32_t* split_off = nullptr;  // decode attention work list offsets
   size_t act_rows_bytes[7] = {};
   int max_splits = 0;
   int dec_rows = 0;
@@ -124,6 +130,61 @@ int gemm_splits(const coco_layer_config& c, int N, int K) {
   return a > b ? a : b;
 }
 
+// Lays out the per-call buffers for `rows` call rows and `dec_seqs` decode
+// sequences from `base`, each piece 256-byte aligned, and returns the bytes
+// they take (base == nullptr: sizes only; `w` may then be null).
+size_t carve_work(const coco_layer_config& c, int64_t rows, int64_t dec_seqs, int max_splits,
+                  char* base, Work* w) {
+  const int eb = elem_bytes(c.dtype);
+  const int64_t R = rows, d = c.d_model, F = c.d_ffn;
+  const int64_t qd = (int64_t)c.n_q_heads * c.head_dim;
+  const int64_t nqkv = (int64_t)(c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
+  int64_t part_elems = 0;
+  const int64_t shapes[4][2] = {{nqkv, d}, {d, qd}, {2 * F, d}, {d, F}};
+  for (auto& sh : shapes) {
+    const int64_t e = (int64_t)gemm_splits(c, (int)sh[0], (int)sh[1]) * R * sh[0];
+    if (e > part_elems) part_elems = e;
+  }
+  const bool bf = c.dtype == COCO_BF16;
+  const size_t sizes[13] = {
+      align256(R * d * eb),    // x
+      align256(R * d * eb),    // h
+      align256(R * qd * eb),   // q
+      align256(R * qd * eb),   // o
+      align256(R * d * eb),    // h2
+      align256(R * F * eb),    // u
+      align256(R * d * 4),     // x1
+      align256(part_elems * 4),  // part
+      bf ? align256((size_t)dec_seqs * c.n_q_heads * max_splits * 128 * 4) : 0,  // attn_o
+      bf ? align256((size_t)dec_seqs * c.n_q_heads * max_splits * 2 * 4) : 0,    // attn_ml
+      align256((size_t)(dec_seqs + 1) * 4),  // split_off
+      // ss: per-slice row sums of squares (decode QKV, at most 16 K-slices)
+      // or per-256-column-tile ones (prefill O projection)
+      align256((size_t)(c.d_model / 256 > 16 ? c.d_model / 256 : 16) * R * 4),
+      align256(R * 8)};  // row_info
+  size_t off[13], total = 0;
+  for (int i = 0; i < 13; ++i) {
+    off[i] = total;
+    total += sizes[i];
+  }
+  if (base && w) {
+    w->x = base + off[0];
+    w->h = base + off[1];
+    w->q = base + off[2];
+    w->o = base + off[3];
+    w->h2 = base + off[4];
+    w->u = base + off[5];
+    w->x1 = (float*)(base + off[6]);
+    w->part = (float*)(base + off[7]);
+    w->attn_o = (float*)(base + off[8]);
+    w->attn_ml = (float*)(base + off[9]);
+    w->split_off = (int32_t*)(base + off[10]);
+    w->ss = (float*)(base + off[11]);
+    w->row_info = (int32_t*)(base + off[12]);
+  }
+  return total;
+}
+
 int check_config(const coco_layer_config* c) {
   if (!c) return fail(COCO_EINVAL, "config is NULL");
   if (c->d_model <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->head_dim <= 0 ||
@@ -163,9 +224,52 @@ int check_config(const coco_layer_config* c) {
 
 }  // namespace
 
+// ----------------------------------------------------------------------------
+// Static scratch of the no-alloc entry point (coco_layer_forward_noalloc).
+// Every GPU the library runs on holds its own copy of this array from module
+// load until the process ends. In host code `scratch` names a host-side
+// stand-in, not a device address: the device address of the current device's
+// copy comes from hipGetSymbolAddress, taken once per device in
+// coco_layer_init and kept in g_scratch; only that address is ever passed to
+// kernels.
+// ----------------------------------------------------------------------------
+namespace {
+
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch[kMaxDevices] = {};
+
+// With `dev` current: look up and keep this device's scratch address.
+int scratch_setup(int dev) {
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(COCO_EINVAL, "device %d beyond the %d the library tracks", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch[dev] != nullptr) return COCO_OK;
+  void* p = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  if (e != hipSuccess || p == nullptr) {
+    (void)hipGetLastError();
+    return fail(COCO_EHIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                hipGetErrorString(e));
+  }
+  g_scratch[dev] = (char*)p;
+  return COCO_OK;
+}
+
+char* scratch_ptr(int dev) {
+  if (dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  return g_scratch[dev];
+}
+
+}  // namespace
+
 extern "C" {
 
-const char* coco_last_error(void) { return g_err.c_str(); }
+const char* coco_last_error(void) { return g_err; }
 
 int coco_version(void) { return 100; }
 
@@ -195,6 +299,7 @@ int coco_layer_init(const coco_layer_config* cfg, const coco_layer_weights* laye
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
       cus <= 0)
     return fail(COCO_EHIP, "cannot query the current device");
+  if ((rc = scratch_setup(dev))) return rc;
   coco_layer* H = new coco_layer();
   H->cfg = c;
   H->layers.assign(layers, layers + c.n_layers);
@@ -204,63 +309,26 @@ int coco_layer_init(const coco_layer_config* cfg, const coco_layer_weights* laye
   const int eb = elem_bytes(c.dtype);
   const int64_t R = c.max_rows, d = c.d_model, F = c.d_ffn;
   const int64_t qd = (int64_t)c.n_q_heads * c.head_dim;
-  const int64_t nqkv = (int64_t)(c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
-  int64_t part_elems = 0;
-  const int64_t shapes[4][2] = {{nqkv, d}, {d, qd}, {2 * F, d}, {d, F}};
-  for (auto& s : shapes) {
-    const int64_t e = (int64_t)gemm_splits(c, (int)s[0], (int)s[1]) * R * s[0];
-    if (e > part_elems) part_elems = e;
-  }
   H->max_splits = decode_max_splits(c.max_blocks_per_seq);
   H->dec_rows = c.max_rows < c.max_seqs ? c.max_rows : c.max_seqs;
 
-  // RoPE table for the fused prefill QKV epilogue (bf16 only).
+  // Per-call buffers for max_rows rows, then the handle's constants: RoPE
+  // inverse frequencies and (bf16) the RoPE table of the fused prefill QKV
+  // epilogue.
   H->rope_rows = c.dtype == COCO_BF16 ? c.max_blocks_per_seq * kBlockTokens : 0;
-  size_t off = 0;
-  size_t offs[15];
-  const size_t sizes[15] = {
-      align256(R * d * eb),          // x
-      align256(R * d * eb),          // h
-      align256(R * qd * eb),         // q
-      align256(R * qd * eb),         // o
-      align256(R * d * eb),          // h2
-      align256(R * F * eb),          // u
-      align256(R * d * 4),           // x1
-      align256(part_elems * 4),      // part
-      c.dtype == COCO_BF16 ? align256((size_t)H->dec_rows * c.n_q_heads * H->max_splits * 128 * 4) : 0,
-      c.dtype == COCO_BF16 ? align256((size_t)H->dec_rows * c.n_q_heads * H->max_splits * 2 * 4) : 0,
-      align256((size_t)(c.head_dim / 2) * 8),  // inv_freq
-      align256((size_t)(H->dec_rows + 1) * 4),  // split_off
-      // ss: per-slice row sums of squares (decode QKV, at most 16 K-slices)
-      // or per-256-column-tile ones (prefill O projection)
-      align256((size_t)(c.d_model / 256 > 16 ? c.d_model / 256 : 16) * R * 4),
-      align256((size_t)H->rope_rows * (c.head_dim / 2) * 8),  // RoPE table
-      align256(R * 8)};  // row_info
-  for (int i = 0; i < 15; ++i) {
-    offs[i] = off;
-    off += sizes[i];
-  }
-  H->ws_bytes = off;
+  const size_t work_bytes = carve_work(c, R, H->dec_rows, H->max_splits, nullptr, nullptr);
+  const size_t freq_bytes = align256((size_t)(c.head_dim / 2) * 8);
+  const size_t rope_bytes = align256((size_t)H->rope_rows * (c.head_dim / 2) * 8);
+  H->ws_bytes = work_bytes + freq_bytes + rope_bytes;
   if (hipMalloc((void**)&H->ws, H->ws_bytes) != hipSuccess) {
     (void)hipGetLastError();
+    const size_t want = H->ws_bytes;
     delete H;
-    return fail(COCO_ENOMEM, "workspace of %zu bytes does not fit", off);
+    return fail(COCO_ENOMEM, "workspace of %zu bytes does not fit", want);
   }
-  H->x = H->ws + offs[0];
-  H->h = H->ws + offs[1];
-  H->q = H->ws + offs[2];
-  H->o = H->ws + offs[3];
-  H->h2 = H->ws + offs[4];
-  H->u = H->ws + offs[5];
-  H->x1 = (float*)(H->ws + offs[6]);
-  H->part = (float*)(H->ws + offs[7]);
-  H->attn_o = (float*)(H->ws + offs[8]);
-  H->attn_ml = (float*)(H->ws + offs[9]);
-  H->inv_freq = (double*)(H->ws + offs[10]);
-  H->split_off = (int32_t*)(H->ws + offs[11]);
-  H->ss = (float*)(H->ws + offs[12]);
-  H->rope = (float*)(H->ws + offs[13]);
-  H->row_info = (int32_t*)(H->ws + offs[14]);
+  carve_work(c, R, H->dec_rows, H->max_splits, H->ws, &H->w);
+  H->inv_freq = (double*)(H->ws + work_bytes);
+  H->rope = (float*)(H->ws + work_bytes + freq_bytes);
   H->act_rows_bytes[COCO_WS_X] = R * d * eb;
   H->act_rows_bytes[COCO_WS_H] = R * d * eb;
   H->act_rows_bytes[COCO_WS_Q] = R * qd * eb;
@@ -274,7 +342,7 @@ int coco_layer_init(const coco_layer_config* cfg, const coco_layer_weights* laye
   for (int j = 0; j < c.head_dim / 2; ++j)
     inv[j] = pow((double)c.rope_theta, -2.0 * j / (double)c.head_dim);
   if (hipMemcpy(H->inv_freq, inv.data(), inv.size() * 8, hipMemcpyHostToDevice) != hipSuccess ||
-      hipMemset(H->ws, 0, offs[10]) != hipSuccess ||
+      hipMemset(H->ws, 0, work_bytes) != hipSuccess ||
       hipEventCreateWithFlags(&H->done, hipEventDisableTiming) != hipSuccess ||
       (H->rope_rows > 0 &&
        (launch_rope_table(H->inv_freq, c.head_dim / 2, H->rope_rows, H->rope, nullptr) !=
@@ -320,6 +388,7 @@ int coco_layer_set_timing(coco_layer_t H, int32_t on) {
   if (on && H->ev.empty()) {
     H->ev.resize(2 * kTimingPairs);
     for (auto& e : H->ev) HIPCHK(hipEventCreate(&e));
+    H->ev_kind.reserve(kTimingPairs);  // timed calls then never allocate
   }
   H->timing = on != 0;
   H->ev_kind.clear();
@@ -355,7 +424,7 @@ int coco_layer_read_timing(coco_layer_t H, double* ms, int64_t* launches, int32_
 int coco_layer_workspace(coco_layer_t H, int32_t which, void* dst, int64_t dst_bytes,
                          coco_stream_t stream) {
   if (!H || !dst) return fail(COCO_EINVAL, "NULL argument");
-  void* p[7] = {H->x, H->h, H->q, H->o, H->x1, H->h2, H->u};
+  void* p[7] = {H->w.x, H->w.h, H->w.q, H->w.o, H->w.x1, H->w.h2, H->w.u};
   if (which < 0 || which > 6) return fail(COCO_EINVAL, "unknown workspace id %d", which);
   if (dst_bytes < 0) return fail(COCO_EINVAL, "dst_bytes < 0");
   const size_t n = (size_t)dst_bytes < H->act_rows_bytes[which] ? (size_t)dst_bytes
@@ -439,30 +508,30 @@ int validate_batch(coco_layer* H, int64_t hidden_rows, const int32_t* row_idx, i
 // Decode uses the weight-streaming plan (split-K from (N, K) only); prefill
 // uses the large-tile kernel with one split.
 template <typename T>
-int gemm(coco_layer* H, const T* A, const T* W, int M, int N, int K, bool prefill, int* S,
+int gemm(float* part, const T* A, const T* W, int M, int N, int K, bool prefill, int* S,
          hipStream_t st);
 
 template <>
-int gemm<bf16_t>(coco_layer* H, const bf16_t* A, const bf16_t* W, int M, int N, int K,
+int gemm<bf16_t>(float* part, const bf16_t* A, const bf16_t* W, int M, int N, int K,
                  bool prefill, int* S, hipStream_t st) {
   if (prefill) {
     *S = tile_splits(N, K);
-    HIPCHK(launch_gemm_tile_bf16(A, W, H->part, M, N, K, *S, st));
+    HIPCHK(launch_gemm_tile_bf16(A, W, part, M, N, K, *S, st));
     return COCO_OK;
   }
   const SkinnyPlan plan = skinny_plan(N, K);
   if (plan.waves == 0) return fail(COCO_EINVAL, "no GEMM plan for N=%d K=%d", N, K);
   *S = plan.S;
-  HIPCHK(launch_gemm_skinny_bf16(A, W, H->part, M, N, K, plan, st));
+  HIPCHK(launch_gemm_skinny_bf16(A, W, part, M, N, K, plan, st));
   return COCO_OK;
 }
 
 template <>
-int gemm<float>(coco_layer* H, const float* A, const float* W, int M, int N, int K,
-                bool prefill, int* S, hipStream_t st) {
+int gemm<float>(float* part, const float* A, const float* W, int M, int N, int K, bool prefill,
+                int* S, hipStream_t st) {
   (void)prefill;
   *S = 1;
-  HIPCHK(launch_gemm_f32(A, W, H->part, M, N, K, st));
+  HIPCHK(launch_gemm_f32(A, W, part, M, N, K, st));
   return COCO_OK;
 }
 
@@ -475,61 +544,61 @@ bool fused_swiglu(bool prefill, int F, int K) {
 }
 
 template <typename T>
-int attention(coco_layer* H, const coco_layer_weights& w, int M, const int32_t* positions,
-              const int32_t* seq_starts, int n_seqs, const int32_t* bt, const int32_t* ctx,
-              hipStream_t st);
+int attention(coco_layer* H, const Work& W, const coco_layer_weights& w, int M,
+              const int32_t* positions, const int32_t* seq_starts, int n_seqs, const int32_t* bt,
+              const int32_t* ctx, hipStream_t st);
 
 template <>
-int attention<bf16_t>(coco_layer* H, const coco_layer_weights& w, int M,
+int attention<bf16_t>(coco_layer* H, const Work& W, const coco_layer_weights& w, int M,
                       const int32_t* positions, const int32_t* seq_starts, int n_seqs,
                       const int32_t* bt, const int32_t* ctx, hipStream_t st) {
   const coco_layer_config& c = H->cfg;
   if (!seq_starts) {
     {
       KernelTimer t(H, COCO_K_ATTENTION, st);
-      HIPCHK(launch_attn_decode_bf16((const bf16_t*)H->q, (const bf16_t*)w.k_cache,
+      HIPCHK(launch_attn_decode_bf16((const bf16_t*)W.q, (const bf16_t*)w.k_cache,
                                      (const bf16_t*)w.v_cache, bt, c.max_blocks_per_seq, ctx,
-                                     positions, H->split_off, n_seqs, c.n_q_heads, c.n_kv_heads,
-                                     H->attn_o, H->attn_ml, H->max_splits, H->num_cus, st));
+                                     positions, W.split_off, n_seqs, c.n_q_heads, c.n_kv_heads,
+                                     W.attn_o, W.attn_ml, H->max_splits, H->num_cus, st));
     }
     KernelTimer t(H, COCO_K_ATTN_COMBINE, st);
-    HIPCHK(launch_attn_combine_bf16(H->attn_o, H->attn_ml, ctx, positions, n_seqs, c.n_q_heads,
-                                    H->max_splits, (bf16_t*)H->o, st));
+    HIPCHK(launch_attn_combine_bf16(W.attn_o, W.attn_ml, ctx, positions, n_seqs, c.n_q_heads,
+                                    H->max_splits, (bf16_t*)W.o, st));
   } else {
     KernelTimer t(H, COCO_K_ATTENTION, st);
-    HIPCHK(launch_attn_prefill_bf16((const bf16_t*)H->q, (const bf16_t*)w.k_cache,
+    HIPCHK(launch_attn_prefill_bf16((const bf16_t*)W.q, (const bf16_t*)w.k_cache,
                                     (const bf16_t*)w.v_cache, bt, c.max_blocks_per_seq, ctx,
                                     positions, seq_starts, n_seqs, M, c.n_q_heads, c.n_kv_heads,
-                                    (bf16_t*)H->o, st));
+                                    (bf16_t*)W.o, st));
   }
   return COCO_OK;
 }
 
 template <>
-int attention<float>(coco_layer* H, const coco_layer_weights& w, int M, const int32_t* positions,
-                     const int32_t* seq_starts, int n_seqs, const int32_t* bt,
-                     const int32_t* ctx, hipStream_t st) {
+int attention<float>(coco_layer* H, const Work& W, const coco_layer_weights& w, int M,
+                     const int32_t* positions, const int32_t* seq_starts, int n_seqs,
+                     const int32_t* bt, const int32_t* ctx, hipStream_t st) {
   const coco_layer_config& c = H->cfg;
   KernelTimer t(H, COCO_K_ATTENTION, st);
-  HIPCHK(launch_attn_f32((const float*)H->q, (const float*)w.k_cache, (const float*)w.v_cache,
+  HIPCHK(launch_attn_f32((const float*)W.q, (const float*)w.k_cache, (const float*)w.v_cache,
                          bt, c.max_blocks_per_seq, ctx, positions, seq_starts, n_seqs, M,
-                         c.n_q_heads, c.n_kv_heads, c.head_dim, (float*)H->o, st));
+                         c.n_q_heads, c.n_kv_heads, c.head_dim, (float*)W.o, st));
   return COCO_OK;
 }
 
 template <typename T>
-int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx, int M,
-             const int32_t* positions, const int32_t* seq_starts, int n_seqs,
+int run_span(coco_layer* H, const Work& W, int first, int nl, T* hidden, const int32_t* row_idx,
+             int M, const int32_t* positions, const int32_t* seq_starts, int n_seqs,
              const int32_t* bt, const int32_t* ctx, hipStream_t st) {
   const coco_layer_config& c = H->cfg;
   const int d = c.d_model, Hq = c.n_q_heads, Hkv = c.n_kv_heads, hd = c.head_dim, F = c.d_ffn;
   const int nqkv = (Hq + 2 * Hkv) * hd;
-  T* x = (T*)H->x;
-  T* h = (T*)H->h;
-  T* q = (T*)H->q;
-  T* o = (T*)H->o;
-  T* h2 = (T*)H->h2;
-  T* u = (T*)H->u;
+  T* x = (T*)W.x;
+  T* h = (T*)W.h;
+  T* q = (T*)W.q;
+  T* o = (T*)W.o;
+  T* h2 = (T*)W.h2;
+  T* u = (T*)W.u;
   int S, rc;
   const bool pre = seq_starts != nullptr;
 #define TIMED(kind, stmt)                     \
@@ -559,7 +628,7 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
       rs.positions = positions;
       rs.seq_starts = seq_starts;
       rs.block_table = bt;
-      rs.row_info = H->row_info;
+      rs.row_info = W.row_info;
       rs.n_seqs = n_seqs;
       rs.max_blocks = c.max_blocks_per_seq;
       rs.rope_rows = H->rope_rows;
@@ -577,13 +646,13 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
       TIMED(COCO_K_GEMM_QKV,
             HIPCHK(launch_gemm_skinny_norm_bf16((const bf16_t*)x_src, x_idx,
                                                 (const bf16_t*)w.gamma_attn,
-                                                (const bf16_t*)w.w_qkv, H->part, H->ss, M, nqkv, d,
+                                                (const bf16_t*)w.w_qkv, W.part, W.ss, M, nqkv, d,
                                                 plan, st)));
     } else if (fuse_qkv) {
       // Prefill (bf16, QKV projection not split along K): RoPE and the cache
       // append run in the GEMM's epilogue.
       TileEpiArgs qa;
-      qa.row_info = H->row_info;
+      qa.row_info = W.row_info;
       qa.rope = H->rope;
       qa.q_out = (uint16_t*)q;
       qa.k_cache = (uint16_t*)w.k_cache;
@@ -594,20 +663,20 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
             HIPCHK(launch_gemm_tile_qkv_bf16((const uint16_t*)h, (const uint16_t*)w.w_qkv, M, d,
                                              qa, st)));
     } else {
-      TIMED(COCO_K_GEMM_QKV, if ((rc = gemm<T>(H, h, (const T*)w.w_qkv, M, nqkv, d, pre, &S, st))) return rc);
+      TIMED(COCO_K_GEMM_QKV, if ((rc = gemm<T>(W.part, h, (const T*)w.w_qkv, M, nqkv, d, pre, &S, st))) return rc);
     }
     if (!fuse_qkv)
       TIMED(COCO_K_QKV_EPILOGUE,
-            HIPCHK(launch_qkv_epilogue<T>(H->part, S, M, Hq, Hkv, hd, positions, seq_starts,
+            HIPCHK(launch_qkv_epilogue<T>(W.part, S, M, Hq, Hkv, hd, positions, seq_starts,
                                           n_seqs, bt, c.max_blocks_per_seq, H->inv_freq, q,
                                           (T*)w.k_cache, (T*)w.v_cache, ctx,
                                           (seq_starts == nullptr && c.dtype == COCO_BF16)
-                                              ? H->split_off
+                                              ? W.split_off
                                               : nullptr,
-                                          H->max_splits, fold_norm ? H->ss : nullptr, d,
+                                          H->max_splits, fold_norm ? W.ss : nullptr, d,
                                           c.rms_eps, st)));
     // Attention over the paged cache.
-    if ((rc = attention<T>(H, w, M, positions, seq_starts, n_seqs, bt, ctx, st))) return rc;
+    if ((rc = attention<T>(H, W, w, M, positions, seq_starts, n_seqs, bt, ctx, st))) return rc;
     // O projection + residual + RMSNorm_2. Prefill (bf16, unsplit O and
     // gate/up projections): the O projection's epilogue adds the residual and
     // writes bf16(x1 * gamma_2) with per-tile sums of x1^2; the gate/up
@@ -616,13 +685,13 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
       TIMED(COCO_K_GEMM_O,
             HIPCHK(launch_gemm_tile_resid_bf16((const uint16_t*)o, (const uint16_t*)w.w_o, M, d,
                                                Hq * hd, (const uint16_t*)x_src, x_idx,
-                                               (const uint16_t*)w.gamma_mlp, H->x1,
-                                               (uint16_t*)h2, H->ss, st)));
+                                               (const uint16_t*)w.gamma_mlp, W.x1,
+                                               (uint16_t*)h2, W.ss, st)));
     } else {
-      TIMED(COCO_K_GEMM_O, if ((rc = gemm<T>(H, o, (const T*)w.w_o, M, d, Hq * hd, pre, &S, st))) return rc);
+      TIMED(COCO_K_GEMM_O, if ((rc = gemm<T>(W.part, o, (const T*)w.w_o, M, d, Hq * hd, pre, &S, st))) return rc);
       TIMED(COCO_K_RESIDUAL_NORM,
-            HIPCHK(launch_residual_rmsnorm<T>(H->part, S, M, d, x_src, x_idx,
-                                              (const T*)w.gamma_mlp, c.rms_eps, H->x1, h2, st)));
+            HIPCHK(launch_residual_rmsnorm<T>(W.part, S, M, d, x_src, x_idx,
+                                              (const T*)w.gamma_mlp, c.rms_eps, W.x1, h2, st)));
     }
     // SwiGLU MLP (prefill: SwiGLU in the gate/up GEMM's epilogue when the
     // GEMM is not split along K).
@@ -631,7 +700,7 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
         TIMED(COCO_K_GEMM_GATE_UP,
               HIPCHK(launch_gemm_tile_swiglu_bf16((const bf16_t*)h2, (const bf16_t*)w.w_gate_up,
                                                   (bf16_t*)u, M, F, d,
-                                                  fold_norm2 ? H->ss : nullptr, c.rms_eps, st)));
+                                                  fold_norm2 ? W.ss : nullptr, c.rms_eps, st)));
       } else {
         TIMED(COCO_K_GEMM_GATE_UP,
               HIPCHK(launch_gemm_skinny_swiglu_bf16((const bf16_t*)h2,
@@ -640,13 +709,13 @@ int run_span(coco_layer* H, int first, int nl, T* hidden, const int32_t* row_idx
       }
     } else {
       TIMED(COCO_K_GEMM_GATE_UP,
-            if ((rc = gemm<T>(H, h2, (const T*)w.w_gate_up, M, 2 * F, d, pre, &S, st))) return rc);
-      TIMED(COCO_K_SWIGLU, HIPCHK(launch_swiglu<T>(H->part, S, M, F, u, st)));
+            if ((rc = gemm<T>(W.part, h2, (const T*)w.w_gate_up, M, 2 * F, d, pre, &S, st))) return rc);
+      TIMED(COCO_K_SWIGLU, HIPCHK(launch_swiglu<T>(W.part, S, M, F, u, st)));
     }
-    TIMED(COCO_K_GEMM_DOWN, if ((rc = gemm<T>(H, u, (const T*)w.w_down, M, d, F, pre, &S, st))) return rc);
+    TIMED(COCO_K_GEMM_DOWN, if ((rc = gemm<T>(W.part, u, (const T*)w.w_down, M, d, F, pre, &S, st))) return rc);
     // Residual; the last layer of the segment scatters to the full batch.
     TIMED(COCO_K_RESIDUAL_SCATTER,
-          HIPCHK(launch_residual_scatter<T>(H->part, S, M, d, H->x1, last_l ? hidden : x,
+          HIPCHK(launch_residual_scatter<T>(W.part, S, M, d, W.x1, last_l ? hidden : x,
                                             last_l ? row_idx : nullptr, st)));
   }
 #undef TIMED
@@ -689,26 +758,41 @@ int mark_done(coco_layer* H, hipStream_t st) {
   return COCO_OK;
 }
 
+// use_static: the per-call buffers come from this device's static scratch
+// array, sized for the call (no allocation anywhere; validation mode, which
+// copies index arrays to the host, is not run).
 int forward_impl(coco_layer* H, int first, int nl, void* hidden, int64_t hidden_rows,
                  const int32_t* row_idx, int n_rows, const int32_t* positions,
                  const int32_t* seq_starts, int n_seqs, const int32_t* bt, const int32_t* ctx,
-                 coco_stream_t stream) {
+                 coco_stream_t stream, bool use_static = false) {
   if (!H) return fail(COCO_EINVAL, "handle is NULL");
   int rc = check_batch(H, first, nl, hidden, hidden_rows, row_idx, n_rows, positions,
                        seq_starts, n_seqs, bt, ctx);
   if (rc || n_rows == 0) return rc;
   hipStream_t st = (hipStream_t)stream;
   HIPCHK(hipSetDevice(H->device));
-  if (H->validate &&
-      (rc = validate_batch(H, hidden_rows, row_idx, n_rows, positions, seq_starts, n_seqs, bt,
-                           ctx, first, nl, st)))
+  Work W = H->w;
+  if (use_static) {
+    const int64_t dec_seqs = seq_starts ? 0 : n_seqs;
+    const size_t need = carve_work(H->cfg, n_rows, dec_seqs, H->max_splits, nullptr, nullptr);
+    if (need > kScratchBytes)
+      return fail(COCO_EINVAL,
+                  "call needs %zu bytes of scratch; the no-alloc entry point has %zu (%d rows)",
+                  need, kScratchBytes, n_rows);
+    char* base = scratch_ptr(H->device);
+    if (!base) return fail(COCO_ESTATE, "static scratch of device %d not set up", H->device);
+    carve_work(H->cfg, n_rows, dec_seqs, H->max_splits, base, &W);
+  } else if (H->validate &&
+             (rc = validate_batch(H, hidden_rows, row_idx, n_rows, positions, seq_starts, n_seqs,
+                                  bt, ctx, first, nl, st))) {
     return rc;
+  }
   if (H->cfg.dtype == COCO_BF16)
-    rc = run_span<bf16_t>(H, first, nl, (bf16_t*)hidden, row_idx, n_rows, positions, seq_starts,
-                          n_seqs, bt, ctx, st);
+    rc = run_span<bf16_t>(H, W, first, nl, (bf16_t*)hidden, row_idx, n_rows, positions,
+                          seq_starts, n_seqs, bt, ctx, st);
   else
-    rc = run_span<float>(H, first, nl, (float*)hidden, row_idx, n_rows, positions, seq_starts,
-                         n_seqs, bt, ctx, st);
+    rc = run_span<float>(H, W, first, nl, (float*)hidden, row_idx, n_rows, positions,
+                         seq_starts, n_seqs, bt, ctx, st);
   if (rc) return rc;
   return mark_done(H, st);
 }
@@ -723,6 +807,15 @@ int coco_layer_forward(coco_layer_t H, int32_t layer, void* hidden, int64_t hidd
                        const int32_t* ctx_lens, coco_stream_t stream) {
   return forward_impl(H, layer, 1, hidden, hidden_rows, row_idx, n_rows, positions, seq_starts,
                       n_seqs, block_table, ctx_lens, stream);
+}
+
+int coco_layer_forward_noalloc(coco_layer_t H, int32_t layer, void* hidden, int64_t hidden_rows,
+                               const int32_t* row_idx, int32_t n_rows, const int32_t* positions,
+                               const int32_t* seq_starts, int32_t n_seqs,
+                               const int32_t* block_table, const int32_t* ctx_lens,
+                               coco_stream_t stream) {
+  return forward_impl(H, layer, 1, hidden, hidden_rows, row_idx, n_rows, positions, seq_starts,
+                      n_seqs, block_table, ctx_lens, stream, true);
 }
 
 int coco_layer_span_forward(coco_layer_t H, int32_t first_layer, int32_t n_layers, void* hidden,
