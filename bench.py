@@ -147,9 +147,11 @@ def build_workload(name, batch=64):
 
 def measure_peaks(num_cus):
     """What this GPU sustains, measured here: a read stream over 2 GiB (the
-    library's read probe), a 1 GiB device copy (torch's copy kernel, read +
-    write) and a loop of bf16 MFMAs (the library's MFMA probe). Medians of 10
-    timed launches after 2 warm-ups."""
+    library's read probe; the best of its load depths and grid sizes), a 1 GiB
+    device copy (torch's copy kernel, read + write) and a loop of bf16 MFMAs
+    (the library's MFMA probe; the best of its chain counts and waves per
+    SIMD). Each configuration: the median of 10 timed launches after 2
+    warm-ups."""
     import torch
     import paper_2607_04181_amd as coco
     stream = torch.cuda.current_stream()
@@ -170,26 +172,42 @@ def measure_peaks(num_cus):
     nbytes = 2 << 30
     buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
     buf.random_(0, 255)
-    blocks = 8 * num_cus
-    out = torch.empty(blocks, dtype=torch.int32, device="cuda")
-    ms_read = timed(lambda: coco.coco_probe_read(buf, out, blocks, stream))
+    out = torch.empty(32 * num_cus, dtype=torch.int32, device="cuda")
+    reads = {}
+    for variant in (0, 1, 2):
+        for per_cu in (4, 8, 16, 32):
+            blocks = per_cu * num_cus
+            reads[(variant, per_cu)] = timed(
+                lambda: coco.coco_probe_read(buf, out, blocks, variant, stream))
+    (best_v, best_cu), ms_read = min(reads.items(), key=lambda kv: kv[1])
     x = buf[: nbytes // 2]
     y = torch.empty_like(x)
     ms_copy = timed(lambda: y.copy_(x))
     del buf, x, y
-    mblocks = 2 * num_cus  # two 4-wave workgroups per CU: two waves per SIMD
-    mout = torch.empty(4 * mblocks, dtype=torch.float32, device="cuda")
-    flops = [0.0]
+    mout = torch.empty(4 * 4 * num_cus, dtype=torch.float32, device="cuda")
+    mfmas = {}
+    for chains in (4, 8):
+        for per_cu in (1, 2, 4):  # 4-wave workgroups per CU: waves per SIMD
+            blocks = per_cu * num_cus
+            flops = [0.0]
 
-    def mfma():
-        flops[0] = coco.coco_probe_mfma_bf16(2000, mout, mblocks, stream)
-    ms_mfma = timed(mfma)
+            def mfma():
+                flops[0] = coco.coco_probe_mfma_bf16(2000 // chains * 4, mout, blocks, chains,
+                                                     stream)
+            ms = timed(mfma)
+            mfmas[(chains, per_cu)] = flops[0] / (ms * 1e-3) / 1e12
+    (best_c, best_w), tflops = max(mfmas.items(), key=lambda kv: kv[1])
     torch.cuda.empty_cache()
     return {"read_GBps": round(nbytes / (ms_read * 1e-3) / 1e9, 1),
             "copy_GBps": round(nbytes / (ms_copy * 1e-3) / 1e9, 1),
-            "mfma_bf16_TFLOPs": round(flops[0] / (ms_mfma * 1e-3) / 1e12, 1),
-            "method": "median of 10 launches: read probe over 2 GiB, 1 GiB device copy "
-                      "(bytes read + written), bf16 MFMA probe (4 chains/wave, 2 waves/SIMD)"}
+            "mfma_bf16_TFLOPs": round(tflops, 1),
+            "method": (f"medians of 10 launches: read probe over 2 GiB (best of 3 load depths "
+                       f"x 4 grid sizes: variant {best_v}, {best_cu} workgroups/CU), 1 GiB "
+                       f"device copy (bytes read + written), bf16 MFMA probe (best of 4/8 "
+                       f"chains x 1/2/4 waves per SIMD: {best_c} chains, {best_w} waves)"),
+            "read_GBps_all": {f"v{v}_{c}": round(nbytes / (ms * 1e-3) / 1e9, 1)
+                              for (v, c), ms in reads.items()},
+            "mfma_TFLOPs_all": {f"c{c}_w{w}": round(t, 1) for (c, w), t in mfmas.items()}}
 
 
 def run_workload(name, batch_rows, args, peaks, flush):
@@ -247,17 +265,28 @@ def run_workload(name, batch_rows, args, peaks, flush):
 
     # Cache-flushed steps: before each, a kernel writes the 1 GiB flush buffer
     # (four times the 256 MB last-level cache), outside the timed interval.
+    # The written lines are dirty, so the step also pays their write-back; a
+    # second series flushes with a read of the buffer (clean lines) instead.
     reps = max(30, args.steps)
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(reps)]
-    for r, (a, b) in enumerate(evs):
-        flush.fill_(float(r))
-        a.record(stream)
-        step()
-        b.record(stream)
-    torch.cuda.synchronize()
-    flushed = sorted(a.elapsed_time(b) for a, b in evs)
+    num_cus = torch.cuda.get_device_properties(0).multi_processor_count
+    probe_out = torch.empty(8 * num_cus, dtype=torch.int32, device="cuda")
+
+    def flushed_series(flush_fn):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(reps)]
+        for r, (a, b) in enumerate(evs):
+            flush_fn(r)
+            a.record(stream)
+            step()
+            b.record(stream)
+        torch.cuda.synchronize()
+        return sorted(a.elapsed_time(b) for a, b in evs)
+
+    flushed = flushed_series(lambda r: flush.fill_(float(r)))
     fms = flushed[len(flushed) // 2]
+    flushed_rd = flushed_series(
+        lambda r: coco.coco_probe_read(flush, probe_out, 8 * num_cus, 0, stream))
+    fms_rd = flushed_rd[len(flushed_rd) // 2]
 
     # The same step captured once as a HIP graph and replayed (the forward
     # only enqueues kernels on fixed buffers, so it is capturable as is).
@@ -327,7 +356,8 @@ def run_workload(name, batch_rows, args, peaks, flush):
             rows.append((k, tot / n, n, tot))
     rows.sort(key=lambda r: -r[3])
     tot_all = sum(r[3] for r in rows)
-    log(f"{wl.name}: hot {ms:.4f} ms/step, flushed median {fms:.4f} ms ({reps} reps)")
+    log(f"{wl.name}: hot {ms:.4f} ms/step, flushed median {fms:.4f} ms (write flush), "
+        f"{fms_rd:.4f} ms (read flush), {reps} reps each")
     log(f"{'kernel':18s} {'avg us':>9s} {'share':>6s} {'GB/s':>8s} {'TFLOP/s':>8s}")
     for k, avg, n, tot in rows:
         gbs = alg_bytes.get(k, 0) / (avg * 1e-3) / 1e9 if k in alg_bytes else float("nan")
@@ -374,13 +404,17 @@ def run_workload(name, batch_rows, args, peaks, flush):
     unit = "layer-steps/s" if is_decode else "tokens/s per layer"
     if graph is not None:
         graph["value"] = round(per_unit / graph["ms_per_step"], 2)
+    def frac(t_ms):
+        return round((step_bytes / (t_ms * 1e-3) / 1e9 / HBM_PEAK_GBS) if is_decode else
+                     (step_flops / (t_ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS), 4)
     flushed_out = {"median_ms": round(fms, 4), "reps": reps,
                    "min_ms": round(flushed[0], 4), "max_ms": round(flushed[-1], 4),
                    "value": round(per_unit / fms, 2), "flush_bytes": flush.numel() * 4,
-                   "step_frac": round((step_bytes / (fms * 1e-3) / 1e9 / HBM_PEAK_GBS)
-                                      if is_decode else
-                                      (step_flops / (fms * 1e-3) / 1e12 /
-                                       MFMA_BF16_PEAK_TFLOPS), 4)}
+                   "flush": "1 GiB written before each step", "step_frac": frac(fms),
+                   "read_flush": {"median_ms": round(fms_rd, 4),
+                                  "value": round(per_unit / fms_rd, 2),
+                                  "flush": "1 GiB read before each step",
+                                  "step_frac": frac(fms_rd)}}
 
     # The paper's speedup model (Sec. 4.2) fed with this measured per-layer
     # time: boundary rows over one xGMI link, bf16 hidden states.

@@ -273,17 +273,19 @@ int coco_layer_read_timing(coco_layer_t h, double* ms, int64_t* launches, int32_
  *
  * coco_probe_read: reads `bytes` (a multiple of 16, 16-byte aligned) of device
  * memory at `buf` once, as 16-byte vector loads spread over `blocks`
- * 256-thread workgroups; writes one 32-bit word per workgroup to `out`
- * (device, >= 4 * blocks bytes).
+ * 256-thread workgroups with a grid-wide stride; variant 0: four loads in
+ * flight per thread, 1: eight, 2: eight non-temporal. Writes one 32-bit word
+ * per workgroup to `out` (device, >= 4 * blocks bytes).
  *
  * coco_probe_mfma_bf16: `blocks` workgroups of four waves, each wave running
- * `iters` rounds of four independent v_mfma_f32_32x32x16_bf16 chains on
- * register operands; writes one float per wave to `out` (device, >= 16 *
- * blocks bytes) and the dense flop count of the launch to *flops (host). */
-int coco_probe_read(const void* buf, int64_t bytes, void* out, int32_t blocks,
+ * `iters` rounds of `chains` (4 or 8) independent v_mfma_f32_32x32x16_bf16
+ * chains on register operands; writes one float per wave to `out` (device,
+ * >= 16 * blocks bytes) and the dense flop count of the launch to *flops
+ * (host). */
+int coco_probe_read(const void* buf, int64_t bytes, void* out, int32_t blocks, int32_t variant,
                     coco_stream_t stream);
-int coco_probe_mfma_bf16(int64_t iters, void* out, int32_t blocks, double* flops,
-                         coco_stream_t stream);
+int coco_probe_mfma_bf16(int64_t iters, void* out, int32_t blocks, int32_t chains,
+                         double* flops, coco_stream_t stream);
 
 #ifdef __cplusplus
 }

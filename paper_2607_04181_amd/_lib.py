@@ -87,9 +87,9 @@ def _load():
         "coco_layer_set_timing": (ctypes.c_int, [vp, i32]),
         "coco_layer_read_timing": (ctypes.c_int, [vp, ctypes.POINTER(ctypes.c_double),
                                                   ctypes.POINTER(i64), i32]),
-        "coco_probe_read": (ctypes.c_int, [vp, i64, vp, i32, vp]),
-        "coco_probe_mfma_bf16": (ctypes.c_int, [i64, vp, i32, ctypes.POINTER(ctypes.c_double),
-                                                vp]),
+        "coco_probe_read": (ctypes.c_int, [vp, i64, vp, i32, i32, vp]),
+        "coco_probe_mfma_bf16": (ctypes.c_int, [i64, vp, i32, i32,
+                                                ctypes.POINTER(ctypes.c_double), vp]),
         "coco_split_batch": (ctypes.c_int, [i64, i32, ctypes.POINTER(i64)]),
         "coco_comm_time": (ctypes.c_double, [ctypes.POINTER(coco_scale_model), i32]),
         "coco_speedup": (ctypes.c_double, [ctypes.POINTER(coco_scale_model), i32, i32]),
@@ -309,20 +309,20 @@ def coco_layer_read_timing(h: Handle) -> dict:
     return {k: (ms[i], cnt[i]) for i, k in enumerate(KERNEL_KINDS)}
 
 
-def coco_probe_read(buf, out, blocks: int, stream=None) -> None:
+def coco_probe_read(buf, out, blocks: int, variant: int = 0, stream=None) -> None:
     """One read pass over the whole of `buf` (device tensor); `out` holds at
     least `blocks` int32 words."""
     nbytes = buf.numel() * buf.element_size()
     _check(_lib.coco_probe_read(_ptr(buf, what="buf"), nbytes, _ptr(out, what="out"), blocks,
-                                _stream(stream)))
+                                variant, _stream(stream)))
 
 
-def coco_probe_mfma_bf16(iters: int, out, blocks: int, stream=None) -> float:
+def coco_probe_mfma_bf16(iters: int, out, blocks: int, chains: int = 4, stream=None) -> float:
     """Enqueues the MFMA loop; returns its dense flop count. `out` holds at
     least 4 * blocks floats."""
     flops = ctypes.c_double()
-    _check(_lib.coco_probe_mfma_bf16(iters, _ptr(out, what="out"), blocks, ctypes.byref(flops),
-                                     _stream(stream)))
+    _check(_lib.coco_probe_mfma_bf16(iters, _ptr(out, what="out"), blocks, chains,
+                                     ctypes.byref(flops), _stream(stream)))
     return flops.value
 
 

@@ -12,20 +12,23 @@ namespace {
 constexpr int kProbeThreads = 256;
 
 // Every thread reads 16-byte vectors with a grid-wide stride (consecutive
-// lanes on consecutive vectors) and folds them into one word; each block
-// writes one word so the loads cannot be dropped.
+// lanes on consecutive vectors), U independent loads in flight per
+// iteration (plain or non-temporal), and folds them into one word; each
+// block writes one word so the loads cannot be dropped.
+template <int U, bool NT>
 __global__ __launch_bounds__(kProbeThreads) void probe_read_kernel(const u32x4_t* __restrict__ buf,
                                                                    int64_t n_vec,
                                                                    uint32_t* __restrict__ out) {
   const int64_t stride = (int64_t)gridDim.x * kProbeThreads;
   uint32_t acc = 0;
   int64_t i = (int64_t)blockIdx.x * kProbeThreads + threadIdx.x;
-  // Four independent loads in flight per thread per iteration.
-  for (; i + 3 * stride < n_vec; i += 4 * stride) {
-    const u32x4_t a = buf[i], b = buf[i + stride], c = buf[i + 2 * stride],
-                  d = buf[i + 3 * stride];
-    acc ^= (a.x ^ a.y ^ a.z ^ a.w) ^ (b.x ^ b.y ^ b.z ^ b.w) ^ (c.x ^ c.y ^ c.z ^ c.w) ^
-           (d.x ^ d.y ^ d.z ^ d.w);
+  for (; i + (U - 1) * stride < n_vec; i += U * stride) {
+    u32x4_t v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      v[u] = NT ? __builtin_nontemporal_load(buf + i + u * stride) : buf[i + u * stride];
+#pragma unroll
+    for (int u = 0; u < U; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
   }
   for (; i < n_vec; i += stride) {
     const u32x4_t a = buf[i];
@@ -44,11 +47,10 @@ __global__ __launch_bounds__(kProbeThreads) void probe_read_kernel(const u32x4_t
 
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-// Four independent chains of v_mfma_f32_32x32x16_bf16 per wave (32*32*16*2
+// C independent chains of v_mfma_f32_32x32x16_bf16 per wave (32*32*16*2
 // flops each), operands held in registers; lane 0 of each wave writes one
 // element of every chain so the chains cannot be dropped.
-constexpr int kMfmaChains = 4;
-
+template <int kMfmaChains>
 __global__ __launch_bounds__(kProbeThreads) void probe_mfma_kernel(int64_t iters,
                                                                    float* __restrict__ out) {
   const int lane = threadIdx.x & (kWave - 1);
@@ -83,21 +85,32 @@ using namespace coco;
 
 extern "C" {
 
-int coco_probe_read(const void* buf, int64_t bytes, void* out, int32_t blocks,
+int coco_probe_read(const void* buf, int64_t bytes, void* out, int32_t blocks, int32_t variant,
                     coco_stream_t stream) {
   if (!buf || !out || bytes < 16 || bytes % 16 || (uintptr_t)buf % 16 || blocks < 1)
     return COCO_EINVAL;
-  COCO_LAUNCH(probe_read_kernel, dim3(blocks), dim3(kProbeThreads), 0, (hipStream_t)stream,
-              (const u32x4_t*)buf, bytes / 16, (uint32_t*)out);
+  const hipStream_t st = (hipStream_t)stream;
+  const u32x4_t* b = (const u32x4_t*)buf;
+  const int64_t n = bytes / 16;
+  switch (variant) {
+    case 0: COCO_LAUNCH((probe_read_kernel<4, false>), dim3(blocks), dim3(kProbeThreads), 0, st, b, n, (uint32_t*)out); break;
+    case 1: COCO_LAUNCH((probe_read_kernel<8, false>), dim3(blocks), dim3(kProbeThreads), 0, st, b, n, (uint32_t*)out); break;
+    case 2: COCO_LAUNCH((probe_read_kernel<8, true>), dim3(blocks), dim3(kProbeThreads), 0, st, b, n, (uint32_t*)out); break;
+    default: return COCO_EINVAL;
+  }
   return hipGetLastError() == hipSuccess ? COCO_OK : COCO_EHIP;
 }
 
-int coco_probe_mfma_bf16(int64_t iters, void* out, int32_t blocks, double* flops,
-                         coco_stream_t stream) {
-  if (!out || !flops || iters < 1 || blocks < 1) return COCO_EINVAL;
-  *flops = 2.0 * 32 * 32 * 16 * kMfmaChains * (double)iters * blocks * (kProbeThreads / kWave);
-  COCO_LAUNCH(probe_mfma_kernel, dim3(blocks), dim3(kProbeThreads), 0, (hipStream_t)stream,
-              iters, (float*)out);
+int coco_probe_mfma_bf16(int64_t iters, void* out, int32_t blocks, int32_t chains,
+                         double* flops, coco_stream_t stream) {
+  if (!out || !flops || iters < 1 || blocks < 1 || (chains != 4 && chains != 8))
+    return COCO_EINVAL;
+  *flops = 2.0 * 32 * 32 * 16 * chains * (double)iters * blocks * (kProbeThreads / kWave);
+  const hipStream_t st = (hipStream_t)stream;
+  if (chains == 4)
+    COCO_LAUNCH((probe_mfma_kernel<4>), dim3(blocks), dim3(kProbeThreads), 0, st, iters, (float*)out);
+  else
+    COCO_LAUNCH((probe_mfma_kernel<8>), dim3(blocks), dim3(kProbeThreads), 0, st, iters, (float*)out);
   return hipGetLastError() == hipSuccess ? COCO_OK : COCO_EHIP;
 }
 
