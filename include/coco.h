@@ -15,8 +15,12 @@
  * ---------------------------------------
  * Pointers. Every data pointer is a DEVICE pointer into memory the caller
  *   owns (weights, caches, hidden buffer, index arrays). The library borrows
- *   weights and caches for the handle's lifetime and the rest for the call.
- *   The only memory the library owns is its workspace, allocated once in
+ *   caches, RMSNorm gains and (fp32) weight matrices for the handle's
+ *   lifetime and the rest for the call. dtype COCO_BF16: coco_layer_init
+ *   copies the four weight matrices of every layer into library memory in
+ *   tile order (below) and never reads the caller's matrices again; the
+ *   caller may free or overwrite them once init has returned.
+ *   The library owns that copy and its workspace, both allocated once in
  *   coco_layer_init and sized by the config (the paper's persistent memory
  *   pool with fixed addresses, Sec. 5.2, CUDA-graph compatibility): per-row
  *   activations and split-K partials for max_rows rows, the decode attention
@@ -45,6 +49,11 @@
  *   w_gate_up [2*F][d]                 F gate rows, then F up rows
  *   w_down    [d][F]
  *   gamma_attn, gamma_mlp [d]          RMSNorm gains
+ * (bf16) The library's copy of a weight matrix [N][K] is in tile order: the
+ *   1 KB block (n / 16) * (K / 32) + k / 32 holds rows 16 (n / 16) .. + 15 and
+ *   k 32 (k / 32) .. + 31 as 64 chunks of 8 consecutive k, chunk
+ *   ((k % 32) / 8) * 16 + n % 16 -- one MFMA operand fragment per 16 rows x
+ *   32 k, read by one contiguous 1 KB load.
  * Paged cache of one layer, with block size B = 16 tokens:
  *   k_cache, v_cache [num_blocks][Hkv][B * hd]: one tile of B tokens x hd
  *   dimensions per (block, kv head), in MFMA operand order. Inside a tile,
@@ -123,14 +132,17 @@ typedef struct {
 /* Create a replica handle for n_layers consecutive layers (Sec. 3.1: the
  * replicated unit is a span of consecutive layers). `layers` points to
  * cfg->n_layers host structs of device pointers; they are copied. Allocates
- * the workspace on the current HIP device. Returns COCO_EINVAL for an
- * unsupported shape (bf16: head_dim != 128, Hq/Hkv > 16, d, F or Hq*hd not
- * multiples of 128), COCO_ENOMEM if the workspace does not fit. */
+ * the workspace on the current HIP device and, for bf16, the tile-order copy
+ * of the weight matrices (the sum of their sizes over the handle's layers),
+ * which it writes before returning (synchronising the device). Returns
+ * COCO_EINVAL for an unsupported shape (bf16: head_dim != 128, Hq/Hkv > 16, d,
+ * F or Hq*hd not multiples of 128), COCO_ENOMEM if the workspace or the
+ * weight copy does not fit. */
 int coco_layer_init(const coco_layer_config* cfg, const coco_layer_weights* layers,
                     coco_layer_t* out);
 
-/* Release the workspace and the handle. First waits for the handle's last
- * call made outside graph capture to finish (an event recorded behind the
+/* Release the workspace, the weight copy and the handle. First waits for the
+ * handle's last call made outside graph capture to finish (an event recorded behind the
  * last kernel of every such call; calls on one handle are ordered, since they
  * share the workspace), not for other work on the device. A graph captured
  * from the handle's calls must not run after this. NULL is ignored. */

@@ -57,6 +57,10 @@ struct coco_layer {
   bool validate = false;
   char* ws = nullptr;
   size_t ws_bytes = 0;
+  // bf16: the library's tile-order copies of every layer's four weight
+  // matrices (layers[l].w_* point into it after init).
+  char* packed = nullptr;
+  size_t packed_bytes = 0;
   Work w;  // the workspace's per-call buffers, sized for max_rows
   double* inv_freq = nullptr;
   float* rope = nullptr;  // RoPE table [rope_rows][head_dim / 2] (cos, sin)
@@ -267,6 +271,55 @@ char* scratch_ptr(int dev) {
 
 }  // namespace
 
+namespace {
+
+// bf16: copy every layer's weight matrices into one library-owned buffer in
+// tile order (the layout the bf16 GEMM kernels read) and point the handle's
+// layer structs at the copies. The caller's matrices are not read again.
+int pack_weights(coco_layer* H) {
+  const coco_layer_config& c = H->cfg;
+  if (c.dtype != COCO_BF16) return COCO_OK;
+  const int64_t d = c.d_model, F = c.d_ffn, qd = (int64_t)c.n_q_heads * c.head_dim;
+  const int64_t nqkv = qd + 2LL * c.n_kv_heads * c.head_dim;
+  struct Mat {
+    int64_t N, K;
+  };
+  const Mat mats[4] = {{nqkv, d}, {d, qd}, {2 * F, d}, {d, F}};
+  size_t per_layer = 0;
+  for (const Mat& m : mats) per_layer += align256((size_t)(m.N * m.K * 2));
+  H->packed_bytes = per_layer * c.n_layers;
+  if (hipMalloc((void**)&H->packed, H->packed_bytes) != hipSuccess) {
+    (void)hipGetLastError();
+    H->packed = nullptr;
+    return fail(COCO_ENOMEM, "tile-order weight copies of %zu bytes do not fit", H->packed_bytes);
+  }
+  char* p = H->packed;
+  for (int l = 0; l < c.n_layers; ++l) {
+    coco_layer_weights& w = H->layers[l];
+    const void** src[4] = {&w.w_qkv, &w.w_o, &w.w_gate_up, &w.w_down};
+    for (int i = 0; i < 4; ++i) {
+      if (launch_pack_tile_order((const uint16_t*)*src[i], (int)mats[i].N, (int)mats[i].K,
+                                 (uint16_t*)p, nullptr) != hipSuccess) {
+        (void)hipGetLastError();
+        (void)hipFree(H->packed);
+        H->packed = nullptr;
+        return fail(COCO_EHIP, "weight packing failed (layer %d)", l);
+      }
+      *src[i] = p;
+      p += align256((size_t)(mats[i].N * mats[i].K * 2));
+    }
+  }
+  if (hipDeviceSynchronize() != hipSuccess) {
+    (void)hipGetLastError();
+    (void)hipFree(H->packed);
+    H->packed = nullptr;
+    return fail(COCO_EHIP, "weight packing failed");
+  }
+  return COCO_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 const char* coco_last_error(void) { return g_err; }
@@ -354,6 +407,12 @@ int coco_layer_init(const coco_layer_config* cfg, const coco_layer_weights* laye
     delete H;
     return fail(COCO_EHIP, "workspace initialisation failed");
   }
+  if ((rc = pack_weights(H))) {
+    (void)hipEventDestroy(H->done);
+    (void)hipFree(H->ws);
+    delete H;
+    return rc;
+  }
   *out = H;
   return COCO_OK;
 }
@@ -372,6 +431,7 @@ void coco_layer_destroy(coco_layer_t H) {
   }
   for (auto& e : H->ev) (void)hipEventDestroy(e);
   (void)hipFree(H->ws);
+  if (H->packed) (void)hipFree(H->packed);
   (void)hipSetDevice(cur);
   delete H;
 }

@@ -2,14 +2,17 @@
 //
 //   part[s][m][n] = sum over k in K-slice s of A[m][k] * W[n][k]
 //
-// A: [M][K] activations, W: [N][K] weights (nn.Linear layout), both bf16.
+// A: [M][K] activations, bf16. W: the [N][K] weights (nn.Linear layout) in
+// tile order (pack_tile_order below): every 16 rows x 32 k of W are one
+// contiguous 1 KB block laid out as the B operand of a
+// v_mfma_f32_16x16x32_bf16 step, lane by lane.
 // Decode is bound by reading W once from HBM, so the kernel is built around
 // that stream:
 //   * a workgroup of WAVES waves owns 16*WAVES output columns and one K-slice;
 //     each wave streams the 16 weight rows of its columns straight into VGPRs
-//     (16-byte loads, 64 contiguous bytes per row per instruction; plain
-//     loads measured faster here than non-temporal ones), keeping two
-//     stages of 128 k in flight;
+//     (each 16-byte-per-lane load one contiguous 1 KB block; plain loads
+//     measured faster here than non-temporal ones), keeping two stages of
+//     128 k in flight;
 //   * the activation tile [rows][128 k] of a stage is shared by the waves
 //     through LDS (double-buffered); its 16-byte chunks are XOR-swizzled
 //     with the row (chunk ^ row % 16), so both the row-wise stores and the
@@ -117,7 +120,11 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
   const int stages = k_slice / kBK;
   float* out = FUSE ? nullptr : part + (int64_t)blockIdx.y * M * N;
 
-  const bf16_t* wrow = W + (int64_t)n_col * K + k_begin + j4 * 8;
+  // This lane's chunk of the stage's step t (row n_col, k = k_begin + 128 st +
+  // 32 t + 8 j4) in tile order: block (n_col / 16) * (K / 32) + k / 32, chunk
+  // j4 * 16 + n_col % 16; a wave's load of one step is one 1 KB block.
+  const bf16_t* wrow =
+      W + ((int64_t)(n_col >> 4) * (K / 32) + k_begin / 32) * 512 + (j4 * 16 + (n_col & 15)) * 8;
 
   // The steady-state loop is branch-free so that the compiler can wait for
   // exactly the loads each step consumes: prefetches past the slice are
@@ -133,9 +140,9 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
     // Weight ring: PF stages x 4 k-steps of 8 bf16 per lane.
     u32x4_t wreg[PF][4];
     auto load_w = [&](int st, int u) {
-      const bf16_t* src = wrow + min(st, stages - 1) * kBK;
+      const bf16_t* src = wrow + min(st, stages - 1) * (kBK / 32) * 512;
 #pragma unroll
-      for (int t = 0; t < 4; ++t) wreg[u][t] = *(const u32x4_t*)(src + t * 32);
+      for (int t = 0; t < 4; ++t) wreg[u][t] = *(const u32x4_t*)(src + t * 512);
     };
 #pragma unroll
     for (int u = 0; u < PF; ++u) load_w(u, u);
@@ -233,11 +240,13 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
 // v_mfma_f32_16x16x32_bf16 (activation fragment as the A operand, weight
 // fragment as B) in ascending k.
 //   * the workgroup's 16*WAVES weight rows of a 64-k stage go straight to LDS
-//     (global_load_lds, 16 bytes per lane; wave w fills rows 16w .. 16w + 15
-//     as two 1 KB loads of eight rows) into a ring of four slots, three stages
-//     in flight; 16-byte chunks are swizzled as chunk ^ (row / 2) % 8,
-//     so the 16 rows a fragment read touches per 16-lane group cover every
-//     bank once;
+//     (global_load_lds, 16 bytes per lane; wave w fills the 16 rows of column
+//     tile w as two 1 KB loads, one per 32 k) into a ring of four slots, three
+//     stages in flight. LDS holds each 16 rows x 32 k in tile order (chunk
+//     (k / 8) * 16 + row), so a load reads one tile-order block of W (or, in
+//     the SwiGLU variant, the halves of two blocks that hold the tile's eight
+//     gate and eight up rows) and a fragment read gives each 16-lane group
+//     256 contiguous bytes;
 //   * row tile t of the pass (rows 16t .. 16t + 15) belongs to wave t % WAVES;
 //     a wave loads its tiles' activation fragments from memory straight into
 //     registers, AST stages deep (stage st + AST once stage st has been
@@ -253,8 +262,6 @@ constexpr int kRK = 64;        // k per stage
 constexpr int kRSlots = 4;     // weight ring slots
 constexpr int kRAhead = 3;     // weight stages in flight
 
-// LDS element offset of 16-byte chunk c (0..7) of row r of a [rows][64] tile.
-__device__ __forceinline__ int w_swz(int r, int c) { return r * kRK + ((c ^ ((r >> 1) & 7)) << 3); }
 
 // Weight ring of the row-split kernel, one LDS object per slot (sized for 8
 // waves), so the compiler tracks each slot's pending direct loads on its own
@@ -297,22 +304,26 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_rows_kernel(
     }
     return blockIdx.x * NR + rho;
   };
-  // Direct load q of this wave: rows 16 wv + 8q .. + 7; lane l lands at row
-  // 16 wv + 8q + l / 8, slot l % 8, which holds chunk (l % 8) ^ (row / 2) % 8.
+  // Direct load q of this wave: k 32q .. 32q + 31 of the stage for the 16
+  // rows of column tile wv; lane l = 16 j4 + c16 lands at LDS chunk l of the
+  // slot's block 2 wv + q and reads row w_row(16 wv + c16), k 32q + 8 j4 ..
+  // + 7, which is chunk j4 * 16 + row % 16 of tile-order block
+  // (row / 16) * (K / 32) + k / 32.
   // Addresses are a uniform base (advanced per stage) plus a fixed 32-bit byte
   // offset per lane, so no address register is rewritten inside the loop (a
   // rewrite of a register that a pending load shares would wait for it).
-  const char* wbase = (const char*)(W + k_begin);
+  const char* wbase = (const char*)(W + (int64_t)(k_begin / 32) * 512);
   uint32_t woff[kDLoads];
+  {
+    const int row = w_row(16 * wv + c16);
 #pragma unroll
-  for (int q = 0; q < kDLoads; ++q) {
-    const int rho = 16 * wv + 8 * q + (lane >> 3);
-    const int c = (lane & 7) ^ ((rho >> 1) & 7);
-    woff[q] = ((uint32_t)w_row(rho) * (uint32_t)K + (uint32_t)(c * 8)) * 2u;
+    for (int q = 0; q < kDLoads; ++q)
+      woff[q] = (uint32_t)((row >> 4) * (K / 32) + q) * 1024u +
+                (uint32_t)((j4 * 16 + (row & 15)) * 16);
   }
   // Stages past the slice repeat its last stage (never multiplied).
   auto issue_w = [&](int st, int slot) {
-    const char* b = wbase + (size_t)min(st, stages - 1) * (kRK * 2);
+    const char* b = wbase + (size_t)min(st, stages - 1) * (kRK / 32) * 1024;
 #pragma unroll
     for (int q = 0; q < kDLoads; ++q)
       __builtin_amdgcn_global_load_lds((const void*)(b + woff[q]),
@@ -382,7 +393,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_rows_kernel(
 #pragma unroll
         for (int j = 0; j < WAVES; ++j) {
           const bf16x8_t b = __builtin_bit_cast(
-              bf16x8_t, *(const u32x4_t*)(&lw[w_swz(16 * j + c16, t * 4 + j4)]));
+              bf16x8_t, *(const u32x4_t*)(&lw[16 * j * kRK + ((t * 4 + j4) * 16 + c16) * 8]));
 #pragma unroll
           for (int i = 0; i < TPW; ++i)
             acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
@@ -587,6 +598,35 @@ hipError_t launch_gemm_skinny_swiglu_bf16(const uint16_t* A, const uint16_t* W_g
       K % kBK != 0)
     return hipErrorInvalidValue;
   return launch_any<true, false>(A, W_gate_up, nullptr, H, M, 2 * F, K, plan, NormArgs{}, st);
+}
+
+// ----------------------------------------------------------------------------
+// Tile order of a bf16 weight matrix [N][K] (N % 16 == 0, K % 32 == 0): the
+// 1 KB block b = (n / 16) * (K / 32) + k / 32 holds rows 16 (n / 16) .. + 15
+// and columns 32 (k / 32) .. + 31 as 64 chunks of 8 consecutive k, chunk
+// ((k % 32) / 8) * 16 + n % 16 -- lane j4 * 16 + c16 of the B operand of a
+// v_mfma_f32_16x16x32_bf16 step (row c16, k 8 j4 .. + 7). One thread per
+// 16-byte chunk, read in row order.
+// ----------------------------------------------------------------------------
+namespace {
+__global__ __launch_bounds__(256) void pack_tile_order_kernel(const u32x4_t* __restrict__ w,
+                                                              int64_t n_chunks, int K,
+                                                              u32x4_t* __restrict__ out) {
+  const int64_t chunk = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (chunk >= n_chunks) return;
+  const int64_t per_row = K / 8;
+  const int64_t n = chunk / per_row, kc = chunk - n * per_row;
+  out[((n >> 4) * (K / 32) + (kc >> 2)) * 64 + (kc & 3) * 16 + (n & 15)] = w[chunk];
+}
+}  // namespace
+
+hipError_t launch_pack_tile_order(const uint16_t* W, int N, int K, uint16_t* out,
+                                  hipStream_t st) {
+  if (N <= 0 || K <= 0 || N % 16 != 0 || K % 32 != 0) return hipErrorInvalidValue;
+  const int64_t n_chunks = (int64_t)N * K / 8;
+  COCO_LAUNCH(pack_tile_order_kernel, dim3((unsigned)((n_chunks + 255) / 256)), dim3(256), 0, st,
+              (const u32x4_t*)W, n_chunks, K, (u32x4_t*)out);
+  return hipGetLastError();
 }
 
 // ----------------------------------------------------------------------------

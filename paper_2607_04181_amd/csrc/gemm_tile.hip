@@ -2,6 +2,10 @@
 //
 //   C[m][n] = sum_k A[m][k] * W[n][k]      A: [M][K], W: [N][K], both bf16
 //
+// W is in tile order (pack_tile_order): each 16 rows x 32 k of it is one
+// contiguous 1 KB block, which one 16-byte-per-lane load copies to LDS
+// unchanged (lane l, chunk l), so the W tile of a stage is 16 such blocks.
+//
 // Prefill is bound by MFMA throughput, so the kernel is built for reuse:
 //   * a 512-thread workgroup computes a 256 x 256 tile; each of its eight
 //     waves owns a 128 x 64 sub-tile as 4 x 2 v_mfma_f32_32x32x16_bf16
@@ -10,9 +14,10 @@
 //   * 32-deep K stages of the A and W tiles go straight from global memory
 //     to LDS (global_load_lds, 16 bytes per lane, no register staging) into
 //     a ring of four buffers, three stages in flight. Each wave fills 32 rows
-//     of both tiles with four 1 KB loads per stage. 16-byte chunks are
+//     of both tiles with four 1 KB loads per stage. A's 16-byte chunks are
 //     XOR-swizzled by row quad (chunk ^ (r / 4) % 4), so the 16 rows a
-//     fragment read touches per 16-lane group fall on distinct banks;
+//     fragment read touches per 16-lane group fall on distinct banks; W's
+//     tile-order blocks give each 16-lane group 256 contiguous bytes;
 //   * one barrier per stage: the barrier at the top of stage st publishes
 //     stage st + 1, so the first fragments of the next stage are read while
 //     the second half of this stage's MFMAs runs, and the stage that the
@@ -52,6 +57,9 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 // banks) = four 64-byte rows; XOR-ing the chunk with (r / 4) % 4 spreads the
 // 16 consecutive rows a fragment read touches over 16 distinct 4-bank slots.
 __device__ __forceinline__ int swz(int r, int c) { return r * kTK + ((c ^ ((r >> 2) & 3)) << 3); }
+// LDS element offset of chunk c (0..3) of tile row r in a W tile of 16
+// tile-order blocks.
+__device__ __forceinline__ int wblk(int r, int c) { return (r >> 4) * 512 + (c * 16 + (r & 15)) * 8; }
 
 // One LDS object per ring slot, so the compiler tracks each slot's pending
 // direct loads on its own and never drains the ring before a fragment read.
@@ -122,9 +130,13 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
   };
 
   // This lane's sources: wave wv fills rows 32 wv .. 32 wv + 31 of both tiles,
-  // 16 rows (1 KB) per load; lane l lands at row + l / 4, slot l % 4, which
-  // holds logical chunk (l % 4) ^ (row / 4) % 4. Rows past M repeat row M - 1
-  // (never stored).
+  // 16 rows (1 KB) per load. A: lane l lands at row + l / 4, slot l % 4,
+  // which holds logical chunk (l % 4) ^ (row / 4) % 4; rows past M repeat
+  // row M - 1 (never stored). W: every 16-row group of tile rows maps to 16
+  // consecutive W rows from a multiple of 16 (w_row), so a stage of the group
+  // is one tile-order block, block (w_row / 16) * (K / 32) + k / 32, which
+  // lane l copies chunk by chunk; groups past N read the last block (never
+  // stored).
   const int stages = k_slice / kTK;
   const bf16_t* src_a[2];
   const bf16_t* src_w[2];
@@ -133,17 +145,18 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
     const int r = 32 * wv + 16 * h + (lane >> 2);
     const int c = (lane & 3) ^ ((r >> 2) & 3);
     src_a[h] = A + (int64_t)min(m0 + r, M - 1) * K + kb + c * 8;
-    src_w[h] = W + (int64_t)w_row(r) * K + kb + c * 8;
+    const int wg = w_row(32 * wv + 16 * h) >> 4;
+    src_w[h] = W + ((int64_t)wg * (K / kTK) + kb / kTK) * 512 + lane * 8;
   }
   // Loads past the slice repeat its last stage (never multiplied).
   auto issue = [&](int st, int slot) {
-    const int ko = min(st, stages - 1) * kTK;
+    const int sc = min(st, stages - 1);
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      __builtin_amdgcn_global_load_lds(src_a[h] + ko,
+      __builtin_amdgcn_global_load_lds(src_a[h] + sc * kTK,
                                        (lds_void_t*)(ta[slot] + (32 * wv + 16 * h) * kTK), 16,
                                        0, 0);
-      __builtin_amdgcn_global_load_lds(src_w[h] + ko,
+      __builtin_amdgcn_global_load_lds(src_w[h] + sc * 512,
                                        (lds_void_t*)(tw[slot] + (32 * wv + 16 * h) * kTK), 16,
                                        0, 0);
     }
@@ -166,7 +179,7 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
 #pragma unroll
     for (int j = 0; j < 2; ++j)
       w[j] = __builtin_bit_cast(
-          bf16x8_t, *(const u32x4_t*)(&lw[swz(wn * 64 + j * 32 + l32, c)]));
+          bf16x8_t, *(const u32x4_t*)(&lw[wblk(wn * 64 + j * 32 + l32, c)]));
   };
   auto mfma_step = [&](const bf16x8_t* a, const bf16x8_t* w) {
 #pragma unroll

@@ -87,6 +87,14 @@ hipError_t launch_kv_append(const T* k, const T* v, const int32_t* seq_idx,
                             T* v_cache, hipStream_t st);
 
 // ---------------------------------------------------------------- GEMMs
+// Every bf16 GEMM below reads its weights W [N][K] in tile order: the 1 KB
+// block (n / 16) * (K / 32) + k / 32 holds rows 16 (n / 16) .. + 15 and k
+// 32 (k / 32) .. + 31 as 64 chunks of 8 k, chunk ((k % 32) / 8) * 16 + n % 16.
+// launch_pack_tile_order writes that layout from nn.Linear layout (N % 16 ==
+// 0, K % 32 == 0).
+hipError_t launch_pack_tile_order(const uint16_t* W, int N, int K, uint16_t* out,
+                                  hipStream_t st);
+
 // part[s][m][n] = sum_{k in slice s} A[m][k] * W[n][k]   (bf16 in, fp32 out)
 // The plan (split count S, workgroup width) and the K-order of every output element depend only on
 // (N, K), never on M: rows are independent and batch-invariant.

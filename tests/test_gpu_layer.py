@@ -219,9 +219,12 @@ def test_zero_output_projections_give_identity_bit_exactly():
     """With W_o = W_d = 0 the layer returns its input rows: pins gather ->
     residual -> scatter bit for bit."""
     shape, b = _small_decode(5)
-    rep = Replica.for_batch(shape, "s5", 1, b)
-    rep.layers[0]["w_o"].zero_()
-    rep.layers[0]["w_down"].zero_()
+    # The library copies the weights at init, so they are zeroed before it.
+    layers = [WD.layer_tensors(shape, "s5", 0, b.num_blocks)]
+    layers[0]["w_o"].zero_()
+    layers[0]["w_down"].zero_()
+    rep = Replica(shape, "s5", 1, b.num_blocks, b.n_rows, b.n_seqs, b.block_table.shape[1],
+                  layers=layers)
     hidden = WD.hidden_tensor(shape, "s5", b.hidden_rows)
     h0 = hidden.clone()
     rep.forward(0, hidden, WD.batch_tensors(b))
