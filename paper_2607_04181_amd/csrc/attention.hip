@@ -321,6 +321,12 @@ constexpr int kTileElems = kBlockTokens * HD;
 constexpr int kXCDs = 8;
 
 typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(3))) const volatile u32x2_t lds_u32x2_cv;
+
+// 8-byte LDS read of p (a pointer into LDS). volatile keeps the two halves of
+// a 16-byte chunk from being merged into one 16-byte read, which would need
+// register moves to split.
+__device__ __forceinline__ u32x2_t lds_read8(const bf16_t* p) { return *(lds_u32x2_cv*)p; }
 
 // WAVES waves of COLS 16-column tiles each cover the workgroup's 128 rows.
 template <int WAVES, int COLS>
@@ -448,13 +454,25 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_prefill_kernel(
         }
       }
       const bool unmasked = (st + 1) * kPfBlk * kBlockTokens - 1 <= w_kmin;
-      // V fragments of the first block pair are read during the softmax.
-      u32x4_t vfr[2][4];
+      // V^T operands of a block pair: this lane's 16-byte chunk of piece pc of
+      // a V tile holds 4 tokens of dim h, then the same 4 tokens of dim h + 16;
+      // each 8-byte half is read from LDS straight into its place in the
+      // operand (dims h: va, dims h + 16: vb; the pair's first block in the
+      // low half). The first pair is read during the softmax.
+      bf16x8_t va[4], vb[4];
+      auto read_v = [&](int pair) {
+        const bf16_t* b0 = vl + 2 * pair * kTileElems;
 #pragma unroll
-      for (int pc = 0; pc < 4; ++pc) {
-        vfr[0][pc] = *(const u32x4_t*)(vl + pc * 512);
-        vfr[1][pc] = *(const u32x4_t*)(vl + kTileElems + pc * 512);
-      }
+        for (int pc = 0; pc < 4; ++pc) {
+          const u32x2_t a0 = lds_read8(b0 + pc * 512);
+          const u32x2_t a1 = lds_read8(b0 + kTileElems + pc * 512);
+          const u32x2_t c0 = lds_read8(b0 + pc * 512 + 4);
+          const u32x2_t c1 = lds_read8(b0 + kTileElems + pc * 512 + 4);
+          va[pc] = __builtin_bit_cast(bf16x8_t, u32x4_t{a0.x, a0.y, a1.x, a1.y});
+          vb[pc] = __builtin_bit_cast(bf16x8_t, u32x4_t{c0.x, c0.y, c1.x, c1.y});
+        }
+      };
+      read_v(0);
       // Online softmax, once per 64 keys (log2 domain: p = 2^(s*scale - m)),
       // P^T packed as two 32-key operands. Stages wholly before the wave's
       // first row skip the causal mask.
@@ -509,24 +527,16 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_prefill_kernel(
       // O^T += V^T P^T over the two block pairs.
 #pragma unroll
       for (int pp = 0; pp < 2; ++pp) {
-        if (pp == 1) {
-#pragma unroll
-          for (int pc = 0; pc < 4; ++pc) {
-            vfr[0][pc] = *(const u32x4_t*)(vl + 2 * kTileElems + pc * 512);
-            vfr[1][pc] = *(const u32x4_t*)(vl + 3 * kTileElems + pc * 512);
-          }
-        }
+        if (pp == 1) read_v(1);
 #pragma unroll
         for (int pc = 0; pc < 4; ++pc) {
-          const u32x4_t v0 = vfr[0][pc], v1 = vfr[1][pc];
-          const bf16x8_t va = __builtin_bit_cast(bf16x8_t, u32x4_t{v0.x, v0.y, v1.x, v1.y});
-          const bf16x8_t vb = __builtin_bit_cast(bf16x8_t, u32x4_t{v0.z, v0.w, v1.z, v1.w});
 #pragma unroll
           for (int c = 0; c < COLS; ++c) {
             const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, pk[c][pp]);
-            acc[c][2 * pc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb, acc[c][2 * pc], 0, 0, 0);
+            acc[c][2 * pc] =
+                __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[pc], pb, acc[c][2 * pc], 0, 0, 0);
             acc[c][2 * pc + 1] =
-                __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb, pb, acc[c][2 * pc + 1], 0, 0, 0);
+                __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb[pc], pb, acc[c][2 * pc + 1], 0, 0, 0);
           }
         }
       }
