@@ -227,8 +227,11 @@ int coco_layer_forward_noalloc(coco_layer_t h, int32_t layer, void* hidden, int6
 
 /* Copy an intermediate buffer of the last call into `dst` (device memory of
  * at least dst_bytes bytes), for inspection by tests. which = COCO_WS_*;
- * row i holds call row i of the last layer run. Copies min(dst_bytes, buffer
- * size) bytes on `stream`. */
+ * row i holds call row i of the last layer run, row-major. Copies
+ * min(dst_bytes, buffer size) bytes on `stream`. (A bf16 prefill call keeps
+ * H, O, H2 and U, the A operands of its four projections, in the tile order
+ * of the weight copies, 16 rows x 32 columns per 1 KB block; this copy puts
+ * the call's rows back in row-major order.) */
 enum {
   COCO_WS_X = 0,  /* layer input rows, [max_rows][d], dtype (written for the
                      second and later layers of a span; the first layer reads

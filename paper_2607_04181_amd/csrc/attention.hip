@@ -544,17 +544,18 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_prefill_kernel(
     __syncthreads();  // stage st+1 landed; buffer st is free for stage st+2
   }
 
+  // The output [rows][Hq * 128] is the O projection's A operand, written in
+  // tile order (four columns from a multiple of 4 are contiguous there).
 #pragma unroll
   for (int c = 0; c < COLS; ++c) {
     const int row = w_row0 + 16 * c + c16;
     const float inv = 1.0f / col_sum4(l[c]);
     if (row < row_end) {
-      bf16_t* op = o + ((int64_t)row * Hq + h) * HD;
 #pragma unroll
       for (int n = 0; n < 8; ++n) {
         const uint32_t lo = pack_bf16x2(acc[c][n][0] * inv, acc[c][n][1] * inv);
         const uint32_t hi = pack_bf16x2(acc[c][n][2] * inv, acc[c][n][3] * inv);
-        *(u32x2_t*)(op + n * 16 + j4 * 4) = u32x2_t{lo, hi};
+        *(u32x2_t*)(o + tile_off(row, h * HD + n * 16 + j4 * 4, Hq * HD)) = u32x2_t{lo, hi};
       }
     }
   }

@@ -68,6 +68,11 @@ struct coco_layer {
   size_t act_rows_bytes[7] = {};
   int max_splits = 0;
   int dec_rows = 0;
+  // Layout of the last regular call's activations: bf16 prefill keeps h, o,
+  // h2 and u in tile order (rows of that call), read back row-major by
+  // coco_layer_workspace.
+  bool acts_tiled = false;
+  int last_rows = 0;
   // Per-kernel timing (benchmark mode).
   bool timing = false;
   std::vector<hipEvent_t> ev;  // pairs: start, stop
@@ -150,13 +155,16 @@ size_t carve_work(const coco_layer_config& c, int64_t rows, int64_t dec_seqs, in
     if (e > part_elems) part_elems = e;
   }
   const bool bf = c.dtype == COCO_BF16;
+  // The prefill GEMMs' A operands (h, o, h2, u) are in tile order, read in
+  // whole 16-row groups: room for the rows rounded up to 16.
+  const int64_t R16 = (R + 15) / 16 * 16;
   const size_t sizes[13] = {
-      align256(R * d * eb),    // x
-      align256(R * d * eb),    // h
-      align256(R * qd * eb),   // q
-      align256(R * qd * eb),   // o
-      align256(R * d * eb),    // h2
-      align256(R * F * eb),    // u
+      align256(R * d * eb),      // x
+      align256(R16 * d * eb),    // h
+      align256(R * qd * eb),     // q
+      align256(R16 * qd * eb),   // o
+      align256(R16 * d * eb),    // h2
+      align256(R16 * F * eb),    // u
       align256(R * d * 4),     // x1
       align256(part_elems * 4),  // part
       bf ? align256((size_t)dec_seqs * c.n_q_heads * max_splits * 128 * 4) : 0,  // attn_o
@@ -490,6 +498,15 @@ int coco_layer_workspace(coco_layer_t H, int32_t which, void* dst, int64_t dst_b
   const size_t n = (size_t)dst_bytes < H->act_rows_bytes[which] ? (size_t)dst_bytes
                                                                  : H->act_rows_bytes[which];
   HIPCHK(hipSetDevice(H->device));
+  const coco_layer_config& c = H->cfg;
+  const int cols[7] = {c.d_model, c.d_model, c.n_q_heads * c.head_dim,
+                       c.n_q_heads * c.head_dim, c.d_model, c.d_model, c.d_ffn};
+  if (H->acts_tiled && (which == COCO_WS_H || which == COCO_WS_O || which == COCO_WS_H2 ||
+                        which == COCO_WS_U)) {
+    HIPCHK(launch_untile((const uint16_t*)p[which], H->last_rows, cols[which],
+                         (uint16_t*)dst, (int64_t)(n / 2), (hipStream_t)stream));
+    return COCO_OK;
+  }
   HIPCHK(hipMemcpyAsync(dst, p[which], n, hipMemcpyDeviceToDevice, (hipStream_t)stream));
   return COCO_OK;
 }
@@ -661,6 +678,8 @@ int run_span(coco_layer* H, const Work& W, int first, int nl, T* hidden, const i
   T* u = (T*)W.u;
   int S, rc;
   const bool pre = seq_starts != nullptr;
+  // bf16 prefill: h, o, h2 and u (the prefill GEMMs' A operands) in tile order.
+  const bool tiled = pre && std::is_same<T, bf16_t>::value;
 #define TIMED(kind, stmt)                     \
   do {                                        \
     KernelTimer timer_(H, kind, st);          \
@@ -697,7 +716,7 @@ int run_span(coco_layer* H, const Work& W, int first, int nl, T* hidden, const i
       TIMED(COCO_K_GATHER_NORM,
             HIPCHK(launch_gather_rmsnorm<T>(first_l ? hidden : x, first_l ? row_idx : nullptr, M,
                                             d, (const T*)w.gamma_attn, c.rms_eps,
-                                            nullptr, h, rs, st)));
+                                            nullptr, h, tiled, rs, st)));
     // QKV projection, RoPE, local cache append.
     if (fold_norm) {
       const SkinnyPlan plan = skinny_plan(nqkv, d);
@@ -751,7 +770,8 @@ int run_span(coco_layer* H, const Work& W, int first, int nl, T* hidden, const i
       TIMED(COCO_K_GEMM_O, if ((rc = gemm<T>(W.part, o, (const T*)w.w_o, M, d, Hq * hd, pre, &S, st))) return rc);
       TIMED(COCO_K_RESIDUAL_NORM,
             HIPCHK(launch_residual_rmsnorm<T>(W.part, S, M, d, x_src, x_idx,
-                                              (const T*)w.gamma_mlp, c.rms_eps, W.x1, h2, st)));
+                                              (const T*)w.gamma_mlp, c.rms_eps, W.x1, h2, tiled,
+                                              st)));
     }
     // SwiGLU MLP (prefill: SwiGLU in the gate/up GEMM's epilogue when the
     // GEMM is not split along K).
@@ -770,7 +790,7 @@ int run_span(coco_layer* H, const Work& W, int first, int nl, T* hidden, const i
     } else {
       TIMED(COCO_K_GEMM_GATE_UP,
             if ((rc = gemm<T>(W.part, h2, (const T*)w.w_gate_up, M, 2 * F, d, pre, &S, st))) return rc);
-      TIMED(COCO_K_SWIGLU, HIPCHK(launch_swiglu<T>(W.part, S, M, F, u, st)));
+      TIMED(COCO_K_SWIGLU, HIPCHK(launch_swiglu<T>(W.part, S, M, F, u, tiled, st)));
     }
     TIMED(COCO_K_GEMM_DOWN, if ((rc = gemm<T>(W.part, u, (const T*)w.w_down, M, d, F, pre, &S, st))) return rc);
     // Residual; the last layer of the segment scatters to the full batch.
@@ -846,6 +866,10 @@ int forward_impl(coco_layer* H, int first, int nl, void* hidden, int64_t hidden_
              (rc = validate_batch(H, hidden_rows, row_idx, n_rows, positions, seq_starts, n_seqs,
                                   bt, ctx, first, nl, st))) {
     return rc;
+  }
+  if (!use_static) {
+    H->acts_tiled = H->cfg.dtype == COCO_BF16 && seq_starts != nullptr;
+    H->last_rows = n_rows;
   }
   if (H->cfg.dtype == COCO_BF16)
     rc = run_span<bf16_t>(H, W, first, nl, (bf16_t*)hidden, row_idx, n_rows, positions,

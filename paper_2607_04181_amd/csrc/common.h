@@ -129,6 +129,17 @@ __device__ __forceinline__ int v_tile_offset(int t, int h) {
   return ((((h >> 5) * 64 + (t >> 2) * 16 + (h & 15)) * 2 + ((h >> 4) & 1)) << 2) + (t & 3);
 }
 
+// Tile order of a bf16 matrix [M][K] (K % 32 == 0; rows padded to a multiple
+// of 16): the 1 KB block (m / 16) * (K / 32) + k / 32 holds rows
+// 16 (m / 16) .. + 15 and columns 32 (k / 32) .. + 31 as 64 chunks of 8
+// consecutive columns, chunk ((k % 32) / 8) * 16 + m % 16 -- the layout of
+// the weight copies, read by the prefill GEMM one block per load. Element
+// offset of (m, k); 8 columns from a multiple of 8 are contiguous.
+__device__ __forceinline__ int64_t tile_off(int64_t m, int k, int K) {
+  return ((((m >> 4) * (K >> 5) + (k >> 5)) << 6) + ((k & 31) >> 3) * 16 + (m & 15)) * 8 +
+         (k & 7);
+}
+
 // Sequence of a call row: identity for decode, else the s with
 // seq_starts[s] <= row < seq_starts[s+1].
 __device__ __forceinline__ int row_to_seq(const int32_t* seq_starts, int n_seqs, int row) {

@@ -2,9 +2,12 @@
 //
 //   C[m][n] = sum_k A[m][k] * W[n][k]      A: [M][K], W: [N][K], both bf16
 //
-// W is in tile order (pack_tile_order): each 16 rows x 32 k of it is one
-// contiguous 1 KB block, which one 16-byte-per-lane load copies to LDS
-// unchanged (lane l, chunk l), so the W tile of a stage is 16 such blocks.
+// W is in tile order (pack_tile_order), and so is A (tile_off: the prefill
+// activations are written in it by their producers): each 16 rows x 32 k of
+// either is one contiguous 1 KB block, which one 16-byte-per-lane load
+// copies to LDS unchanged (lane l, chunk l), so each tile of a stage is 16
+// such blocks. The bf16 activation outputs (SwiGLU and residual variants)
+// are written in tile order for the next projection.
 //
 // Prefill is bound by MFMA throughput, so the kernel is built for reuse:
 //   * a 512-thread workgroup computes a 256 x 256 tile; each of its eight
@@ -14,10 +17,8 @@
 //   * 32-deep K stages of the A and W tiles go straight from global memory
 //     to LDS (global_load_lds, 16 bytes per lane, no register staging) into
 //     a ring of four buffers, three stages in flight. Each wave fills 32 rows
-//     of both tiles with four 1 KB loads per stage. A's 16-byte chunks are
-//     XOR-swizzled by row quad (chunk ^ (r / 4) % 4), so the 16 rows a
-//     fragment read touches per 16-lane group fall on distinct banks; W's
-//     tile-order blocks give each 16-lane group 256 contiguous bytes;
+//     of both tiles with four 1 KB loads per stage; the tile-order blocks
+//     give each 16-lane group of a fragment read 256 contiguous bytes;
 //   * one barrier per stage: the barrier at the top of stage st publishes
 //     stage st + 1, so the first fragments of the next stage are read while
 //     the second half of this stage's MFMAs runs, and the stage that the
@@ -52,12 +53,7 @@ constexpr int kXCDs = 8;
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-// LDS element offset of 16-byte chunk c (0..3) of row r in a [256][32] tile.
-// A 16-lane group of a 16-byte-per-lane access covers 256 bytes (all 64
-// banks) = four 64-byte rows; XOR-ing the chunk with (r / 4) % 4 spreads the
-// 16 consecutive rows a fragment read touches over 16 distinct 4-bank slots.
-__device__ __forceinline__ int swz(int r, int c) { return r * kTK + ((c ^ ((r >> 2) & 3)) << 3); }
-// LDS element offset of chunk c (0..3) of tile row r in a W tile of 16
+// LDS element offset of chunk c (0..3) of tile row r in a tile of 16
 // tile-order blocks.
 __device__ __forceinline__ int wblk(int r, int c) { return (r >> 4) * 512 + (c * 16 + (r & 15)) * 8; }
 
@@ -130,21 +126,19 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
   };
 
   // This lane's sources: wave wv fills rows 32 wv .. 32 wv + 31 of both tiles,
-  // 16 rows (1 KB) per load. A: lane l lands at row + l / 4, slot l % 4,
-  // which holds logical chunk (l % 4) ^ (row / 4) % 4; rows past M repeat
-  // row M - 1 (never stored). W: every 16-row group of tile rows maps to 16
-  // consecutive W rows from a multiple of 16 (w_row), so a stage of the group
-  // is one tile-order block, block (w_row / 16) * (K / 32) + k / 32, which
-  // lane l copies chunk by chunk; groups past N read the last block (never
-  // stored).
+  // 16 rows (1 KB) per load, a stage of a 16-row group being one tile-order
+  // block that lane l copies chunk by chunk. A: rows m0 + 16 g' ..; groups
+  // past the last row read the last group (its rows past M are stale and
+  // never stored). W: every 16-row group of tile rows maps to 16 consecutive
+  // W rows from a multiple of 16 (w_row); groups past N read the last block
+  // (never stored).
   const int stages = k_slice / kTK;
   const bf16_t* src_a[2];
   const bf16_t* src_w[2];
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
-    const int r = 32 * wv + 16 * h + (lane >> 2);
-    const int c = (lane & 3) ^ ((r >> 2) & 3);
-    src_a[h] = A + (int64_t)min(m0 + r, M - 1) * K + kb + c * 8;
+    const int ag = min((m0 + 32 * wv + 16 * h) >> 4, (M - 1) >> 4);
+    src_a[h] = A + ((int64_t)ag * (K / kTK) + kb / kTK) * 512 + lane * 8;
     const int wg = w_row(32 * wv + 16 * h) >> 4;
     src_w[h] = W + ((int64_t)wg * (K / kTK) + kb / kTK) * 512 + lane * 8;
   }
@@ -153,7 +147,7 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
     const int sc = min(st, stages - 1);
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      __builtin_amdgcn_global_load_lds(src_a[h] + sc * kTK,
+      __builtin_amdgcn_global_load_lds(src_a[h] + sc * 512,
                                        (lds_void_t*)(ta[slot] + (32 * wv + 16 * h) * kTK), 16,
                                        0, 0);
       __builtin_amdgcn_global_load_lds(src_w[h] + sc * 512,
@@ -175,7 +169,7 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
 #pragma unroll
     for (int i = 0; i < 4; ++i)
       a[i] = __builtin_bit_cast(
-          bf16x8_t, *(const u32x4_t*)(&la[swz(wm * 128 + i * 32 + l32, c)]));
+          bf16x8_t, *(const u32x4_t*)(&la[wblk(wm * 128 + i * 32 + l32, c)]));
 #pragma unroll
     for (int j = 0; j < 2; ++j)
       w[j] = __builtin_bit_cast(
@@ -374,7 +368,7 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
             sq += x1 * x1;
             if (m < M) {
               C[(int64_t)m * N + n0 + col] = x1;
-              H[(int64_t)m * N + n0 + col] = (bf16_t)f32_to_bf16(x1 * gam[j]);
+              H[tile_off(m, n0 + col, N)] = (bf16_t)f32_to_bf16(x1 * gam[j]);
             }
           }
           v[i][jj][r] = sq;
@@ -418,7 +412,7 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
             g *= rs;
             u *= rs;
           }
-          if (m < M) H[(int64_t)m * F + o] = (bf16_t)f32_to_bf16(g / (1.0f + expf(-g)) * u);
+          if (m < M) H[tile_off(m, o, F)] = (bf16_t)f32_to_bf16(g / (1.0f + expf(-g)) * u);
         }
     }
     return;

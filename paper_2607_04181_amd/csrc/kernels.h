@@ -37,9 +37,11 @@ struct RowSlotArgs {
 
 // x_out[i] = src[row_idx ? row_idx[i] : i];  h_out[i] = RMSNorm(x) * gamma.
 // x_out may be null (span layers after the first read x in place).
+// tiled (bf16 prefill): h_out in tile order (tile_off), the prefill GEMM's A
+// operand layout; otherwise row-major.
 template <typename T>
 hipError_t launch_gather_rmsnorm(const T* src, const int32_t* row_idx, int M, int d,
-                                 const T* gamma, float eps, T* x_out, T* h_out,
+                                 const T* gamma, float eps, T* x_out, T* h_out, bool tiled,
                                  const RowSlotArgs& rs, hipStream_t st);
 
 // RoPE table rope[p][j] = (cos, sin)(p * inv_freq[j]) for p < n_pos and
@@ -64,15 +66,21 @@ hipError_t launch_qkv_epilogue(const float* part, int S, int M, int Hq, int Hkv,
                                const float* ss, int d, float eps, hipStream_t st);
 
 // x1 = x + sum_s part[s]  (fp32);  h2 = RMSNorm(x1) * gamma. Row i of x is
-// x[row_idx ? row_idx[i] : i].
+// x[row_idx ? row_idx[i] : i]. tiled: h2 in tile order.
 template <typename T>
 hipError_t launch_residual_rmsnorm(const float* part, int S, int M, int d, const T* x,
                                    const int32_t* row_idx, const T* gamma, float eps, float* x1,
-                                   T* h2, hipStream_t st);
+                                   T* h2, bool tiled, hipStream_t st);
 
-// u = silu(sum_s gate) * sum_s up, part rows [2F] = gate then up.
+// u = silu(sum_s gate) * sum_s up, part rows [2F] = gate then up. tiled: u in
+// tile order.
 template <typename T>
-hipError_t launch_swiglu(const float* part, int S, int M, int F, T* u, hipStream_t st);
+hipError_t launch_swiglu(const float* part, int S, int M, int F, T* u, bool tiled,
+                         hipStream_t st);
+
+// dst[m][k] (row-major, at most dst_elems elements) = src (tile order, [M][K]).
+hipError_t launch_untile(const uint16_t* src, int M, int K, uint16_t* dst, int64_t dst_elems,
+                         hipStream_t st);
 
 // y = x1 + sum_s part[s];  out[row_idx ? row_idx[i] : i] = y.
 template <typename T>
@@ -120,7 +128,9 @@ hipError_t launch_gemm_skinny_swiglu_bf16(const uint16_t* A, const uint16_t* W_g
 
 // part[s][m][n] = sum_{k in slice s} A[m][k] * W[n][k] with 256 x 256 MFMA
 // tiles (prefill; K a multiple of 64 * S). S = tile_splits(N, K); the k
-// order is fixed and M-independent.
+// order is fixed and M-independent. The tile GEMMs read A in tile order
+// (tile_off; its buffer holds M rounded up to 16 rows) and write their bf16
+// activation outputs (SwiGLU and residual variants) in tile order.
 int tile_splits(int N, int K);
 hipError_t launch_gemm_tile_bf16(const uint16_t* A, const uint16_t* W, float* C, int M, int N,
                                  int K, int S, hipStream_t st);
@@ -193,6 +203,8 @@ hipError_t launch_attn_combine_bf16(const float* part_o, const float* part_ml,
                                     int n_seqs, int Hq, int max_splits, uint16_t* o,
                                     hipStream_t st);
 
+// Causal attention of prefill rows over their sequences' caches; o [n_rows]
+// [Hq * 128] is written in tile order (the O projection's A operand).
 hipError_t launch_attn_prefill_bf16(const uint16_t* q, const uint16_t* k_cache,
                                     const uint16_t* v_cache, const int32_t* block_table,
                                     int max_blocks, const int32_t* ctx_lens,

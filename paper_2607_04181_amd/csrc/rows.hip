@@ -79,7 +79,8 @@ template <typename T>
 __global__ __launch_bounds__(kRowThreads) void gather_rmsnorm_kernel(
     const T* __restrict__ src, const int32_t* __restrict__ row_idx, int d,
     const T* __restrict__ gamma, float eps, T* __restrict__ x_out, T* __restrict__ h_out,
-    RowSlotArgs rs) {
+    bool tiled, RowSlotArgs rs) {
+  (void)tiled;  // bf16 only
   __shared__ float red[kRowThreads / kWave];
   const int i = blockIdx.x;
   if (rs.row_info != nullptr && threadIdx.x == 0) write_row_slot(rs, i);
@@ -103,7 +104,7 @@ template <>
 __global__ __launch_bounds__(kRowThreads) void gather_rmsnorm_kernel<bf16_t>(
     const bf16_t* __restrict__ src, const int32_t* __restrict__ row_idx, int d,
     const bf16_t* __restrict__ gamma, float eps, bf16_t* __restrict__ x_out,
-    bf16_t* __restrict__ h_out, RowSlotArgs rs) {
+    bf16_t* __restrict__ h_out, bool tiled, RowSlotArgs rs) {
   __shared__ float red[kRowThreads / kWave];
   constexpr int kMaxVec = 8;  // d <= 16384
   const int i = blockIdx.x;
@@ -145,20 +146,22 @@ __global__ __launch_bounds__(kRowThreads) void gather_rmsnorm_kernel<bf16_t>(
       unpack_bf16x8(gv[u], gf);
 #pragma unroll
       for (int e = 0; e < 8; ++e) f[e] = f[e] * inv * gf[e];
-      ((u32x4_t*)(h_out + (int64_t)i * d))[v] = pack_bf16x8(f);
+      *(u32x4_t*)(h_out + (tiled ? tile_off(i, 8 * v, d) : (int64_t)i * d + 8 * v)) =
+          pack_bf16x8(f);
     }
   }
 }
 
 template <typename T>
 hipError_t launch_gather_rmsnorm(const T* src, const int32_t* row_idx, int M, int d,
-                                 const T* gamma, float eps, T* x_out, T* h_out,
+                                 const T* gamma, float eps, T* x_out, T* h_out, bool tiled,
                                  const RowSlotArgs& rs, hipStream_t st) {
   if (M <= 0) return hipSuccess;
   if (rs.row_info != nullptr && (rs.n_seqs < 1 || rs.max_blocks < 1 || rs.rope_rows < 1))
     return hipErrorInvalidValue;
+  if (tiled && (!std::is_same<T, bf16_t>::value || d % 32 != 0)) return hipErrorInvalidValue;
   COCO_LAUNCH(gather_rmsnorm_kernel<T>, dim3(M), dim3(kRowThreads), 0, st, src, row_idx,
-                     d, gamma, eps, x_out, h_out, rs);
+                     d, gamma, eps, x_out, h_out, tiled, rs);
   return hipGetLastError();
 }
 
@@ -361,7 +364,7 @@ template <typename T, int S>
 __global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_kernel(
     const float* __restrict__ part, int M, int d, const T* __restrict__ x,
     const int32_t* __restrict__ row_idx, const T* __restrict__ gamma, float eps,
-    float* __restrict__ x1, T* __restrict__ h2) {
+    float* __restrict__ x1, T* __restrict__ h2, bool tiled) {
   __shared__ float red[kNormThreads / kWave];
   constexpr int kMaxVec = 4;  // d <= 16384
   const int i = blockIdx.x;
@@ -400,9 +403,10 @@ __global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_kernel(
     const int v = threadIdx.x + u * kNormThreads;
     if (v < nv) {
       const int c = 4 * v;
+      // Four columns from a multiple of 4 stay contiguous in tile order.
+      T* dst = h2 + (tiled ? tile_off(i, c, d) : (int64_t)i * d + c);
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        Elem<T>::store(h2 + (int64_t)i * d + c + e, a[u][e] * inv * g[u][e]);
+      for (int e = 0; e < 4; ++e) Elem<T>::store(dst + e, a[u][e] * inv * g[u][e]);
     }
   }
 }
@@ -410,12 +414,13 @@ __global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_kernel(
 template <typename T>
 hipError_t launch_residual_rmsnorm(const float* part, int S, int M, int d, const T* x,
                                    const int32_t* row_idx, const T* gamma, float eps, float* x1,
-                                   T* h2, hipStream_t st) {
+                                   T* h2, bool tiled, hipStream_t st) {
   if (M <= 0) return hipSuccess;
   if (d % 4 != 0 || d > 4 * 4 * kNormThreads) return hipErrorInvalidValue;
+  if (tiled && (!std::is_same<T, bf16_t>::value || d % 32 != 0)) return hipErrorInvalidValue;
   COCO_SWITCH_S(S, COCO_LAUNCH((residual_rmsnorm_kernel<T, S_>), dim3(M),
                                       dim3(kNormThreads), 0, st, part, M, d, x, row_idx, gamma,
-                                      eps, x1, h2));
+                                      eps, x1, h2, tiled));
   return hipGetLastError();
 }
 
@@ -425,7 +430,8 @@ hipError_t launch_residual_rmsnorm(const float* part, int S, int M, int d, const
 // ----------------------------------------------------------------------------
 template <typename T, int S>
 __global__ __launch_bounds__(kRowThreads) void swiglu_kernel(const float* __restrict__ part,
-                                                             int M, int F, T* __restrict__ u) {
+                                                             int M, int F, T* __restrict__ u,
+                                                             bool tiled) {
   const int i = blockIdx.y;
   const int c = 4 * (blockIdx.x * kRowThreads + threadIdx.x);
   if (c >= F) return;
@@ -433,18 +439,48 @@ __global__ __launch_bounds__(kRowThreads) void swiglu_kernel(const float* __rest
   const float* p = part + (int64_t)i * 2 * F + c;
   const f32x4_t g = sum_parts4<S>(p, pstride);
   const f32x4_t up = sum_parts4<S>(p + F, pstride);
+  T* dst = u + (tiled ? tile_off(i, c, F) : (int64_t)i * F + c);
 #pragma unroll
-  for (int e = 0; e < 4; ++e)
-    Elem<T>::store(u + (int64_t)i * F + c + e, g[e] / (1.0f + expf(-g[e])) * up[e]);
+  for (int e = 0; e < 4; ++e) Elem<T>::store(dst + e, g[e] / (1.0f + expf(-g[e])) * up[e]);
 }
 
 template <typename T>
-hipError_t launch_swiglu(const float* part, int S, int M, int F, T* u, hipStream_t st) {
+hipError_t launch_swiglu(const float* part, int S, int M, int F, T* u, bool tiled,
+                         hipStream_t st) {
   if (M <= 0) return hipSuccess;
   if (F % 4 != 0) return hipErrorInvalidValue;
+  if (tiled && (!std::is_same<T, bf16_t>::value || F % 32 != 0)) return hipErrorInvalidValue;
   const dim3 grid((F / 4 + kRowThreads - 1) / kRowThreads, M);
   COCO_SWITCH_S(S, COCO_LAUNCH((swiglu_kernel<T, S_>), grid, dim3(kRowThreads), 0, st,
-                                      part, M, F, u));
+                                      part, M, F, u, tiled));
+  return hipGetLastError();
+}
+
+// ----------------------------------------------------------------------------
+// Tile order back to row-major (inspection of the prefill activations): one
+// thread per 8-column chunk, 16-byte copies.
+// ----------------------------------------------------------------------------
+namespace {
+__global__ __launch_bounds__(kRowThreads) void untile_kernel(const uint16_t* __restrict__ src,
+                                                             int K, int64_t n_chunks,
+                                                             int64_t dst_elems,
+                                                             uint16_t* __restrict__ dst) {
+  const int64_t c = (int64_t)blockIdx.x * kRowThreads + threadIdx.x;
+  if (c >= n_chunks) return;
+  const int64_t m = c / (K / 8);
+  const int k = (int)(c - m * (K / 8)) * 8;
+  if (m * K + k + 8 > dst_elems) return;
+  *(u32x4_t*)(dst + m * K + k) = *(const u32x4_t*)(src + tile_off(m, k, K));
+}
+}  // namespace
+
+hipError_t launch_untile(const uint16_t* src, int M, int K, uint16_t* dst, int64_t dst_elems,
+                         hipStream_t st) {
+  if (M <= 0 || dst_elems <= 0) return hipSuccess;
+  if (K % 32 != 0) return hipErrorInvalidValue;
+  const int64_t n_chunks = (int64_t)M * (K / 8);
+  COCO_LAUNCH(untile_kernel, dim3((unsigned)((n_chunks + kRowThreads - 1) / kRowThreads)),
+              dim3(kRowThreads), 0, st, src, K, n_chunks, dst_elems, dst);
   return hipGetLastError();
 }
 
@@ -512,7 +548,7 @@ hipError_t launch_kv_append(const T* k, const T* v, const int32_t* seq_idx,
 
 #define COCO_INSTANTIATE(T)                                                                   \
   template hipError_t launch_gather_rmsnorm<T>(const T*, const int32_t*, int, int, const T*, \
-                                               float, T*, T*, const RowSlotArgs&,            \
+                                               float, T*, T*, bool, const RowSlotArgs&,      \
                                                hipStream_t);                                 \
   template hipError_t launch_qkv_epilogue<T>(const float*, int, int, int, int, int,          \
                                              const int32_t*, const int32_t*, int,            \
@@ -521,8 +557,8 @@ hipError_t launch_kv_append(const T* k, const T* v, const int32_t* seq_idx,
                                              int, float, hipStream_t);                       \
   template hipError_t launch_residual_rmsnorm<T>(const float*, int, int, int, const T*,      \
                                                  const int32_t*, const T*, float, float*, T*, \
-                                                 hipStream_t);                               \
-  template hipError_t launch_swiglu<T>(const float*, int, int, int, T*, hipStream_t);        \
+                                                 bool, hipStream_t);                         \
+  template hipError_t launch_swiglu<T>(const float*, int, int, int, T*, bool, hipStream_t);  \
   template hipError_t launch_residual_scatter<T>(const float*, int, int, int, const float*,  \
                                                  T*, const int32_t*, hipStream_t);           \
   template hipError_t launch_kv_append<T>(const T*, const T*, const int32_t*, const int32_t*, \
