@@ -248,7 +248,7 @@ __global__ __launch_bounds__(HD) void attn_combine_kernel(const float* __restric
                                                           const int32_t* __restrict__ ctx_lens,
                                                           const int32_t* __restrict__ positions,
                                                           int Hq, int max_splits,
-                                                          bf16_t* __restrict__ o) {
+                                                          bf16_t* __restrict__ o, bool tiled) {
   extern __shared__ float sm[];  // [0, max_splits): weights; [max_splits, 2*max_splits): l
   __shared__ float red[HD / kWave];
   const int h = blockIdx.x, s = blockIdx.y, dim = threadIdx.x;
@@ -299,7 +299,8 @@ __global__ __launch_bounds__(HD) void attn_combine_kernel(const float* __restric
   }
   for (; sp < nsp; ++sp) acc += sm[sp] * po[sp * HD];
   for (sp = 0; sp < nsp; ++sp) L += sm[sp] * sm[max_splits + sp];
-  o[((int64_t)s * Hq + h) * HD + dim] = (bf16_t)f32_to_bf16(nsp > 0 ? acc / L : 0.f);
+  o[tiled ? tile_off(s, h * HD + dim, Hq * HD) : ((int64_t)s * Hq + h) * HD + dim] =
+      (bf16_t)f32_to_bf16(nsp > 0 ? acc / L : 0.f);
 }
 
 // ---------------------------------------------------------------- prefill
@@ -646,12 +647,12 @@ hipError_t launch_attn_decode_bf16(const uint16_t* q, const uint16_t* k_cache,
 
 hipError_t launch_attn_combine_bf16(const float* part_o, const float* part_ml,
                                     const int32_t* ctx_lens, const int32_t* positions,
-                                    int n_seqs, int Hq, int max_splits, uint16_t* o,
+                                    int n_seqs, int Hq, int max_splits, uint16_t* o, bool tiled,
                                     hipStream_t st) {
   if (n_seqs <= 0) return hipSuccess;
   COCO_LAUNCH(attn_combine_kernel, dim3(Hq, n_seqs), dim3(HD),
                      2 * max_splits * sizeof(float), st, part_o, part_ml, ctx_lens, positions,
-                     Hq, max_splits, o);
+                     Hq, max_splits, o, tiled);
   return hipGetLastError();
 }
 

@@ -68,10 +68,10 @@ struct coco_layer {
   size_t act_rows_bytes[7] = {};
   int max_splits = 0;
   int dec_rows = 0;
-  // Layout of the last regular call's activations: bf16 prefill keeps h, o,
-  // h2 and u in tile order (rows of that call), read back row-major by
-  // coco_layer_workspace.
-  bool acts_tiled = false;
+  // Which of the last regular call's activations h, o, h2, u are in tile
+  // order (act_layout), read back row-major by coco_layer_workspace, and
+  // that call's rows.
+  bool ws_tiled[7] = {};
   int last_rows = 0;
   // Per-kernel timing (benchmark mode).
   bool timing = false;
@@ -501,8 +501,7 @@ int coco_layer_workspace(coco_layer_t H, int32_t which, void* dst, int64_t dst_b
   const coco_layer_config& c = H->cfg;
   const int cols[7] = {c.d_model, c.d_model, c.n_q_heads * c.head_dim,
                        c.n_q_heads * c.head_dim, c.d_model, c.d_model, c.d_ffn};
-  if (H->acts_tiled && (which == COCO_WS_H || which == COCO_WS_O || which == COCO_WS_H2 ||
-                        which == COCO_WS_U)) {
+  if (H->ws_tiled[which]) {
     HIPCHK(launch_untile((const uint16_t*)p[which], H->last_rows, cols[which],
                          (uint16_t*)dst, (int64_t)(n / 2), (hipStream_t)stream));
     return COCO_OK;
@@ -620,15 +619,35 @@ bool fused_swiglu(bool prefill, int F, int K) {
   return prefill ? tile_splits(2 * F, K) == 1 : skinny_plan(2 * F, K).S == 1;
 }
 
+// Layout of the four projections' A operands in a call: tile order
+// (tile_off) wherever the consuming GEMM reads it so -- every bf16 prefill
+// GEMM, and the decode GEMMs that run the row-split kernel -- else row-major.
+struct ActLayout {
+  bool h = false, o = false, h2 = false, u = false;
+};
+ActLayout act_layout(const coco_layer_config& c, bool prefill, int M) {
+  ActLayout a;
+  if (c.dtype != COCO_BF16) return a;
+  if (prefill) {
+    a.h = a.o = a.h2 = a.u = true;
+    return a;
+  }
+  const int d = c.d_model, F = c.d_ffn, qd = c.n_q_heads * c.head_dim;
+  a.o = skinny_reads_tiled(d, qd, M, false);
+  a.h2 = skinny_reads_tiled(2 * F, d, M, skinny_plan(2 * F, d).S == 1);
+  a.u = skinny_reads_tiled(d, F, M, false);
+  return a;
+}
+
 template <typename T>
 int attention(coco_layer* H, const Work& W, const coco_layer_weights& w, int M,
               const int32_t* positions, const int32_t* seq_starts, int n_seqs, const int32_t* bt,
-              const int32_t* ctx, hipStream_t st);
+              const int32_t* ctx, bool o_tiled, hipStream_t st);
 
 template <>
 int attention<bf16_t>(coco_layer* H, const Work& W, const coco_layer_weights& w, int M,
                       const int32_t* positions, const int32_t* seq_starts, int n_seqs,
-                      const int32_t* bt, const int32_t* ctx, hipStream_t st) {
+                      const int32_t* bt, const int32_t* ctx, bool o_tiled, hipStream_t st) {
   const coco_layer_config& c = H->cfg;
   if (!seq_starts) {
     {
@@ -640,7 +659,7 @@ int attention<bf16_t>(coco_layer* H, const Work& W, const coco_layer_weights& w,
     }
     KernelTimer t(H, COCO_K_ATTN_COMBINE, st);
     HIPCHK(launch_attn_combine_bf16(W.attn_o, W.attn_ml, ctx, positions, n_seqs, c.n_q_heads,
-                                    H->max_splits, (bf16_t*)W.o, st));
+                                    H->max_splits, (bf16_t*)W.o, o_tiled, st));
   } else {
     KernelTimer t(H, COCO_K_ATTENTION, st);
     HIPCHK(launch_attn_prefill_bf16((const bf16_t*)W.q, (const bf16_t*)w.k_cache,
@@ -654,7 +673,8 @@ int attention<bf16_t>(coco_layer* H, const Work& W, const coco_layer_weights& w,
 template <>
 int attention<float>(coco_layer* H, const Work& W, const coco_layer_weights& w, int M,
                      const int32_t* positions, const int32_t* seq_starts, int n_seqs,
-                     const int32_t* bt, const int32_t* ctx, hipStream_t st) {
+                     const int32_t* bt, const int32_t* ctx, bool o_tiled, hipStream_t st) {
+  (void)o_tiled;  // fp32: row-major throughout
   const coco_layer_config& c = H->cfg;
   KernelTimer t(H, COCO_K_ATTENTION, st);
   HIPCHK(launch_attn_f32((const float*)W.q, (const float*)w.k_cache, (const float*)w.v_cache,
@@ -678,8 +698,7 @@ int run_span(coco_layer* H, const Work& W, int first, int nl, T* hidden, const i
   T* u = (T*)W.u;
   int S, rc;
   const bool pre = seq_starts != nullptr;
-  // bf16 prefill: h, o, h2 and u (the prefill GEMMs' A operands) in tile order.
-  const bool tiled = pre && std::is_same<T, bf16_t>::value;
+  const ActLayout lay = act_layout(c, pre, M);
 #define TIMED(kind, stmt)                     \
   do {                                        \
     KernelTimer timer_(H, kind, st);          \
@@ -716,7 +735,7 @@ int run_span(coco_layer* H, const Work& W, int first, int nl, T* hidden, const i
       TIMED(COCO_K_GATHER_NORM,
             HIPCHK(launch_gather_rmsnorm<T>(first_l ? hidden : x, first_l ? row_idx : nullptr, M,
                                             d, (const T*)w.gamma_attn, c.rms_eps,
-                                            nullptr, h, tiled, rs, st)));
+                                            nullptr, h, lay.h, rs, st)));
     // QKV projection, RoPE, local cache append.
     if (fold_norm) {
       const SkinnyPlan plan = skinny_plan(nqkv, d);
@@ -755,7 +774,8 @@ int run_span(coco_layer* H, const Work& W, int first, int nl, T* hidden, const i
                                           H->max_splits, fold_norm ? W.ss : nullptr, d,
                                           c.rms_eps, st)));
     // Attention over the paged cache.
-    if ((rc = attention<T>(H, W, w, M, positions, seq_starts, n_seqs, bt, ctx, st))) return rc;
+    if ((rc = attention<T>(H, W, w, M, positions, seq_starts, n_seqs, bt, ctx, lay.o, st)))
+      return rc;
     // O projection + residual + RMSNorm_2. Prefill (bf16, unsplit O and
     // gate/up projections): the O projection's epilogue adds the residual and
     // writes bf16(x1 * gamma_2) with per-tile sums of x1^2; the gate/up
@@ -770,7 +790,7 @@ int run_span(coco_layer* H, const Work& W, int first, int nl, T* hidden, const i
       TIMED(COCO_K_GEMM_O, if ((rc = gemm<T>(W.part, o, (const T*)w.w_o, M, d, Hq * hd, pre, &S, st))) return rc);
       TIMED(COCO_K_RESIDUAL_NORM,
             HIPCHK(launch_residual_rmsnorm<T>(W.part, S, M, d, x_src, x_idx,
-                                              (const T*)w.gamma_mlp, c.rms_eps, W.x1, h2, tiled,
+                                              (const T*)w.gamma_mlp, c.rms_eps, W.x1, h2, lay.h2,
                                               st)));
     }
     // SwiGLU MLP (prefill: SwiGLU in the gate/up GEMM's epilogue when the
@@ -785,12 +805,12 @@ int run_span(coco_layer* H, const Work& W, int first, int nl, T* hidden, const i
         TIMED(COCO_K_GEMM_GATE_UP,
               HIPCHK(launch_gemm_skinny_swiglu_bf16((const bf16_t*)h2,
                                                     (const bf16_t*)w.w_gate_up, (bf16_t*)u, M, F,
-                                                    d, skinny_plan(2 * F, d), st)));
+                                                    d, skinny_plan(2 * F, d), lay.u, st)));
       }
     } else {
       TIMED(COCO_K_GEMM_GATE_UP,
             if ((rc = gemm<T>(W.part, h2, (const T*)w.w_gate_up, M, 2 * F, d, pre, &S, st))) return rc);
-      TIMED(COCO_K_SWIGLU, HIPCHK(launch_swiglu<T>(W.part, S, M, F, u, tiled, st)));
+      TIMED(COCO_K_SWIGLU, HIPCHK(launch_swiglu<T>(W.part, S, M, F, u, lay.u, st)));
     }
     TIMED(COCO_K_GEMM_DOWN, if ((rc = gemm<T>(W.part, u, (const T*)w.w_down, M, d, F, pre, &S, st))) return rc);
     // Residual; the last layer of the segment scatters to the full batch.
@@ -868,7 +888,12 @@ int forward_impl(coco_layer* H, int first, int nl, void* hidden, int64_t hidden_
     return rc;
   }
   if (!use_static) {
-    H->acts_tiled = H->cfg.dtype == COCO_BF16 && seq_starts != nullptr;
+    const ActLayout a = act_layout(H->cfg, seq_starts != nullptr, n_rows);
+    for (bool& t : H->ws_tiled) t = false;
+    H->ws_tiled[COCO_WS_H] = a.h;
+    H->ws_tiled[COCO_WS_O] = a.o;
+    H->ws_tiled[COCO_WS_H2] = a.h2;
+    H->ws_tiled[COCO_WS_U] = a.u;
     H->last_rows = n_rows;
   }
   if (H->cfg.dtype == COCO_BF16)

@@ -43,6 +43,17 @@ template <> struct Elem<float> {
   static __device__ __forceinline__ void store(float* p, float v) { *p = v; }
 };
 
+// Four consecutive elements (p 8-byte aligned for bf16, 16-byte for fp32) in
+// one store.
+__device__ __forceinline__ void store4(bf16_t* p, float a, float b, float c, float d) {
+  typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+  *(u2*)p = u2{pack_bf16x2(a, b), pack_bf16x2(c, d)};
+}
+__device__ __forceinline__ void store4(float* p, float a, float b, float c, float d) {
+  typedef float f4 __attribute__((ext_vector_type(4)));
+  *(f4*)p = f4{a, b, c, d};
+}
+
 // Waits until at most N vector-memory operations of this wave are in flight
 // (vmcnt only; direct global-to-LDS loads count there). N counts the loads
 // issued before this point in program order, so no memory operation may move

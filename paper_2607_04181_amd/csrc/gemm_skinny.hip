@@ -104,7 +104,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
     const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, float* __restrict__ part,
     bf16_t* __restrict__ H, int M, int N, int K, int k_slice,
     const int32_t* __restrict__ row_idx, const bf16_t* __restrict__ gamma,
-    float* __restrict__ ss) {
+    float* __restrict__ ss, bool h_tiled) {
   constexpr int NT = WAVES * 64;
   constexpr int kChunks = MT * 16 * (kBK / 8);  // 16-byte A chunks per stage
   constexpr int kPerT = (kChunks + NT - 1) / NT;
@@ -225,7 +225,8 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
           const float u = __shfl_down(acc[mt][r], 8, 16);
           const float g = acc[mt][r];
           if (c16 < 8 && m < M)
-            H[(int64_t)m * (N / 2) + o0 + c16] = (bf16_t)f32_to_bf16(g / (1.0f + expf(-g)) * u);
+            H[h_tiled ? tile_off(m, o0 + c16, N / 2) : (int64_t)m * (N / 2) + o0 + c16] =
+                (bf16_t)f32_to_bf16(g / (1.0f + expf(-g)) * u);
         } else if (m < M) {
           // Non-temporal: the partials are read once, by the next kernel.
           __builtin_nontemporal_store(acc[mt][r], out + (int64_t)m * N + n_col);
@@ -249,7 +250,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
 //     256 contiguous bytes;
 //   * row tile t of the pass (rows 16t .. 16t + 15) belongs to wave t % WAVES;
 //     a wave loads its tiles' activation fragments from memory straight into
-//     registers, AST stages deep (stage st + AST once stage st has been
+//     registers (A in tile order: one 1 KB block per load), AST stages deep (stage st + AST once stage st has been
 //     multiplied), and multiplies them with all 16*WAVES weight rows (LDS
 //     reads per stage: WAVES * 2 KB per wave);
 //   * one barrier per stage: the wait before it covers this wave's direct
@@ -275,7 +276,7 @@ __shared__ __attribute__((aligned(16))) bf16_t g_rw0[kRMaxRows * kRK], g_rw1[kRM
 template <int WAVES, bool FUSE, int ROWT, int AST>
 __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_rows_kernel(
     const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, float* __restrict__ part,
-    bf16_t* __restrict__ H, int M, int N, int K, int k_slice) {
+    bf16_t* __restrict__ H, int M, int N, int K, int k_slice, bool h_tiled) {
   static_assert(kRSlots % AST == 0, "activation slots must follow the unrolled stages");
   constexpr int kRowTiles = ROWT;
   constexpr int kRAst = AST;
@@ -333,22 +334,24 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_rows_kernel(
 
   for (int m0 = 0; m0 < M; m0 += kRowTiles * 16) {
     // Activation fragments: lane (c16, j4) of row tile i holds, for k-step t,
-    // elements 32t + 8j4 .. + 7 of the stage of row m0 + 16 tile + c16 (rows
-    // past M repeat row M - 1 and are never stored).
-    const char* abase = (const char*)(A + k_begin);
+    // elements 32t + 8j4 .. + 7 of the stage of row m0 + 16 tile + c16. A is
+    // in tile order (tile_off), so that fragment is chunk j4 * 16 + c16 = lane
+    // of a 1 KB block and each load reads one whole block. Row tiles past the
+    // last row read the last tile (its rows past M are stale, never stored).
+    const char* abase = (const char*)(A + (int64_t)(k_begin / 32) * 512);
     uint32_t aoff[TPW];
 #pragma unroll
     for (int i = 0; i < TPW; ++i) {
-      const int m = min(m0 + (wv + i * WAVES) * 16 + c16, M - 1);
-      aoff[i] = ((uint32_t)m * (uint32_t)K + (uint32_t)(j4 * 8)) * 2u;
+      const int rt = min((m0 >> 4) + wv + i * WAVES, (M - 1) >> 4);
+      aoff[i] = (uint32_t)rt * (uint32_t)(K / 32) * 1024u + (uint32_t)lane * 16u;
     }
     u32x4_t areg[kRAst][TPW][2];
     auto load_a = [&](int st, int slot) {
-      const char* b = abase + (size_t)min(st, stages - 1) * (kRK * 2);
+      const char* b = abase + (size_t)min(st, stages - 1) * ((kRK / 32) * 1024);
 #pragma unroll
       for (int i = 0; i < TPW; ++i)
 #pragma unroll
-        for (int t = 0; t < 2; ++t) areg[slot][i][t] = *(const u32x4_t*)(b + aoff[i] + t * 64);
+        for (int t = 0; t < 2; ++t) areg[slot][i][t] = *(const u32x4_t*)(b + aoff[i] + t * 1024);
     };
 
     f32x4_t acc[TPW][WAVES];
@@ -448,7 +451,8 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_rows_kernel(
             const float g = acc[i][j][r];
             const int o = (blockIdx.x * WAVES + j) * 8;
             if (c16 < 8 && m < M)
-              H[(int64_t)m * (N / 2) + o + c16] = (bf16_t)f32_to_bf16(g / (1.0f + expf(-g)) * u);
+              H[h_tiled ? tile_off(m, o + c16, N / 2) : (int64_t)m * (N / 2) + o + c16] =
+                  (bf16_t)f32_to_bf16(g / (1.0f + expf(-g)) * u);
           } else if (m < M) {
             __builtin_nontemporal_store(acc[i][j][r],
                                         out + (int64_t)m * N + blockIdx.x * NR + 16 * j + c16);
@@ -467,7 +471,7 @@ struct NormArgs {
 
 template <int WAVES, int MT, bool FUSE, bool NORM>
 hipError_t launch_plan(const uint16_t* A, const uint16_t* W, float* part, uint16_t* H, int M,
-                       int N, int K, int S, NormArgs na, hipStream_t st) {
+                       int N, int K, int S, NormArgs na, bool h_tiled, hipStream_t st) {
   // Two stages of weights in flight per wave (~56 KB per CU at 7 waves) cover
   // HBM latency for 64-row tiles; deeper rings measured slower there (more
   // requests queued behind each other) and cost registers. With 128-row tiles
@@ -476,47 +480,60 @@ hipError_t launch_plan(const uint16_t* A, const uint16_t* W, float* part, uint16
   constexpr int PF = (MT == 8 && WAVES == 8 && !NORM) ? 4 : 2;
   COCO_LAUNCH((gemm_skinny_kernel<WAVES, MT, PF, FUSE, NORM>), dim3(N / (16 * WAVES), S),
                      dim3(WAVES * 64), 0, st, A, W, part, H, M, N, K, K / S, na.row_idx,
-                     (const bf16_t*)na.gamma, na.ss);
+                     (const bf16_t*)na.gamma, na.ss, h_tiled);
   return hipGetLastError();
+}
+
+// Which kernel a plan of `waves` waves runs for M rows: the row-split kernel
+// where it measured faster, above 128 rows for 7- and 8-wave plans (8B
+// gate/up and down at 256 rows: 113 -> 89 us and 64 -> 46 us against two
+// 128-row passes; with fewer waves or the folded norm it measured slower),
+// and for 128-row passes of 8-wave plans. (No decode shape here has an
+// unfused 7-wave plan; those keep the 128-row kernel.) Its per-lane byte
+// offsets are 32-bit: both operands must be under 4 GB.
+enum RowsKind { kNoRows = 0, kRows16, kRows8 };
+RowsKind rows_kind(int waves, bool fuse, bool norm, int N, int K, int M) {
+  if (M <= 64 || norm || !(waves == 8 || (waves == 7 && fuse))) return kNoRows;
+  const bool fits = (int64_t)N * K * 2 < (int64_t(1) << 32) &&
+                    (int64_t)((M + 15) / 16 * 16) * K * 2 < (int64_t(1) << 32);
+  if (!fits) return kNoRows;
+  if (M > 128) return kRows16;
+  return waves == 8 ? kRows8 : kNoRows;
 }
 
 template <int WAVES, bool FUSE, bool NORM>
 hipError_t launch_waves(const uint16_t* A, const uint16_t* W, float* part, uint16_t* H, int M,
-                        int N, int K, int S, NormArgs na, hipStream_t st) {
-  if (M <= 64) return launch_plan<WAVES, 4, FUSE, NORM>(A, W, part, H, M, N, K, S, na, st);
-  // The row-split kernel where it measured faster: above 128 rows for 7- and
-  // 8-wave plans (8B gate/up and down at 256 rows: 113 -> 89 us and
-  // 64 -> 46 us against two 128-row passes; with fewer waves or the folded
-  // norm it measured slower), and 128-row passes of 8-wave plans. (No decode
-  // shape here has an unfused 7-wave plan; those keep the 128-row kernel.)
+                        int N, int K, int S, NormArgs na, bool h_tiled, hipStream_t st) {
+  if (M <= 64)
+    return launch_plan<WAVES, 4, FUSE, NORM>(A, W, part, H, M, N, K, S, na, h_tiled, st);
   if constexpr ((WAVES == 8 || (WAVES == 7 && FUSE)) && !NORM) {
-    // Its per-lane byte offsets are 32-bit: both operands under 4 GB.
-    const bool fits = (int64_t)N * K * 2 < (int64_t(1) << 32) &&
-                      (int64_t)M * K * 2 < (int64_t(1) << 32);
-    if (fits && M > 128) {
-      COCO_LAUNCH((gemm_skinny_rows_kernel<WAVES, FUSE, 16, WAVES == 8 ? 4 : 2>),
-                  dim3(N / (16 * WAVES), S), dim3(WAVES * 64), 0, st, A, W, part, H, M, N, K,
-                  K / S);
-      return hipGetLastError();
-    }
-    if (fits && WAVES == 8 && M > 64) {
-      COCO_LAUNCH((gemm_skinny_rows_kernel<8, FUSE, 8, 4>), dim3(N / 128, S), dim3(512), 0, st,
-                  A, W, part, H, M, N, K, K / S);
-      return hipGetLastError();
+    switch (rows_kind(WAVES, FUSE, NORM, N, K, M)) {
+      case kRows16:
+        COCO_LAUNCH((gemm_skinny_rows_kernel<WAVES, FUSE, 16, WAVES == 8 ? 4 : 2>),
+                    dim3(N / (16 * WAVES), S), dim3(WAVES * 64), 0, st, A, W, part, H, M, N,
+                    K, K / S, h_tiled);
+        return hipGetLastError();
+      case kRows8:
+        COCO_LAUNCH((gemm_skinny_rows_kernel<8, FUSE, 8, 4>), dim3(N / 128, S), dim3(512), 0,
+                    st, A, W, part, H, M, N, K, K / S, h_tiled);
+        return hipGetLastError();
+      default:
+        break;
     }
   }
-  return launch_plan<WAVES, 8, FUSE, NORM>(A, W, part, H, M, N, K, S, na, st);
+  return launch_plan<WAVES, 8, FUSE, NORM>(A, W, part, H, M, N, K, S, na, h_tiled, st);
 }
 
 template <bool FUSE, bool NORM>
 hipError_t launch_any(const uint16_t* A, const uint16_t* W, float* part, uint16_t* H, int M,
-                      int N, int K, SkinnyPlan plan, NormArgs na, hipStream_t st) {
+                      int N, int K, SkinnyPlan plan, NormArgs na, bool h_tiled,
+                      hipStream_t st) {
   switch (plan.waves) {
-    case 4: return launch_waves<4, FUSE, NORM>(A, W, part, H, M, N, K, plan.S, na, st);
-    case 5: return launch_waves<5, FUSE, NORM>(A, W, part, H, M, N, K, plan.S, na, st);
-    case 6: return launch_waves<6, FUSE, NORM>(A, W, part, H, M, N, K, plan.S, na, st);
-    case 7: return launch_waves<7, FUSE, NORM>(A, W, part, H, M, N, K, plan.S, na, st);
-    default: return launch_waves<8, FUSE, NORM>(A, W, part, H, M, N, K, plan.S, na, st);
+    case 4: return launch_waves<4, FUSE, NORM>(A, W, part, H, M, N, K, plan.S, na, h_tiled, st);
+    case 5: return launch_waves<5, FUSE, NORM>(A, W, part, H, M, N, K, plan.S, na, h_tiled, st);
+    case 6: return launch_waves<6, FUSE, NORM>(A, W, part, H, M, N, K, plan.S, na, h_tiled, st);
+    case 7: return launch_waves<7, FUSE, NORM>(A, W, part, H, M, N, K, plan.S, na, h_tiled, st);
+    default: return launch_waves<8, FUSE, NORM>(A, W, part, H, M, N, K, plan.S, na, h_tiled, st);
   }
 }
 
@@ -572,7 +589,12 @@ hipError_t launch_gemm_skinny_bf16(const uint16_t* A, const uint16_t* W, float* 
   if (plan.waves < 4 || plan.waves > 8 || N % (16 * plan.waves) != 0 ||
       K % (plan.S * kBK) != 0)
     return hipErrorInvalidValue;
-  return launch_any<false, false>(A, W, part, nullptr, M, N, K, plan, NormArgs{}, st);
+  return launch_any<false, false>(A, W, part, nullptr, M, N, K, plan, NormArgs{}, false, st);
+}
+
+bool skinny_reads_tiled(int N, int K, int M, bool fuse) {
+  const SkinnyPlan plan = skinny_plan(N, K);
+  return plan.waves != 0 && rows_kind(plan.waves, fuse, false, N, K, M) != kNoRows;
 }
 
 hipError_t launch_gemm_skinny_norm_bf16(const uint16_t* X, const int32_t* row_idx,
@@ -587,17 +609,18 @@ hipError_t launch_gemm_skinny_norm_bf16(const uint16_t* X, const int32_t* row_id
   na.row_idx = row_idx;
   na.gamma = gamma;
   na.ss = ss;
-  return launch_any<false, true>(X, W, part, nullptr, M, N, K, plan, na, st);
+  return launch_any<false, true>(X, W, part, nullptr, M, N, K, plan, na, false, st);
 }
 
 hipError_t launch_gemm_skinny_swiglu_bf16(const uint16_t* A, const uint16_t* W_gate_up,
                                           uint16_t* H, int M, int F, int K, SkinnyPlan plan,
-                                          hipStream_t st) {
+                                          bool h_tiled, hipStream_t st) {
   if (M <= 0) return hipSuccess;
   if (plan.S != 1 || plan.waves < 4 || plan.waves > 8 || (2 * F) % (16 * plan.waves) != 0 ||
       K % kBK != 0)
     return hipErrorInvalidValue;
-  return launch_any<true, false>(A, W_gate_up, nullptr, H, M, 2 * F, K, plan, NormArgs{}, st);
+  return launch_any<true, false>(A, W_gate_up, nullptr, H, M, 2 * F, K, plan, NormArgs{},
+                                 h_tiled, st);
 }
 
 // ----------------------------------------------------------------------------

@@ -122,9 +122,14 @@ hipError_t launch_gemm_skinny_norm_bf16(const uint16_t* X, const int32_t* row_id
                                         hipStream_t st);
 // Decode gate/up GEMM with the SwiGLU epilogue: H[M][F] = bf16(silu(A W_g^T) *
 // (A W_u^T)), W_gate_up = [W_g; W_u] [2F][K]; plan = skinny_plan(2F, K) with S == 1.
+// h_tiled: H in tile order (for a down projection that reads it so).
 hipError_t launch_gemm_skinny_swiglu_bf16(const uint16_t* A, const uint16_t* W_gate_up,
                                           uint16_t* H, int M, int F, int K, SkinnyPlan plan,
-                                          hipStream_t st);
+                                          bool h_tiled, hipStream_t st);
+// Whether the decode GEMM of (N, K) at M rows (fuse: the SwiGLU variant) runs
+// the row-split kernel, which reads its activations A in tile order
+// (tile_off); the other decode kernels read A row-major.
+bool skinny_reads_tiled(int N, int K, int M, bool fuse);
 
 // part[s][m][n] = sum_{k in slice s} A[m][k] * W[n][k] with 256 x 256 MFMA
 // tiles (prefill; K a multiple of 64 * S). S = tile_splits(N, K); the k
@@ -198,9 +203,10 @@ hipError_t launch_attn_decode_bf16(const uint16_t* q, const uint16_t* k_cache,
                                    const int32_t* positions, const int32_t* split_off,
                                    int n_seqs, int Hq, int Hkv, float* part_o, float* part_ml,
                                    int max_splits, int num_cus, hipStream_t st);
+// tiled: o in tile order (for an O projection that reads it so).
 hipError_t launch_attn_combine_bf16(const float* part_o, const float* part_ml,
                                     const int32_t* ctx_lens, const int32_t* positions,
-                                    int n_seqs, int Hq, int max_splits, uint16_t* o,
+                                    int n_seqs, int Hq, int max_splits, uint16_t* o, bool tiled,
                                     hipStream_t st);
 
 // Causal attention of prefill rows over their sequences' caches; o [n_rows]

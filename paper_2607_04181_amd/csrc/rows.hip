@@ -405,8 +405,8 @@ __global__ __launch_bounds__(kNormThreads) void residual_rmsnorm_kernel(
       const int c = 4 * v;
       // Four columns from a multiple of 4 stay contiguous in tile order.
       T* dst = h2 + (tiled ? tile_off(i, c, d) : (int64_t)i * d + c);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) Elem<T>::store(dst + e, a[u][e] * inv * g[u][e]);
+      store4(dst, a[u][0] * inv * g[u][0], a[u][1] * inv * g[u][1], a[u][2] * inv * g[u][2],
+             a[u][3] * inv * g[u][3]);
     }
   }
 }
@@ -440,8 +440,10 @@ __global__ __launch_bounds__(kRowThreads) void swiglu_kernel(const float* __rest
   const f32x4_t g = sum_parts4<S>(p, pstride);
   const f32x4_t up = sum_parts4<S>(p + F, pstride);
   T* dst = u + (tiled ? tile_off(i, c, F) : (int64_t)i * F + c);
+  float r[4];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) Elem<T>::store(dst + e, g[e] / (1.0f + expf(-g[e])) * up[e]);
+  for (int e = 0; e < 4; ++e) r[e] = g[e] / (1.0f + expf(-g[e])) * up[e];
+  store4(dst, r[0], r[1], r[2], r[3]);
 }
 
 template <typename T>
