@@ -23,7 +23,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-Wall",
          "-Wno-unused-function", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          f"-I{os.path.join(ROOT, 'include')}"]
-SOURCES = ["rows.hip", "gemm_skinny.hip", "gemm_tile.hip", "attention.hip", "coco_api.hip",
+SOURCES = ["rows.hip", "gemm_skinny.hip", "gemm_tile.hip", "gemm_narrow.hip", "attention.hip", "coco_api.hip",
            "probe.hip", "scaling.cpp"]
 
 

@@ -171,8 +171,8 @@ size_t carve_work(const coco_layer_config& c, int64_t rows, int64_t dec_seqs, in
       bf ? align256((size_t)dec_seqs * c.n_q_heads * max_splits * 2 * 4) : 0,    // attn_ml
       align256((size_t)(dec_seqs + 1) * 4),  // split_off
       // ss: per-slice row sums of squares (decode QKV, at most 16 K-slices)
-      // or per-256-column-tile ones (prefill O projection)
-      align256((size_t)(c.d_model / 256 > 16 ? c.d_model / 256 : 16) * R * 4),
+      // or per-column-tile ones (prefill O projection, at most 32 tiles)
+      align256((size_t)32 * R * 4),
       align256(R * 8)};  // row_info
   size_t off[13], total = 0;
   for (int i = 0; i < 13; ++i) {
@@ -715,8 +715,17 @@ int run_span(coco_layer* H, const Work& W, int first, int nl, T* hidden, const i
     // them is made.
     const bool fold_norm = !pre && std::is_same<T, bf16_t>::value;
     const bool fuse_qkv = pre && std::is_same<T, bf16_t>::value && tile_qkv_fusable(Hq, Hkv, d);
+    // Prefill O and down projections on the narrow-tile GEMM (256 x d/32
+    // tiles, unsplit), when d has such a plan and the SwiGLU runs in the
+    // gate/up epilogue: the O epilogue then folds in the residual and
+    // RMSNorm_2's first half, the down epilogue the residual and the scatter.
+    const int ntn = pre && std::is_same<T, bf16_t>::value ? narrow_tile_n(d) : 0;
+    const bool narrow_o = ntn != 0 && (Hq * hd) % 128 == 0 && fused_swiglu<T>(pre, F, d);
+    const bool narrow_down = ntn != 0 && F % 128 == 0;
     const bool fold_norm2 =
-        pre && std::is_same<T, bf16_t>::value && tile_norm2_foldable(d, Hq * hd, F);
+        narrow_o ||
+        (pre && std::is_same<T, bf16_t>::value && tile_norm2_foldable(d, Hq * hd, F));
+    const int norm_tiles = narrow_o ? d / ntn : d / 256;
     const T* x_src = first_l ? hidden : x;                     // this layer's input rows
     const int32_t* x_idx = first_l ? row_idx : nullptr;
     // The fused prefill QKV epilogue reads each row's (position, cache block),
@@ -780,7 +789,13 @@ int run_span(coco_layer* H, const Work& W, int first, int nl, T* hidden, const i
     // gate/up projections): the O projection's epilogue adds the residual and
     // writes bf16(x1 * gamma_2) with per-tile sums of x1^2; the gate/up
     // epilogue applies each row's 1/rms, so no separate norm kernel runs.
-    if (fold_norm2) {
+    if (narrow_o) {
+      TIMED(COCO_K_GEMM_O,
+            HIPCHK(launch_gemm_narrow_resid_bf16((const uint16_t*)o, (const uint16_t*)w.w_o, M,
+                                                 d, Hq * hd, (const uint16_t*)x_src, x_idx,
+                                                 (const uint16_t*)w.gamma_mlp, W.x1,
+                                                 (uint16_t*)h2, W.ss, st)));
+    } else if (fold_norm2) {
       TIMED(COCO_K_GEMM_O,
             HIPCHK(launch_gemm_tile_resid_bf16((const uint16_t*)o, (const uint16_t*)w.w_o, M, d,
                                                Hq * hd, (const uint16_t*)x_src, x_idx,
@@ -800,7 +815,8 @@ int run_span(coco_layer* H, const Work& W, int first, int nl, T* hidden, const i
         TIMED(COCO_K_GEMM_GATE_UP,
               HIPCHK(launch_gemm_tile_swiglu_bf16((const bf16_t*)h2, (const bf16_t*)w.w_gate_up,
                                                   (bf16_t*)u, M, F, d,
-                                                  fold_norm2 ? W.ss : nullptr, c.rms_eps, st)));
+                                                  fold_norm2 ? W.ss : nullptr, norm_tiles,
+                                                  c.rms_eps, st)));
       } else {
         TIMED(COCO_K_GEMM_GATE_UP,
               HIPCHK(launch_gemm_skinny_swiglu_bf16((const bf16_t*)h2,
@@ -812,11 +828,20 @@ int run_span(coco_layer* H, const Work& W, int first, int nl, T* hidden, const i
             if ((rc = gemm<T>(W.part, h2, (const T*)w.w_gate_up, M, 2 * F, d, pre, &S, st))) return rc);
       TIMED(COCO_K_SWIGLU, HIPCHK(launch_swiglu<T>(W.part, S, M, F, u, lay.u, st)));
     }
-    TIMED(COCO_K_GEMM_DOWN, if ((rc = gemm<T>(W.part, u, (const T*)w.w_down, M, d, F, pre, &S, st))) return rc);
-    // Residual; the last layer of the segment scatters to the full batch.
-    TIMED(COCO_K_RESIDUAL_SCATTER,
-          HIPCHK(launch_residual_scatter<T>(W.part, S, M, d, W.x1, last_l ? hidden : x,
-                                            last_l ? row_idx : nullptr, st)));
+    // Down projection and residual; the last layer of the segment scatters to
+    // the full batch.
+    if (narrow_down) {
+      TIMED(COCO_K_GEMM_DOWN,
+            HIPCHK(launch_gemm_narrow_scatter_bf16((const uint16_t*)u, (const uint16_t*)w.w_down,
+                                                   M, d, F, W.x1,
+                                                   (uint16_t*)(last_l ? hidden : x),
+                                                   last_l ? row_idx : nullptr, st)));
+    } else {
+      TIMED(COCO_K_GEMM_DOWN, if ((rc = gemm<T>(W.part, u, (const T*)w.w_down, M, d, F, pre, &S, st))) return rc);
+      TIMED(COCO_K_RESIDUAL_SCATTER,
+            HIPCHK(launch_residual_scatter<T>(W.part, S, M, d, W.x1, last_l ? hidden : x,
+                                              last_l ? row_idx : nullptr, st)));
+    }
   }
 #undef TIMED
   return COCO_OK;

@@ -1,0 +1,320 @@
+// Narrow-output GEMM for prefill (bf16 MFMA): the O and down projections,
+// whose output width is the model width d.
+//
+//   acc[m][n] = sum_k A[m][k] * W[n][k]      A: [M][K], W: [N][K], both bf16
+//
+// A and W are in tile order (tile_off / pack_tile_order): every 16 rows x
+// 32 k is one contiguous 1 KB block, laid out lane by lane as a
+// v_mfma_f32_16x16x32_bf16 operand, so one 16-byte-per-lane load copies a
+// block to LDS unchanged and one 16-byte LDS read per lane is a fragment.
+//
+// A 256 x 256 tile grid leaves these projections with d / 256 column tiles
+// per 256 rows: 160 tiles for d = 5120 and a 2048-row chunk, on 256 CUs.
+// Here a tile is 256 rows x TN columns with TN = 160 or 128 (narrow_tile_n:
+// d / TN <= 32 column tiles), so the chunk is exactly 256 tiles for
+// d = 5120 (TN = 160) and d = 4096 (TN = 128), and each projection runs
+// unsplit along K with its consumer's work in the epilogue:
+//   * residual variant (O projection): x1 = acc + residual row (fp32 out),
+//     h = bf16(x1 * gamma) in tile order for the gate/up projection, and the
+//     tile's row sums of x1^2 (RMSNorm_2's statistics, finished by the
+//     gate/up epilogue);
+//   * scatter variant (down projection): out[out_idx[m]] = bf16(x1 + acc),
+//     the layer output written straight to its row of the full batch.
+// The main loop:
+//   * 512 threads, eight waves as 4 (rows) x 2 (columns); each wave owns a
+//     64 x TN/2 sub-tile as 4 x TN/32 accumulators of 16 x 16, two waves per
+//     SIMD so one wave's MFMAs issue while the other reads LDS;
+//   * 32-deep K stages of both tiles go straight from global memory to LDS
+//     (global_load_lds, no register staging) into a ring of six slots, five
+//     stages in flight (the loads come from L2, the MALL or HBM, whose
+//     latency under this load is several stages of MFMA work); wave w copies A blocks 2w, 2w + 1 and W block
+//     w (for TN = 160 waves 0 and 1 also W blocks 8 and 9);
+//   * one barrier per stage, which publishes stage st + 1 and guarantees
+//     that the slot the next loads overwrite was read by every wave;
+//   * workgroups are remapped so that the tiles sharing a W column slab run
+//     on the same XCD (blockIdx % 8) and hit its L2.
+// Every output element is one chain of MFMAs over k in ascending 32-steps,
+// and the tile width depends on N only, so a row's result does not depend on
+// M or on the other rows of the call.
+#include <type_traits>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace coco {
+
+namespace {
+
+constexpr int kNM = 256;        // tile rows
+constexpr int kNK = 32;         // k per stage
+constexpr int kNBuf = 6;        // LDS ring slots (even: fragment registers alternate)
+constexpr int kNAhead = kNBuf - 1;  // stages in flight
+constexpr int kNThreads = 512;  // 8 waves, two per SIMD
+constexpr int kNXCDs = 8;
+constexpr int kNMaxTN = 160;
+constexpr int kNMaxTiles = 32;  // column tiles (the gate/up fold's limit)
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// One LDS object per ring slot, so the compiler tracks each slot's pending
+// direct loads on its own and never drains the ring before a fragment read.
+__shared__ __attribute__((aligned(16))) bf16_t g_na0[kNM * kNK], g_na1[kNM * kNK],
+    g_na2[kNM * kNK], g_na3[kNM * kNK], g_na4[kNM * kNK], g_na5[kNM * kNK];
+__shared__ __attribute__((aligned(16))) bf16_t g_nw0[kNMaxTN * kNK], g_nw1[kNMaxTN * kNK],
+    g_nw2[kNMaxTN * kNK], g_nw3[kNMaxTN * kNK], g_nw4[kNMaxTN * kNK], g_nw5[kNMaxTN * kNK];
+// Target of the loads that only keep the per-wave load count uniform (never
+// read; several waves may write it at once).
+__shared__ __attribute__((aligned(16))) bf16_t g_nspare[512];
+
+enum { kNarrowResid = 0, kNarrowScatter = 1 };
+
+template <int TN, int MODE>
+__global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __restrict__ A,
+                                                                 const bf16_t* __restrict__ W,
+                                                                 int M, int N, int K,
+                                                                 NarrowEpiArgs ea) {
+  static_assert(TN % 32 == 0 && TN <= kNMaxTN && TN / 16 >= 8, "tile width");
+  constexpr int WB = TN / 32;          // 16-column blocks per wave
+  constexpr int kWBlocks = TN / 16;    // W blocks per stage
+  constexpr int kExtra = kWBlocks - 8; // waves that copy a second W block
+  // Loads per stage and wave. With a second W block (TN = 160) every wave
+  // issues one: waves past kExtra copy their first block again into a spare
+  // block that is never read, so all waves wait on the same counts and the
+  // loop has no branch around a load.
+  constexpr int kLoads = kExtra > 0 ? 4 : 3;
+  bf16_t* const ta[kNBuf] = {g_na0, g_na1, g_na2, g_na3, g_na4, g_na5};
+  bf16_t* const tw[kNBuf] = {g_nw0, g_nw1, g_nw2, g_nw3, g_nw4, g_nw5};
+
+  const int tiles_m = (M + kNM - 1) / kNM;
+  const int nb = gridDim.x;
+  const int b = blockIdx.x;
+  const int full = (nb / kNXCDs) * kNXCDs;
+  const int lid = b < full ? (b % kNXCDs) * (nb / kNXCDs) + b / kNXCDs : b;
+  const int m0 = (lid % tiles_m) * kNM;
+  const int n0 = (lid / tiles_m) * TN;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wv & 3, wn = wv >> 2;  // 64-row quarter, column half
+  const int c16 = lane & 15, j4 = lane >> 4;
+
+  // This wave's sources: A blocks of row groups 2 wv, 2 wv + 1 of the tile
+  // (groups past the last row read the last group; their rows are never
+  // stored), W block wv and, for TN = 160, W block 8 + wv (waves 0, 1) or a
+  // spare copy of block wv (the others).
+  const int stages = K / kNK;
+  const bf16_t* src_a[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int ag = min((m0 + 32 * wv + 16 * h) >> 4, (M - 1) >> 4);
+    src_a[h] = A + (int64_t)ag * (K / kNK) * 512 + lane * 8;
+  }
+  const bf16_t* src_w0 = W + (int64_t)((n0 >> 4) + wv) * (K / kNK) * 512 + lane * 8;
+  const bf16_t* src_w1 =
+      W + (int64_t)((n0 >> 4) + (wv < kExtra ? 8 + wv : wv)) * (K / kNK) * 512 + lane * 8;
+  // Loads past the slice repeat its last stage (never multiplied).
+  auto issue = [&](int st, int slot) {
+    const int sc = min(st, stages - 1);
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      __builtin_amdgcn_global_load_lds(src_a[h] + sc * 512,
+                                       (lds_void_t*)(ta[slot] + (2 * wv + h) * 512), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(src_w0 + sc * 512, (lds_void_t*)(tw[slot] + wv * 512), 16,
+                                     0, 0);
+    if constexpr (kExtra > 0)
+      __builtin_amdgcn_global_load_lds(
+          src_w1 + sc * 512, (lds_void_t*)(wv < kExtra ? tw[slot] + (8 + wv) * 512 : g_nspare),
+          16, 0, 0);
+  };
+
+  f32x4_t acc[4][WB];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < WB; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  auto read_frags = [&](const bf16_t* la, const bf16_t* lw, bf16x8_t* a, bf16x8_t* w) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      a[i] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(la + (wm * 4 + i) * 512 + lane * 8));
+#pragma unroll
+    for (int j = 0; j < WB; ++j)
+      w[j] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(lw + (wn * WB + j) * 512 + lane * 8));
+  };
+  auto mfma_step = [&](const bf16x8_t* a, const bf16x8_t* w) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < WB; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], w[j], acc[i][j], 0, 0, 0);
+    // Interleave the fragment reads issued next to these MFMAs.
+    for (int g = 0; g < 4 + WB; ++g) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4 * WB - 4 - WB, 0);
+  };
+
+  // The epilogue's row of each tile row, loaded ahead of the ring so the
+  // stage waits below also cover it.
+  int erow = 0;
+  if (tid < kNM) {
+    const int m = min(m0 + tid, M - 1);
+    const int32_t* idx = MODE == kNarrowResid ? ea.res_idx : ea.out_idx;
+    erow = idx ? idx[m] : m;
+  }
+
+#pragma unroll
+  for (int st = 0; st < kNAhead; ++st) issue(st, st);
+  wait_vmcnt<(kNAhead - 1) * kLoads>();  // this wave's stage-0 loads are in LDS
+  stage_barrier();                          // ... and every wave's
+  bf16x8_t fa[2][4], fw[2][WB];
+  read_frags(ta[0], tw[0], fa[0], fw[0]);
+  // One round of the ring: stages st0 .. st0 + kNBuf - 1. In the last,
+  // partial round (MASKED) stages past the end load the last stage again and
+  // multiply nothing.
+  auto ring_round = [&](int st0, auto masked) {
+#pragma unroll
+    for (int u = 0; u < kNBuf; ++u) {
+      const int st = st0 + u;
+      wait_vmcnt<(kNAhead - 2) * kLoads>();  // this wave's loads of stage st + 1 are in LDS
+      stage_barrier();  // every wave's: stage st + 1 published, stage st - 1 read
+      issue(st + kNAhead, (u + kNAhead) % kNBuf);
+      read_frags(ta[(u + 1) % kNBuf], tw[(u + 1) % kNBuf], fa[(u + 1) & 1], fw[(u + 1) & 1]);
+      if (!decltype(masked)::value || st < stages) mfma_step(fa[u & 1], fw[u & 1]);
+    }
+  };
+  const int full_end = stages - stages % kNBuf;
+  for (int st0 = 0; st0 < full_end; st0 += kNBuf) ring_round(st0, std::false_type{});
+  if (full_end < stages) ring_round(full_end, std::true_type{});
+  wait_vmcnt<0>();  // no direct load outlives the workgroup
+
+  // The idle ring holds the epilogue's per-row values: the row of each tile
+  // row, and (residual variant) the row sums of x1^2 of each column half.
+  __syncthreads();  // every wave is done with the ring
+  int* const g_nrow = (int*)g_na0;
+  float(*const g_nss)[kNM] = (float(*)[kNM])g_na1;
+  if (tid < kNM) g_nrow[tid] = erow;
+  __syncthreads();
+  // Accumulator layout: lane (j4, c16) of block (i, j) holds rows
+  // 16 (4 wm + i) + 4 j4 + r, r < 4, of column 16 (WB wn + j) + c16.
+  const int cbase = n0 + wn * (TN / 2) + c16;
+  if constexpr (MODE == kNarrowResid) {
+    float gam[WB];
+#pragma unroll
+    for (int j = 0; j < WB; ++j) gam[j] = bf16_to_f32(ea.gamma[cbase + 16 * j]);
+    float res[4][4][WB];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int lr = wm * 64 + i * 16 + 4 * j4 + r;
+        const bf16_t* xr = ea.res_x + (int64_t)g_nrow[lr] * N + cbase;
+#pragma unroll
+        for (int j = 0; j < WB; ++j) res[i][r][j] = bf16_to_f32(xr[16 * j]);
+      }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int lr = wm * 64 + i * 16 + 4 * j4 + r;
+        const int m = m0 + lr;
+        float sq = 0.f;
+#pragma unroll
+        for (int j = 0; j < WB; ++j) {
+          const int col = cbase + 16 * j;
+          const float x1 = acc[i][j][r] + res[i][r][j];
+          sq += x1 * x1;
+          if (m < M) {
+            ea.x1[(int64_t)m * N + col] = x1;
+            ea.h[tile_off(m, col, N)] = (bf16_t)f32_to_bf16(x1 * gam[j]);
+          }
+        }
+        // Over the 16 columns c16 of this lane group, in a fixed butterfly.
+        sq += __shfl_xor(sq, 1, 16);
+        sq += __shfl_xor(sq, 2, 16);
+        sq += __shfl_xor(sq, 4, 16);
+        sq += __shfl_xor(sq, 8, 16);
+        if (c16 == 0) g_nss[wn][lr] = sq;
+      }
+    __syncthreads();
+    if (tid < kNM && m0 + tid < M)
+      ea.ss_part[(int64_t)(n0 / TN) * M + m0 + tid] = g_nss[0][tid] + g_nss[1][tid];
+  } else {
+    float x1v[4][4][WB];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = min(m0 + wm * 64 + i * 16 + 4 * j4 + r, M - 1);
+        const float* xr = ea.x1_in + (int64_t)m * N + cbase;
+#pragma unroll
+        for (int j = 0; j < WB; ++j) x1v[i][r][j] = xr[16 * j];
+      }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int lr = wm * 64 + i * 16 + 4 * j4 + r;
+        if (m0 + lr >= M) continue;
+        bf16_t* orow = ea.out + (int64_t)g_nrow[lr] * N + cbase;
+#pragma unroll
+        for (int j = 0; j < WB; ++j)
+          orow[16 * j] = (bf16_t)f32_to_bf16(x1v[i][r][j] + acc[i][j][r]);
+      }
+  }
+}
+
+template <int MODE>
+hipError_t launch_narrow(const uint16_t* A, const uint16_t* W, int M, int N, int K,
+                         const NarrowEpiArgs& ea, hipStream_t st) {
+  const int tn = narrow_tile_n(N);
+  if (tn == 0 || K % kNK != 0) return hipErrorInvalidValue;
+  const dim3 grid(((M + kNM - 1) / kNM) * (N / tn));
+  if (tn == 160)
+    COCO_LAUNCH((gemm_narrow_kernel<160, MODE>), grid, dim3(kNThreads), 0, st,
+                (const bf16_t*)A, (const bf16_t*)W, M, N, K, ea);
+  else
+    COCO_LAUNCH((gemm_narrow_kernel<128, MODE>), grid, dim3(kNThreads), 0, st,
+                (const bf16_t*)A, (const bf16_t*)W, M, N, K, ea);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int narrow_tile_n(int N) {
+  if (N > 0 && N % 128 == 0 && N / 128 <= kNMaxTiles) return 128;
+  if (N > 0 && N % 160 == 0 && N / 160 <= kNMaxTiles) return 160;
+  return 0;
+}
+
+hipError_t launch_gemm_narrow_resid_bf16(const uint16_t* A, const uint16_t* W, int M, int N,
+                                         int K, const uint16_t* res_x, const int32_t* res_idx,
+                                         const uint16_t* gamma, float* x1, uint16_t* h,
+                                         float* ss_part, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  if (!res_x || !gamma || !x1 || !h || !ss_part) return hipErrorInvalidValue;
+  NarrowEpiArgs ea{};
+  ea.res_x = res_x;
+  ea.res_idx = res_idx;
+  ea.gamma = gamma;
+  ea.x1 = x1;
+  ea.h = h;
+  ea.ss_part = ss_part;
+  return launch_narrow<kNarrowResid>(A, W, M, N, K, ea, st);
+}
+
+hipError_t launch_gemm_narrow_scatter_bf16(const uint16_t* A, const uint16_t* W, int M, int N,
+                                           int K, const float* x1, uint16_t* out,
+                                           const int32_t* out_idx, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  if (!x1 || !out) return hipErrorInvalidValue;
+  NarrowEpiArgs ea{};
+  ea.x1_in = x1;
+  ea.out = out;
+  ea.out_idx = out_idx;
+  return launch_narrow<kNarrowScatter>(A, W, M, N, K, ea, st);
+}
+
+}  // namespace coco

@@ -16,7 +16,8 @@
 //     the other waits on LDS or the barrier;
 //   * 32-deep K stages of the A and W tiles go straight from global memory
 //     to LDS (global_load_lds, 16 bytes per lane, no register staging) into
-//     a ring of four buffers, three stages in flight. Each wave fills 32 rows
+//     a ring of four buffers, three stages in flight (a fifth buffer, the
+//     whole 160 KB of LDS, measured no faster). Each wave fills 32 rows
 //     of both tiles with four 1 KB loads per stage; the tile-order blocks
 //     give each 16-lane group of a fragment read 256 contiguous bytes;
 //   * one barrier per stage: the barrier at the top of stage st publishes
@@ -38,6 +39,8 @@
 // Every output element is summed over k in ascending 16-steps within its
 // slice, independent of M and of the tile it falls in, so request-aligned
 // prefill splits give identical bits.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -47,6 +50,8 @@ namespace {
 
 constexpr int kTM = 256, kTN = 256, kTK = 32;
 constexpr int kTBuf = 4;        // LDS ring depth (stages)
+constexpr int kTAhead = kTBuf - 1;  // stages in flight
+constexpr int kSliceQuant = 128;    // K-slice granularity of the plans
 constexpr int kTThreads = 512;  // 8 waves, two per SIMD
 constexpr int kXCDs = 8;
 
@@ -68,7 +73,7 @@ __shared__ __attribute__((aligned(16))) bf16_t g_tw0[kTN * kTK], g_tw1[kTN * kTK
 // with RMSNorm_2 folded in: the row's 1/rms (bits of a float).
 __shared__ int g_row_pos[kTM], g_row_blk[kTM];
 
-enum { kTilePartial = 0, kTileSwiglu = 1, kTileQkv = 2, kTileResid = 3 };
+enum { kTilePartial = 0, kTileSwiglu = 1, kTileQkv = 2, kTileResid = 3, kTileSwigluNorm = 4 };
 constexpr int kMaxNormTiles = 32;  // d <= 32 * 256 for the folded RMSNorm_2
 
 // kTilePartial: C is the fp32 partial of K-slice blockIdx.y.
@@ -81,9 +86,9 @@ constexpr int kMaxNormTiles = 32;  // d <= 32 * 256 for the folded RMSNorm_2
 // kTileResid: one K-slice, N a multiple of 256; C = x1 = A W^T + residual
 // (fp32), H = bf16(x1 * gamma) and ea.ss_part[n0 / 256][m] = sum over the
 // tile's columns of x1^2.
-// kTileSwiglu with ea.ss_in: gate and up of row m are first scaled by
+// kTileSwigluNorm: kTileSwiglu whose gate and up of row m are first scaled by
 // 1 / sqrt(sum_t ss_in[t][m] / ea.d + ea.eps), t < ea.n_ss, in tile order.
-// k_slice is a multiple of kTK * kTBuf.
+// k_slice is a multiple of kTK.
 template <int MODE>
 __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __restrict__ A,
                                                                  const bf16_t* __restrict__ W,
@@ -91,7 +96,7 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
                                                                  bf16_t* __restrict__ H, int M,
                                                                  int N, int K, int k_slice,
                                                                  TileEpiArgs ea) {
-  constexpr bool FUSE = MODE == kTileSwiglu;
+  constexpr bool FUSE = MODE == kTileSwiglu || MODE == kTileSwigluNorm;
   bf16_t* const ta[kTBuf] = {g_ta0, g_ta1, g_ta2, g_ta3};
   bf16_t* const tw[kTBuf] = {g_tw0, g_tw1, g_tw2, g_tw3};
 
@@ -195,47 +200,60 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
   u32x2_t rinfo = {0u, 0u};
   int rrow = 0;
   float ssv[kMaxNormTiles];
-  const bool fold_norm = MODE == kTileSwiglu && ea.ss_in != nullptr;
+  constexpr bool fold_norm = MODE == kTileSwigluNorm;
   if (tid < kTM) {
     const int m = min(m0 + tid, M - 1);
     if constexpr (MODE == kTileQkv) rinfo = *(const u32x2_t*)(ea.row_info + 2 * m);
     if constexpr (MODE == kTileResid) rrow = ea.res_idx ? ea.res_idx[m] : m;
-    if (fold_norm) {
-#pragma unroll
-      for (int t = 0; t < kMaxNormTiles; ++t)
-        ssv[t] = t < ea.n_ss ? ea.ss_in[(int64_t)t * M + m] : 0.f;
-    }
   }
-
-  issue(0, 0);
-  issue(1, 1);
-  issue(2, 2);
-  // The row's 1/rms (sums in tile order), once the loads above are in.
-  float rnorm = 1.f;
-  if (fold_norm && tid < kTM) {
-    float t2 = 0.f;
+  // Every thread loads the sums of row m0 + tid % 256, all kMaxNormTiles of
+  // them (tiles past n_ss repeat the last one and are not added), with no
+  // branch around a load: the wait for them then counts only the ring loads
+  // issued after them.
+  if constexpr (fold_norm) {
+    const int m = min(m0 + (tid & (kTM - 1)), M - 1);
 #pragma unroll
     for (int t = 0; t < kMaxNormTiles; ++t)
-      if (t < ea.n_ss) t2 += ssv[t];
+      ssv[t] = ea.ss_in[(int64_t)min(t, ea.n_ss - 1) * M + m];
+  }
+
+#pragma unroll
+  for (int st = 0; st < kTAhead; ++st) issue(st, st);
+  wait_vmcnt<4 * (kTAhead - 1)>();  // this wave's stage-0 loads are in LDS
+  // The row's 1/rms (sums in tile order): its loads, older than the stage-0
+  // loads, are in too. Nothing moves across this point, so the sums are
+  // read after the wait above and need no wait of their own.
+  float rnorm = 1.f;
+  if constexpr (fold_norm) {
+    __builtin_amdgcn_sched_barrier(0);
+    float t2 = 0.f;
+#pragma unroll
+    for (int t = 0; t < kMaxNormTiles; ++t) t2 += t < ea.n_ss ? ssv[t] : 0.f;
     rnorm = 1.0f / sqrtf(t2 / (float)ea.d + ea.eps);
   }
-  wait_vmcnt<8>();  // this wave's stage-0 loads are in LDS
-  stage_barrier();  // ... and every wave's
+  stage_barrier();                   // ... and every wave's
   bf16x8_t a0[4], w0[2], a1[4], w1[2];
   read_frags(ta[0], tw[0], 0, a0, w0);
-  for (int st0 = 0; st0 < stages; st0 += kTBuf) {
+  // One round of the ring: stages st0 .. st0 + kTBuf - 1. In the last,
+  // partial round (MASKED) stages past the end load the last stage again and
+  // multiply nothing.
+  auto ring_round = [&](int st0, auto masked) {
 #pragma unroll
     for (int u = 0; u < kTBuf; ++u) {
       const int st = st0 + u;
-      wait_vmcnt<4>();  // this wave's loads of stage st + 1 are in LDS
+      const bool live = !decltype(masked)::value || st < stages;
+      wait_vmcnt<4 * (kTAhead - 2)>();  // this wave's loads of stage st + 1 are in LDS
       stage_barrier();  // every wave's: stage st + 1 published, stage st - 1 read
-      issue(st + 3, (u + 3) % kTBuf);
+      issue(st + kTAhead, (u + kTAhead) % kTBuf);
       read_frags(ta[u], tw[u], 1, a1, w1);
-      mfma_step(a0, w0);
+      if (live) mfma_step(a0, w0);
       read_frags(ta[(u + 1) % kTBuf], tw[(u + 1) % kTBuf], 0, a0, w0);
-      mfma_step(a1, w1);
+      if (live) mfma_step(a1, w1);
     }
-  }
+  };
+  const int full_end = stages - stages % kTBuf;
+  for (int st0 = 0; st0 < full_end; st0 += kTBuf) ring_round(st0, std::false_type{});
+  if (full_end < stages) ring_round(full_end, std::true_type{});
   wait_vmcnt<0>();  // no direct load outlives the workgroup
 
   if constexpr (MODE == kTileQkv) {
@@ -393,7 +411,7 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
     return;
   }
   if (FUSE) {
-    if (fold_norm) {
+    if constexpr (fold_norm) {
       if (tid < kTM) g_row_pos[tid] = __float_as_int(rnorm);
       __syncthreads();
     }
@@ -407,7 +425,7 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
           const int lr = wm * 128 + i * 32 + 8 * jj + 4 * hi + r;
           const int m = m0 + lr;
           float g = acc[i][0][4 * jj + r], u = acc[i][1][4 * jj + r];
-          if (fold_norm) {
+          if constexpr (fold_norm) {
             const float rs = __int_as_float(g_row_pos[lr]);
             g *= rs;
             u *= rs;
@@ -443,14 +461,14 @@ int tile_splits(int N, int K) {
   int S = (K + 4096) / 8192;
   if (S < 1) S = 1;
   if (S > 4) S = 4;
-  while (S > 1 && (K / (kTK * kTBuf)) % S != 0) --S;
+  while (S > 1 && (K / kSliceQuant) % S != 0) --S;
   return S;  // 1..4: the split counts the epilogues are built for
 }
 
 hipError_t launch_gemm_tile_bf16(const uint16_t* A, const uint16_t* W, float* C, int M, int N,
                                  int K, int S, hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  if (S < 1 || K % (kTK * kTBuf * S) != 0) return hipErrorInvalidValue;
+  if (S < 1 || K % (kSliceQuant * S) != 0) return hipErrorInvalidValue;
   const int tiles = ((M + kTM - 1) / kTM) * ((N + kTN - 1) / kTN);
   COCO_LAUNCH(gemm_tile_kernel<kTilePartial>, dim3(tiles, S), dim3(kTThreads), 0, st, A,
                      W, C, nullptr, M, N, K, K / S, TileEpiArgs{});
@@ -459,26 +477,30 @@ hipError_t launch_gemm_tile_bf16(const uint16_t* A, const uint16_t* W, float* C,
 
 hipError_t launch_gemm_tile_swiglu_bf16(const uint16_t* A, const uint16_t* W_gate_up,
                                         uint16_t* H, int M, int F, int K, const float* ss_in,
-                                        float eps, hipStream_t st) {
+                                        int ss_tiles, float eps, hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  if (F % (kTN / 2) != 0 || K % (kTK * kTBuf) != 0 || tile_splits(2 * F, K) != 1)
+  if (F % (kTN / 2) != 0 || K % kSliceQuant != 0 || tile_splits(2 * F, K) != 1)
     return hipErrorInvalidValue;
   TileEpiArgs ea{};
   if (ss_in) {
-    if (K % kTN != 0 || K / kTN > kMaxNormTiles) return hipErrorInvalidValue;
+    if (ss_tiles < 1 || ss_tiles > kMaxNormTiles) return hipErrorInvalidValue;
     ea.ss_in = ss_in;
-    ea.n_ss = K / kTN;
+    ea.n_ss = ss_tiles;
     ea.d = K;
     ea.eps = eps;
   }
   const int tiles = ((M + kTM - 1) / kTM) * (2 * F / kTN);
-  COCO_LAUNCH(gemm_tile_kernel<kTileSwiglu>, dim3(tiles, 1), dim3(kTThreads), 0, st, A,
-                     W_gate_up, nullptr, H, M, 2 * F, K, K, ea);
+  if (ss_in)
+    COCO_LAUNCH(gemm_tile_kernel<kTileSwigluNorm>, dim3(tiles, 1), dim3(kTThreads), 0, st, A,
+                W_gate_up, nullptr, H, M, 2 * F, K, K, ea);
+  else
+    COCO_LAUNCH(gemm_tile_kernel<kTileSwiglu>, dim3(tiles, 1), dim3(kTThreads), 0, st, A,
+                W_gate_up, nullptr, H, M, 2 * F, K, K, ea);
   return hipGetLastError();
 }
 
 bool tile_norm2_foldable(int d, int qdim, int F) {
-  return d % kTN == 0 && d / kTN <= kMaxNormTiles && qdim % (kTK * kTBuf) == 0 &&
+  return d % kTN == 0 && d / kTN <= kMaxNormTiles && qdim % kSliceQuant == 0 &&
          tile_splits(d, qdim) == 1 && F % (kTN / 2) == 0 && tile_splits(2 * F, d) == 1;
 }
 
@@ -487,7 +509,7 @@ hipError_t launch_gemm_tile_resid_bf16(const uint16_t* A, const uint16_t* W, int
                                        const uint16_t* gamma, float* x1, uint16_t* h,
                                        float* ss_part, hipStream_t st) {
   if (M <= 0) return hipSuccess;
-  if (N % kTN != 0 || N / kTN > kMaxNormTiles || K % (kTK * kTBuf) != 0 ||
+  if (N % kTN != 0 || N / kTN > kMaxNormTiles || K % kSliceQuant != 0 ||
       tile_splits(N, K) != 1 || !res_x || !gamma || !x1 || !h || !ss_part)
     return hipErrorInvalidValue;
   TileEpiArgs ea{};
@@ -503,7 +525,7 @@ hipError_t launch_gemm_tile_resid_bf16(const uint16_t* A, const uint16_t* W, int
 
 bool tile_qkv_fusable(int Hq, int Hkv, int K) {
   const int N = (Hq + 2 * Hkv) * 128;
-  return N % kTN == 0 && K % (kTK * kTBuf) == 0 && tile_splits(N, K) == 1;
+  return N % kTN == 0 && K % kSliceQuant == 0 && tile_splits(N, K) == 1;
 }
 
 hipError_t launch_gemm_tile_qkv_bf16(const uint16_t* A, const uint16_t* W_qkv, int M, int K,

@@ -163,10 +163,10 @@ struct TileEpiArgs {
 // where W_gate_up = [W_g; W_u] is [2F][K]; only for tile_splits(2F, K) == 1.
 // With ss_in non-null (RMSNorm_2 folded in: A = bf16(x1 * gamma)), gate and
 // up of row m are first scaled by 1 / sqrt(sum_t ss_in[t][m] / K + eps),
-// t < K / 256 in order.
+// t < ss_tiles (at most 32) in order.
 hipError_t launch_gemm_tile_swiglu_bf16(const uint16_t* A, const uint16_t* W_gate_up,
                                         uint16_t* H, int M, int F, int K, const float* ss_in,
-                                        float eps, hipStream_t st);
+                                        int ss_tiles, float eps, hipStream_t st);
 // Prefill QKV projection with the QKV epilogue in the GEMM's own epilogue
 // (head_dim 128): RoPE on query and key heads with the rotations of the RoPE
 // table, queries to q_out [M][Hq*128] in bf16, keys and values into the
@@ -184,6 +184,37 @@ hipError_t launch_gemm_tile_resid_bf16(const uint16_t* A, const uint16_t* W, int
                                        const uint16_t* res_x, const int32_t* res_idx,
                                        const uint16_t* gamma, float* x1, uint16_t* h,
                                        float* ss_part, hipStream_t st);
+
+// Narrow-output prefill GEMMs (N = the model width): 256 x TN tiles,
+// TN = narrow_tile_n(N) (128 or 160, N / TN <= 32 column tiles; 0: no plan),
+// unsplit along K (K a multiple of 128), A and W in tile order.
+int narrow_tile_n(int N);
+struct NarrowEpiArgs {
+  // residual variant (O projection)
+  const uint16_t* res_x = nullptr;   // residual rows [*][N] (bf16)
+  const int32_t* res_idx = nullptr;  // row m's residual row (null: m)
+  const uint16_t* gamma = nullptr;   // RMSNorm_2 gains [N]
+  float* x1 = nullptr;               // [M][N] fp32
+  uint16_t* h = nullptr;             // bf16(x1 * gamma), tile order
+  float* ss_part = nullptr;          // [N / TN][M] per-tile row sums of x1^2
+  // scatter variant (down projection)
+  const float* x1_in = nullptr;      // [M][N] fp32 residual
+  uint16_t* out = nullptr;           // output rows [*][N] (bf16)
+  const int32_t* out_idx = nullptr;  // row m's output row (null: m)
+};
+// O projection with the residual and the first half of RMSNorm_2 in its
+// epilogue: x1[m] = A W^T + res_x[res_idx ? res_idx[m] : m] (fp32),
+// h[m] = bf16(x1 * gamma) in tile order, ss_part[t][m] = sum of x1^2 over
+// columns TN t .. TN t + TN - 1, summed in a fixed order.
+hipError_t launch_gemm_narrow_resid_bf16(const uint16_t* A, const uint16_t* W, int M, int N,
+                                         int K, const uint16_t* res_x, const int32_t* res_idx,
+                                         const uint16_t* gamma, float* x1, uint16_t* h,
+                                         float* ss_part, hipStream_t st);
+// Down projection with the residual and the scatter in its epilogue:
+// out[out_idx ? out_idx[m] : m] = bf16(x1[m] + A W^T).
+hipError_t launch_gemm_narrow_scatter_bf16(const uint16_t* A, const uint16_t* W, int M, int N,
+                                           int K, const float* x1, uint16_t* out,
+                                           const int32_t* out_idx, hipStream_t st);
 
 // part[0][m][n] = sum_k A[m][k] * W[n][k], fp32 (tiny fp32 configurations).
 hipError_t launch_gemm_f32(const float* A, const float* W, float* part, int M, int N, int K,
