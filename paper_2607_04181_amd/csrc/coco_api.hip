@@ -811,7 +811,12 @@ int run_span(coco_layer* H, const Work& W, int first, int nl, T* hidden, const i
     // SwiGLU MLP (prefill: SwiGLU in the gate/up GEMM's epilogue when the
     // GEMM is not split along K).
     if (fused_swiglu<T>(pre, F, d)) {
-      if (pre) {
+      if (pre && fold_norm2 && narrow_swiglu_fits(F, d)) {
+        TIMED(COCO_K_GEMM_GATE_UP,
+              HIPCHK(launch_gemm_narrow_swiglu_bf16((const uint16_t*)h2,
+                                                    (const uint16_t*)w.w_gate_up, (uint16_t*)u,
+                                                    M, F, d, W.ss, norm_tiles, c.rms_eps, st)));
+      } else if (pre) {
         TIMED(COCO_K_GEMM_GATE_UP,
               HIPCHK(launch_gemm_tile_swiglu_bf16((const bf16_t*)h2, (const bf16_t*)w.w_gate_up,
                                                   (bf16_t*)u, M, F, d,

@@ -47,43 +47,49 @@ namespace {
 
 constexpr int kNM = 256;        // tile rows
 constexpr int kNK = 32;         // k per stage
-constexpr int kNBuf = 6;        // LDS ring slots (even: fragment registers alternate)
-constexpr int kNAhead = kNBuf - 1;  // stages in flight
 constexpr int kNThreads = 512;  // 8 waves, two per SIMD
 constexpr int kNXCDs = 8;
-constexpr int kNMaxTN = 160;
 constexpr int kNMaxTiles = 32;  // column tiles (the gate/up fold's limit)
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-// One LDS object per ring slot, so the compiler tracks each slot's pending
-// direct loads on its own and never drains the ring before a fragment read.
-__shared__ __attribute__((aligned(16))) bf16_t g_na0[kNM * kNK], g_na1[kNM * kNK],
-    g_na2[kNM * kNK], g_na3[kNM * kNK], g_na4[kNM * kNK], g_na5[kNM * kNK];
-__shared__ __attribute__((aligned(16))) bf16_t g_nw0[kNMaxTN * kNK], g_nw1[kNMaxTN * kNK],
-    g_nw2[kNMaxTN * kNK], g_nw3[kNMaxTN * kNK], g_nw4[kNMaxTN * kNK], g_nw5[kNMaxTN * kNK];
-// Target of the loads that only keep the per-wave load count uniform (never
-// read; several waves may write it at once).
-__shared__ __attribute__((aligned(16))) bf16_t g_nspare[512];
+// LDS ring slots for a tile width: as many stages of 256 x 32 A and TN x 32
+// W as fit beside the spare block in 160 KB.
+constexpr int narrow_slots(int TN) { return TN <= 160 ? 6 : 5; }
 
-enum { kNarrowResid = 0, kNarrowScatter = 1 };
+enum { kNarrowResid = 0, kNarrowScatter = 1, kNarrowSwiglu = 2 };
 
 template <int TN, int MODE>
 __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __restrict__ A,
                                                                  const bf16_t* __restrict__ W,
                                                                  int M, int N, int K,
                                                                  NarrowEpiArgs ea) {
-  static_assert(TN % 32 == 0 && TN <= kNMaxTN && TN / 16 >= 8, "tile width");
+  static_assert(TN % 32 == 0 && TN / 16 >= 8 && TN / 16 <= 16, "tile width");
+  static_assert(MODE != kNarrowSwiglu || TN % 64 == 0, "SwiGLU pairs gate and up blocks");
   constexpr int WB = TN / 32;          // 16-column blocks per wave
   constexpr int kWBlocks = TN / 16;    // W blocks per stage
   constexpr int kExtra = kWBlocks - 8; // waves that copy a second W block
-  // Loads per stage and wave. With a second W block (TN = 160) every wave
+  // Loads per stage and wave. With a second W block (TN > 128) every wave
   // issues one: waves past kExtra copy their first block again into a spare
   // block that is never read, so all waves wait on the same counts and the
   // loop has no branch around a load.
   constexpr int kLoads = kExtra > 0 ? 4 : 3;
-  bf16_t* const ta[kNBuf] = {g_na0, g_na1, g_na2, g_na3, g_na4, g_na5};
-  bf16_t* const tw[kNBuf] = {g_nw0, g_nw1, g_nw2, g_nw3, g_nw4, g_nw5};
+  constexpr int kBuf = narrow_slots(TN);
+  constexpr int kAhead = kBuf - 1;  // stages in flight
+  // Stages per unrolled round: fragment registers alternate with the stage's
+  // parity, so a round is an even number of stages.
+  constexpr int kRound = kBuf % 2 ? 2 * kBuf : kBuf;
+  // One LDS object per ring slot, so the compiler tracks each slot's pending
+  // direct loads on its own and never drains the ring before a fragment read.
+  __shared__ __attribute__((aligned(16))) bf16_t sa0[kNM * kNK], sa1[kNM * kNK],
+      sa2[kNM * kNK], sa3[kNM * kNK], sa4[kNM * kNK], sa5[kNM * kNK];
+  __shared__ __attribute__((aligned(16))) bf16_t sw0[TN * kNK], sw1[TN * kNK], sw2[TN * kNK],
+      sw3[TN * kNK], sw4[TN * kNK], sw5[TN * kNK];
+  // Target of the loads that only keep the per-wave load count uniform
+  // (never read; several waves may write it at once).
+  __shared__ __attribute__((aligned(16))) bf16_t spare[512];
+  bf16_t* const ta[6] = {sa0, sa1, sa2, sa3, sa4, sa5};
+  bf16_t* const tw[6] = {sw0, sw1, sw2, sw3, sw4, sw5};
 
   const int tiles_m = (M + kNM - 1) / kNM;
   const int nb = gridDim.x;
@@ -99,10 +105,23 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
   const int wm = wv & 3, wn = wv >> 2;  // 64-row quarter, column half
   const int c16 = lane & 15, j4 = lane >> 4;
 
+  // W block (16 rows) of the tile's block b. SwiGLU: W is [W_g; W_u], [2F][K];
+  // the tile holds outputs o0 .. o0 + TN/2 - 1, and the WB blocks of column
+  // half h are the gate blocks of outputs o0 + TN/4 h + 16 q (q < WB/2), then
+  // the matching up blocks, so a lane holds both factors of its outputs.
+  const int F = N / 2, o0 = n0 / 2;
+  auto w_block = [&](int blk) -> int {
+    if constexpr (MODE == kNarrowSwiglu) {
+      const int h = blk / WB, r = blk % WB;
+      const int o = o0 + h * (TN / 4) + 16 * (r % (WB / 2));
+      return ((r < WB / 2 ? 0 : F) + o) >> 4;
+    }
+    return (n0 >> 4) + blk;
+  };
   // This wave's sources: A blocks of row groups 2 wv, 2 wv + 1 of the tile
   // (groups past the last row read the last group; their rows are never
-  // stored), W block wv and, for TN = 160, W block 8 + wv (waves 0, 1) or a
-  // spare copy of block wv (the others).
+  // stored), W block wv and, for TN > 128, W block 8 + wv (waves below
+  // kExtra) or a spare copy of block wv (the others).
   const int stages = K / kNK;
   const bf16_t* src_a[2];
 #pragma unroll
@@ -110,9 +129,9 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
     const int ag = min((m0 + 32 * wv + 16 * h) >> 4, (M - 1) >> 4);
     src_a[h] = A + (int64_t)ag * (K / kNK) * 512 + lane * 8;
   }
-  const bf16_t* src_w0 = W + (int64_t)((n0 >> 4) + wv) * (K / kNK) * 512 + lane * 8;
+  const bf16_t* src_w0 = W + (int64_t)w_block(wv) * (K / kNK) * 512 + lane * 8;
   const bf16_t* src_w1 =
-      W + (int64_t)((n0 >> 4) + (wv < kExtra ? 8 + wv : wv)) * (K / kNK) * 512 + lane * 8;
+      W + (int64_t)w_block(wv < kExtra ? 8 + wv : wv) * (K / kNK) * 512 + lane * 8;
   // Loads past the slice repeat its last stage (never multiplied).
   auto issue = [&](int st, int slot) {
     const int sc = min(st, stages - 1);
@@ -124,7 +143,7 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
                                      0, 0);
     if constexpr (kExtra > 0)
       __builtin_amdgcn_global_load_lds(
-          src_w1 + sc * 512, (lds_void_t*)(wv < kExtra ? tw[slot] + (8 + wv) * 512 : g_nspare),
+          src_w1 + sc * 512, (lds_void_t*)(wv < kExtra ? tw[slot] + (8 + wv) * 512 : spare),
           16, 0, 0);
   };
 
@@ -156,46 +175,65 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
     __builtin_amdgcn_sched_group_barrier(0x008, 4 * WB - 4 - WB, 0);
   };
 
-  // The epilogue's row of each tile row, loaded ahead of the ring so the
-  // stage waits below also cover it.
+  // The epilogue's row of each tile row (residual and scatter variants) or
+  // RMSNorm_2's per-tile sums of the row (SwiGLU: every thread loads those of
+  // row m0 + tid % 256, all kNMaxTiles of them, tiles past n_ss repeating the
+  // last one), loaded ahead of the ring with no branch around a load, so the
+  // first stage wait below covers them.
   int erow = 0;
-  if (tid < kNM) {
+  float ssv[kNMaxTiles];
+  if constexpr (MODE == kNarrowSwiglu) {
+    const int m = min(m0 + (tid & (kNM - 1)), M - 1);
+#pragma unroll
+    for (int t = 0; t < kNMaxTiles; ++t) ssv[t] = ea.ss_in[(int64_t)min(t, ea.n_ss - 1) * M + m];
+  } else if (tid < kNM) {
     const int m = min(m0 + tid, M - 1);
     const int32_t* idx = MODE == kNarrowResid ? ea.res_idx : ea.out_idx;
     erow = idx ? idx[m] : m;
   }
 
 #pragma unroll
-  for (int st = 0; st < kNAhead; ++st) issue(st, st);
-  wait_vmcnt<(kNAhead - 1) * kLoads>();  // this wave's stage-0 loads are in LDS
-  stage_barrier();                          // ... and every wave's
+  for (int st = 0; st < kAhead; ++st) issue(st, st);
+  wait_vmcnt<(kAhead - 1) * kLoads>();  // this wave's stage-0 loads are in LDS
+  // SwiGLU: the row's 1/rms (sums in tile order). Its loads are older than
+  // the stage-0 loads, so they are in too; nothing moves across this point.
+  float rnorm = 1.f;
+  if constexpr (MODE == kNarrowSwiglu) {
+    __builtin_amdgcn_sched_barrier(0);
+    float t2 = 0.f;
+#pragma unroll
+    for (int t = 0; t < kNMaxTiles; ++t) t2 += t < ea.n_ss ? ssv[t] : 0.f;
+    rnorm = 1.0f / sqrtf(t2 / (float)K + ea.eps);
+  }
+  stage_barrier();  // every wave's stage-0 loads are in LDS
   bf16x8_t fa[2][4], fw[2][WB];
   read_frags(ta[0], tw[0], fa[0], fw[0]);
-  // One round of the ring: stages st0 .. st0 + kNBuf - 1. In the last,
-  // partial round (MASKED) stages past the end load the last stage again and
-  // multiply nothing.
+  // One unrolled round: stages st0 .. st0 + kRound - 1. In the last, partial
+  // round (masked) stages past the end load the last stage again and multiply
+  // nothing.
   auto ring_round = [&](int st0, auto masked) {
 #pragma unroll
-    for (int u = 0; u < kNBuf; ++u) {
+    for (int u = 0; u < kRound; ++u) {
       const int st = st0 + u;
-      wait_vmcnt<(kNAhead - 2) * kLoads>();  // this wave's loads of stage st + 1 are in LDS
+      wait_vmcnt<(kAhead - 2) * kLoads>();  // this wave's loads of stage st + 1 are in LDS
       stage_barrier();  // every wave's: stage st + 1 published, stage st - 1 read
-      issue(st + kNAhead, (u + kNAhead) % kNBuf);
-      read_frags(ta[(u + 1) % kNBuf], tw[(u + 1) % kNBuf], fa[(u + 1) & 1], fw[(u + 1) & 1]);
+      issue(st + kAhead, (u + kAhead) % kBuf);
+      read_frags(ta[(u + 1) % kBuf], tw[(u + 1) % kBuf], fa[(u + 1) & 1], fw[(u + 1) & 1]);
       if (!decltype(masked)::value || st < stages) mfma_step(fa[u & 1], fw[u & 1]);
     }
   };
-  const int full_end = stages - stages % kNBuf;
-  for (int st0 = 0; st0 < full_end; st0 += kNBuf) ring_round(st0, std::false_type{});
+  const int full_end = stages - stages % kRound;
+  for (int st0 = 0; st0 < full_end; st0 += kRound) ring_round(st0, std::false_type{});
   if (full_end < stages) ring_round(full_end, std::true_type{});
   wait_vmcnt<0>();  // no direct load outlives the workgroup
 
   // The idle ring holds the epilogue's per-row values: the row of each tile
-  // row, and (residual variant) the row sums of x1^2 of each column half.
+  // row (SwiGLU: its 1/rms), and (residual variant) the row sums of x1^2 of
+  // each column half.
   __syncthreads();  // every wave is done with the ring
-  int* const g_nrow = (int*)g_na0;
-  float(*const g_nss)[kNM] = (float(*)[kNM])g_na1;
-  if (tid < kNM) g_nrow[tid] = erow;
+  int* const g_nrow = (int*)sa0;
+  float(*const g_nss)[kNM] = (float(*)[kNM])sa1;
+  if (tid < kNM) g_nrow[tid] = MODE == kNarrowSwiglu ? __float_as_int(rnorm) : erow;
   __syncthreads();
   // Accumulator layout: lane (j4, c16) of block (i, j) holds rows
   // 16 (4 wm + i) + 4 j4 + r, r < 4, of column 16 (WB wn + j) + c16.
@@ -241,6 +279,24 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
     __syncthreads();
     if (tid < kNM && m0 + tid < M)
       ea.ss_part[(int64_t)(n0 / TN) * M + m0 + tid] = g_nss[0][tid] + g_nss[1][tid];
+  } else if constexpr (MODE == kNarrowSwiglu) {
+    // Gate in blocks q < WB/2, up in blocks WB/2 + q, of outputs
+    // o0 + TN/4 wn + 16 q + c16; h = silu(gate) * up in tile order [M][F].
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int lr = wm * 64 + i * 16 + 4 * j4 + r;
+        const int m = m0 + lr;
+        if (m >= M) continue;
+        const float rs = __int_as_float(g_nrow[lr]);
+#pragma unroll
+        for (int q = 0; q < WB / 2; ++q) {
+          const float g = acc[i][q][r] * rs, u = acc[i][WB / 2 + q][r] * rs;
+          const int o = o0 + wn * (TN / 4) + 16 * q + c16;
+          ea.h[tile_off(m, o, F)] = (bf16_t)f32_to_bf16(g / (1.0f + expf(-g)) * u);
+        }
+      }
   } else {
     float x1v[4][4][WB];
 #pragma unroll
@@ -267,17 +323,23 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
 }
 
 template <int MODE>
-hipError_t launch_narrow(const uint16_t* A, const uint16_t* W, int M, int N, int K,
+hipError_t launch_narrow(int tn, const uint16_t* A, const uint16_t* W, int M, int N, int K,
                          const NarrowEpiArgs& ea, hipStream_t st) {
-  const int tn = narrow_tile_n(N);
-  if (tn == 0 || K % kNK != 0) return hipErrorInvalidValue;
+  if (tn == 0 || N % tn != 0 || K % kNK != 0) return hipErrorInvalidValue;
   const dim3 grid(((M + kNM - 1) / kNM) * (N / tn));
-  if (tn == 160)
+  if constexpr (MODE == kNarrowSwiglu) {
+    if (tn != 192) return hipErrorInvalidValue;
+    COCO_LAUNCH((gemm_narrow_kernel<192, MODE>), grid, dim3(kNThreads), 0, st,
+                (const bf16_t*)A, (const bf16_t*)W, M, N, K, ea);
+  } else if (tn == 160) {
     COCO_LAUNCH((gemm_narrow_kernel<160, MODE>), grid, dim3(kNThreads), 0, st,
                 (const bf16_t*)A, (const bf16_t*)W, M, N, K, ea);
-  else
+  } else if (tn == 128) {
     COCO_LAUNCH((gemm_narrow_kernel<128, MODE>), grid, dim3(kNThreads), 0, st,
                 (const bf16_t*)A, (const bf16_t*)W, M, N, K, ea);
+  } else {
+    return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
@@ -302,7 +364,7 @@ hipError_t launch_gemm_narrow_resid_bf16(const uint16_t* A, const uint16_t* W, i
   ea.x1 = x1;
   ea.h = h;
   ea.ss_part = ss_part;
-  return launch_narrow<kNarrowResid>(A, W, M, N, K, ea, st);
+  return launch_narrow<kNarrowResid>(narrow_tile_n(N), A, W, M, N, K, ea, st);
 }
 
 hipError_t launch_gemm_narrow_scatter_bf16(const uint16_t* A, const uint16_t* W, int M, int N,
@@ -314,7 +376,23 @@ hipError_t launch_gemm_narrow_scatter_bf16(const uint16_t* A, const uint16_t* W,
   ea.x1_in = x1;
   ea.out = out;
   ea.out_idx = out_idx;
-  return launch_narrow<kNarrowScatter>(A, W, M, N, K, ea, st);
+  return launch_narrow<kNarrowScatter>(narrow_tile_n(N), A, W, M, N, K, ea, st);
+}
+
+bool narrow_swiglu_fits(int F, int K) { return F > 0 && (2 * F) % 192 == 0 && K % kNK == 0; }
+
+hipError_t launch_gemm_narrow_swiglu_bf16(const uint16_t* A, const uint16_t* W_gate_up,
+                                          uint16_t* H, int M, int F, int K, const float* ss_in,
+                                          int ss_tiles, float eps, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  if (!narrow_swiglu_fits(F, K) || !H || !ss_in || ss_tiles < 1 || ss_tiles > kNMaxTiles)
+    return hipErrorInvalidValue;
+  NarrowEpiArgs ea{};
+  ea.h = H;
+  ea.ss_in = ss_in;
+  ea.n_ss = ss_tiles;
+  ea.eps = eps;
+  return launch_narrow<kNarrowSwiglu>(192, A, W_gate_up, M, 2 * F, K, ea, st);
 }
 
 }  // namespace coco

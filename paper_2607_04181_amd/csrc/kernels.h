@@ -201,6 +201,11 @@ struct NarrowEpiArgs {
   const float* x1_in = nullptr;      // [M][N] fp32 residual
   uint16_t* out = nullptr;           // output rows [*][N] (bf16)
   const int32_t* out_idx = nullptr;  // row m's output row (null: m)
+  // SwiGLU variant (gate/up projection, RMSNorm_2 folded in); h above is
+  // its output [M][N / 2] in tile order
+  const float* ss_in = nullptr;      // [n_ss][M] from the residual variant
+  int n_ss = 0;
+  float eps = 0.f;
 };
 // O projection with the residual and the first half of RMSNorm_2 in its
 // epilogue: x1[m] = A W^T + res_x[res_idx ? res_idx[m] : m] (fp32),
@@ -210,6 +215,15 @@ hipError_t launch_gemm_narrow_resid_bf16(const uint16_t* A, const uint16_t* W, i
                                          int K, const uint16_t* res_x, const int32_t* res_idx,
                                          const uint16_t* gamma, float* x1, uint16_t* h,
                                          float* ss_part, hipStream_t st);
+// Gate/up projection with RMSNorm_2's 1/rms and the SwiGLU in its epilogue,
+// on 256 x 192 tiles (96 outputs each): H[m] = bf16(silu(g) * u) in tile
+// order [M][F], where (g, u) = (A W_g^T, A W_u^T)[m] / sqrt(sum_t ss_in[t][m]
+// / K + eps), t < ss_tiles (at most 32) in order, and W_gate_up = [W_g; W_u]
+// is [2F][K]. Only when narrow_swiglu_fits(F, K): 2F a multiple of 192.
+bool narrow_swiglu_fits(int F, int K);
+hipError_t launch_gemm_narrow_swiglu_bf16(const uint16_t* A, const uint16_t* W_gate_up,
+                                          uint16_t* H, int M, int F, int K, const float* ss_in,
+                                          int ss_tiles, float eps, hipStream_t st);
 // Down projection with the residual and the scatter in its epilogue:
 // out[out_idx ? out_idx[m] : m] = bf16(x1[m] + A W^T).
 hipError_t launch_gemm_narrow_scatter_bf16(const uint16_t* A, const uint16_t* W, int M, int N,
