@@ -714,7 +714,13 @@ int run_span(coco_layer* H, const Work& W, int first, int nl, T* hidden, const i
     // are (hidden[row_idx] in the first layer of the call), so no copy of
     // them is made.
     const bool fold_norm = !pre && std::is_same<T, bf16_t>::value;
-    const bool fuse_qkv = pre && std::is_same<T, bf16_t>::value && tile_qkv_fusable(Hq, Hkv, d);
+    // Prefill QKV projection with RoPE and the cache append in its epilogue:
+    // the narrow-tile GEMM (whole rotation pairs per tile) when the head
+    // count has a plan, else the 256 x 256 tile GEMM.
+    const bool narrow_qkv =
+        pre && std::is_same<T, bf16_t>::value && hd == 128 && narrow_qkv_tile_n(Hq, Hkv, d) != 0;
+    const bool fuse_qkv =
+        narrow_qkv || (pre && std::is_same<T, bf16_t>::value && tile_qkv_fusable(Hq, Hkv, d));
     // Prefill O and down projections on the narrow-tile GEMM (256 x d/32
     // tiles, unsplit), when d has such a plan and the SwiGLU runs in the
     // gate/up epilogue: the O epilogue then folds in the residual and
@@ -755,6 +761,18 @@ int run_span(coco_layer* H, const Work& W, int first, int nl, T* hidden, const i
                                                 (const bf16_t*)w.gamma_attn,
                                                 (const bf16_t*)w.w_qkv, W.part, W.ss, M, nqkv, d,
                                                 plan, st)));
+    } else if (narrow_qkv) {
+      NarrowEpiArgs qa;
+      qa.row_info = W.row_info;
+      qa.rope = H->rope;
+      qa.q_out = (uint16_t*)q;
+      qa.k_cache = (uint16_t*)w.k_cache;
+      qa.v_cache = (uint16_t*)w.v_cache;
+      qa.Hq = Hq;
+      qa.Hkv = Hkv;
+      TIMED(COCO_K_GEMM_QKV,
+            HIPCHK(launch_gemm_narrow_qkv_bf16((const uint16_t*)h, (const uint16_t*)w.w_qkv, M,
+                                               d, qa, st)));
     } else if (fuse_qkv) {
       // Prefill (bf16, QKV projection not split along K): RoPE and the cache
       // append run in the GEMM's epilogue.

@@ -57,7 +57,7 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 // W as fit beside the spare block in 160 KB.
 constexpr int narrow_slots(int TN) { return TN <= 160 ? 6 : 5; }
 
-enum { kNarrowResid = 0, kNarrowScatter = 1, kNarrowSwiglu = 2 };
+enum { kNarrowResid = 0, kNarrowScatter = 1, kNarrowSwiglu = 2, kNarrowQkv = 3 };
 
 template <int TN, int MODE>
 __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __restrict__ A,
@@ -66,6 +66,7 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
                                                                  NarrowEpiArgs ea) {
   static_assert(TN % 32 == 0 && TN / 16 >= 8 && TN / 16 <= 16, "tile width");
   static_assert(MODE != kNarrowSwiglu || TN % 64 == 0, "SwiGLU pairs gate and up blocks");
+  static_assert(MODE != kNarrowQkv || (TN >= 160 && TN <= 224), "QKV exchange areas");
   constexpr int WB = TN / 32;          // 16-column blocks per wave
   constexpr int kWBlocks = TN / 16;    // W blocks per stage
   constexpr int kExtra = kWBlocks - 8; // waves that copy a second W block
@@ -115,6 +116,16 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
       const int h = blk / WB, r = blk % WB;
       const int o = o0 + h * (TN / 4) + 16 * (r % (WB / 2));
       return ((r < WB / 2 ? 0 : F) + o) >> 4;
+    }
+    if constexpr (MODE == kNarrowQkv) {
+      // Rotation pairs: pair p = 64 hh + j holds dims j and j + 64 of head hh.
+      // The tile holds pairs TN/2 (n0/TN) .. + TN/2 - 1 as WB groups of 16;
+      // column half 0 holds the j dims of group q in block q, half 1 the
+      // j + 64 dims, so both dims of a pair sit in the same lane of the two
+      // waves of a row quarter.
+      const int h = blk / WB, q = blk % WB;
+      const int p0 = 16 * ((n0 / TN) * WB + q);
+      return ((p0 >> 6) * 128 + (p0 & 63) + 64 * h) >> 4;
     }
     return (n0 >> 4) + blk;
   };
@@ -181,8 +192,11 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
   // last one), loaded ahead of the ring with no branch around a load, so the
   // first stage wait below covers them.
   int erow = 0;
+  u32x2_t rinfo = {0u, 0u};
   float ssv[kNMaxTiles];
-  if constexpr (MODE == kNarrowSwiglu) {
+  if constexpr (MODE == kNarrowQkv) {
+    if (tid < kNM) rinfo = *(const u32x2_t*)(ea.row_info + 2 * min(m0 + tid, M - 1));
+  } else if constexpr (MODE == kNarrowSwiglu) {
     const int m = min(m0 + (tid & (kNM - 1)), M - 1);
 #pragma unroll
     for (int t = 0; t < kNMaxTiles; ++t) ssv[t] = ea.ss_in[(int64_t)min(t, ea.n_ss - 1) * M + m];
@@ -233,7 +247,13 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
   __syncthreads();  // every wave is done with the ring
   int* const g_nrow = (int*)sa0;
   float(*const g_nss)[kNM] = (float(*)[kNM])sa1;
-  if (tid < kNM) g_nrow[tid] = MODE == kNarrowSwiglu ? __float_as_int(rnorm) : erow;
+  if constexpr (MODE == kNarrowQkv) {
+    // (position clamped to the RoPE table, cache block) of each tile row, at
+    // the end of slot 4 (its first 14 KB stage output rows below)
+    if (tid < kNM) ((u32x2_t*)(sa4 + kNM * kNK) - kNM)[tid] = rinfo;
+  } else {
+    if (tid < kNM) g_nrow[tid] = MODE == kNarrowSwiglu ? __float_as_int(rnorm) : erow;
+  }
   __syncthreads();
   // Accumulator layout: lane (j4, c16) of block (i, j) holds rows
   // 16 (4 wm + i) + 4 j4 + r, r < 4, of column 16 (WB wn + j) + c16.
@@ -279,6 +299,190 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
     __syncthreads();
     if (tid < kNM && m0 + tid < M)
       ea.ss_part[(int64_t)(n0 / TN) * M + m0 + tid] = g_nss[0][tid] + g_nss[1][tid];
+  } else if constexpr (MODE == kNarrowQkv) {
+    // Wave (wm, 0) holds dims j of the WB pair groups of its rows, wave
+    // (wm, 1) the dims j + 64. The first QA groups are rotated by wave
+    // (wm, 0), the rest by wave (wm, 1): each hands the other the halves it
+    // lacks through LDS ([group][i][r][lane] floats, conflict-free). The
+    // rotated bf16 values go back into LDS as [row][group][half][16 dims]
+    // and leave in 16-byte pieces of 8 dims: queries to q_out [M][Hq][128],
+    // keys (rotated) to their cache slot (block, position % 16), both 8
+    // contiguous dims; values (not rotated) element by element.
+    constexpr int kHd = 128, kTile = kBlockTokens * kHd;
+    constexpr int QA = (WB + 1) / 2;
+    static_assert(32 * TN <= TN * kNK && 32 * TN + 4 * kNM <= kNM * kNK,
+                  "32 staged rows fit a W slot, and slot 4 beside the row slots");
+    float* const x_hi =  // dims j + 64 of groups q < QA
+        (float*)(wm == 0 ? sa0 : wm == 1 ? sa1 : wm == 2 ? sa2 : sa3);
+    float* const x_lo =  // dims j of groups q >= QA
+        (float*)(wm == 0 ? sw0 : wm == 1 ? sw1 : wm == 2 ? sw2 : sw3);
+    const u32x2_t* const slots = (const u32x2_t*)(sa4 + kNM * kNK) - kNM;
+    if (wn == 1) {
+#pragma unroll
+      for (int q = 0; q < QA; ++q)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) x_hi[((q * 4 + i) * 4 + r) * 64 + lane] = acc[i][q][r];
+    } else {
+#pragma unroll
+      for (int q = QA; q < WB; ++q)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            x_lo[(((q - QA) * 4 + i) * 4 + r) * 64 + lane] = acc[i][q][r];
+    }
+    __syncthreads();
+    const int g0 = (n0 / TN) * WB;  // first pair group of the tile
+    // This lane's rotated (j, j + 64) pairs as packed bf16, per row group i,
+    // row r and pair group QB + k it finishes (QB = 0 on wave (wm, 0), QA on
+    // wave (wm, 1): the two cases are compiled apart so every index is a
+    // constant). The cos/sin of its (row, j) come from the RoPE table, one
+    // row group ahead.
+    uint32_t rot[4][4][QA];
+    auto rotate_half = [&](auto half) {
+      constexpr int QB = decltype(half)::value == 0 ? 0 : QA;
+      constexpr int NQ = decltype(half)::value == 0 ? QA : WB - QA;
+      f32x2_t cs[2][4][QA];
+      auto load_cs = [&](int i, int b) {
+#pragma unroll
+        for (int k = 0; k < NQ; ++k) {
+          const int q = QB + k;
+          if (((g0 + q) >> 2) >= ea.Hq + ea.Hkv) continue;  // values: not rotated
+          const int jd = 16 * ((g0 + q) & 3) + c16;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int lr = wm * 64 + i * 16 + 4 * j4 + r;
+            cs[b][r][k] = ((const f32x2_t*)ea.rope)[(int64_t)slots[lr].x * (kHd / 2) + jd];
+          }
+        }
+      };
+      load_cs(0, 0);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (i + 1 < 4) load_cs(i + 1, (i + 1) & 1);
+#pragma unroll
+        for (int k = 0; k < NQ; ++k) {
+          const int q = QB + k;
+          const bool rotate = ((g0 + q) >> 2) < ea.Hq + ea.Hkv;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            float lo, up;
+            if constexpr (QB == 0) {
+              lo = acc[i][q][r];
+              up = x_hi[((q * 4 + i) * 4 + r) * 64 + lane];
+            } else {
+              lo = x_lo[(((q - QA) * 4 + i) * 4 + r) * 64 + lane];
+              up = acc[i][q][r];
+            }
+            if (rotate) {
+              const f32x2_t c = cs[i & 1][r][k];
+              const float rlo = lo * c.x - up * c.y, rup = up * c.x + lo * c.y;
+              lo = rlo;
+              up = rup;
+            }
+            rot[i][r][k] = pack_bf16x2(lo, up);
+          }
+        }
+      }
+    };
+    if (wn == 0)
+      rotate_half(std::integral_constant<int, 0>{});
+    else
+      rotate_half(std::integral_constant<int, 1>{});
+    __syncthreads();  // every wave is done with the exchange areas
+    // Staged rows: 32 rows per LDS object (rows 32 k .. 32 k + 31 in object k).
+    auto stage_row = [&](int k) -> bf16_t* {  // k wave-uniform
+      switch (k) {
+        case 0: return sa0;
+        case 1: return sa1;
+        case 2: return sa2;
+        case 3: return sa3;
+        case 4: return sa4;
+        case 5: return sw0;
+        case 6: return sw1;
+        default: return sw2;
+      }
+    };
+    auto stage_half = [&](auto half) {
+      constexpr int QB = decltype(half)::value == 0 ? 0 : QA;
+      constexpr int NQ = decltype(half)::value == 0 ? QA : WB - QA;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        bf16_t* const obj = stage_row(2 * wm + (i >> 1));
+#pragma unroll
+        for (int k = 0; k < NQ; ++k) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int rr = (i & 1) * 16 + 4 * j4 + r;  // row within the object
+            bf16_t* const p = obj + rr * TN + (QB + k) * 32 + c16;
+            p[0] = (bf16_t)(rot[i][r][k] & 0xFFFFu);
+            p[16] = (bf16_t)(rot[i][r][k] >> 16);
+          }
+        }
+      }
+    };
+    if (wn == 0)
+      stage_half(std::integral_constant<int, 0>{});
+    else
+      stage_half(std::integral_constant<int, 1>{});
+    __syncthreads();
+    // Queries and keys in 16-byte pieces: (row, group, half, 8-dim chunk),
+    // the chunk fastest.
+    constexpr int kPieces = kNM * WB * 4;
+    for (int it = tid; it < kPieces; it += kNThreads) {
+      const int c8 = it & 1, h = (it >> 1) & 1, q = (it >> 2) % WB, lr = (it >> 2) / WB;
+      const int hh = (g0 + q) >> 2;
+      const int m = m0 + lr;
+      if (m >= M || hh >= ea.Hq + ea.Hkv) continue;  // values below
+      const u32x4_t v = *(const u32x4_t*)(stage_row(lr >> 5) + (lr & 31) * TN + q * 32 +
+                                          h * 16 + c8 * 8);
+      const int dim = 64 * h + 16 * ((g0 + q) & 3) + 8 * c8;  // first of the 8 dims
+      if (hh < ea.Hq) {
+        *(u32x4_t*)(ea.q_out + ((int64_t)m * ea.Hq + hh) * kHd + dim) = v;
+      } else {
+        const u32x2_t sl = slots[lr];
+        bf16_t* tile = ea.k_cache + ((int64_t)(int)sl.y * ea.Hkv + (hh - ea.Hq)) * kTile;
+        *(u32x4_t*)(tile + k_tile_offset((int)sl.x % kBlockTokens, dim)) = v;
+      }
+    }
+    // Values: the tile keeps four consecutive tokens of a dim together, so a
+    // run of four rows that fill slots 4a .. 4a + 3 of one block leaves as one
+    // 8-byte store per dim, any other row element by element. Items: (row
+    // quad, group, 32 dims), the dim fastest.
+    constexpr int kVItems = (kNM / 4) * WB * 32;
+    for (int it = tid; it < kVItems; it += kNThreads) {
+      const int d32 = it & 31, q = (it >> 5) % WB, quad = (it >> 5) / WB;
+      const int hh = (g0 + q) >> 2;
+      if (hh < ea.Hq + ea.Hkv) continue;  // queries and keys above
+      const int dim = 64 * (d32 >> 4) + 16 * ((g0 + q) & 3) + (d32 & 15);
+      const int col = q * 32 + d32;  // staged column
+      const int lr0 = 4 * quad;
+      bf16_t* const vbase = ea.v_cache + (int64_t)(hh - ea.Hq - ea.Hkv) * kTile;
+      uint32_t e4[4];
+      u32x2_t sl[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        e4[e] = stage_row((lr0 + e) >> 5)[((lr0 + e) & 31) * TN + col];
+        sl[e] = slots[lr0 + e];
+      }
+      const int t0 = (int)sl[0].x % kBlockTokens;
+      bool run = m0 + lr0 + 3 < M && t0 % 4 == 0;
+#pragma unroll
+      for (int e = 1; e < 4; ++e)
+        run = run && sl[e].y == sl[0].y && (int)sl[e].x % kBlockTokens == t0 + e;
+      if (run) {
+        *(u32x2_t*)(vbase + (int64_t)(int)sl[0].y * ea.Hkv * kTile + v_tile_offset(t0, dim)) =
+            u32x2_t{e4[0] | (e4[1] << 16), e4[2] | (e4[3] << 16)};
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (m0 + lr0 + e < M)
+            vbase[(int64_t)(int)sl[e].y * ea.Hkv * kTile +
+                  v_tile_offset((int)sl[e].x % kBlockTokens, dim)] = (bf16_t)e4[e];
+      }
+    }
   } else if constexpr (MODE == kNarrowSwiglu) {
     // Gate in blocks q < WB/2, up in blocks WB/2 + q, of outputs
     // o0 + TN/4 wn + 16 q + c16; h = silu(gate) * up in tile order [M][F].
@@ -331,6 +535,18 @@ hipError_t launch_narrow(int tn, const uint16_t* A, const uint16_t* W, int M, in
     if (tn != 192) return hipErrorInvalidValue;
     COCO_LAUNCH((gemm_narrow_kernel<192, MODE>), grid, dim3(kNThreads), 0, st,
                 (const bf16_t*)A, (const bf16_t*)W, M, N, K, ea);
+  } else if constexpr (MODE == kNarrowQkv) {
+    if (tn == 224)
+      COCO_LAUNCH((gemm_narrow_kernel<224, MODE>), grid, dim3(kNThreads), 0, st,
+                  (const bf16_t*)A, (const bf16_t*)W, M, N, K, ea);
+    else if (tn == 192)
+      COCO_LAUNCH((gemm_narrow_kernel<192, MODE>), grid, dim3(kNThreads), 0, st,
+                  (const bf16_t*)A, (const bf16_t*)W, M, N, K, ea);
+    else if (tn == 160)
+      COCO_LAUNCH((gemm_narrow_kernel<160, MODE>), grid, dim3(kNThreads), 0, st,
+                  (const bf16_t*)A, (const bf16_t*)W, M, N, K, ea);
+    else
+      return hipErrorInvalidValue;
   } else if (tn == 160) {
     COCO_LAUNCH((gemm_narrow_kernel<160, MODE>), grid, dim3(kNThreads), 0, st,
                 (const bf16_t*)A, (const bf16_t*)W, M, N, K, ea);
@@ -393,6 +609,27 @@ hipError_t launch_gemm_narrow_swiglu_bf16(const uint16_t* A, const uint16_t* W_g
   ea.n_ss = ss_tiles;
   ea.eps = eps;
   return launch_narrow<kNarrowSwiglu>(192, A, W_gate_up, M, 2 * F, K, ea, st);
+}
+
+int narrow_qkv_tile_n(int Hq, int Hkv, int K) {
+  const int N = (Hq + 2 * Hkv) * 128;
+  if (K % kNK != 0) return 0;
+  // Prefer a width whose tile count is a multiple of 32 (whole rounds of 256
+  // CUs over a 2048-row chunk), else the widest that divides N.
+  for (int tn : {224, 192, 160})
+    if (N % tn == 0 && (N / tn) % 32 == 0) return tn;
+  for (int tn : {224, 192, 160})
+    if (N % tn == 0) return tn;
+  return 0;
+}
+
+hipError_t launch_gemm_narrow_qkv_bf16(const uint16_t* A, const uint16_t* W_qkv, int M, int K,
+                                       const NarrowEpiArgs& ea, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  const int tn = narrow_qkv_tile_n(ea.Hq, ea.Hkv, K);
+  if (tn == 0 || !ea.row_info || !ea.rope || !ea.q_out || !ea.k_cache || !ea.v_cache)
+    return hipErrorInvalidValue;
+  return launch_narrow<kNarrowQkv>(tn, A, W_qkv, M, (ea.Hq + 2 * ea.Hkv) * 128, K, ea, st);
 }
 
 }  // namespace coco

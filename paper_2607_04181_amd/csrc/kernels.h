@@ -206,6 +206,13 @@ struct NarrowEpiArgs {
   const float* ss_in = nullptr;      // [n_ss][M] from the residual variant
   int n_ss = 0;
   float eps = 0.f;
+  // QKV variant (head_dim 128)
+  const int32_t* row_info = nullptr;  // [M][2] row slots from the gather kernel
+  const float* rope = nullptr;        // [rope_rows][64] (cos, sin) pairs
+  uint16_t* q_out = nullptr;
+  uint16_t* k_cache = nullptr;
+  uint16_t* v_cache = nullptr;
+  int Hq = 0, Hkv = 0;
 };
 // O projection with the residual and the first half of RMSNorm_2 in its
 // epilogue: x1[m] = A W^T + res_x[res_idx ? res_idx[m] : m] (fp32),
@@ -224,6 +231,14 @@ bool narrow_swiglu_fits(int F, int K);
 hipError_t launch_gemm_narrow_swiglu_bf16(const uint16_t* A, const uint16_t* W_gate_up,
                                           uint16_t* H, int M, int F, int K, const float* ss_in,
                                           int ss_tiles, float eps, hipStream_t st);
+// Prefill QKV projection with RoPE and the cache append in its epilogue
+// (head_dim 128), on 256 x TN tiles that each hold TN/2 whole rotation pairs
+// (dims j and j + 64 of a head), TN = narrow_qkv_tile_n(Hq, Hkv, K) (224,
+// 192 or 160; 0: no plan): queries to q_out [M][Hq*128] in bf16, keys
+// (rotated) and values into the paged cache tiles.
+int narrow_qkv_tile_n(int Hq, int Hkv, int K);
+hipError_t launch_gemm_narrow_qkv_bf16(const uint16_t* A, const uint16_t* W_qkv, int M, int K,
+                                       const NarrowEpiArgs& ea, hipStream_t st);
 // Down projection with the residual and the scatter in its epilogue:
 // out[out_idx ? out_idx[m] : m] = bf16(x1[m] + A W^T).
 hipError_t launch_gemm_narrow_scatter_bf16(const uint16_t* A, const uint16_t* W, int M, int N,

@@ -304,12 +304,14 @@ def test_prefill_span_equals_successive_layers_bit_exactly():
             assert torch.equal(t[k].view(torch.int16), p[k].view(torch.int16)), k
 
 
-def test_prefill_with_an_odd_head_count_matches_oracle():
-    """Five query heads, one KV head and d = 384: neither the QKV width (7
-    heads) nor d is a multiple of the prefill GEMM's 256-column tile, so the
-    projections write fp32 partials, the separate QKV epilogue applies RoPE
-    and the cache append, and the separate residual + RMSNorm_2 kernel runs."""
-    shape = small_bf16_shape(d=384, hq=5, hkv=1, ffn=768)
+@pytest.mark.parametrize("hq", [5, 3])
+def test_prefill_with_an_odd_head_count_matches_oracle(hq):
+    """One KV head with five (three) query heads and d = 384: the QKV width
+    of 7 (5) heads takes the narrow-tile QKV GEMM with 224-column (160-column)
+    tiles of whole rotation pairs, split unevenly between the two waves of a
+    row quarter, and d takes the narrow O and down GEMMs with three
+    128-column tiles."""
+    shape = small_bf16_shape(d=384, hq=hq, hkv=1, ffn=768)
     b = ragged_prefill_batch(13, priors=[0, 50, 17], lens=[30, 70, 16], max_ctx=256,
                              hidden_rows=150)
     rep = Replica.for_batch(shape, "s11", 1, b)
@@ -319,6 +321,29 @@ def test_prefill_with_an_odd_head_count_matches_oracle():
     torch.cuda.synchronize()
     ref, _, cache, _ = oracle_prefill_seqs(shape, "s11", 0, b, range(b.n_seqs), h0)
     _check_rows("odd-head prefill", to64(hidden)[b.row_idx], ref, h0[b.row_idx])
+    for s in range(b.n_seqs):
+        t0, t1 = int(b.prior_lens[s]), int(b.ctx_lens[s])
+        K, V = gpu_cache_tokens(rep.layers[0], b, s, t0, t1)
+        assert normwise_err(K, cache.K[s][t0:t1]) < TOL
+        assert normwise_err(V, cache.V[s][t0:t1]) < TOL
+
+
+def test_prefill_without_fused_projections_matches_oracle():
+    """d = 4224 (33 x 128) and nine query heads with one KV head (11 heads):
+    no prefill GEMM plan fuses the QKV projection (1408 columns) or the O and
+    down projections, so the projections write fp32 partials, the separate
+    QKV epilogue applies RoPE and the cache append, the separate residual +
+    RMSNorm_2 kernel and the residual + scatter kernel run, and the gate/up
+    GEMM's SwiGLU epilogue takes RMSNorm_2's output as it is."""
+    shape = small_bf16_shape(d=4224, hq=9, hkv=1, ffn=768)
+    b = ragged_prefill_batch(17, priors=[0, 33], lens=[40, 25], max_ctx=128, hidden_rows=90)
+    rep = Replica.for_batch(shape, "s17", 1, b)
+    hidden = WD.hidden_tensor(shape, "s17", b.hidden_rows)
+    h0 = to64(hidden)
+    rep.forward(0, hidden, WD.batch_tensors(b))
+    torch.cuda.synchronize()
+    ref, _, cache, _ = oracle_prefill_seqs(shape, "s17", 0, b, range(b.n_seqs), h0)
+    _check_rows("unfused prefill", to64(hidden)[b.row_idx], ref, h0[b.row_idx])
     for s in range(b.n_seqs):
         t0, t1 = int(b.prior_lens[s]), int(b.ctx_lens[s])
         K, V = gpu_cache_tokens(rep.layers[0], b, s, t0, t1)
