@@ -150,7 +150,9 @@ def measure_peaks(num_cus):
     library's read probe; the best of its load depths and grid sizes), a 1 GiB
     device copy (torch's copy kernel, read + write) and a loop of bf16 MFMAs
     (the library's MFMA probe; the best of its chain counts and waves per
-    SIMD). Each configuration: the median of 10 timed launches after 2
+    SIMD), on random operands that change from one instruction to the next
+    (the rate the power draw of real data allows: the MFMA ceiling used) and
+    on constant ones. Each configuration: the median of 10 timed launches after 2
     warm-ups."""
     import torch
     import paper_2607_04181_amd as coco
@@ -186,28 +188,35 @@ def measure_peaks(num_cus):
     del buf, x, y
     mout = torch.empty(4 * 4 * num_cus, dtype=torch.float32, device="cuda")
     mfmas = {}
-    for chains in (4, 8):
-        for per_cu in (1, 2, 4):  # 4-wave workgroups per CU: waves per SIMD
-            blocks = per_cu * num_cus
-            flops = [0.0]
+    for operands in (0, 1):  # constant operands; random operands changing per instruction
+        for chains in (4, 8):
+            for per_cu in (1, 2, 4):  # 4-wave workgroups per CU: waves per SIMD
+                blocks = per_cu * num_cus
+                flops = [0.0]
 
-            def mfma():
-                flops[0] = coco.coco_probe_mfma_bf16(2000 // chains * 4, mout, blocks, chains,
-                                                     stream)
-            ms = timed(mfma)
-            mfmas[(chains, per_cu)] = flops[0] / (ms * 1e-3) / 1e12
-    (best_c, best_w), tflops = max(mfmas.items(), key=lambda kv: kv[1])
+                def mfma():
+                    flops[0] = coco.coco_probe_mfma_bf16(40000 // chains, mout, blocks, chains,
+                                                         operands, stream)
+                ms = timed(mfma)
+                mfmas[(operands, chains, per_cu)] = flops[0] / (ms * 1e-3) / 1e12
+    best = {op: max(((c, w, t) for (o, c, w), t in mfmas.items() if o == op),
+                    key=lambda x: x[2]) for op in (0, 1)}
     torch.cuda.empty_cache()
     return {"read_GBps": round(nbytes / (ms_read * 1e-3) / 1e9, 1),
             "copy_GBps": round(nbytes / (ms_copy * 1e-3) / 1e9, 1),
-            "mfma_bf16_TFLOPs": round(tflops, 1),
+            "mfma_bf16_TFLOPs": round(best[1][2], 1),
+            "mfma_bf16_const_operands_TFLOPs": round(best[0][2], 1),
             "method": (f"medians of 10 launches: read probe over 2 GiB (best of 3 load depths "
                        f"x 4 grid sizes: variant {best_v}, {best_cu} workgroups/CU), 1 GiB "
                        f"device copy (bytes read + written), bf16 MFMA probe (best of 4/8 "
-                       f"chains x 1/2/4 waves per SIMD: {best_c} chains, {best_w} waves)"),
+                       f"chains x 1/2/4 waves per SIMD) with random operands that change "
+                       f"from one instruction to the next ({best[1][0]} chains, {best[1][1]} "
+                       f"waves; the rate under a GEMM's power draw, mfma_bf16_TFLOPs) and "
+                       f"with constant operands ({best[0][0]} chains, {best[0][1]} waves)"),
             "read_GBps_all": {f"v{v}_{c}": round(nbytes / (ms * 1e-3) / 1e9, 1)
                               for (v, c), ms in reads.items()},
-            "mfma_TFLOPs_all": {f"c{c}_w{w}": round(t, 1) for (c, w), t in mfmas.items()}}
+            "mfma_TFLOPs_all": {f"{'rand' if o else 'const'}_c{c}_w{w}": round(t, 1)
+                                for (o, c, w), t in mfmas.items()}}
 
 
 def run_workload(name, batch_rows, args, peaks, flush):

@@ -293,14 +293,18 @@ int coco_layer_read_timing(coco_layer_t h, double* ms, int64_t* launches, int32_
  * per workgroup to `out` (device, >= 4 * blocks bytes).
  *
  * coco_probe_mfma_bf16: `blocks` workgroups of four waves, each wave running
- * `iters` rounds of `chains` (4 or 8) independent v_mfma_f32_32x32x16_bf16
- * chains on register operands; writes one float per wave to `out` (device,
- * >= 16 * blocks bytes) and the dense flop count of the launch to *flops
- * (host). */
+ * `iters` rounds (a multiple of 8) of `chains` (4 or 8) independent
+ * v_mfma_f32_32x32x16_bf16 chains on register operands; writes one float per
+ * wave to `out` (device, >= 16 * blocks bytes) and the dense flop count of
+ * the launch to *flops (host). operands 0: the same small constants in every
+ * instruction; 1: random bf16 values with random signs and magnitudes in
+ * [0.5, 2), eight operand sets per lane taken in turn, so consecutive
+ * instructions of a chain see different data (the rate under the power draw
+ * of data like a GEMM's). */
 int coco_probe_read(const void* buf, int64_t bytes, void* out, int32_t blocks, int32_t variant,
                     coco_stream_t stream);
 int coco_probe_mfma_bf16(int64_t iters, void* out, int32_t blocks, int32_t chains,
-                         double* flops, coco_stream_t stream);
+                         int32_t operands, double* flops, coco_stream_t stream);
 
 #ifdef __cplusplus
 }

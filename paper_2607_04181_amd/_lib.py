@@ -88,7 +88,7 @@ def _load():
         "coco_layer_read_timing": (ctypes.c_int, [vp, ctypes.POINTER(ctypes.c_double),
                                                   ctypes.POINTER(i64), i32]),
         "coco_probe_read": (ctypes.c_int, [vp, i64, vp, i32, i32, vp]),
-        "coco_probe_mfma_bf16": (ctypes.c_int, [i64, vp, i32, i32,
+        "coco_probe_mfma_bf16": (ctypes.c_int, [i64, vp, i32, i32, i32,
                                                 ctypes.POINTER(ctypes.c_double), vp]),
         "coco_split_batch": (ctypes.c_int, [i64, i32, ctypes.POINTER(i64)]),
         "coco_comm_time": (ctypes.c_double, [ctypes.POINTER(coco_scale_model), i32]),
@@ -317,11 +317,12 @@ def coco_probe_read(buf, out, blocks: int, variant: int = 0, stream=None) -> Non
                                 variant, _stream(stream)))
 
 
-def coco_probe_mfma_bf16(iters: int, out, blocks: int, chains: int = 4, stream=None) -> float:
+def coco_probe_mfma_bf16(iters: int, out, blocks: int, chains: int = 4, operands: int = 0,
+                         stream=None) -> float:
     """Enqueues the MFMA loop; returns its dense flop count. `out` holds at
-    least 4 * blocks floats."""
+    least 4 * blocks floats; operands 0: constants, 1: random data."""
     flops = ctypes.c_double()
-    _check(_lib.coco_probe_mfma_bf16(iters, _ptr(out, what="out"), blocks, chains,
+    _check(_lib.coco_probe_mfma_bf16(iters, _ptr(out, what="out"), blocks, chains, operands,
                                      ctypes.byref(flops), _stream(stream)))
     return flops.value
 

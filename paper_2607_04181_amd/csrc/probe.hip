@@ -49,26 +49,52 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 // C independent chains of v_mfma_f32_32x32x16_bf16 per wave (32*32*16*2
 // flops each), operands held in registers; lane 0 of each wave writes one
-// element of every chain so the chains cannot be dropped.
-template <int kMfmaChains>
+// element of every chain so the chains cannot be dropped. RANDOM: eight
+// operand sets per lane of random bf16 values (hashed from the lane and the
+// set), instruction k of a round taking set (c + k) % 8 for A and
+// (3c + k) % 8 for B; otherwise one set of small constants.
+__device__ __forceinline__ uint32_t probe_hash(uint32_t x) {
+  x ^= x >> 16;
+  x *= 0x7feb352du;
+  x ^= x >> 15;
+  x *= 0x846ca68bu;
+  x ^= x >> 16;
+  return x;
+}
+
+template <int kMfmaChains, bool RANDOM>
 __global__ __launch_bounds__(kProbeThreads) void probe_mfma_kernel(int64_t iters,
                                                                    float* __restrict__ out) {
   const int lane = threadIdx.x & (kWave - 1);
-  bf16x8_t a, b;
+  constexpr int kSets = RANDOM ? 8 : 1;
+  bf16x8_t a[kSets], b[kSets];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    a[e] = (__bf16)(0.001f * (float)(lane + e));
-    b[e] = (__bf16)(0.002f * (float)(lane - e));
+  for (int s = 0; s < kSets; ++s) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      if (RANDOM) {
+        // Sign and 7 mantissa bits random, exponent that of [0.5, 2).
+        const uint32_t h = probe_hash(((blockIdx.x * kProbeThreads + threadIdx.x) * 8 + s) * 8 + e);
+        a[s][e] = __builtin_bit_cast(__bf16, (uint16_t)((h & 0x807Fu) | ((h & 0x100u) ? 0x3F80u : 0x3F00u)));
+        b[s][e] = __builtin_bit_cast(__bf16, (uint16_t)(((h >> 16) & 0x807Fu) | ((h & 0x200u) ? 0x3F80u : 0x3F00u)));
+      } else {
+        a[s][e] = (__bf16)(0.001f * (float)(lane + e));
+        b[s][e] = (__bf16)(0.002f * (float)(lane - e));
+      }
+    }
   }
   f32x16_t acc[kMfmaChains];
 #pragma unroll
   for (int c = 0; c < kMfmaChains; ++c)
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[c][e] = 0.f;
-  for (int64_t it = 0; it < iters; ++it) {
+  for (int64_t it = 0; it < iters; it += 8) {
 #pragma unroll
-    for (int c = 0; c < kMfmaChains; ++c)
-      acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[c], 0, 0, 0);
+    for (int k = 0; k < 8; ++k)
+#pragma unroll
+      for (int c = 0; c < kMfmaChains; ++c)
+        acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[(c + k) % kSets], b[(3 * c + k) % kSets],
+                                                         acc[c], 0, 0, 0);
   }
   if (lane == 0) {
     float t = 0.f;
@@ -102,15 +128,22 @@ int coco_probe_read(const void* buf, int64_t bytes, void* out, int32_t blocks, i
 }
 
 int coco_probe_mfma_bf16(int64_t iters, void* out, int32_t blocks, int32_t chains,
-                         double* flops, coco_stream_t stream) {
-  if (!out || !flops || iters < 1 || blocks < 1 || (chains != 4 && chains != 8))
+                         int32_t operands, double* flops, coco_stream_t stream) {
+  if (!out || !flops || iters < 8 || iters % 8 || blocks < 1 || (chains != 4 && chains != 8) ||
+      (operands != 0 && operands != 1))
     return COCO_EINVAL;
   *flops = 2.0 * 32 * 32 * 16 * chains * (double)iters * blocks * (kProbeThreads / kWave);
   const hipStream_t st = (hipStream_t)stream;
-  if (chains == 4)
-    COCO_LAUNCH((probe_mfma_kernel<4>), dim3(blocks), dim3(kProbeThreads), 0, st, iters, (float*)out);
+  const dim3 g(blocks), b(kProbeThreads);
+  float* o = (float*)out;
+  if (chains == 4 && operands == 0)
+    COCO_LAUNCH((probe_mfma_kernel<4, false>), g, b, 0, st, iters, o);
+  else if (chains == 4)
+    COCO_LAUNCH((probe_mfma_kernel<4, true>), g, b, 0, st, iters, o);
+  else if (operands == 0)
+    COCO_LAUNCH((probe_mfma_kernel<8, false>), g, b, 0, st, iters, o);
   else
-    COCO_LAUNCH((probe_mfma_kernel<8>), dim3(blocks), dim3(kProbeThreads), 0, st, iters, (float*)out);
+    COCO_LAUNCH((probe_mfma_kernel<8, true>), g, b, 0, st, iters, o);
   return hipGetLastError() == hipSuccess ? COCO_OK : COCO_EHIP;
 }
 
