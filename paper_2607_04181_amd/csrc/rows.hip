@@ -9,6 +9,8 @@
 // (row, column chunk) rather than one workgroup per row where no row-wide
 // reduction is needed. Every reduction order is fixed by the block shape and
 // S alone, so a row's result never depends on the other rows of the call.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -100,32 +102,61 @@ __global__ __launch_bounds__(kRowThreads) void gather_rmsnorm_kernel(
 }
 
 // bf16 rows, d % 8 == 0: 16-byte vectors, row held in registers.
-template <>
-__global__ __launch_bounds__(kRowThreads) void gather_rmsnorm_kernel<bf16_t>(
+//   * Row of a workgroup: with `tiled`, consecutive rows run on one XCD
+//     (blockIdx % 8 is the XCD), so the 16 rows that share each 1 KB
+//     tile-order block fill it in that XCD's L2 and it leaves as whole lines;
+//   * the row slot (prefill QKV epilogue) is found by the first wave with
+//     scalar loads through the constant address space, which wait on their
+//     own counter, so the chain of dependent loads overlaps the row's vector
+//     loads instead of following them.
+typedef __attribute__((address_space(4))) const int32_t* cint_ptr;
+
+__device__ __forceinline__ void write_row_slot_uniform(const RowSlotArgs& rs, int i) {
+  const cint_ptr positions = (cint_ptr)rs.positions;
+  const cint_ptr seq_starts = (cint_ptr)rs.seq_starts;
+  const cint_ptr block_table = (cint_ptr)rs.block_table;
+  const int pos = positions[i];
+  int lo = 0, hi = rs.n_seqs - 1;  // the s with seq_starts[s] <= i < seq_starts[s + 1]
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (seq_starts[mid] <= i) lo = mid; else hi = mid - 1;
+  }
+  const int blk =
+      block_table[(int64_t)lo * rs.max_blocks + min(max(pos, 0) / kBlockTokens, rs.max_blocks - 1)];
+  if (threadIdx.x == 0) {
+    rs.row_info[2 * i] = min(max(pos, 0), rs.rope_rows - 1);
+    rs.row_info[2 * i + 1] = blk;
+  }
+}
+
+// NV: 16-byte vectors per thread (the row's d / 8 vectors over the block),
+// all loaded up front without a branch (past the row: its last vector again).
+template <int NV>
+__global__ __launch_bounds__(kRowThreads) void gather_rmsnorm_bf16_kernel(
     const bf16_t* __restrict__ src, const int32_t* __restrict__ row_idx, int d,
     const bf16_t* __restrict__ gamma, float eps, bf16_t* __restrict__ x_out,
     bf16_t* __restrict__ h_out, bool tiled, RowSlotArgs rs) {
   __shared__ float red[kRowThreads / kWave];
-  constexpr int kMaxVec = 8;  // d <= 16384
-  const int i = blockIdx.x;
-  if (rs.row_info != nullptr && threadIdx.x == 0) write_row_slot(rs, i);
+  constexpr int kXCDs = 8;
+  const int nb = gridDim.x, b = blockIdx.x;
+  const int full = (nb / kXCDs) * kXCDs;
+  const int i = tiled && b < full ? (b % kXCDs) * (nb / kXCDs) + b / kXCDs : b;
   const int64_t r = row_idx ? (int64_t)row_idx[i] : (int64_t)i;
   const int nv = d / 8;
   const u32x4_t* x = (const u32x4_t*)(src + r * d);
   const u32x4_t* g = (const u32x4_t*)gamma;
   // The gains are loaded together with the row: one memory round trip.
-  u32x4_t xv[kMaxVec], gv[kMaxVec];
+  u32x4_t xv[NV], gv[NV];
 #pragma unroll
-  for (int u = 0; u < kMaxVec; ++u) {
-    const int v = threadIdx.x + u * kRowThreads;
-    if (v < nv) {
-      xv[u] = x[v];
-      gv[u] = g[v];
-    }
+  for (int u = 0; u < NV; ++u) {
+    const int v = min((int)threadIdx.x + u * kRowThreads, nv - 1);
+    xv[u] = x[v];
+    gv[u] = g[v];
   }
+  if (rs.row_info != nullptr && threadIdx.x < kWave) write_row_slot_uniform(rs, i);
   float ss = 0.f;
 #pragma unroll
-  for (int u = 0; u < kMaxVec; ++u) {
+  for (int u = 0; u < NV; ++u) {
     const int v = threadIdx.x + u * kRowThreads;
     if (v < nv) {
       float f[8];
@@ -138,7 +169,7 @@ __global__ __launch_bounds__(kRowThreads) void gather_rmsnorm_kernel<bf16_t>(
   ss = block_sum<kRowThreads>(ss, red);
   const float inv = 1.0f / sqrtf(ss / (float)d + eps);
 #pragma unroll
-  for (int u = 0; u < kMaxVec; ++u) {
+  for (int u = 0; u < NV; ++u) {
     const int v = threadIdx.x + u * kRowThreads;
     if (v < nv) {
       float f[8], gf[8];
@@ -160,8 +191,24 @@ hipError_t launch_gather_rmsnorm(const T* src, const int32_t* row_idx, int M, in
   if (rs.row_info != nullptr && (rs.n_seqs < 1 || rs.max_blocks < 1 || rs.rope_rows < 1))
     return hipErrorInvalidValue;
   if (tiled && (!std::is_same<T, bf16_t>::value || d % 32 != 0)) return hipErrorInvalidValue;
-  COCO_LAUNCH(gather_rmsnorm_kernel<T>, dim3(M), dim3(kRowThreads), 0, st, src, row_idx,
-                     d, gamma, eps, x_out, h_out, tiled, rs);
+  if constexpr (std::is_same<T, bf16_t>::value) {
+    if (d % 8 != 0 || d > 8 * kRowThreads * 8) return hipErrorInvalidValue;
+    const int nvt = (d / 8 + kRowThreads - 1) / kRowThreads;  // vectors per thread, 1..8
+    switch (nvt) {
+#define COCO_GN_CASE(n)                                                                       \
+  case n:                                                                                     \
+    COCO_LAUNCH(gather_rmsnorm_bf16_kernel<n>, dim3(M), dim3(kRowThreads), 0, st, src,         \
+                row_idx, d, gamma, eps, x_out, h_out, tiled, rs);                             \
+    break;
+      COCO_GN_CASE(1) COCO_GN_CASE(2) COCO_GN_CASE(3) COCO_GN_CASE(4)
+      COCO_GN_CASE(5) COCO_GN_CASE(6) COCO_GN_CASE(7) COCO_GN_CASE(8)
+#undef COCO_GN_CASE
+      default: return hipErrorInvalidValue;
+    }
+  } else {
+    COCO_LAUNCH(gather_rmsnorm_kernel<T>, dim3(M), dim3(kRowThreads), 0, st, src, row_idx, d,
+                gamma, eps, x_out, h_out, tiled, rs);
+  }
   return hipGetLastError();
 }
 
