@@ -314,10 +314,16 @@ __global__ __launch_bounds__(HD) void attn_combine_kernel(const float* __restric
 // Per stage a wave scores the 64 keys (S^T = K Q^T), updates its online
 // softmax once, and accumulates O^T += V^T P^T in 32-key MFMA steps: the
 // V^T fragments of two blocks side by side against P^T packed to match (any
-// fixed assignment of keys to MFMA k-slots gives the same sum).
+// fixed assignment of keys to MFMA k-slots gives the same sum). The row sums
+// of P come from the same MFMA with an all-ones operand in place of V^T, and
+// the running max moves only when a stage's max exceeds it by kPfLazy.
 constexpr int kPfRows = 128;  // query rows per workgroup
 constexpr int kPfLaunchWaves = 8;  // waves per workgroup, one 16-row column tile each (measured faster than 4 x 2)
 constexpr int kPfBlk = 4;     // key blocks per stage
+// The running max of a row is kept while a stage's max stays within this
+// many log2 units of it (P then stays below 2^8): rescaling the
+// accumulators, a multiply per element, is needed only when the max jumps.
+constexpr float kPfLazy = 8.f;
 constexpr int kTileElems = kBlockTokens * HD;
 constexpr int kXCDs = 8;
 
@@ -411,12 +417,17 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_prefill_kernel(
     }
   };
 
-  float m[COLS], l[COLS];
+  // l: the row sums of P, accumulated by an MFMA against an all-ones V^T
+  // operand (every element of it holds the column's sum).
+  float m[COLS];
+  f32x4_t l[COLS];
   f32x4_t acc[COLS][8];
+  const bf16x8_t ones =
+      __builtin_bit_cast(bf16x8_t, u32x4_t{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u});
 #pragma unroll
   for (int c = 0; c < COLS; ++c) {
     m[c] = -INFINITY;
-    l[c] = 0.f;
+    l[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
 #pragma unroll
   for (int c = 0; c < COLS; ++c)
@@ -499,9 +510,10 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_prefill_kernel(
           }
         }
         mx = col_max4(mx) * scale_log2;
-        const float m_new = fmaxf(m[c], mx);  // finite: stage 0 always holds key 0
+        // Stage 0 always holds key 0, so mx is finite and the first stage
+        // sets the max.
+        const float m_new = mx > m[c] + kPfLazy ? mx : m[c];
         const float alpha = __builtin_amdgcn_exp2f(m[c] - m_new);
-        float ps = 0.f;
         uint32_t pw[kPfBlk][2];
 #pragma unroll
         for (int i = 0; i < kPfBlk; ++i) {
@@ -509,26 +521,29 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_prefill_kernel(
 #pragma unroll
           for (int r = 0; r < 4; ++r)
             pr[r] = __builtin_amdgcn_exp2f(fmaf(sc[c][i][r], scale_log2, -m_new));
-          ps += (pr[0] + pr[1]) + (pr[2] + pr[3]);
           pw[i][0] = pack_bf16x2(pr[0], pr[1]);
           pw[i][1] = pack_bf16x2(pr[2], pr[3]);
         }
-        l[c] = l[c] * alpha + ps;
         m[c] = m_new;
-        // alpha is exactly 1 for a column whose max did not move: rescale only
-        // when some column's did (multiplying by 1 would change nothing).
+        // alpha is exactly 1 for a column whose max was kept: rescale only
+        // when some column's moved (multiplying by 1 would change nothing).
         if (__ballot(alpha != 1.f) != 0) {
 #pragma unroll
           for (int n = 0; n < 8; ++n) acc[c][n] = acc[c][n] * alpha;
+          l[c] = l[c] * alpha;
         }
 #pragma unroll
         for (int pp = 0; pp < 2; ++pp)
           pk[c][pp] = u32x4_t{pw[2 * pp][0], pw[2 * pp][1], pw[2 * pp + 1][0], pw[2 * pp + 1][1]};
       }
-      // O^T += V^T P^T over the two block pairs.
+      // O^T += V^T P^T over the two block pairs; l += 1^T P^T.
 #pragma unroll
       for (int pp = 0; pp < 2; ++pp) {
         if (pp == 1) read_v(1);
+#pragma unroll
+        for (int c = 0; c < COLS; ++c)
+          l[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              ones, __builtin_bit_cast(bf16x8_t, pk[c][pp]), l[c], 0, 0, 0);
 #pragma unroll
         for (int pc = 0; pc < 4; ++pc) {
 #pragma unroll
@@ -550,7 +565,7 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_prefill_kernel(
 #pragma unroll
   for (int c = 0; c < COLS; ++c) {
     const int row = w_row0 + 16 * c + c16;
-    const float inv = 1.0f / col_sum4(l[c]);
+    const float inv = 1.0f / l[c][0];
     if (row < row_end) {
 #pragma unroll
       for (int n = 0; n < 8; ++n) {
