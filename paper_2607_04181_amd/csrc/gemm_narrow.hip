@@ -245,7 +245,7 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
   // row (SwiGLU: its 1/rms), and (residual variant) the row sums of x1^2 of
   // each column half.
   __syncthreads();  // every wave is done with the ring
-  int* const g_nrow = (int*)sa0;
+  int* const g_nrow = (int*)(MODE == kNarrowSwiglu ? sa4 : sa0);
   float(*const g_nss)[kNM] = (float(*)[kNM])sa1;
   if constexpr (MODE == kNarrowQkv) {
     // (position clamped to the RoPE table, cache block) of each tile row, at
@@ -485,22 +485,39 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
     }
   } else if constexpr (MODE == kNarrowSwiglu) {
     // Gate in blocks q < WB/2, up in blocks WB/2 + q, of outputs
-    // o0 + TN/4 wn + 16 q + c16; h = silu(gate) * up in tile order [M][F].
+    // o0 + TN/4 wn + 16 q + c16; h = silu(gate) * up, staged in LDS (row
+    // quarter wm in slot wm, rows padded to kSS) and written in tile order
+    // [M][F] as whole 1 KB blocks, one per wave store.
+    constexpr int kSO = TN / 2;   // outputs per tile row
+    constexpr int kSS = kSO + 8;  // staged row stride: 16-byte rows, conflict-free reads
+    static_assert(kSO % 32 == 0 && 64 * kSS <= kNM * kNK, "staged quarter fits a slot");
+    auto stg = [&](int k) -> bf16_t* {  // k wave-uniform
+      return k == 0 ? sa0 : k == 1 ? sa1 : k == 2 ? sa2 : sa3;
+    };
+    bf16_t* const mine = stg(wm);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int lr = wm * 64 + i * 16 + 4 * j4 + r;
-        const int m = m0 + lr;
-        if (m >= M) continue;
-        const float rs = __int_as_float(g_nrow[lr]);
+        const int rl = i * 16 + 4 * j4 + r;  // row within the quarter
+        const float rs = __int_as_float(g_nrow[wm * 64 + rl]);
 #pragma unroll
         for (int q = 0; q < WB / 2; ++q) {
           const float g = acc[i][q][r] * rs, u = acc[i][WB / 2 + q][r] * rs;
-          const int o = o0 + wn * (TN / 4) + 16 * q + c16;
-          ea.h[tile_off(m, o, F)] = (bf16_t)f32_to_bf16(g / (1.0f + expf(-g)) * u);
+          mine[rl * kSS + wn * (TN / 4) + 16 * q + c16] =
+              (bf16_t)f32_to_bf16(g / (1.0f + expf(-g)) * u);
         }
       }
+    __syncthreads();
+    // Block (16-row group, 32-output group); lane l holds chunk l: row
+    // l % 16 of the group, outputs 8 (l / 16) .. + 7 of the block.
+    constexpr int kBlocks = (kNM / 16) * (kSO / 32);
+    for (int bi = wv; bi < kBlocks; bi += kNThreads / kWave) {
+      const int rg = bi / (kSO / 32), kb = bi % (kSO / 32);
+      const int row = rg * 16 + (lane & 15), oc = kb * 32 + (lane >> 4) * 8;
+      const u32x4_t v = *(const u32x4_t*)(stg(row >> 6) + (row & 63) * kSS + oc);
+      if (m0 + row < M) *(u32x4_t*)(ea.h + tile_off(m0 + row, o0 + oc, F)) = v;
+    }
   } else {
     float x1v[4][4][WB];
 #pragma unroll
