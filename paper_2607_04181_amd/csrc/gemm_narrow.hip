@@ -241,247 +241,231 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
   if (full_end < stages) ring_round(full_end, std::true_type{});
   wait_vmcnt<0>();  // no direct load outlives the workgroup
 
-  // The idle ring holds the epilogue's per-row values: the row of each tile
-  // row (SwiGLU: its 1/rms), and (residual variant) the row sums of x1^2 of
-  // each column half.
+  // Epilogues. The idle ring holds each tile row's epilogue value in slot 4
+  // (its row of the residual or the output, SwiGLU: its 1/rms; QKV: its
+  // (position clamped to the RoPE table, cache block)). The residual,
+  // scatter and QKV epilogues work one row quarter at a time: the waves of
+  // quarter p put their fp32 accumulators in LDS as rows of TN + 4 floats
+  // (16-row groups in slots 0-3; the 4-float pad spreads the four rows a
+  // wave store touches over all banks), then every thread takes 8-column
+  // pieces of those 64 rows, so each load and store is 16 contiguous bytes
+  // per lane.
   __syncthreads();  // every wave is done with the ring
-  int* const g_nrow = (int*)(MODE == kNarrowSwiglu ? sa4 : sa0);
-  float(*const g_nss)[kNM] = (float(*)[kNM])sa1;
-  if constexpr (MODE == kNarrowQkv) {
-    // (position clamped to the RoPE table, cache block) of each tile row, at
-    // the end of slot 4 (its first 14 KB stage output rows below)
-    if (tid < kNM) ((u32x2_t*)(sa4 + kNM * kNK) - kNM)[tid] = rinfo;
-  } else {
-    if (tid < kNM) g_nrow[tid] = MODE == kNarrowSwiglu ? __float_as_int(rnorm) : erow;
+  int* const g_nrow = (int*)sa4;
+  u32x2_t* const slots = (u32x2_t*)sa4;
+  if (tid < kNM) {
+    if constexpr (MODE == kNarrowQkv)
+      slots[tid] = rinfo;
+    else
+      g_nrow[tid] = MODE == kNarrowSwiglu ? __float_as_int(rnorm) : erow;
   }
   __syncthreads();
+  constexpr int TNP = TN + 4;  // staged row stride (floats)
+  static_assert(16 * TNP * 4 <= kNM * kNK * 2, "a 16-row group fits a slot");
+  auto st_row = [&](int rq) -> float* {  // row rq (0..63) of the staged quarter
+    const int g = rq >> 4;
+    return (float*)(g == 0 ? sa0 : g == 1 ? sa1 : g == 2 ? sa2 : sa3) + (rq & 15) * TNP;
+  };
   // Accumulator layout: lane (j4, c16) of block (i, j) holds rows
   // 16 (4 wm + i) + 4 j4 + r, r < 4, of column 16 (WB wn + j) + c16.
-  const int cbase = n0 + wn * (TN / 2) + c16;
+  auto stage_quarter = [&](int p) {
+    if (wm == p) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float* const row = st_row(16 * i + 4 * j4 + r);
+#pragma unroll
+          for (int j = 0; j < WB; ++j) row[16 * (WB * wn + j) + c16] = acc[i][j][r];
+        }
+    }
+  };
+  constexpr int kCh = TN / 8;                                  // 8-column pieces per row
+  constexpr int kPer = (64 * kCh + kNThreads - 1) / kNThreads;  // pieces per thread and quarter
   if constexpr (MODE == kNarrowResid) {
-    float gam[WB];
+    // x1 = acc + residual row (fp32 out), h = bf16(x1 * gamma) in tile
+    // order, and the row's sum of x1^2 over the tile: per piece in column
+    // order, then the pieces in order (slot 4, after the row indices).
+    float* const ssp = (float*)sa4 + kNM;
+    for (int p = 0; p < 4; ++p) {
+      stage_quarter(p);
+      __syncthreads();
+      // All of a thread's loads first, for clamped pieces (no branch).
+      u32x4_t rv[kPer], gv[kPer];
 #pragma unroll
-    for (int j = 0; j < WB; ++j) gam[j] = bf16_to_f32(ea.gamma[cbase + 16 * j]);
-    float res[4][4][WB];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int lr = wm * 64 + i * 16 + 4 * j4 + r;
-        const bf16_t* xr = ea.res_x + (int64_t)g_nrow[lr] * N + cbase;
-#pragma unroll
-        for (int j = 0; j < WB; ++j) res[i][r][j] = bf16_to_f32(xr[16 * j]);
+      for (int u = 0; u < kPer; ++u) {
+        const int it = min(tid + u * kNThreads, 64 * kCh - 1);
+        const int rq = it / kCh, ch = it - rq * kCh;
+        rv[u] = *(const u32x4_t*)(ea.res_x + (int64_t)g_nrow[64 * p + rq] * N + n0 + 8 * ch);
+        gv[u] = *(const u32x4_t*)(ea.gamma + n0 + 8 * ch);
       }
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int lr = wm * 64 + i * 16 + 4 * j4 + r;
-        const int m = m0 + lr;
+      for (int u = 0; u < kPer; ++u) {
+        const int it = tid + u * kNThreads;
+        if (it >= 64 * kCh) continue;
+        const int rq = it / kCh, ch = it - rq * kCh;
+        const float* a = st_row(rq) + 8 * ch;
+        const f32x4_t a0 = *(const f32x4_t*)a, a1 = *(const f32x4_t*)(a + 4);
+        float x1[8], y[8];
         float sq = 0.f;
 #pragma unroll
-        for (int j = 0; j < WB; ++j) {
-          const int col = cbase + 16 * j;
-          const float x1 = acc[i][j][r] + res[i][r][j];
-          sq += x1 * x1;
-          if (m < M) {
-            ea.x1[(int64_t)m * N + col] = x1;
-            ea.h[tile_off(m, col, N)] = (bf16_t)f32_to_bf16(x1 * gam[j]);
-          }
+        for (int e = 0; e < 4; ++e) {
+          x1[2 * e] = (e < 2 ? a0[2 * e] : a1[2 * e - 4]) + bf16_to_f32(rv[u][e] & 0xFFFFu);
+          x1[2 * e + 1] = (e < 2 ? a0[2 * e + 1] : a1[2 * e - 3]) + bf16_to_f32(rv[u][e] >> 16);
         }
-        // Over the 16 columns c16 of this lane group, in a fixed butterfly.
-        sq += __shfl_xor(sq, 1, 16);
-        sq += __shfl_xor(sq, 2, 16);
-        sq += __shfl_xor(sq, 4, 16);
-        sq += __shfl_xor(sq, 8, 16);
-        if (c16 == 0) g_nss[wn][lr] = sq;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          sq += x1[e] * x1[e];
+          y[e] = x1[e] * bf16_to_f32(e & 1 ? gv[u][e >> 1] >> 16 : gv[u][e >> 1] & 0xFFFFu);
+        }
+        ssp[rq * kCh + ch] = sq;
+        const int m = m0 + 64 * p + rq;
+        if (m < M) {
+          float* xo = ea.x1 + (int64_t)m * N + n0 + 8 * ch;
+          *(f32x4_t*)xo = f32x4_t{x1[0], x1[1], x1[2], x1[3]};
+          *(f32x4_t*)(xo + 4) = f32x4_t{x1[4], x1[5], x1[6], x1[7]};
+          *(u32x4_t*)(ea.h + tile_off(m, n0 + 8 * ch, N)) =
+              u32x4_t{pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]), pack_bf16x2(y[4], y[5]),
+                      pack_bf16x2(y[6], y[7])};
+        }
       }
-    __syncthreads();
-    if (tid < kNM && m0 + tid < M)
-      ea.ss_part[(int64_t)(n0 / TN) * M + m0 + tid] = g_nss[0][tid] + g_nss[1][tid];
+      __syncthreads();
+      if (tid < 64 && m0 + 64 * p + tid < M) {
+        float t = 0.f;
+        for (int ch = 0; ch < kCh; ++ch) t += ssp[tid * kCh + ch];
+        ea.ss_part[(int64_t)(n0 / TN) * M + m0 + 64 * p + tid] = t;
+      }
+      __syncthreads();  // the quarter's staging and sums are read
+    }
+  } else if constexpr (MODE == kNarrowScatter) {
+    // out[out_idx[m]] = bf16(x1 + acc), 8 columns per piece.
+    for (int p = 0; p < 4; ++p) {
+      stage_quarter(p);
+      __syncthreads();
+      f32x4_t xv[kPer][2];
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {
+        const int it = min(tid + u * kNThreads, 64 * kCh - 1);
+        const int rq = it / kCh, ch = it - rq * kCh;
+        const float* xr = ea.x1_in + (int64_t)min(m0 + 64 * p + rq, M - 1) * N + n0 + 8 * ch;
+        xv[u][0] = *(const f32x4_t*)xr;
+        xv[u][1] = *(const f32x4_t*)(xr + 4);
+      }
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {
+        const int it = tid + u * kNThreads;
+        if (it >= 64 * kCh) continue;
+        const int rq = it / kCh, ch = it - rq * kCh;
+        const int m = m0 + 64 * p + rq;
+        if (m >= M) continue;
+        const float* a = st_row(rq) + 8 * ch;
+        const f32x4_t a0 = *(const f32x4_t*)a, a1 = *(const f32x4_t*)(a + 4);
+        const f32x4_t s0 = xv[u][0] + a0, s1 = xv[u][1] + a1;
+        *(u32x4_t*)(ea.out + (int64_t)g_nrow[64 * p + rq] * N + n0 + 8 * ch) =
+            u32x4_t{pack_bf16x2(s0[0], s0[1]), pack_bf16x2(s0[2], s0[3]),
+                    pack_bf16x2(s1[0], s1[1]), pack_bf16x2(s1[2], s1[3])};
+      }
+      __syncthreads();  // the quarter's staging is read
+    }
   } else if constexpr (MODE == kNarrowQkv) {
-    // Wave (wm, 0) holds dims j of the WB pair groups of its rows, wave
-    // (wm, 1) the dims j + 64. The first QA groups are rotated by wave
-    // (wm, 0), the rest by wave (wm, 1): each hands the other the halves it
-    // lacks through LDS ([group][i][r][lane] floats, conflict-free). The
-    // rotated bf16 values go back into LDS as [row][group][half][16 dims]
-    // and leave in 16-byte pieces of 8 dims: queries to q_out [M][Hq][128],
-    // keys (rotated) to their cache slot (block, position % 16), both 8
-    // contiguous dims; values (not rotated) element by element.
+    // Column block q of half 0 holds dims j of pair group q, block WB + q
+    // the dims j + 64, so a staged row has both halves of each pair. Per
+    // quarter: queries and keys in pieces of 8 pairs (rotate-half RoPE with
+    // the table's fp32 cos/sin of (position, j), then 16-byte stores of the 8
+    // j dims and of the 8 j + 64 dims: q_out [M][Hq][128], or the key tile
+    // of the row's cache slot); values (not rotated) as 8-byte runs of four
+    // tokens (the value tile order) where four staged rows fill slots
+    // 4a .. 4a + 3 of one block, element by element otherwise.
     constexpr int kHd = 128, kTile = kBlockTokens * kHd;
-    constexpr int QA = (WB + 1) / 2;
-    static_assert(32 * TN <= TN * kNK && 32 * TN + 4 * kNM <= kNM * kNK,
-                  "32 staged rows fit a W slot, and slot 4 beside the row slots");
-    float* const x_hi =  // dims j + 64 of groups q < QA
-        (float*)(wm == 0 ? sa0 : wm == 1 ? sa1 : wm == 2 ? sa2 : sa3);
-    float* const x_lo =  // dims j of groups q >= QA
-        (float*)(wm == 0 ? sw0 : wm == 1 ? sw1 : wm == 2 ? sw2 : sw3);
-    const u32x2_t* const slots = (const u32x2_t*)(sa4 + kNM * kNK) - kNM;
-    if (wn == 1) {
-#pragma unroll
-      for (int q = 0; q < QA; ++q)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) x_hi[((q * 4 + i) * 4 + r) * 64 + lane] = acc[i][q][r];
-    } else {
-#pragma unroll
-      for (int q = QA; q < WB; ++q)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            x_lo[(((q - QA) * 4 + i) * 4 + r) * 64 + lane] = acc[i][q][r];
-    }
-    __syncthreads();
     const int g0 = (n0 / TN) * WB;  // first pair group of the tile
-    // This lane's rotated (j, j + 64) pairs as packed bf16, per row group i,
-    // row r and pair group QB + k it finishes (QB = 0 on wave (wm, 0), QA on
-    // wave (wm, 1): the two cases are compiled apart so every index is a
-    // constant). The cos/sin of its (row, j) come from the RoPE table, one
-    // row group ahead.
-    uint32_t rot[4][4][QA];
-    auto rotate_half = [&](auto half) {
-      constexpr int QB = decltype(half)::value == 0 ? 0 : QA;
-      constexpr int NQ = decltype(half)::value == 0 ? QA : WB - QA;
-      f32x2_t cs[2][4][QA];
-      auto load_cs = [&](int i, int b) {
+    constexpr int kQK = 64 * WB * 2;  // (row, group, 8-pair half) pieces per quarter
+    constexpr int kQKPer = (kQK + kNThreads - 1) / kNThreads;
+    for (int p = 0; p < 4; ++p) {
+      stage_quarter(p);
+      __syncthreads();
+      f32x4_t cs[kQKPer][4];  // (cos, sin) of 8 pairs
 #pragma unroll
-        for (int k = 0; k < NQ; ++k) {
-          const int q = QB + k;
-          if (((g0 + q) >> 2) >= ea.Hq + ea.Hkv) continue;  // values: not rotated
-          const int jd = 16 * ((g0 + q) & 3) + c16;
+      for (int u = 0; u < kQKPer; ++u) {
+        const int it = min(tid + u * kNThreads, kQK - 1);
+        const int c8 = it & 1, q = (it >> 1) % WB, rq = (it >> 1) / WB;
+        const int jd0 = 16 * ((g0 + q) & 3) + 8 * c8;
+        const f32x4_t* t =
+            (const f32x4_t*)(ea.rope + ((int64_t)slots[64 * p + rq].x * (kHd / 2) + jd0) * 2);
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int lr = wm * 64 + i * 16 + 4 * j4 + r;
-            cs[b][r][k] = ((const f32x2_t*)ea.rope)[(int64_t)slots[lr].x * (kHd / 2) + jd];
-          }
-        }
-      };
-      load_cs(0, 0);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        if (i + 1 < 4) load_cs(i + 1, (i + 1) & 1);
-#pragma unroll
-        for (int k = 0; k < NQ; ++k) {
-          const int q = QB + k;
-          const bool rotate = ((g0 + q) >> 2) < ea.Hq + ea.Hkv;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            float lo, up;
-            if constexpr (QB == 0) {
-              lo = acc[i][q][r];
-              up = x_hi[((q * 4 + i) * 4 + r) * 64 + lane];
-            } else {
-              lo = x_lo[(((q - QA) * 4 + i) * 4 + r) * 64 + lane];
-              up = acc[i][q][r];
-            }
-            if (rotate) {
-              const f32x2_t c = cs[i & 1][r][k];
-              const float rlo = lo * c.x - up * c.y, rup = up * c.x + lo * c.y;
-              lo = rlo;
-              up = rup;
-            }
-            rot[i][r][k] = pack_bf16x2(lo, up);
-          }
-        }
+        for (int v = 0; v < 4; ++v) cs[u][v] = t[v];
       }
-    };
-    if (wn == 0)
-      rotate_half(std::integral_constant<int, 0>{});
-    else
-      rotate_half(std::integral_constant<int, 1>{});
-    __syncthreads();  // every wave is done with the exchange areas
-    // Staged rows: 32 rows per LDS object (rows 32 k .. 32 k + 31 in object k).
-    auto stage_row = [&](int k) -> bf16_t* {  // k wave-uniform
-      switch (k) {
-        case 0: return sa0;
-        case 1: return sa1;
-        case 2: return sa2;
-        case 3: return sa3;
-        case 4: return sa4;
-        case 5: return sw0;
-        case 6: return sw1;
-        default: return sw2;
-      }
-    };
-    auto stage_half = [&](auto half) {
-      constexpr int QB = decltype(half)::value == 0 ? 0 : QA;
-      constexpr int NQ = decltype(half)::value == 0 ? QA : WB - QA;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        bf16_t* const obj = stage_row(2 * wm + (i >> 1));
+      for (int u = 0; u < kQKPer; ++u) {
+        const int it = tid + u * kNThreads;
+        if (it >= kQK) continue;
+        const int c8 = it & 1, q = (it >> 1) % WB, rq = (it >> 1) / WB;
+        const int hh = (g0 + q) >> 2;
+        const int m = m0 + 64 * p + rq;
+        if (m >= M || hh >= ea.Hq + ea.Hkv) continue;  // values below
+        const float* lo = st_row(rq) + 16 * q + 8 * c8;
+        const float* up = st_row(rq) + 16 * (WB + q) + 8 * c8;
+        uint32_t wl[4], wu[4];
 #pragma unroll
-        for (int k = 0; k < NQ; ++k) {
+        for (int e = 0; e < 4; ++e) {
+          float rl[2], ru[2];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int rr = (i & 1) * 16 + 4 * j4 + r;  // row within the object
-            bf16_t* const p = obj + rr * TN + (QB + k) * 32 + c16;
-            p[0] = (bf16_t)(rot[i][r][k] & 0xFFFFu);
-            p[16] = (bf16_t)(rot[i][r][k] >> 16);
+          for (int f = 0; f < 2; ++f) {
+            const int k = 2 * e + f;  // pair k of the piece
+            const float c = cs[u][k >> 1][2 * (k & 1)], sn = cs[u][k >> 1][2 * (k & 1) + 1];
+            rl[f] = lo[k] * c - up[k] * sn;
+            ru[f] = up[k] * c + lo[k] * sn;
           }
+          wl[e] = pack_bf16x2(rl[0], rl[1]);
+          wu[e] = pack_bf16x2(ru[0], ru[1]);
+        }
+        const int jd0 = 16 * ((g0 + q) & 3) + 8 * c8;
+        const u32x4_t vl = {wl[0], wl[1], wl[2], wl[3]}, vu = {wu[0], wu[1], wu[2], wu[3]};
+        if (hh < ea.Hq) {
+          bf16_t* dst = ea.q_out + ((int64_t)m * ea.Hq + hh) * kHd + jd0;
+          *(u32x4_t*)dst = vl;
+          *(u32x4_t*)(dst + 64) = vu;
+        } else {
+          const u32x2_t sl = slots[64 * p + rq];
+          const int slot = (int)sl.x % kBlockTokens;
+          bf16_t* tile = ea.k_cache + ((int64_t)(int)sl.y * ea.Hkv + (hh - ea.Hq)) * kTile;
+          *(u32x4_t*)(tile + k_tile_offset(slot, jd0)) = vl;
+          *(u32x4_t*)(tile + k_tile_offset(slot, jd0 + 64)) = vu;
         }
       }
-    };
-    if (wn == 0)
-      stage_half(std::integral_constant<int, 0>{});
-    else
-      stage_half(std::integral_constant<int, 1>{});
-    __syncthreads();
-    // Queries and keys in 16-byte pieces: (row, group, half, 8-dim chunk),
-    // the chunk fastest.
-    constexpr int kPieces = kNM * WB * 4;
-    for (int it = tid; it < kPieces; it += kNThreads) {
-      const int c8 = it & 1, h = (it >> 1) & 1, q = (it >> 2) % WB, lr = (it >> 2) / WB;
-      const int hh = (g0 + q) >> 2;
-      const int m = m0 + lr;
-      if (m >= M || hh >= ea.Hq + ea.Hkv) continue;  // values below
-      const u32x4_t v = *(const u32x4_t*)(stage_row(lr >> 5) + (lr & 31) * TN + q * 32 +
-                                          h * 16 + c8 * 8);
-      const int dim = 64 * h + 16 * ((g0 + q) & 3) + 8 * c8;  // first of the 8 dims
-      if (hh < ea.Hq) {
-        *(u32x4_t*)(ea.q_out + ((int64_t)m * ea.Hq + hh) * kHd + dim) = v;
-      } else {
-        const u32x2_t sl = slots[lr];
-        bf16_t* tile = ea.k_cache + ((int64_t)(int)sl.y * ea.Hkv + (hh - ea.Hq)) * kTile;
-        *(u32x4_t*)(tile + k_tile_offset((int)sl.x % kBlockTokens, dim)) = v;
-      }
-    }
-    // Values: the tile keeps four consecutive tokens of a dim together, so a
-    // run of four rows that fill slots 4a .. 4a + 3 of one block leaves as one
-    // 8-byte store per dim, any other row element by element. Items: (row
-    // quad, group, 32 dims), the dim fastest.
-    constexpr int kVItems = (kNM / 4) * WB * 32;
-    for (int it = tid; it < kVItems; it += kNThreads) {
-      const int d32 = it & 31, q = (it >> 5) % WB, quad = (it >> 5) / WB;
-      const int hh = (g0 + q) >> 2;
-      if (hh < ea.Hq + ea.Hkv) continue;  // queries and keys above
-      const int dim = 64 * (d32 >> 4) + 16 * ((g0 + q) & 3) + (d32 & 15);
-      const int col = q * 32 + d32;  // staged column
-      const int lr0 = 4 * quad;
-      bf16_t* const vbase = ea.v_cache + (int64_t)(hh - ea.Hq - ea.Hkv) * kTile;
-      uint32_t e4[4];
-      u32x2_t sl[4];
+      // Values: (row quad, group, 32 dims), the dim fastest.
+      constexpr int kV = 16 * WB * 32;
+      for (int it = tid; it < kV; it += kNThreads) {
+        const int d32 = it & 31, q = (it >> 5) % WB, quad = (it >> 5) / WB;
+        const int hh = (g0 + q) >> 2;
+        if (hh < ea.Hq + ea.Hkv) continue;  // queries and keys above
+        const int dim = 64 * (d32 >> 4) + 16 * ((g0 + q) & 3) + (d32 & 15);
+        const int col = 16 * ((d32 >> 4) * WB + q) + (d32 & 15);  // staged column
+        const int lr0 = 64 * p + 4 * quad;
+        bf16_t* const vbase = ea.v_cache + (int64_t)(hh - ea.Hq - ea.Hkv) * kTile;
+        uint32_t e4[4];
+        u32x2_t sl[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        e4[e] = stage_row((lr0 + e) >> 5)[((lr0 + e) & 31) * TN + col];
-        sl[e] = slots[lr0 + e];
-      }
-      const int t0 = (int)sl[0].x % kBlockTokens;
-      bool run = m0 + lr0 + 3 < M && t0 % 4 == 0;
+        for (int e = 0; e < 4; ++e) {
+          e4[e] = f32_to_bf16(st_row(4 * quad + e)[col]);
+          sl[e] = slots[lr0 + e];
+        }
+        const int t0 = (int)sl[0].x % kBlockTokens;
+        bool run = m0 + lr0 + 3 < M && t0 % 4 == 0;
 #pragma unroll
-      for (int e = 1; e < 4; ++e)
-        run = run && sl[e].y == sl[0].y && (int)sl[e].x % kBlockTokens == t0 + e;
-      if (run) {
-        *(u32x2_t*)(vbase + (int64_t)(int)sl[0].y * ea.Hkv * kTile + v_tile_offset(t0, dim)) =
-            u32x2_t{e4[0] | (e4[1] << 16), e4[2] | (e4[3] << 16)};
-      } else {
+        for (int e = 1; e < 4; ++e)
+          run = run && sl[e].y == sl[0].y && (int)sl[e].x % kBlockTokens == t0 + e;
+        if (run) {
+          *(u32x2_t*)(vbase + (int64_t)(int)sl[0].y * ea.Hkv * kTile + v_tile_offset(t0, dim)) =
+              u32x2_t{e4[0] | (e4[1] << 16), e4[2] | (e4[3] << 16)};
+        } else {
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (m0 + lr0 + e < M)
-            vbase[(int64_t)(int)sl[e].y * ea.Hkv * kTile +
-                  v_tile_offset((int)sl[e].x % kBlockTokens, dim)] = (bf16_t)e4[e];
+          for (int e = 0; e < 4; ++e)
+            if (m0 + lr0 + e < M)
+              vbase[(int64_t)(int)sl[e].y * ea.Hkv * kTile +
+                    v_tile_offset((int)sl[e].x % kBlockTokens, dim)] = (bf16_t)e4[e];
+        }
       }
+      __syncthreads();  // the quarter's staging is read
     }
   } else if constexpr (MODE == kNarrowSwiglu) {
     // Gate in blocks q < WB/2, up in blocks WB/2 + q, of outputs
@@ -518,28 +502,6 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
       const u32x4_t v = *(const u32x4_t*)(stg(row >> 6) + (row & 63) * kSS + oc);
       if (m0 + row < M) *(u32x4_t*)(ea.h + tile_off(m0 + row, o0 + oc, F)) = v;
     }
-  } else {
-    float x1v[4][4][WB];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = min(m0 + wm * 64 + i * 16 + 4 * j4 + r, M - 1);
-        const float* xr = ea.x1_in + (int64_t)m * N + cbase;
-#pragma unroll
-        for (int j = 0; j < WB; ++j) x1v[i][r][j] = xr[16 * j];
-      }
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int lr = wm * 64 + i * 16 + 4 * j4 + r;
-        if (m0 + lr >= M) continue;
-        bf16_t* orow = ea.out + (int64_t)g_nrow[lr] * N + cbase;
-#pragma unroll
-        for (int j = 0; j < WB; ++j)
-          orow[16 * j] = (bf16_t)f32_to_bf16(x1v[i][r][j] + acc[i][j][r]);
-      }
   }
 }
 
