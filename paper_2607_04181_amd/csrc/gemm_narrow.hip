@@ -489,7 +489,7 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
         for (int q = 0; q < WB / 2; ++q) {
           const float g = acc[i][q][r] * rs, u = acc[i][WB / 2 + q][r] * rs;
           mine[rl * kSS + wn * (TN / 4) + 16 * q + c16] =
-              (bf16_t)f32_to_bf16(g / (1.0f + expf(-g)) * u);
+              (bf16_t)f32_to_bf16(silu_mul(g, u));
         }
       }
     __syncthreads();

@@ -226,7 +226,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_kernel(
           const float g = acc[mt][r];
           if (c16 < 8 && m < M)
             H[h_tiled ? tile_off(m, o0 + c16, N / 2) : (int64_t)m * (N / 2) + o0 + c16] =
-                (bf16_t)f32_to_bf16(g / (1.0f + expf(-g)) * u);
+                (bf16_t)f32_to_bf16(silu_mul(g, u));
         } else if (m < M) {
           // Non-temporal: the partials are read once, by the next kernel.
           __builtin_nontemporal_store(acc[mt][r], out + (int64_t)m * N + n_col);
@@ -452,7 +452,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemm_skinny_rows_kernel(
             const int o = (blockIdx.x * WAVES + j) * 8;
             if (c16 < 8 && m < M)
               H[h_tiled ? tile_off(m, o + c16, N / 2) : (int64_t)m * (N / 2) + o + c16] =
-                  (bf16_t)f32_to_bf16(g / (1.0f + expf(-g)) * u);
+                  (bf16_t)f32_to_bf16(silu_mul(g, u));
           } else if (m < M) {
             __builtin_nontemporal_store(acc[i][j][r],
                                         out + (int64_t)m * N + blockIdx.x * NR + 16 * j + c16);

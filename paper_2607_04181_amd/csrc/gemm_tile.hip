@@ -430,7 +430,7 @@ __global__ __launch_bounds__(kTThreads) void gemm_tile_kernel(const bf16_t* __re
             g *= rs;
             u *= rs;
           }
-          if (m < M) H[tile_off(m, o, F)] = (bf16_t)f32_to_bf16(g / (1.0f + expf(-g)) * u);
+          if (m < M) H[tile_off(m, o, F)] = (bf16_t)f32_to_bf16(silu_mul(g, u));
         }
     }
     return;

@@ -489,7 +489,7 @@ __global__ __launch_bounds__(kRowThreads) void swiglu_kernel(const float* __rest
   T* dst = u + (tiled ? tile_off(i, c, F) : (int64_t)i * F + c);
   float r[4];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) r[e] = g[e] / (1.0f + expf(-g[e])) * up[e];
+  for (int e = 0; e < 4; ++e) r[e] = silu_mul(g[e], up[e]);
   store4(dst, r[0], r[1], r[2], r[3]);
 }
 
