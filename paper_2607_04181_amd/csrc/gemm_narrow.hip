@@ -56,6 +56,11 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 // LDS ring slots for a tile width: as many stages of 256 x 32 A and TN x 32
 // W as fit beside the spare block in 160 KB.
 constexpr int narrow_slots(int TN) { return TN <= 160 ? 6 : 5; }
+// Stages per unrolled round of the main loop: fragment registers alternate
+// with the stage's parity, so a round is an even number of stages.
+constexpr int narrow_round(int TN) {
+  return narrow_slots(TN) % 2 ? 2 * narrow_slots(TN) : narrow_slots(TN);
+}
 
 enum { kNarrowResid = 0, kNarrowScatter = 1, kNarrowSwiglu = 2, kNarrowQkv = 3 };
 
@@ -77,9 +82,7 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
   constexpr int kLoads = kExtra > 0 ? 4 : 3;
   constexpr int kBuf = narrow_slots(TN);
   constexpr int kAhead = kBuf - 1;  // stages in flight
-  // Stages per unrolled round: fragment registers alternate with the stage's
-  // parity, so a round is an even number of stages.
-  constexpr int kRound = kBuf % 2 ? 2 * kBuf : kBuf;
+  constexpr int kRound = narrow_round(TN);
   // One LDS object per ring slot, so the compiler tracks each slot's pending
   // direct loads on its own and never drains the ring before a fragment read.
   __shared__ __attribute__((aligned(16))) bf16_t sa0[kNM * kNK], sa1[kNM * kNK],
@@ -287,18 +290,23 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
     // order, and the row's sum of x1^2 over the tile: per piece in column
     // order, then the pieces in order (slot 4, after the row indices).
     float* const ssp = (float*)sa4 + kNM;
+    // A thread's residual pieces of all four quarters and its gamma pieces
+    // (the same columns in every quarter), for clamped pieces (no branch),
+    // before the first quarter: one memory round trip for the epilogue.
+    u32x4_t rv[4][kPer], gv[kPer];
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int it = min(tid + u * kNThreads, 64 * kCh - 1);
+      const int rq = it / kCh, ch = it - rq * kCh;
+      gv[u] = *(const u32x4_t*)(ea.gamma + n0 + 8 * ch);
+#pragma unroll
+      for (int p = 0; p < 4; ++p)
+        rv[p][u] = *(const u32x4_t*)(ea.res_x + (int64_t)g_nrow[64 * p + rq] * N + n0 + 8 * ch);
+    }
+#pragma unroll
     for (int p = 0; p < 4; ++p) {
       stage_quarter(p);
       __syncthreads();
-      // All of a thread's loads first, for clamped pieces (no branch).
-      u32x4_t rv[kPer], gv[kPer];
-#pragma unroll
-      for (int u = 0; u < kPer; ++u) {
-        const int it = min(tid + u * kNThreads, 64 * kCh - 1);
-        const int rq = it / kCh, ch = it - rq * kCh;
-        rv[u] = *(const u32x4_t*)(ea.res_x + (int64_t)g_nrow[64 * p + rq] * N + n0 + 8 * ch);
-        gv[u] = *(const u32x4_t*)(ea.gamma + n0 + 8 * ch);
-      }
 #pragma unroll
       for (int u = 0; u < kPer; ++u) {
         const int it = tid + u * kNThreads;
@@ -310,8 +318,8 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
         float sq = 0.f;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          x1[2 * e] = (e < 2 ? a0[2 * e] : a1[2 * e - 4]) + bf16_to_f32(rv[u][e] & 0xFFFFu);
-          x1[2 * e + 1] = (e < 2 ? a0[2 * e + 1] : a1[2 * e - 3]) + bf16_to_f32(rv[u][e] >> 16);
+          x1[2 * e] = (e < 2 ? a0[2 * e] : a1[2 * e - 4]) + bf16_to_f32(rv[p][u][e] & 0xFFFFu);
+          x1[2 * e + 1] = (e < 2 ? a0[2 * e + 1] : a1[2 * e - 3]) + bf16_to_f32(rv[p][u][e] >> 16);
         }
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
@@ -338,19 +346,23 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
       __syncthreads();  // the quarter's staging and sums are read
     }
   } else if constexpr (MODE == kNarrowScatter) {
-    // out[out_idx[m]] = bf16(x1 + acc), 8 columns per piece.
-    for (int p = 0; p < 4; ++p) {
-      stage_quarter(p);
-      __syncthreads();
-      f32x4_t xv[kPer][2];
+    // out[out_idx[m]] = bf16(x1 + acc), 8 columns per piece. A thread's x1
+    // pieces of all four quarters are loaded before the first quarter.
+    f32x4_t xv[4][kPer][2];
+#pragma unroll
+    for (int p = 0; p < 4; ++p)
 #pragma unroll
       for (int u = 0; u < kPer; ++u) {
         const int it = min(tid + u * kNThreads, 64 * kCh - 1);
         const int rq = it / kCh, ch = it - rq * kCh;
         const float* xr = ea.x1_in + (int64_t)min(m0 + 64 * p + rq, M - 1) * N + n0 + 8 * ch;
-        xv[u][0] = *(const f32x4_t*)xr;
-        xv[u][1] = *(const f32x4_t*)(xr + 4);
+        xv[p][u][0] = *(const f32x4_t*)xr;
+        xv[p][u][1] = *(const f32x4_t*)(xr + 4);
       }
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      stage_quarter(p);
+      __syncthreads();
 #pragma unroll
       for (int u = 0; u < kPer; ++u) {
         const int it = tid + u * kNThreads;
@@ -360,7 +372,7 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
         if (m >= M) continue;
         const float* a = st_row(rq) + 8 * ch;
         const f32x4_t a0 = *(const f32x4_t*)a, a1 = *(const f32x4_t*)(a + 4);
-        const f32x4_t s0 = xv[u][0] + a0, s1 = xv[u][1] + a1;
+        const f32x4_t s0 = xv[p][u][0] + a0, s1 = xv[p][u][1] + a1;
         *(u32x4_t*)(ea.out + (int64_t)g_nrow[64 * p + rq] * N + n0 + 8 * ch) =
             u32x4_t{pack_bf16x2(s0[0], s0[1]), pack_bf16x2(s0[2], s0[3]),
                     pack_bf16x2(s1[0], s1[1]), pack_bf16x2(s1[2], s1[3])};
@@ -380,10 +392,9 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
     const int g0 = (n0 / TN) * WB;  // first pair group of the tile
     constexpr int kQK = 64 * WB * 2;  // (row, group, 8-pair half) pieces per quarter
     constexpr int kQKPer = (kQK + kNThreads - 1) / kNThreads;
-    for (int p = 0; p < 4; ++p) {
-      stage_quarter(p);
-      __syncthreads();
-      f32x4_t cs[kQKPer][4];  // (cos, sin) of 8 pairs
+    // The (cos, sin) of 8 pairs per piece, one quarter ahead.
+    f32x4_t cs[2][kQKPer][4];
+    auto load_cs = [&](int p, f32x4_t (&dst)[kQKPer][4]) {
 #pragma unroll
       for (int u = 0; u < kQKPer; ++u) {
         const int it = min(tid + u * kNThreads, kQK - 1);
@@ -392,8 +403,15 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
         const f32x4_t* t =
             (const f32x4_t*)(ea.rope + ((int64_t)slots[64 * p + rq].x * (kHd / 2) + jd0) * 2);
 #pragma unroll
-        for (int v = 0; v < 4; ++v) cs[u][v] = t[v];
+        for (int v = 0; v < 4; ++v) dst[u][v] = t[v];
       }
+    };
+    load_cs(0, cs[0]);
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      if (p + 1 < 4) load_cs(p + 1, cs[(p + 1) & 1]);
+      stage_quarter(p);
+      __syncthreads();
 #pragma unroll
       for (int u = 0; u < kQKPer; ++u) {
         const int it = tid + u * kNThreads;
@@ -411,7 +429,8 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
 #pragma unroll
           for (int f = 0; f < 2; ++f) {
             const int k = 2 * e + f;  // pair k of the piece
-            const float c = cs[u][k >> 1][2 * (k & 1)], sn = cs[u][k >> 1][2 * (k & 1) + 1];
+            const float c = cs[p & 1][u][k >> 1][2 * (k & 1)];
+            const float sn = cs[p & 1][u][k >> 1][2 * (k & 1) + 1];
             rl[f] = lo[k] * c - up[k] * sn;
             ru[f] = up[k] * c + lo[k] * sn;
           }
@@ -505,6 +524,221 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
   }
 }
 
+// Persistent SwiGLU variant (gate/up projection with RMSNorm_2 folded in):
+// one workgroup per CU keeps a row tile and walks a list of column tiles, so
+// the direct-load ring streams on across tile boundaries (the next tile's
+// first stages load while a tile's epilogue runs, and no workgroup starts
+// cold after the first), and the rows' 1/rms are taken once. Same main loop,
+// stage order and epilogue arithmetic as gemm_narrow_kernel's SwiGLU mode,
+// so every output is bit-identical to it.
+//   * Grid: 256 workgroups, 32 per XCD (blockIdx % 8). Workgroup k of XCD x
+//     takes row tile k % tiles_m and the column tiles
+//     x + 8 (k / tiles_m + ng s), s = 0, 1, ..., ng = 32 / tiles_m: at each
+//     step the workgroups of one XCD share ng W tiles in its L2, each read by
+//     tiles_m of them.
+//   * The ring's slots are in use during an epilogue, so each wave stages its
+//     SwiGLU outputs through a private 16-row buffer and writes them as
+//     16-byte tile-order pieces. After an epilogue all vector memory
+//     operations are waited for: the partial wait counts of the ring assume
+//     that only its loads are outstanding.
+template <int TN>
+__global__ __launch_bounds__(kNThreads) void gemm_narrow_swiglu_persistent_kernel(
+    const bf16_t* __restrict__ A, const bf16_t* __restrict__ W, int M, int F, int K,
+    bf16_t* __restrict__ H, const float* __restrict__ ss_in, int n_ss, float eps) {
+  static_assert(TN % 64 == 0 && TN / 16 >= 8 && TN / 16 <= 16, "tile width");
+  constexpr int WB = TN / 32, kWBlocks = TN / 16, kExtra = kWBlocks - 8;
+  constexpr int kLoads = kExtra > 0 ? 4 : 3;
+  constexpr int kBuf = narrow_slots(TN);
+  constexpr int kAhead = kBuf - 1;
+  constexpr int kRound = narrow_round(TN);
+  constexpr int kWO = TN / 4;  // outputs of a wave's column half
+  static_assert(kWO % 8 == 0, "16-byte output pieces");
+  __shared__ __attribute__((aligned(16))) bf16_t sa0[kNM * kNK], sa1[kNM * kNK],
+      sa2[kNM * kNK], sa3[kNM * kNK], sa4[kNM * kNK], sa5[kNM * kNK];
+  __shared__ __attribute__((aligned(16))) bf16_t sw0[TN * kNK], sw1[TN * kNK], sw2[TN * kNK],
+      sw3[TN * kNK], sw4[TN * kNK], sw5[TN * kNK];
+  __shared__ __attribute__((aligned(16))) bf16_t spare[512];
+  __shared__ __attribute__((aligned(16))) bf16_t stg[8][16 * kWO];  // per-wave output rows
+  __shared__ float rn[kNM];                                         // the rows' 1/rms
+  bf16_t* const ta[6] = {sa0, sa1, sa2, sa3, sa4, sa5};
+  bf16_t* const tw[6] = {sw0, sw1, sw2, sw3, sw4, sw5};
+
+  const int N = 2 * F;
+  const int tiles_m = (M + kNM - 1) / kNM;  // divides 32 (host check)
+  const int tiles_n = N / TN;
+  const int x = blockIdx.x % kNXCDs, kx = blockIdx.x / kNXCDs;
+  const int ng = 32 / tiles_m;
+  const int n_first = x + kNXCDs * (kx / tiles_m), n_step = kNXCDs * ng;
+  const int T = n_first < tiles_n ? (tiles_n - 1 - n_first) / n_step + 1 : 0;
+  if (T == 0) return;  // the whole workgroup leaves
+  const int m0 = (kx % tiles_m) * kNM;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wv & 3, wn = wv >> 2;
+  const int c16 = lane & 15, j4 = lane >> 4;
+  const int stages = K / kNK;
+
+  // W block of the first tile's block blk (the gate/up pairing of
+  // gemm_narrow_kernel); later tiles are n_step tiles further, a fixed
+  // number of blocks.
+  const int o_first = n_first * (TN / 2);
+  auto w_block = [&](int blk) -> int {
+    const int h = blk / WB, r = blk % WB;
+    const int o = o_first + h * (TN / 4) + 16 * (r % (WB / 2));
+    return ((r < WB / 2 ? 0 : F) + o) >> 4;
+  };
+  const int64_t blk_elems = (int64_t)(K / kNK) * 512;
+  const int64_t w_step = (int64_t)n_step * (TN / 32) * blk_elems;
+  const bf16_t* src_a[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int ag = min((m0 + 32 * wv + 16 * h) >> 4, (M - 1) >> 4);
+    src_a[h] = A + (int64_t)ag * blk_elems + lane * 8;
+  }
+  const bf16_t* src_w0 = W + (int64_t)w_block(wv) * blk_elems + lane * 8;
+  const bf16_t* src_w1 = W + (int64_t)w_block(wv < kExtra ? 8 + wv : wv) * blk_elems + lane * 8;
+  // Stage st of the tile whose W blocks are w_off past the first tile's.
+  // The stage offsets pass through empty asm statements: the compiler then
+  // forms each address where it is used, instead of keeping precomputed
+  // addresses of the unrolled stages (and of the prologue's, which the last
+  // round's next-tile loads repeat) in registers.
+  auto issue = [&](int64_t w_off, int st, int slot) {
+    int64_t oa = (int64_t)st * 512, ow = w_off + (int64_t)st * 512;
+    asm volatile("" : "+s"(oa), "+s"(ow));
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      __builtin_amdgcn_global_load_lds(src_a[h] + oa,
+                                       (lds_void_t*)(ta[slot] + (2 * wv + h) * 512), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(src_w0 + ow, (lds_void_t*)(tw[slot] + wv * 512), 16, 0,
+                                     0);
+    if constexpr (kExtra > 0)
+      __builtin_amdgcn_global_load_lds(
+          src_w1 + ow, (lds_void_t*)(wv < kExtra ? tw[slot] + (8 + wv) * 512 : spare), 16, 0,
+          0);
+  };
+
+  f32x4_t acc[4][WB];
+  auto read_frags = [&](const bf16_t* la, const bf16_t* lw, bf16x8_t* a, bf16x8_t* w) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      a[i] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(la + (wm * 4 + i) * 512 + lane * 8));
+#pragma unroll
+    for (int j = 0; j < WB; ++j)
+      w[j] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(lw + (wn * WB + j) * 512 + lane * 8));
+  };
+  auto mfma_step = [&](const bf16x8_t* a, const bf16x8_t* w) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < WB; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], w[j], acc[i][j], 0, 0, 0);
+    for (int g = 0; g < 4 + WB; ++g) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4 * WB - 4 - WB, 0);
+  };
+
+  // RMSNorm_2's per-tile sums of row m0 + tid % 256 (tiles past n_ss repeat
+  // the last), loaded ahead of the ring so the first stage wait covers them.
+  float ssv[kNMaxTiles];
+  {
+    const int m = min(m0 + (tid & (kNM - 1)), M - 1);
+#pragma unroll
+    for (int t = 0; t < kNMaxTiles; ++t) ssv[t] = ss_in[(int64_t)min(t, n_ss - 1) * M + m];
+  }
+#pragma unroll
+  for (int st = 0; st < kAhead; ++st) issue(0, st, st);
+  wait_vmcnt<(kAhead - 1) * kLoads>();
+  __builtin_amdgcn_sched_barrier(0);
+  if (tid < kNM) {
+    float t2 = 0.f;
+#pragma unroll
+    for (int t = 0; t < kNMaxTiles; ++t) t2 += t < n_ss ? ssv[t] : 0.f;
+    rn[tid] = 1.0f / sqrtf(t2 / (float)K + eps);
+  }
+  stage_barrier();  // stage 0 and the 1/rms are in LDS
+  bf16x8_t fa[2][4], fw[2][WB];
+  read_frags(ta[0], tw[0], fa[0], fw[0]);
+  // One unrolled round: stages st0 .. st0 + kRound - 1 of the tile at w_off
+  // (a tile is a whole number of rounds, kAhead < kRound). Only in a tile's
+  // last round do the loads run into the next tile (at w_next; after the
+  // last tile, that tile again: loaded, never multiplied), and that round
+  // leaves the next tile's first fragments unread, so they are not held
+  // through the epilogue.
+  auto ring_round = [&](int st0, int64_t w_off, int64_t w_next, auto last) {
+#pragma unroll
+    for (int u = 0; u < kRound; ++u) {
+      wait_vmcnt<(kAhead - 2) * kLoads>();
+      stage_barrier();
+      if (!decltype(last)::value || u + kAhead < kRound)
+        issue(w_off, st0 + u + kAhead, (u + kAhead) % kBuf);
+      else
+        issue(w_next, u + kAhead - kRound, (u + kAhead) % kBuf);
+      if (!decltype(last)::value || u + 1 < kRound)
+        read_frags(ta[(u + 1) % kBuf], tw[(u + 1) % kBuf], fa[(u + 1) & 1], fw[(u + 1) & 1]);
+      mfma_step(fa[u & 1], fw[u & 1]);
+    }
+  };
+  bf16_t* const mine = stg[wv];
+  for (int s = 0; s < T; ++s) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < WB; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    if (s > 0) {
+      // After an epilogue: every vector memory operation done (its stores
+      // too, which the ring's partial wait counts do not allow for), then
+      // the tile's first stage is published and read.
+      wait_vmcnt<0>();
+      stage_barrier();
+      read_frags(ta[0], tw[0], fa[0], fw[0]);
+    }
+    const int64_t w_off = (int64_t)s * w_step;
+    const int64_t w_next = s + 1 < T ? w_off + w_step : w_off;
+    for (int st0 = 0; st0 + kRound < stages; st0 += kRound)
+      ring_round(st0, w_off, w_off, std::false_type{});
+    ring_round(stages - kRound, w_off, w_next, std::true_type{});
+    // Epilogue: h = silu(gate) * up for outputs o0 + kWO wn + 16 q + c16
+    // (gate in blocks q < WB / 2, up in WB / 2 + q), 16 rows at a time
+    // through this wave's buffer, then 16-byte pieces of 8 outputs of a row
+    // to H in tile order [M][F].
+    const int o0 = (n_first + n_step * s) * (TN / 2) + kWO * wn;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float rs = rn[64 * wm + 16 * i + 4 * j4 + r];
+#pragma unroll
+        for (int q = 0; q < WB / 2; ++q) {
+          const float g = acc[i][q][r] * rs, u = acc[i][WB / 2 + q][r] * rs;
+          mine[(4 * j4 + r) * kWO + 16 * q + c16] = (bf16_t)f32_to_bf16(silu_mul(g, u));
+        }
+      }
+      // Reads of the rows just written by this wave (LDS operations of a
+      // wave are performed in order). tile_off(m, o0 + 8 pc, F) for
+      // m = mr + row (mr a multiple of 16) splits into a wave-uniform block
+      // offset and a lane part, so the address is a scalar base plus a
+      // 32-bit offset.
+      const int mr = m0 + 64 * wm + 16 * i;
+      bf16_t* const hb = H + ((int64_t)(mr >> 4) * (F >> 5) + (o0 >> 5)) * 512;
+#pragma unroll
+      for (int c0 = 0; c0 < 16 * kWO / 8; c0 += 64) {
+        const int c = c0 + lane;
+        const int row = c / (kWO / 8), pc = c % (kWO / 8);
+        const int kk = (o0 & 31) + 8 * pc;
+        if (c < 16 * kWO / 8) {
+          const u32x4_t v = *(const u32x4_t*)(mine + row * kWO + pc * 8);
+          if (mr + row < M) *(u32x4_t*)(hb + ((kk >> 5) * 512 + ((kk & 31) >> 3) * 128 + row * 8)) = v;
+        }
+      }
+    }
+  }
+  wait_vmcnt<0>();  // no direct load outlives the workgroup
+}
+
 template <int MODE>
 hipError_t launch_narrow(int tn, const uint16_t* A, const uint16_t* W, int M, int N, int K,
                          const NarrowEpiArgs& ea, hipStream_t st) {
@@ -582,6 +816,15 @@ hipError_t launch_gemm_narrow_swiglu_bf16(const uint16_t* A, const uint16_t* W_g
   if (M <= 0) return hipSuccess;
   if (!narrow_swiglu_fits(F, K) || !H || !ss_in || ss_tiles < 1 || ss_tiles > kNMaxTiles)
     return hipErrorInvalidValue;
+  // Persistent when the row tiles divide the 32 workgroups of an XCD and a
+  // tile is a whole number of unrolled rounds.
+  const int tiles_m = (M + kNM - 1) / kNM;
+  if (32 % tiles_m == 0 && (K / kNK) % narrow_round(192) == 0) {
+    COCO_LAUNCH((gemm_narrow_swiglu_persistent_kernel<192>), dim3(256), dim3(kNThreads), 0, st,
+                (const bf16_t*)A, (const bf16_t*)W_gate_up, M, F, K, (bf16_t*)H, ss_in,
+                ss_tiles, eps);
+    return hipGetLastError();
+  }
   NarrowEpiArgs ea{};
   ea.h = H;
   ea.ss_in = ss_in;

@@ -215,6 +215,41 @@ def test_prefill_request_aligned_split_is_bit_identical():
         assert np.array_equal(k1, k2) and np.array_equal(v1, v2)
 
 
+def test_prefill_gate_up_plans_agree_bit_exactly_and_match_oracle():
+    """d = 640, F = 3456 (36 gate/up column tiles of 96 outputs), 2048 rows: the
+    persistent gate/up GEMM, where a workgroup takes its row tile through
+    several column tiles (here up to two) with the load ring running across
+    them, against request-aligned shares of 900 rows (persistent, one tile per
+    workgroup) and 1148 rows (five row tiles: the one-tile-per-workgroup
+    kernel). Rows and appended cache bytes are bit-identical; a request's rows
+    and cache match the oracle."""
+    shape = small_bf16_shape(d=640, hq=5, hkv=1, ffn=3456)
+    b = ragged_prefill_batch(31, priors=[0, 100, 37], lens=[900, 248, 900], max_ctx=1024,
+                             hidden_rows=2100)
+    rep = Replica.for_batch(shape, "s31", 1, b)
+    hidden = WD.hidden_tensor(shape, "s31", b.hidden_rows)
+    h0 = to64(hidden)
+    snap = PoolSnapshot(rep.layers[0], pool_blocks_of_new_tokens(b))
+    whole = hidden.clone()
+    rep.forward(0, whole, WD.batch_tensors(b))
+    torch.cuda.synchronize()
+    kv_whole = _kv_snapshot(rep, b)
+    ref, _, cache, sub = oracle_prefill_seqs(shape, "s31", 0, b, [1], h0)
+    _check_rows("gate/up plans, request 1", to64(whole)[sub.row_idx], ref, h0[sub.row_idx])
+    t0, t1 = int(b.prior_lens[1]), int(b.ctx_lens[1])
+    K, V = gpu_cache_tokens(rep.layers[0], b, 1, t0, t1)
+    assert normwise_err(K, cache.K[0][t0:t1]) < TOL
+    assert normwise_err(V, cache.V[0][t0:t1]) < TOL
+    snap.restore()
+    split = hidden.clone()
+    for seqs in ([0], [1, 2]):
+        rep.forward(0, split, WD.batch_tensors(b.select_seqs(seqs)))
+    torch.cuda.synchronize()
+    assert torch.equal(split.view(torch.int16), whole.view(torch.int16))
+    for (k1, v1), (k2, v2) in zip(_kv_snapshot(rep, b), kv_whole):
+        assert np.array_equal(k1, k2) and np.array_equal(v1, v2)
+
+
 def test_zero_output_projections_give_identity_bit_exactly():
     """With W_o = W_d = 0 the layer returns its input rows: pins gather ->
     residual -> scatter bit for bit."""
