@@ -181,12 +181,16 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
 #pragma unroll
       for (int j = 0; j < WB; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], w[j], acc[i][j], 0, 0, 0);
-    // Interleave the fragment reads issued next to these MFMAs.
+    // The stage's direct loads after the first four MFMAs (the MFMA pipe
+    // restarts right after the barrier), then the fragment reads of the next
+    // stage interleaved with these MFMAs.
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);       // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x020, kLoads, 0);  // VMEM read
     for (int g = 0; g < 4 + WB; ++g) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 4 * WB - 4 - WB, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 4 * WB - 8 - WB, 0);
   };
 
   // The epilogue's row of each tile row (residual and scatter variants) or
@@ -634,11 +638,13 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_swiglu_persistent_kerne
 #pragma unroll
       for (int j = 0; j < WB; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], w[j], acc[i][j], 0, 0, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);       // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x020, kLoads, 0);  // VMEM read
     for (int g = 0; g < 4 + WB; ++g) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 4 * WB - 4 - WB, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 4 * WB - 8 - WB, 0);
   };
 
   // RMSNorm_2's per-tile sums of row m0 + tid % 256 (tiles past n_ss repeat
