@@ -1,5 +1,5 @@
-// Narrow-output GEMM for prefill (bf16 MFMA): the O and down projections,
-// whose output width is the model width d.
+// Prefill GEMMs on 256-row tiles of TN columns (bf16 MFMA), each unsplit
+// along K with its consumer's work in the epilogue.
 //
 //   acc[m][n] = sum_k A[m][k] * W[n][k]      A: [M][K], W: [N][K], both bf16
 //
@@ -8,27 +8,34 @@
 // v_mfma_f32_16x16x32_bf16 operand, so one 16-byte-per-lane load copies a
 // block to LDS unchanged and one 16-byte LDS read per lane is a fragment.
 //
-// A 256 x 256 tile grid leaves these projections with d / 256 column tiles
-// per 256 rows: 160 tiles for d = 5120 and a 2048-row chunk, on 256 CUs.
-// Here a tile is 256 rows x TN columns with TN = 160 or 128 (narrow_tile_n:
-// d / TN <= 32 column tiles), so the chunk is exactly 256 tiles for
-// d = 5120 (TN = 160) and d = 4096 (TN = 128), and each projection runs
-// unsplit along K with its consumer's work in the epilogue:
-//   * residual variant (O projection): x1 = acc + residual row (fp32 out),
+// A 256 x 256 tile grid leaves the d-wide projections with d / 256 column
+// tiles per 256 rows: 160 tiles for d = 5120 and a 2048-row chunk, on 256
+// CUs. Here TN comes from N alone: 160 or 128 for the O and down projections
+// (narrow_tile_n: d / TN <= 32 column tiles, so a 2048-row chunk is exactly
+// 256 tiles for d = 5120 and 4096), 192 for gate/up, 224, 192 or 160 for
+// QKV. Epilogue variants:
+//   * residual (O projection): x1 = acc + residual row (fp32 out),
 //     h = bf16(x1 * gamma) in tile order for the gate/up projection, and the
 //     tile's row sums of x1^2 (RMSNorm_2's statistics, finished by the
 //     gate/up epilogue);
-//   * scatter variant (down projection): out[out_idx[m]] = bf16(x1 + acc),
-//     the layer output written straight to its row of the full batch.
+//   * scatter (down projection): out[out_idx[m]] = bf16(x1 + acc), the layer
+//     output written straight to its row of the full batch;
+//   * SwiGLU (gate/up projection): each lane holds the gate and up values of
+//     its outputs; h = silu(gate / rms) * up / rms in tile order;
+//   * QKV: a tile holds whole RoPE pairs; queries are rotated into q, keys
+//     rotated and values copied into the paged cache.
+// gemm_narrow_swiglu_persistent_kernel runs the SwiGLU variant with one
+// workgroup per CU walking several column tiles of one row tile.
 // The main loop:
 //   * 512 threads, eight waves as 4 (rows) x 2 (columns); each wave owns a
 //     64 x TN/2 sub-tile as 4 x TN/32 accumulators of 16 x 16, two waves per
 //     SIMD so one wave's MFMAs issue while the other reads LDS;
 //   * 32-deep K stages of both tiles go straight from global memory to LDS
-//     (global_load_lds, no register staging) into a ring of six slots, five
-//     stages in flight (the loads come from L2, the MALL or HBM, whose
-//     latency under this load is several stages of MFMA work); wave w copies A blocks 2w, 2w + 1 and W block
-//     w (for TN = 160 waves 0 and 1 also W blocks 8 and 9);
+//     (global_load_lds, no register staging) into a ring of six slots (five
+//     for TN > 160), all but one stage in flight (the loads come from L2, the
+//     MALL or HBM, whose latency under this load is several stages of MFMA
+//     work); wave w copies A blocks 2w, 2w + 1 and W block w, and for
+//     TN > 128 a second W block (or a spare copy);
 //   * one barrier per stage, which publishes stage st + 1 and guarantees
 //     that the slot the next loads overwrite was read by every wave;
 //   * workgroups are remapped so that the tiles sharing a W column slab run
