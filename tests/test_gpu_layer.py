@@ -215,17 +215,28 @@ def test_prefill_request_aligned_split_is_bit_identical():
         assert np.array_equal(k1, k2) and np.array_equal(v1, v2)
 
 
-def test_prefill_gate_up_plans_agree_bit_exactly_and_match_oracle():
-    """d = 640, F = 3456 (36 gate/up column tiles of 96 outputs), 2048 rows: the
-    persistent gate/up GEMM, where a workgroup takes its row tile through
-    several column tiles (here up to two) with the load ring running across
-    them, against request-aligned shares of 900 rows (persistent, one tile per
-    workgroup) and 1148 rows (five row tiles: the one-tile-per-workgroup
-    kernel). Rows and appended cache bytes are bit-identical; a request's rows
-    and cache match the oracle."""
+# Gate/up plans at d = 640, F = 3456 (36 column tiles of 96 outputs): (priors,
+# lengths, request-aligned shares, request checked against the oracle). The
+# whole batch takes the persistent kernel (row tiles dividing 32): 2048 rows
+# (8 row tiles, up to two column tiles per workgroup) and 4096 rows (16 row
+# tiles, up to three); the shares of 900 rows (persistent, one tile each),
+# 1148, 1500 and 2596 rows (5, 6 and 11 row tiles) take the one-tile kernel.
+GATE_UP_PLANS = [
+    ([0, 100, 37], [900, 248, 900], ([0], [1, 2]), 1),
+    ([0, 64, 5], [1500, 300, 2296], ([0], [1, 2]), 1),
+]
+
+
+@pytest.mark.parametrize("priors,lens,shares,req", GATE_UP_PLANS)
+def test_prefill_gate_up_plans_agree_bit_exactly_and_match_oracle(priors, lens, shares, req):
+    """The persistent gate/up GEMM, where a workgroup takes its row tile
+    through several column tiles with the load ring running across them,
+    against request-aligned shares on the one-tile kernel: rows and appended
+    cache bytes bit-identical; a request's rows and cache against the
+    oracle."""
     shape = small_bf16_shape(d=640, hq=5, hkv=1, ffn=3456)
-    b = ragged_prefill_batch(31, priors=[0, 100, 37], lens=[900, 248, 900], max_ctx=1024,
-                             hidden_rows=2100)
+    b = ragged_prefill_batch(31, priors=priors, lens=lens, max_ctx=2560,
+                             hidden_rows=sum(lens) + 52)
     rep = Replica.for_batch(shape, "s31", 1, b)
     hidden = WD.hidden_tensor(shape, "s31", b.hidden_rows)
     h0 = to64(hidden)
@@ -234,20 +245,39 @@ def test_prefill_gate_up_plans_agree_bit_exactly_and_match_oracle():
     rep.forward(0, whole, WD.batch_tensors(b))
     torch.cuda.synchronize()
     kv_whole = _kv_snapshot(rep, b)
-    ref, _, cache, sub = oracle_prefill_seqs(shape, "s31", 0, b, [1], h0)
-    _check_rows("gate/up plans, request 1", to64(whole)[sub.row_idx], ref, h0[sub.row_idx])
-    t0, t1 = int(b.prior_lens[1]), int(b.ctx_lens[1])
-    K, V = gpu_cache_tokens(rep.layers[0], b, 1, t0, t1)
+    ref, _, cache, sub = oracle_prefill_seqs(shape, "s31", 0, b, [req], h0)
+    _check_rows(f"gate/up plans, {sum(lens)} rows, request {req}", to64(whole)[sub.row_idx], ref,
+                h0[sub.row_idx])
+    t0, t1 = int(b.prior_lens[req]), int(b.ctx_lens[req])
+    K, V = gpu_cache_tokens(rep.layers[0], b, req, t0, t1)
     assert normwise_err(K, cache.K[0][t0:t1]) < TOL
     assert normwise_err(V, cache.V[0][t0:t1]) < TOL
     snap.restore()
     split = hidden.clone()
-    for seqs in ([0], [1, 2]):
+    for seqs in shares:
         rep.forward(0, split, WD.batch_tensors(b.select_seqs(seqs)))
     torch.cuda.synchronize()
     assert torch.equal(split.view(torch.int16), whole.view(torch.int16))
     for (k1, v1), (k2, v2) in zip(_kv_snapshot(rep, b), kv_whole):
         assert np.array_equal(k1, k2) and np.array_equal(v1, v2)
+
+
+def test_prefill_gate_up_single_row_tile_matches_oracle():
+    """One request of 200 rows at d = 640, F = 3456: a single row tile, so the
+    persistent gate/up GEMM gives each of 36 workgroups one column tile and
+    the other 220 leave at once."""
+    shape = small_bf16_shape(d=640, hq=5, hkv=1, ffn=3456)
+    b = ragged_prefill_batch(32, priors=[40], lens=[200], max_ctx=256, hidden_rows=230)
+    rep = Replica.for_batch(shape, "s32", 1, b)
+    hidden = WD.hidden_tensor(shape, "s32", b.hidden_rows)
+    h0 = to64(hidden)
+    rep.forward(0, hidden, WD.batch_tensors(b))
+    torch.cuda.synchronize()
+    ref, _, cache, _ = oracle_prefill_seqs(shape, "s32", 0, b, [0], h0)
+    _check_rows("gate/up, one row tile", to64(hidden)[b.row_idx], ref, h0[b.row_idx])
+    untouched = np.setdiff1d(np.arange(b.hidden_rows), b.row_idx)
+    assert torch.equal(hidden[untouched].view(torch.int16), WD.hidden_tensor(
+        shape, "s32", b.hidden_rows)[untouched].view(torch.int16))
 
 
 def test_zero_output_projections_give_identity_bit_exactly():
