@@ -840,6 +840,15 @@ int run_span(coco_layer* H, const Work& W, int first, int nl, T* hidden, const i
                                                   (bf16_t*)u, M, F, d,
                                                   fold_norm2 ? W.ss : nullptr, norm_tiles,
                                                   c.rms_eps, st)));
+      } else if (c.dtype == COCO_BF16 && M > 128 && lay.h2 && lay.u &&
+                 narrow_swiglu_plain_fits(M, F, d)) {
+        // 129-256 rows with one round of 256 x 128 tiles (the 8B shape): the
+        // prefill tile kernel, bit-identical to the decode GEMM, in ~half its
+        // time (the row-split decode kernel streams 2.8 TB/s there).
+        TIMED(COCO_K_GEMM_GATE_UP,
+              HIPCHK(launch_gemm_narrow_swiglu_plain_bf16((const uint16_t*)h2,
+                                                          (const uint16_t*)w.w_gate_up,
+                                                          (uint16_t*)u, M, F, d, st)));
       } else {
         TIMED(COCO_K_GEMM_GATE_UP,
               HIPCHK(launch_gemm_skinny_swiglu_bf16((const bf16_t*)h2,

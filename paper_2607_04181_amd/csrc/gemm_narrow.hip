@@ -69,7 +69,9 @@ constexpr int narrow_round(int TN) {
   return narrow_slots(TN) % 2 ? 2 * narrow_slots(TN) : narrow_slots(TN);
 }
 
-enum { kNarrowResid = 0, kNarrowScatter = 1, kNarrowSwiglu = 2, kNarrowQkv = 3 };
+// kNarrowSwigluPlain: the SwiGLU epilogue without RMSNorm_2's 1/rms (the
+// operand is already normalised).
+enum { kNarrowResid = 0, kNarrowScatter = 1, kNarrowSwiglu = 2, kNarrowQkv = 3, kNarrowSwigluPlain = 4 };
 
 template <int TN, int MODE>
 __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __restrict__ A,
@@ -77,7 +79,8 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
                                                                  int M, int N, int K,
                                                                  NarrowEpiArgs ea) {
   static_assert(TN % 32 == 0 && TN / 16 >= 8 && TN / 16 <= 16, "tile width");
-  static_assert(MODE != kNarrowSwiglu || TN % 64 == 0, "SwiGLU pairs gate and up blocks");
+  constexpr bool kSwi = MODE == kNarrowSwiglu || MODE == kNarrowSwigluPlain;
+  static_assert(!kSwi || TN % 64 == 0, "SwiGLU pairs gate and up blocks");
   static_assert(MODE != kNarrowQkv || (TN >= 160 && TN <= 224), "QKV exchange areas");
   constexpr int WB = TN / 32;          // 16-column blocks per wave
   constexpr int kWBlocks = TN / 16;    // W blocks per stage
@@ -122,7 +125,7 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
   // the matching up blocks, so a lane holds both factors of its outputs.
   const int F = N / 2, o0 = n0 / 2;
   auto w_block = [&](int blk) -> int {
-    if constexpr (MODE == kNarrowSwiglu) {
+    if constexpr (kSwi) {
       const int h = blk / WB, r = blk % WB;
       const int o = o0 + h * (TN / 4) + 16 * (r % (WB / 2));
       return ((r < WB / 2 ? 0 : F) + o) >> 4;
@@ -271,7 +274,7 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
     if constexpr (MODE == kNarrowQkv)
       slots[tid] = rinfo;
     else
-      g_nrow[tid] = MODE == kNarrowSwiglu ? __float_as_int(rnorm) : erow;
+      g_nrow[tid] = kSwi ? __float_as_int(rnorm) : erow;
   }
   __syncthreads();
   constexpr int TNP = TN + 4;  // staged row stride (floats)
@@ -497,7 +500,7 @@ __global__ __launch_bounds__(kNThreads) void gemm_narrow_kernel(const bf16_t* __
       }
       __syncthreads();  // the quarter's staging is read
     }
-  } else if constexpr (MODE == kNarrowSwiglu) {
+  } else if constexpr (kSwi) {
     // Gate in blocks q < WB/2, up in blocks WB/2 + q, of outputs
     // o0 + TN/4 wn + 16 q + c16; h = silu(gate) * up, staged in LDS (row
     // quarter wm in slot wm, rows padded to kSS) and written in tile order
@@ -761,6 +764,10 @@ hipError_t launch_narrow(int tn, const uint16_t* A, const uint16_t* W, int M, in
     if (tn != 192) return hipErrorInvalidValue;
     COCO_LAUNCH((gemm_narrow_kernel<192, MODE>), grid, dim3(kNThreads), 0, st,
                 (const bf16_t*)A, (const bf16_t*)W, M, N, K, ea);
+  } else if constexpr (MODE == kNarrowSwigluPlain) {
+    if (tn != 128) return hipErrorInvalidValue;
+    COCO_LAUNCH((gemm_narrow_kernel<128, MODE>), grid, dim3(kNThreads), 0, st,
+                (const bf16_t*)A, (const bf16_t*)W, M, N, K, ea);
   } else if constexpr (MODE == kNarrowQkv) {
     if (tn == 224)
       COCO_LAUNCH((gemm_narrow_kernel<224, MODE>), grid, dim3(kNThreads), 0, st,
@@ -844,6 +851,21 @@ hipError_t launch_gemm_narrow_swiglu_bf16(const uint16_t* A, const uint16_t* W_g
   ea.n_ss = ss_tiles;
   ea.eps = eps;
   return launch_narrow<kNarrowSwiglu>(192, A, W_gate_up, M, 2 * F, K, ea, st);
+}
+
+bool narrow_swiglu_plain_fits(int M, int F, int K) {
+  if (M <= 0 || F <= 0 || (2 * F) % 128 != 0 || K % kNK != 0) return false;
+  return (int64_t)((M + kNM - 1) / kNM) * (2 * F / 128) <= 256;  // one round of workgroups
+}
+
+hipError_t launch_gemm_narrow_swiglu_plain_bf16(const uint16_t* A, const uint16_t* W_gate_up,
+                                                uint16_t* H, int M, int F, int K,
+                                                hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  if (!narrow_swiglu_plain_fits(M, F, K) || !H) return hipErrorInvalidValue;
+  NarrowEpiArgs ea{};
+  ea.h = H;
+  return launch_narrow<kNarrowSwigluPlain>(128, A, W_gate_up, M, 2 * F, K, ea, st);
 }
 
 int narrow_qkv_tile_n(int Hq, int Hkv, int K) {

@@ -231,6 +231,16 @@ bool narrow_swiglu_fits(int F, int K);
 hipError_t launch_gemm_narrow_swiglu_bf16(const uint16_t* A, const uint16_t* W_gate_up,
                                           uint16_t* H, int M, int F, int K, const float* ss_in,
                                           int ss_tiles, float eps, hipStream_t st);
+// The same SwiGLU epilogue without the 1/rms (A already normalised), on
+// 256 x 128 tiles, for decode batches whose gate/up GEMM takes one round of
+// workgroups: narrow_swiglu_plain_fits(M, F, K). A is in tile order, H is
+// written in tile order [M][F]. Every output is the v_mfma_f32_16x16x32_bf16
+// chain over k in ascending 32-steps of the decode GEMMs, with the same
+// epilogue arithmetic, so the bits equal theirs.
+bool narrow_swiglu_plain_fits(int M, int F, int K);
+hipError_t launch_gemm_narrow_swiglu_plain_bf16(const uint16_t* A, const uint16_t* W_gate_up,
+                                                uint16_t* H, int M, int F, int K,
+                                                hipStream_t st);
 // Prefill QKV projection with RoPE and the cache append in its epilogue
 // (head_dim 128), on 256 x TN tiles that each hold TN/2 whole rotation pairs
 // (dims j and j + 64 of a head), TN = narrow_qkv_tile_n(Hq, Hkv, K) (224,
