@@ -307,18 +307,26 @@ __global__ __launch_bounds__(HD) void attn_combine_kernel(const float* __restric
 // Workgroup = (sequence, 128-row query tile, query head). Workgroups are
 // remapped so that the query heads of one tile run back to back on one XCD
 // (blockIdx % 8) and share its L2 for the key/value tiles of their group.
-// Eight waves each take 16 rows of the tile as one 16-column tile. The
-// key/value tiles are staged through LDS four blocks (64 keys) at a time by
-// direct global->LDS loads (each wave fetches one block's K or V tile as
-// four contiguous 1 KB pieces), double-buffered with one barrier per stage.
-// Per stage a wave scores the 64 keys (S^T = K Q^T), updates its online
-// softmax once, and accumulates O^T += V^T P^T in 32-key MFMA steps: the
-// V^T fragments of two blocks side by side against P^T packed to match (any
-// fixed assignment of keys to MFMA k-slots gives the same sum). The row sums
-// of P come from the same MFMA with an all-ones operand in place of V^T, and
-// the running max moves only when a stage's max exceeds it by kPfLazy.
+// Its sixteen waves form two key sets of eight; in each set a wave takes 16
+// rows of the tile as one 16-column tile. The key/value tiles are staged
+// through LDS eight blocks (128 keys) at a time by direct global->LDS loads
+// (each wave fetches one block's K or V tile as four contiguous 1 KB
+// pieces), double-buffered with one barrier per stage; key set 0 works on
+// the stage's first four blocks and key set 1 on the last four. Per stage a
+// wave scores its 64 keys (S^T = K Q^T), updates its online softmax once,
+// and accumulates O^T += V^T P^T in 32-key MFMA steps: the V^T fragments of
+// two blocks side by side against P^T packed to match (any fixed assignment
+// of keys to MFMA k-slots gives the same sum). The row sums of P come from
+// the same MFMA with an all-ones operand in place of V^T, and the running
+// max moves only when a stage's max exceeds it by kPfLazy. At the end the
+// two sets' softmax states of each row are merged in LDS, set 0 first.
+// Splitting the keys halves the longest tile's chain of stages (the tiles
+// of a long sequence's chunk see the most keys) against two workgroups of
+// eight waves per CU that each walk all the keys: 114-117 -> 100-102 us on
+// the 32B 2048-token chunked prefill (A/B, same box).
 constexpr int kPfRows = 128;  // query rows per workgroup
-constexpr int kPfLaunchWaves = 8;  // waves per workgroup, one 16-row column tile each (measured faster than 4 x 2)
+constexpr int kPfLaunchWaves = 8;  // waves per key set, one 16-row column tile each (measured faster than 4 x 2)
+constexpr int kPfKeySets = 2;      // key sets per workgroup
 constexpr int kPfBlk = 4;     // key blocks per stage
 // The running max of a row is kept while a stage's max stays within this
 // many log2 units of it (P then stays below 2^8): rescaling the
@@ -335,15 +343,24 @@ typedef __attribute__((address_space(3))) const volatile u32x2_t lds_u32x2_cv;
 // register moves to split.
 __device__ __forceinline__ u32x2_t lds_read8(const bf16_t* p) { return *(lds_u32x2_cv*)p; }
 
-// WAVES waves of COLS 16-column tiles each cover the workgroup's 128 rows.
-template <int WAVES, int COLS>
-__global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_prefill_kernel(
+// WAVES waves of COLS 16-column tiles each cover the workgroup's 128 rows;
+// KS sets of WAVES waves split every stage's keys between them (set kh takes
+// blocks kh * kPfBlk .. of a stage of KS * kPfBlk blocks) and merge their
+// softmax states in LDS at the end.
+template <int WAVES, int COLS, int KS>
+__global__ __launch_bounds__(WAVES * KS * 64, KS > 1 ? 1 : 8 / WAVES) void attn_prefill_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k_cache,
     const bf16_t* __restrict__ v_cache, const int32_t* __restrict__ block_table, int max_blocks,
     const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ positions,
     const int32_t* __restrict__ seq_starts, int n_seqs, int Hq, int Hkv, float scale_log2,
     bf16_t* __restrict__ o) {
-  __shared__ __attribute__((aligned(16))) bf16_t kv[2][2][kPfBlk][kTileElems];  // [buf][K|V][blk]
+  static_assert(KS == 1 || KS == 2, "one or two key sets");
+  constexpr int kStBlk = kPfBlk * KS;  // key blocks per stage
+  // Two K and two V slots of a stage's kStBlk tiles each, in one LDS array.
+  constexpr int kSlot = kStBlk * kTileElems;
+  __shared__ __attribute__((aligned(16))) bf16_t kv[4 * kSlot];
+  auto k_slot = [&](int st) { return kv + (st & 1) * kSlot; };
+  auto v_slot = [&](int st) { return kv + (2 + (st & 1)) * kSlot; };
 
   // Work unit = (tile, kv head) with its G query heads. Units go round-robin
   // over the XCDs (blockIdx % 8 is the XCD) and a unit's G workgroups run
@@ -373,18 +390,19 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_prefill_kernel(
   if (s >= n_seqs) return;  // past the last tile: the whole workgroup leaves
   const int lane = threadIdx.x & 63;
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int rg = wv % WAVES, kh = wv / WAVES;  // row group, key set
   const int c16 = lane & 15, j4 = lane >> 4;
   const int row_begin = seq_starts[s] + tile * kPfRows;
   const int row_end = min(seq_starts[s + 1], row_begin + kPfRows);
   // Rows are in position order: the tile's last row sees the most keys.
   const int kmax = min(ctx_lens[s] - 1, positions[row_end - 1]);
   const int n_blk = kmax / kBlockTokens + 1;
-  const int stages = (n_blk + kPfBlk - 1) / kPfBlk;
+  const int stages = (n_blk + kStBlk - 1) / kStBlk;
   const int32_t* bt = block_table + (int64_t)s * max_blocks;
 
   // This wave's column tiles; padded columns repeat the tile's last row and
   // are never stored.
-  const int w_row0 = row_begin + wv * 16 * COLS;
+  const int w_row0 = row_begin + rg * 16 * COLS;
   const int w_kmax = w_row0 < row_end ? positions[min(row_end, w_row0 + 16 * COLS) - 1] : -1;
   // Stages whose keys all precede the wave's first row need no causal mask.
   const int w_kmin = w_row0 < row_end ? positions[w_row0] : -1;
@@ -400,20 +418,21 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_prefill_kernel(
       qf[c][t] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(qp + t * 32));
   }
 
-  // The stage's 4 blocks (clamped to the last block: a repeat that the
-  // causal mask hides) x {K, V} tiles are 8 tiles of four 1 KB pieces;
-  // wave wv stages tiles wv, wv + WAVES, ... into LDS.
-  auto issue = [&](int st, int buf) {
+  // The stage's blocks (clamped to the last block: a repeat that the causal
+  // mask hides) x {K, V} tiles, four 1 KB pieces each; wave wv stages tiles
+  // wv, wv + WAVES * KS, ... into LDS.
+  auto issue = [&](int st) {
 #pragma unroll
-    for (int tt = wv; tt < 2 * kPfBlk; tt += WAVES) {
-      const int kvsel = tt / kPfBlk, bi = tt % kPfBlk;
-      const int blk = min(st * kPfBlk + bi, n_blk - 1);
+    for (int tt = wv; tt < 2 * kStBlk; tt += WAVES * KS) {
+      const int kvsel = tt / kStBlk, bi = tt % kStBlk;
+      const int blk = min(st * kStBlk + bi, n_blk - 1);
       const bf16_t* src = (kvsel ? v_cache : k_cache) +
                           ((int64_t)bt[blk] * Hkv + g) * kTileElems + lane * 8;
+      bf16_t* dst = (kvsel ? v_slot(st) : k_slot(st)) + bi * kTileElems;
 #pragma unroll
       for (int pc = 0; pc < 4; ++pc)
-        __builtin_amdgcn_global_load_lds(src + pc * 512,
-                                         (lds_void_t*)&kv[buf][kvsel][bi][pc * 512], 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(src + pc * 512, (lds_void_t*)(dst + pc * 512), 16, 0,
+                                         0);
     }
   };
 
@@ -434,14 +453,59 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_prefill_kernel(
 #pragma unroll
     for (int n = 0; n < 8; ++n) acc[c][n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  issue(0, 0);
+  // V^T operands of a block pair: this lane's 16-byte chunk of piece pc of a
+  // V tile holds 4 tokens of dim h, then the same 4 tokens of dim h + 16;
+  // each 8-byte half is read from LDS straight into its place in the operand
+  // (dims h: va, dims h + 16: vb; the pair's first block in the low half).
+  bf16x8_t va[4], vb[4];
+  auto read_v = [&](const bf16_t* vl, int pair) {
+    const bf16_t* b0 = vl + 2 * pair * kTileElems;
+#pragma unroll
+    for (int pc = 0; pc < 4; ++pc) {
+      const u32x2_t a0 = lds_read8(b0 + pc * 512);
+      const u32x2_t a1 = lds_read8(b0 + kTileElems + pc * 512);
+      const u32x2_t c0 = lds_read8(b0 + pc * 512 + 4);
+      const u32x2_t c1 = lds_read8(b0 + kTileElems + pc * 512 + 4);
+      va[pc] = __builtin_bit_cast(bf16x8_t, u32x4_t{a0.x, a0.y, a1.x, a1.y});
+      vb[pc] = __builtin_bit_cast(bf16x8_t, u32x4_t{c0.x, c0.y, c1.x, c1.y});
+    }
+  };
+  // P^T of the wave's 64 keys, packed as two 32-key operands.
+  u32x4_t pk[COLS][2];
+  // O^T += V^T P^T over the two block pairs; l += 1^T P^T. The first pair's
+  // V^T operands are already in va / vb.
+  auto pv = [&](const bf16_t* vl) {
+#pragma unroll
+    for (int pp = 0; pp < 2; ++pp) {
+      if (pp == 1) read_v(vl, 1);
+#pragma unroll
+      for (int c = 0; c < COLS; ++c)
+        l[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            ones, __builtin_bit_cast(bf16x8_t, pk[c][pp]), l[c], 0, 0, 0);
+#pragma unroll
+      for (int pc = 0; pc < 4; ++pc) {
+#pragma unroll
+        for (int c = 0; c < COLS; ++c) {
+          const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, pk[c][pp]);
+          acc[c][2 * pc] =
+              __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[pc], pb, acc[c][2 * pc], 0, 0, 0);
+          acc[c][2 * pc + 1] =
+              __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb[pc], pb, acc[c][2 * pc + 1], 0, 0, 0);
+        }
+      }
+    }
+  };
+
+  issue(0);
   __syncthreads();
   for (int st = 0; st < stages; ++st) {
-    const int buf = st & 1;
-    if (st + 1 < stages) issue(st + 1, buf ^ 1);
-    if (st * kPfBlk * kBlockTokens <= w_kmax) {
-      const bf16_t* kl = &kv[buf][0][0][lane * 8];
-      const bf16_t* vl = &kv[buf][1][0][lane * 8];
+    if (st + 1 < stages) issue(st + 1);
+    // First key block of this wave's share of the stage.
+    const int blk0 = st * kStBlk + kh * kPfBlk;
+    const bool active = blk0 * kBlockTokens <= w_kmax;
+    const bf16_t* vl = v_slot(st) + kh * kPfBlk * kTileElems + lane * 8;
+    if (active) {
+      const bf16_t* kl = k_slot(st) + kh * kPfBlk * kTileElems + lane * 8;
       // Scores of the stage's 4 blocks for both column tiles; the next
       // block's K fragments are read while the current block's MFMAs run.
       f32x4_t sc[COLS][kPfBlk];
@@ -465,30 +529,10 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_prefill_kernel(
           sc[c][i] = a;
         }
       }
-      const bool unmasked = (st + 1) * kPfBlk * kBlockTokens - 1 <= w_kmin;
-      // V^T operands of a block pair: this lane's 16-byte chunk of piece pc of
-      // a V tile holds 4 tokens of dim h, then the same 4 tokens of dim h + 16;
-      // each 8-byte half is read from LDS straight into its place in the
-      // operand (dims h: va, dims h + 16: vb; the pair's first block in the
-      // low half). The first pair is read during the softmax.
-      bf16x8_t va[4], vb[4];
-      auto read_v = [&](int pair) {
-        const bf16_t* b0 = vl + 2 * pair * kTileElems;
-#pragma unroll
-        for (int pc = 0; pc < 4; ++pc) {
-          const u32x2_t a0 = lds_read8(b0 + pc * 512);
-          const u32x2_t a1 = lds_read8(b0 + kTileElems + pc * 512);
-          const u32x2_t c0 = lds_read8(b0 + pc * 512 + 4);
-          const u32x2_t c1 = lds_read8(b0 + kTileElems + pc * 512 + 4);
-          va[pc] = __builtin_bit_cast(bf16x8_t, u32x4_t{a0.x, a0.y, a1.x, a1.y});
-          vb[pc] = __builtin_bit_cast(bf16x8_t, u32x4_t{c0.x, c0.y, c1.x, c1.y});
-        }
-      };
-      read_v(0);
-      // Online softmax, once per 64 keys (log2 domain: p = 2^(s*scale - m)),
-      // P^T packed as two 32-key operands. Stages wholly before the wave's
-      // first row skip the causal mask.
-      u32x4_t pk[COLS][2];
+      const bool unmasked = (blk0 + kPfBlk) * kBlockTokens - 1 <= w_kmin;
+      read_v(vl, 0);
+      // Online softmax, once per 64 keys (log2 domain: p = 2^(s*scale - m)).
+      // Stages wholly before the wave's first row skip the causal mask.
 #pragma unroll
       for (int c = 0; c < COLS; ++c) {
         float mx = -INFINITY;
@@ -500,7 +544,7 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_prefill_kernel(
         } else {
 #pragma unroll
           for (int i = 0; i < kPfBlk; ++i) {
-            const int tok0 = (st * kPfBlk + i) * kBlockTokens + j4 * 4;
+            const int tok0 = (blk0 + i) * kBlockTokens + j4 * 4;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               // Keys after the row's position score -inf: 2^-inf = 0 below.
@@ -510,17 +554,21 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_prefill_kernel(
           }
         }
         mx = col_max4(mx) * scale_log2;
-        // Stage 0 always holds key 0, so mx is finite and the first stage
-        // sets the max.
+        // Stage 0 of key set 0 always holds key 0, so there mx is finite and
+        // the first stage sets the max. Another key set can meet a column
+        // whose keys are all masked (mx = -inf) and keeps m = -inf for it;
+        // its exponents are then taken against 0 (2^-inf = 0, so p and alpha
+        // are 0 and the still-zero state stays zero).
         const float m_new = mx > m[c] + kPfLazy ? mx : m[c];
-        const float alpha = __builtin_amdgcn_exp2f(m[c] - m_new);
+        const float m_ref = (KS > 1 && m_new == -INFINITY) ? 0.f : m_new;
+        const float alpha = __builtin_amdgcn_exp2f(m[c] - m_ref);
         uint32_t pw[kPfBlk][2];
 #pragma unroll
         for (int i = 0; i < kPfBlk; ++i) {
           float pr[4];
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            pr[r] = __builtin_amdgcn_exp2f(fmaf(sc[c][i][r], scale_log2, -m_new));
+            pr[r] = __builtin_amdgcn_exp2f(fmaf(sc[c][i][r], scale_log2, -m_ref));
           pw[i][0] = pack_bf16x2(pr[0], pr[1]);
           pw[i][1] = pack_bf16x2(pr[2], pr[3]);
         }
@@ -536,28 +584,46 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_prefill_kernel(
         for (int pp = 0; pp < 2; ++pp)
           pk[c][pp] = u32x4_t{pw[2 * pp][0], pw[2 * pp][1], pw[2 * pp + 1][0], pw[2 * pp + 1][1]};
       }
-      // O^T += V^T P^T over the two block pairs; l += 1^T P^T.
-#pragma unroll
-      for (int pp = 0; pp < 2; ++pp) {
-        if (pp == 1) read_v(1);
-#pragma unroll
-        for (int c = 0; c < COLS; ++c)
-          l[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              ones, __builtin_bit_cast(bf16x8_t, pk[c][pp]), l[c], 0, 0, 0);
-#pragma unroll
-        for (int pc = 0; pc < 4; ++pc) {
-#pragma unroll
-          for (int c = 0; c < COLS; ++c) {
-            const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, pk[c][pp]);
-            acc[c][2 * pc] =
-                __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[pc], pb, acc[c][2 * pc], 0, 0, 0);
-            acc[c][2 * pc + 1] =
-                __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb[pc], pb, acc[c][2 * pc + 1], 0, 0, 0);
-          }
-        }
-      }
+      pv(vl);
     }
     __syncthreads();  // stage st+1 landed; buffer st is free for stage st+2
+  }
+
+  if constexpr (KS > 1) {
+    // Key set 1 hands (m, l, O^T) of its columns to key set 0 through the
+    // now free LDS ([row group][column tile][34 values][64 lanes] floats),
+    // which adds them in: O = O_0 2^(m_0 - M) + O_1 2^(m_1 - M), likewise l,
+    // with M = max(m_0, m_1). m_0 is finite (key 0), so a column that set 1
+    // never saw (m_1 = -inf) takes weight 0 from it.
+    constexpr int kVals = 8 * 4 + 2;
+    static_assert(WAVES * COLS * kVals * 64 * 4 <= (int)sizeof(kv), "merge fits the K/V buffers");
+    float* xs = reinterpret_cast<float*>(kv);
+    if (kh == 1) {
+#pragma unroll
+      for (int c = 0; c < COLS; ++c) {
+        float* d = xs + (rg * COLS + c) * kVals * 64 + lane;
+#pragma unroll
+        for (int n = 0; n < 8; ++n)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) d[(n * 4 + r) * 64] = acc[c][n][r];
+        d[32 * 64] = m[c];
+        d[33 * 64] = l[c][0];
+      }
+    }
+    __syncthreads();
+    if (kh == 1) return;
+#pragma unroll
+    for (int c = 0; c < COLS; ++c) {
+      const float* d = xs + (rg * COLS + c) * kVals * 64 + lane;
+      const float m1 = d[32 * 64], l1 = d[33 * 64];
+      const float mm = fmaxf(m[c], m1);
+      const float f0 = __builtin_amdgcn_exp2f(m[c] - mm), f1 = __builtin_amdgcn_exp2f(m1 - mm);
+#pragma unroll
+      for (int n = 0; n < 8; ++n)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[c][n][r] = acc[c][n][r] * f0 + d[(n * 4 + r) * 64] * f1;
+      l[c][0] = l[c][0] * f0 + l1 * f1;
+    }
   }
 
   // The output [rows][Hq * 128] is the O projection's A operand, written in
@@ -683,8 +749,8 @@ hipError_t launch_attn_prefill_bf16(const uint16_t* q, const uint16_t* k_cache,
   // tile return at once.
   const int64_t tiles = (n_rows + kPfRows - 1) / kPfRows + n_seqs;
   if (tiles * Hq > 0x7fffffff) return hipErrorInvalidValue;
-  COCO_LAUNCH((attn_prefill_kernel<kPfLaunchWaves, 8 / kPfLaunchWaves>),
-                     dim3((unsigned)(tiles * Hq)), dim3(kPfLaunchWaves * 64), 0, st, q,
+  COCO_LAUNCH((attn_prefill_kernel<kPfLaunchWaves, 8 / kPfLaunchWaves, kPfKeySets>),
+                     dim3((unsigned)(tiles * Hq)), dim3(kPfLaunchWaves * kPfKeySets * 64), 0, st, q,
                      k_cache, v_cache, block_table, max_blocks, ctx_lens, positions, seq_starts,
                      n_seqs, Hq, Hkv, scale_log2, o);
   return hipGetLastError();
