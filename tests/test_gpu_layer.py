@@ -123,6 +123,35 @@ def test_small_bf16_prefill_matches_oracle():
         assert normwise_err(V, cache.V[s][t0:t1]) < TOL
 
 
+def test_prefill_attention_key_set_edges_match_oracle():
+    """The prefill attention splits every 128-key stage between two sets of
+    waves (keys 0-63 and 64-127 of the stage) and merges their softmax states
+    per row. Chunks here put rows on both sides of those edges: rows whose
+    second-set keys are all masked (positions 50-63 of a 16-row group that
+    reaches 64), single rows at keys 63/64/65 and 127/128/129, and groups that
+    end inside the second set. Every row of the attention output is checked
+    against the oracle on its own."""
+    shape = small_bf16_shape()
+    priors = [50, 63, 64, 65, 112, 127, 128, 129, 0, 190]
+    lens = [30, 1, 1, 1, 40, 1, 1, 1, 140, 70]
+    b = ragged_prefill_batch(21, priors=priors, lens=lens, max_ctx=512, hidden_rows=300)
+    rep = Replica.for_batch(shape, "s21", 1, b)
+    hidden = WD.hidden_tensor(shape, "s21", b.hidden_rows)
+    h0 = to64(hidden)
+    rep.forward(0, hidden, WD.batch_tensors(b))
+    torch.cuda.synchronize()
+    ref, rec, _, _ = oracle_prefill_seqs(shape, "s21", 0, b, range(b.n_seqs), h0, record=True)
+    o = to64(rep.workspace(coco.COCO_WS_O, b.n_rows, shape.n_q_heads * 128, torch.bfloat16))
+    ro = np.asarray(rec["o"], np.float64).reshape(o.shape)
+    per_row = [normwise_err(o[i], ro[i]) for i in range(b.n_rows)]
+    worst = int(np.argmax(per_row))
+    log(f"key-set edges: attention output err {normwise_err(o, ro):.2e}, worst row {worst} "
+        f"(position {int(b.positions[worst])}) {per_row[worst]:.2e}")
+    assert np.all(np.isfinite(o))
+    assert max(per_row) < TOL
+    _check_rows("key-set edges", to64(hidden)[b.row_idx], ref, h0[b.row_idx])
+
+
 def _kv_snapshot(rep, b):
     out = []
     for s in range(b.n_seqs):
