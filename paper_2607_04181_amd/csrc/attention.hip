@@ -68,6 +68,7 @@ constexpr int kDecBPW = kDecodeSplit / kBlockTokens / kDecWaves;
 
 struct DecItem {
   int s, g, sp, t1, b_first, b_last;
+  int64_t pb[kDecBPW];  // physical blocks of this wave's share (clamped to b_last)
 };
 
 // Keys a decode row attends: positions 0 .. its own position, within the
@@ -100,6 +101,17 @@ __device__ __forceinline__ DecItem decode_item(int w, int Hkv, const int32_t* sp
   return it;
 }
 
+// The block-table entries of wave wv's blocks of item it: unconditional
+// (blocks past the partition repeat its last block, an L2 hit that is then
+// ignored), so that the waits before each MFMA can count exactly the loads
+// still in flight behind the ones it needs.
+__device__ __forceinline__ void decode_item_blocks(DecItem& it, const int32_t* block_table,
+                                                   int max_blocks, int wv) {
+  const int32_t* bt = block_table + (int64_t)it.s * max_blocks;
+#pragma unroll
+  for (int u = 0; u < kDecBPW; ++u) it.pb[u] = bt[min(it.b_first + wv + kDecWaves * u, it.b_last)];
+}
+
 __global__ __launch_bounds__(kDecWaves * 64, 4) void attn_decode_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k_cache,
     const bf16_t* __restrict__ v_cache, const int32_t* __restrict__ block_table, int max_blocks,
@@ -127,24 +139,29 @@ __global__ __launch_bounds__(kDecWaves * 64, 4) void attn_decode_kernel(
     const bf16_t* qp = q + ((int64_t)it.s * Hq + it.g * G + cq) * HD + j4 * 8;
 #pragma unroll
     for (int t = 0; t < 4; ++t) qr[t] = *(const u32x4_t*)(qp + t * 32);
-    // Unconditional (blocks past the partition re-read its last block, an
-    // L2 hit that is then ignored), so that the waits before each MFMA can
-    // count exactly the loads still in flight behind the ones it needs.
-    const int32_t* bt = block_table + (int64_t)it.s * max_blocks;
 #pragma unroll
-    for (int u = 0; u < kDecBPW; ++u) {
-      const int b = min(it.b_first + wv + kDecWaves * u, it.b_last);
-      const int64_t pb = bt[b];
-      load_kv(k_cache + (pb * Hkv + it.g) * tile, v_cache + (pb * Hkv + it.g) * tile, c16, j4,
-              kf[u], vf[u]);
-    }
+    for (int u = 0; u < kDecBPW; ++u)
+      load_kv(k_cache + (it.pb[u] * Hkv + it.g) * tile, v_cache + (it.pb[u] * Hkv + it.g) * tile,
+              c16, j4, kf[u], vf[u]);
+  };
+  // The descriptor of the item after the current one, block-table entries
+  // included, is looked up one item ahead: its chain of dependent scalar
+  // loads runs while the current item's key/value loads are in flight, and
+  // the next issue has its addresses at hand. Past the last item it repeats
+  // the last one, which is never used.
+  auto lookup = [&](int wi) {
+    DecItem it = decode_item(min(wi, total - 1), Hkv, split_off, ctx_lens, positions, n_seqs,
+                             max_blocks);
+    decode_item_blocks(it, block_table, max_blocks, wv);
+    return it;
   };
 
   int w = blockIdx.x;
-  DecItem cur{};
+  DecItem cur{}, nxt{};
   if (w < total) {
-    cur = decode_item(w, Hkv, split_off, ctx_lens, positions, n_seqs, max_blocks);
+    cur = lookup(w);
     issue(cur);
+    nxt = lookup(w + (int)gridDim.x);
   }
   for (; w < total; w += gridDim.x) {
     // Columns c16 >= G repeat head G-1; their results are never stored.
@@ -204,12 +221,12 @@ __global__ __launch_bounds__(kDecWaves * 64, 4) void attn_decode_kernel(
     for (int n = 0; n < 8; ++n)
 #pragma unroll
       for (int r = 0; r < 4; ++r) sm_o[wv][c16][n * 16 + j4 * 4 + r] = o[n][r];
-    // The registers are free: start the next item's reads now (past the
-    // last item, a repeat of the last one that is never used).
+    // The registers are free: start the next item's reads now, then look up
+    // the one after it.
     const DecItem it = cur;
-    cur = decode_item(min(w + (int)gridDim.x, total - 1), Hkv, split_off, ctx_lens, positions,
-                      n_seqs, max_blocks);
+    cur = nxt;
     issue(cur);
+    nxt = lookup(w + 2 * (int)gridDim.x);
     __syncthreads();
 
     for (int e = threadIdx.x; e < G * HD; e += kDecWaves * 64) {
