@@ -54,9 +54,14 @@ __device__ __forceinline__ void load_kv(const bf16_t* kb, const bf16_t* vb, int 
 }
 
 // ---------------------------------------------------------------- decode
-// Persistent workgroups walk the work list (partition, kv head) in order;
-// partition offsets per sequence (split_off, an exclusive prefix sum of
-// ceil(ctx / 256)) were written by the QKV epilogue. Eight waves take two
+// Persistent workgroups walk the work list of (partition, kv head) items that
+// the QKV epilogue wrote (split_off): every full 256-key partition first, then
+// each sequence's partial last partition, largest first. Workgroup b takes
+// list positions k * grid + b for even k and k * grid + grid - 1 - b for odd
+// k, so that every workgroup gets about the same number of keys (the items
+// that differ in size come last, dealt out largest first and snake-wise).
+// The order changes which workgroup computes an item, never what it computes
+// or where its result goes. Eight waves take two
 // blocks each of the 256-token partition; each wave scores both blocks
 // first, takes one column max and then accumulates exp * V against it, and
 // the eight wave results are merged in LDS in wave order. As soon as a
@@ -78,6 +83,10 @@ __device__ __forceinline__ int decode_keys(const int32_t* ctx_lens, const int32_
   return max(0, min(ctx_lens[s], positions[s] + 1));
 }
 
+// Item w of the work list: split_off[0 .. n_seqs] is the exclusive prefix sum
+// of each sequence's full partitions, split_off[n_seqs + 1] the number of
+// partial last partitions and split_off[n_seqs + 2 ..] their sequences,
+// largest first.
 __device__ __forceinline__ DecItem decode_item(int w, int Hkv, const int32_t* split_off,
                                                const int32_t* ctx_lens,
                                                const int32_t* positions, int n_seqs,
@@ -85,13 +94,20 @@ __device__ __forceinline__ DecItem decode_item(int w, int Hkv, const int32_t* sp
   DecItem it;
   const int item = w / Hkv;
   it.g = w - item * Hkv;
-  int lo = 0, hi = n_seqs - 1;  // the s with split_off[s] <= item < split_off[s + 1]
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (split_off[mid] <= item) lo = mid; else hi = mid - 1;
+  const int n_full = split_off[n_seqs];
+  if (item < n_full) {
+    int lo = 0, hi = n_seqs - 1;  // the s with split_off[s] <= item < split_off[s + 1]
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (split_off[mid] <= item) lo = mid; else hi = mid - 1;
+    }
+    it.s = lo;
+    it.sp = item - split_off[lo];
+  } else {
+    it.s = split_off[n_seqs + 2 + (item - n_full)];
+    it.sp = split_off[it.s + 1] - split_off[it.s];
   }
-  it.s = lo;
-  it.sp = item - split_off[lo];
+  const int lo = it.s;
   const int t0 = it.sp * kDecodeSplit;
   // Capped at the block table's width (only invalid lengths reach the cap).
   it.t1 = min(min(decode_keys(ctx_lens, positions, lo), t0 + kDecodeSplit),
@@ -121,7 +137,7 @@ __global__ __launch_bounds__(kDecWaves * 64, 4) void attn_decode_kernel(
   __shared__ float sm_m[kDecWaves][16], sm_l[kDecWaves][16];
   __shared__ float sm_o[kDecWaves][16][HD + 4];
 
-  const int total = split_off[n_seqs] * Hkv;
+  const int total = (split_off[n_seqs] + split_off[n_seqs + 1]) * Hkv;
   const int G = Hq / Hkv;
   const int lane = threadIdx.x & 63;
   // Wave index as a uniform value: block-table reads then go through the
@@ -156,14 +172,17 @@ __global__ __launch_bounds__(kDecWaves * 64, 4) void attn_decode_kernel(
     return it;
   };
 
-  int w = blockIdx.x;
+  // List position of this workgroup's k-th item (snake order).
+  const int grid = gridDim.x;
+  auto pos_of = [&](int k) { return k * grid + ((k & 1) ? grid - 1 - (int)blockIdx.x : (int)blockIdx.x); };
+  int k = 0, w = pos_of(0);
   DecItem cur{}, nxt{};
   if (w < total) {
     cur = lookup(w);
     issue(cur);
-    nxt = lookup(w + (int)gridDim.x);
+    nxt = lookup(pos_of(1));
   }
-  for (; w < total; w += gridDim.x) {
+  for (; w < total; w = pos_of(++k)) {
     // Columns c16 >= G repeat head G-1; their results are never stored.
     bf16x8_t qf[4];
 #pragma unroll
@@ -226,7 +245,7 @@ __global__ __launch_bounds__(kDecWaves * 64, 4) void attn_decode_kernel(
     const DecItem it = cur;
     cur = nxt;
     issue(cur);
-    nxt = lookup(w + 2 * (int)gridDim.x);
+    nxt = lookup(pos_of(k + 2));
     __syncthreads();
 
     for (int e = threadIdx.x; e < G * HD; e += kDecWaves * 64) {

@@ -45,7 +45,7 @@ struct Work {
   // Row sums of squares: per K-slice (decode QKV with RMSNorm_1 folded in) or
   // per 256-column tile (prefill O projection with RMSNorm_2 folded in).
   float* ss = nullptr;
-  int32_t* split_off = nullptr;  // decode attention work list offsets
+  int32_t* split_off = nullptr;  // decode attention work list
   int32_t* row_info = nullptr;   // prefill row slots [rows][2] (position, cache block)
 };
 
@@ -169,7 +169,7 @@ size_t carve_work(const coco_layer_config& c, int64_t rows, int64_t dec_seqs, in
       align256(part_elems * 4),  // part
       bf ? align256((size_t)dec_seqs * c.n_q_heads * max_splits * 128 * 4) : 0,  // attn_o
       bf ? align256((size_t)dec_seqs * c.n_q_heads * max_splits * 2 * 4) : 0,    // attn_ml
-      align256((size_t)(dec_seqs + 1) * 4),  // split_off
+      align256((size_t)(2 * dec_seqs + 2) * 4),  // split_off (decode attention work list)
       // ss: per-slice row sums of squares (decode QKV, at most 16 K-slices)
       // or per-column-tile ones (prefill O projection, at most 32 tiles)
       align256((size_t)32 * R * 4),

@@ -55,8 +55,9 @@ hipError_t launch_rope_table(const double* inv_freq, int half, int n_pos, float*
 // With ss non-null (decode, RMSNorm_1 folded into the projection), each row's
 // sums are first scaled by 1 / sqrt(sum_s ss[s][row] / d + eps).
 // With split_off non-null (decode), one workgroup also writes the decode
-// attention's partition offsets from the keys each row attends,
-// min(ctx_lens, positions + 1) (counts capped at max_splits).
+// attention's work list (layout at launch_attn_decode_bf16) from the keys
+// each row attends, min(ctx_lens, positions + 1) (partition counts capped at
+// max_splits).
 template <typename T>
 hipError_t launch_qkv_epilogue(const float* part, int S, int M, int Hq, int Hkv, int hd,
                                const int32_t* positions, const int32_t* seq_starts,
@@ -264,8 +265,11 @@ constexpr int kDecodeSplit = 256;  // tokens per split-KV partition
 int decode_max_splits(int max_blocks_per_seq);
 bool attn_combine_fits(int max_splits);
 
-// split_off[n_seqs + 1]: exclusive prefix sum of each sequence's partition
-// count (written by the QKV epilogue of the same call).
+// split_off (at most 2 n_seqs + 2 entries, written by the QKV epilogue of the
+// same call): [0 .. n_seqs] the exclusive prefix sum of each sequence's full
+// 256-key partitions; [n_seqs + 1] the number of sequences whose last
+// partition is partial; [n_seqs + 2 ..] those sequences, longest last
+// partition first.
 // Decode row s attends min(ctx_lens[s], positions[s] + 1) keys.
 hipError_t launch_attn_decode_bf16(const uint16_t* q, const uint16_t* k_cache,
                                    const uint16_t* v_cache, const int32_t* block_table,

@@ -247,7 +247,7 @@ hipError_t launch_rope_table(const double* inv_freq, int half, int n_pos, float*
 // value to the sequence's cache slot. The partial loads, which depend on
 // nothing, are issued first; the cache slot lookup and the angles overlap
 // them (a dependent load of the RoPE table measured slower here). In decode,
-// one wave also writes the attention's partition offsets.
+// one wave also writes the decode attention's work list.
 // ----------------------------------------------------------------------------
 constexpr int kEpiHeads = 8;
 
@@ -260,6 +260,7 @@ __global__ __launch_bounds__(kEpiHeads * kWave) void qkv_epilogue_kernel(
     const int32_t* __restrict__ ctx_lens, int32_t* __restrict__ split_off, int max_splits,
     const float* __restrict__ ss, int d, float eps) {
   __shared__ float rot[2][128];  // cos, sin of the row's angles (hd / 2 <= 128)
+  __shared__ int wl_rank[kDecodeSplit];  // work list: partial partitions per size, then ranks
   const int i = blockIdx.y, lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
   const int nh = Hq + 2 * Hkv;
   const int h = blockIdx.x * kEpiHeads + wv;
@@ -313,15 +314,24 @@ __global__ __launch_bounds__(kEpiHeads * kWave) void qkv_epilogue_kernel(
   }
   __syncthreads();
   if (split_off != nullptr && blockIdx.x == 0 && i == 0 && wv == 0) {
-    // Decode attention work list: exclusive prefix sum of ceil(n / 256) for
-    // the n = min(ctx_lens[s], positions[s] + 1) keys row s attends, capped
-    // at max_splits (only invalid lengths reach the cap).
+    // Decode attention work list over the n = min(ctx_lens[s], positions[s]
+    // + 1) keys row s attends, in 256-key partitions (at most max_splits; only
+    // invalid lengths reach the cap). First every full partition: an
+    // exclusive prefix sum of their counts in split_off[0 .. n_seqs]. Then
+    // each sequence's last partition if it is partial, largest first: their
+    // count in split_off[n_seqs + 1], the sequences in that order from
+    // split_off[n_seqs + 2]. Dealt out in that order (snake-wise over the
+    // workgroups), items of similar size meet at the end of the kernel.
+    for (int r = lane; r < kDecodeSplit; r += kWave) wl_rank[r] = 0;
     int run = 0;
     if (lane == 0) split_off[0] = 0;
     for (int base = 0; base < n_seqs; base += kWave) {
       const int s = base + lane;
       const int n = s < n_seqs ? max(0, min(ctx_lens[s], positions[s] + 1)) : 0;
-      int v = min((n + kDecodeSplit - 1) / kDecodeSplit, max_splits);
+      const int nsp = (n + kDecodeSplit - 1) / kDecodeSplit;
+      const int rem = (nsp <= max_splits) ? n % kDecodeSplit : 0;
+      int v = min(nsp, max_splits) - (rem != 0);
+      if (rem != 0) atomicAdd(&wl_rank[rem], 1);
 #pragma unroll
       for (int o = 1; o < kWave; o <<= 1) {
         const int t = __shfl_up(v, o, kWave);
@@ -329,6 +339,34 @@ __global__ __launch_bounds__(kEpiHeads * kWave) void qkv_epilogue_kernel(
       }
       if (s < n_seqs) split_off[s + 1] = run + v;
       run += __shfl(v, kWave - 1, kWave);
+    }
+    // Sizes largest first: wl_rank[r] becomes the number of partial
+    // partitions longer than r keys (a suffix sum, four sizes per lane).
+    int c[4], tot = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      c[e] = wl_rank[kDecodeSplit - 1 - (lane * 4 + e)];
+      tot += c[e];
+    }
+    int incl = tot;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int t = __shfl_up(incl, o, kWave);
+      if (lane >= o) incl += t;
+    }
+    int acc = incl - tot;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      wl_rank[kDecodeSplit - 1 - (lane * 4 + e)] = acc;
+      acc += c[e];
+    }
+    if (lane == kWave - 1) split_off[n_seqs + 1] = incl;
+    for (int base = 0; base < n_seqs; base += kWave) {
+      const int s = base + lane;
+      const int n = s < n_seqs ? max(0, min(ctx_lens[s], positions[s] + 1)) : 0;
+      const int nsp = (n + kDecodeSplit - 1) / kDecodeSplit;
+      const int rem = (nsp <= max_splits) ? n % kDecodeSplit : 0;
+      if (rem != 0) split_off[n_seqs + 2 + atomicAdd(&wl_rank[rem], 1)] = s;
     }
   }
   if (!live) return;
