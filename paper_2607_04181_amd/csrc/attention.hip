@@ -107,10 +107,9 @@ __device__ __forceinline__ DecItem decode_item(int w, int Hkv, const int32_t* sp
     it.s = split_off[n_seqs + 2 + (item - n_full)];
     it.sp = split_off[it.s + 1] - split_off[it.s];
   }
-  const int lo = it.s;
   const int t0 = it.sp * kDecodeSplit;
   // Capped at the block table's width (only invalid lengths reach the cap).
-  it.t1 = min(min(decode_keys(ctx_lens, positions, lo), t0 + kDecodeSplit),
+  it.t1 = min(min(decode_keys(ctx_lens, positions, it.s), t0 + kDecodeSplit),
               max_blocks * kBlockTokens);
   it.b_first = t0 / kBlockTokens;
   it.b_last = (it.t1 - 1) / kBlockTokens;

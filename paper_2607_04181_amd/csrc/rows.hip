@@ -342,6 +342,7 @@ __global__ __launch_bounds__(kEpiHeads * kWave) void qkv_epilogue_kernel(
     }
     // Sizes largest first: wl_rank[r] becomes the number of partial
     // partitions longer than r keys (a suffix sum, four sizes per lane).
+    static_assert(kDecodeSplit == 4 * kWave, "four partition sizes per lane");
     int c[4], tot = 0;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
