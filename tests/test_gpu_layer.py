@@ -190,10 +190,10 @@ def test_decode_split_batch_is_bit_identical():
 
 
 def test_decode_of_many_sequences_matches_oracle_and_splits():
-    """300 decode sequences (the attention's partition offsets are a prefix
-    sum over 64 sequences at a time) with lengths on block and partition
-    edges: sampled rows against the oracle, the whole batch bit-identical to
-    two uneven halves."""
+    """300 decode sequences with lengths on block and partition edges, each
+    length 25 times (the attention's work list is built over 64 sequences at a
+    time and orders the partial partitions by size, ties included): every row
+    against the oracle, the whole batch bit-identical to two uneven halves."""
     shape = small_bf16_shape()
     edges = [0, 1, 15, 254, 255, 256, 257, 510, 511, 512, 700, 16]
     priors = [edges[i % len(edges)] for i in range(300)]
@@ -207,7 +207,7 @@ def test_decode_of_many_sequences_matches_oracle_and_splits():
     rep.forward(0, whole, WD.batch_tensors(b))
     torch.cuda.synchronize()
     kv_whole = _kv_snapshot(rep, b)
-    rows = [0, 5, 63, 64, 130, 255, 256, 257, 270, 299]
+    rows = list(range(300))
     ref, _, _ = oracle_decode_rows(shape, "s9", 0, b, rows, h0)
     got = to64(whole)[b.row_idx[rows]]
     _check_rows("300-sequence decode", got, ref, h0[b.row_idx[rows]])
