@@ -221,6 +221,33 @@ def test_decode_of_many_sequences_matches_oracle_and_splits():
         assert np.array_equal(k1, k2) and np.array_equal(v1, v2)
 
 
+def test_decode_of_short_sequences_only_matches_oracle_and_splits():
+    """Every sequence shorter than one 256-key partition, so the attention's
+    work list holds partial partitions only (sorted by size, with ties and
+    single-key sequences): every row against the oracle, the batch bit-identical
+    to two uneven halves."""
+    shape = small_bf16_shape()
+    priors = [0, 3, 100, 254, 17, 100, 0, 200, 63, 64, 3, 150] * 6
+    b = ragged_decode_batch(19, priors, max_ctx=256, hidden_rows=80,
+                            row_idx=np.random.default_rng(19).permutation(80)[:len(priors)])
+    rep = Replica.for_batch(shape, "s19", 1, b)
+    hidden = WD.hidden_tensor(shape, "s19", b.hidden_rows)
+    h0 = to64(hidden)
+    snap = PoolSnapshot(rep.layers[0], pool_blocks_of_new_tokens(b))
+    whole = hidden.clone()
+    rep.forward(0, whole, WD.batch_tensors(b))
+    torch.cuda.synchronize()
+    rows = list(range(b.n_rows))
+    ref, _, _ = oracle_decode_rows(shape, "s19", 0, b, rows, h0)
+    _check_rows("short-sequence decode", to64(whole)[b.row_idx], ref, h0[b.row_idx])
+    snap.restore()
+    split = hidden.clone()
+    for part in (np.arange(0, 29), np.arange(29, b.n_rows)):
+        rep.forward(0, split, WD.batch_tensors(b.select(part)))
+    torch.cuda.synchronize()
+    assert torch.equal(split.view(torch.int16), whole.view(torch.int16))
+
+
 def test_prefill_request_aligned_split_is_bit_identical():
     """Request-aligned shares of a prefill batch, run from the cache state
     before the whole batch, give its output rows and appended cache bytes."""
